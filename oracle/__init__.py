@@ -1,0 +1,297 @@
+"""CPU oracle of the AVSG per-decode-step operator (test infrastructure only).
+
+The oracle is plain C (``avsg_oracle.c``), compiled with gcc into
+``liboracle_avsg.so`` and driven through ctypes with NumPy arrays.  Only the
+test suite, the smoke check and the benchmark's CPU-baseline leg use it; the
+product path never imports this package.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liboracle_avsg.so")
+_SRC = os.path.join(_HERE, "avsg_oracle.c")
+
+# Default probe primes (two distinct primes, Section 3.2).
+A1_DEFAULT = 2654435761
+A2_DEFAULT = 2246822519
+
+
+def build(force: bool = True, sanitize: bool = False) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP over requests)."""
+    out = LIB_PATH if not sanitize else os.path.join(_HERE, "liboracle_avsg_asan.so")
+    if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(_SRC):
+        flags = ["-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11", "-Wall", "-Wextra"]
+        if sanitize:
+            flags += ["-fsanitize=address,undefined", "-fno-omit-frame-pointer", "-O1"]
+        tmp = out + ".tmp"
+        subprocess.check_call(["gcc", *flags, "-o", tmp, _SRC])
+        os.replace(tmp, out)
+    return out
+
+
+class _Cfg(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("topk", ctypes.c_int32), ("n_q", ctypes.c_int32),
+                ("slots", ctypes.c_int32), ("retry", ctypes.c_int32), ("max_life", ctypes.c_int32),
+                ("a1", ctypes.c_uint32), ("a2", ctypes.c_uint32)]
+
+
+class RefStats(ctypes.Structure):
+    _fields_ = [("hits", ctypes.c_uint64), ("misses", ctypes.c_uint64),
+                ("lost_exhausted", ctypes.c_uint64), ("lost_collision", ctypes.c_uint64),
+                ("alloc_decays", ctypes.c_uint64), ("revivals", ctypes.c_uint64),
+                ("invalidations", ctypes.c_uint64), ("max_step_alloc_decays", ctypes.c_int32),
+                ("pad", ctypes.c_int32)]
+
+    def as_dict(self):
+        return {f: int(getattr(self, f)) for f, _ in self._fields_ if f != "pad"}
+
+
+_lib = None
+_P = ctypes.c_void_p
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            build(force=False)
+        lib = ctypes.CDLL(LIB_PATH)
+        lib.avsg_ref_create.restype = _P
+        lib.avsg_ref_create.argtypes = [ctypes.POINTER(_Cfg), ctypes.POINTER(ctypes.c_int32)]
+        lib.avsg_ref_destroy.argtypes = [_P]
+        lib.avsg_ref_step.restype = ctypes.c_int32
+        lib.avsg_ref_step.argtypes = [_P, _P, _P, _P, _P, _P, _P, ctypes.c_int32, _P, _P, _P, _P,
+                                      ctypes.c_int32]
+        lib.avsg_ref_export.argtypes = [_P, ctypes.c_int32, _P, _P]
+        lib.avsg_ref_import.argtypes = [_P, ctypes.c_int32, _P, _P]
+        lib.avsg_ref_stats.argtypes = [_P, ctypes.c_int32, ctypes.POINTER(RefStats)]
+        lib.avsg_ref_pack.restype = ctypes.c_uint32
+        lib.avsg_ref_pack.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                      ctypes.c_int64, ctypes.c_int64]
+        lib.avsg_ref_decode.argtypes = [ctypes.c_int32, ctypes.c_uint32, _P, _P, _P, _P]
+        lib.avsg_ref_phi.restype = ctypes.c_int64
+        lib.avsg_ref_phi.argtypes = [ctypes.c_int32, ctypes.c_int64]
+        lib.avsg_ref_probe.argtypes = [_P, ctypes.c_int32, ctypes.c_int32, _P, _P]
+        lib.avsg_ref_dp_create.restype = _P
+        lib.avsg_ref_dp_create.argtypes = [ctypes.c_int32, ctypes.c_int32]
+        lib.avsg_ref_dp_destroy.argtypes = [_P]
+        lib.avsg_ref_dp_step.restype = ctypes.c_int32
+        lib.avsg_ref_dp_step.argtypes = [_P, _P, _P, _P, _P, _P, ctypes.c_int32, _P, _P, _P,
+                                         ctypes.c_int32]
+        lib.avsg_ref_dp_export.argtypes = [_P, ctypes.c_int32, _P]
+        lib.avsg_ref_partition_balanced.argtypes = [ctypes.c_int64, ctypes.c_int32, _P]
+        lib.avsg_ref_partition_request.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                                   ctypes.c_int32, _P]
+        lib.avsg_ref_partition_position.argtypes = [ctypes.c_int64, ctypes.c_int32, _P]
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def _ptr_array(ptrs: Sequence[int]):
+    arr = (ctypes.c_void_p * len(ptrs))(*[ctypes.c_void_p(int(p)) for p in ptrs])
+    return arr
+
+
+def default_threads() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(n, 16))
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+class Oracle:
+    """Stateful CPU reference: one Hash-State table per request."""
+
+    def __init__(self, batch, topk, n_q, slots, retry=3, max_life=16, a1=A1_DEFAULT,
+                 a2=A2_DEFAULT, nthreads: Optional[int] = None):
+        self.lib = _load()
+        self.cfg = _Cfg(batch, topk, n_q, slots, retry, max_life, a1, a2)
+        st = ctypes.c_int32(0)
+        self.h = self.lib.avsg_ref_create(ctypes.byref(self.cfg), ctypes.byref(st))
+        if not self.h:
+            raise OracleError(f"avsg_ref_create failed with status {st.value}")
+        self.B, self.K, self.n_q, self.S = batch, topk, n_q, slots
+        self.nthreads = nthreads or default_threads()
+        self.miss_x = np.zeros((batch, n_q * topk), dtype=np.int32)
+        self.miss_o = np.zeros((batch, n_q * topk), dtype=np.int32)
+
+    @staticmethod
+    def create_status(batch, topk, n_q, slots, retry=3, max_life=16, a1=A1_DEFAULT,
+                      a2=A2_DEFAULT) -> int:
+        lib = _load()
+        cfg = _Cfg(batch, topk, n_q, slots, retry, max_life, a1, a2)
+        st = ctypes.c_int32(0)
+        h = lib.avsg_ref_create(ctypes.byref(cfg), ctypes.byref(st))
+        if h:
+            lib.avsg_ref_destroy(h)
+        return st.value
+
+    def close(self):
+        if self.h:
+            self.lib.avsg_ref_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def step(self, X: np.ndarray, verified: Optional[np.ndarray] = None, host=None, buf=None,
+             row_bytes=None, rows: Optional[np.ndarray] = None):
+        """Run one decode step.  host/buf: lists of per-(stream, request)
+        addresses ordered s*B + r; row_bytes: per stream.
+        Returns (O [B][n_q][K], n [B][n_q]); the transfer lists are in
+        self.miss_x / self.miss_o."""
+        X = np.ascontiguousarray(X, dtype=np.int32)
+        assert X.shape == (self.B, self.n_q, self.K), X.shape
+        O = np.empty_like(X)
+        n = np.empty((self.B, self.n_q), dtype=np.int32)
+        ver = None if verified is None else np.ascontiguousarray(verified, dtype=np.int64)
+        rws = None if rows is None else np.ascontiguousarray(rows, dtype=np.int64)
+        ns = 0
+        hp = bp = rbp = None
+        if host is not None:
+            ns = len(row_bytes)
+            hp = _ptr_array(host)
+            bp = _ptr_array(buf)
+            rb = np.ascontiguousarray(row_bytes, dtype=np.int64)
+            rbp = _ptr(rb)
+        rc = self.lib.avsg_ref_step(self.h, _ptr(X), _ptr(ver), _ptr(O), _ptr(n),
+                                    _ptr(self.miss_x), _ptr(self.miss_o), ns, hp, bp, rbp,
+                                    _ptr(rws), self.nthreads)
+        if rc != 0:
+            raise OracleError(f"avsg_ref_step returned {rc}")
+        return O, n
+
+    def misses(self, r: int, n_r: np.ndarray):
+        tot = int(np.sum(n_r))
+        return self.miss_x[r, :tot].copy(), self.miss_o[r, :tot].copy()
+
+    def export(self, r: int):
+        c = np.empty(self.S, dtype=np.int32)
+        q = np.empty(self.S, dtype=np.uint32)
+        self.lib.avsg_ref_export(self.h, r, _ptr(c), _ptr(q))
+        return c, q
+
+    def import_table(self, r: int, c: np.ndarray, q: np.ndarray):
+        c = np.ascontiguousarray(c, dtype=np.int32)
+        q = np.ascontiguousarray(q, dtype=np.uint32)
+        assert c.shape == (self.S,) and q.shape == (self.S,)
+        self.lib.avsg_ref_import(self.h, r, _ptr(c), _ptr(q))
+
+    def stats(self, r: int) -> dict:
+        s = RefStats()
+        self.lib.avsg_ref_stats(self.h, r, ctypes.byref(s))
+        return s.as_dict()
+
+    def total_stats(self) -> dict:
+        tot = {}
+        for r in range(self.B):
+            for k, v in self.stats(r).items():
+                if k == "max_step_alloc_decays":
+                    tot[k] = max(tot.get(k, 0), v)
+                else:
+                    tot[k] = tot.get(k, 0) + v
+        return tot
+
+    def probe(self, r: int, x: int):
+        hit = ctypes.c_int32(0)
+        h = ctypes.c_int32(0)
+        self.lib.avsg_ref_probe(self.h, r, x, ctypes.byref(hit), ctypes.byref(h))
+        return bool(hit.value), h.value
+
+
+class DualPointerOracle:
+    """Scalar sort-merge matching baseline with an S = K buffer."""
+
+    def __init__(self, batch, topk, nthreads: Optional[int] = None):
+        self.lib = _load()
+        self.h = self.lib.avsg_ref_dp_create(batch, topk)
+        if not self.h:
+            raise OracleError("avsg_ref_dp_create failed")
+        self.B, self.K = batch, topk
+        self.nthreads = nthreads or default_threads()
+        self.miss_x = np.zeros((batch, topk), dtype=np.int32)
+        self.miss_o = np.zeros((batch, topk), dtype=np.int32)
+
+    def close(self):
+        if self.h:
+            self.lib.avsg_ref_dp_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def step(self, X: np.ndarray, host=None, buf=None, row_bytes=None):
+        X = np.ascontiguousarray(X, dtype=np.int32).reshape(self.B, 1, self.K)
+        O = np.empty_like(X)
+        n = np.empty((self.B, 1), dtype=np.int32)
+        ns = 0
+        hp = bp = rbp = None
+        if host is not None:
+            ns = len(row_bytes)
+            hp, bp = _ptr_array(host), _ptr_array(buf)
+            rb = np.ascontiguousarray(row_bytes, dtype=np.int64)
+            rbp = _ptr(rb)
+        self.lib.avsg_ref_dp_step(self.h, _ptr(X), _ptr(O), _ptr(n), _ptr(self.miss_x),
+                                  _ptr(self.miss_o), ns, hp, bp, rbp, self.nthreads)
+        return O, n
+
+    def export(self, r: int):
+        c = np.empty(self.K, dtype=np.int32)
+        self.lib.avsg_ref_dp_export(self.h, r, _ptr(c))
+        return c
+
+
+def pack(m, lifetime, invalid, fingerprint, slot) -> int:
+    return int(_load().avsg_ref_pack(m, lifetime, invalid, fingerprint, slot))
+
+
+def decode(m, q):
+    l, b = ctypes.c_int32(), ctypes.c_int32()
+    fp, o = ctypes.c_int64(), ctypes.c_int64()
+    _load().avsg_ref_decode(m, ctypes.c_uint32(q), ctypes.byref(l), ctypes.byref(b),
+                            ctypes.byref(fp), ctypes.byref(o))
+    return l.value, b.value, fp.value, o.value
+
+
+def phi(m, x) -> int:
+    return int(_load().avsg_ref_phi(m, x))
+
+
+def partition_balanced(n_miss: int, C: int) -> np.ndarray:
+    out = np.empty(C + 1, dtype=np.int64)
+    _load().avsg_ref_partition_balanced(n_miss, C, _ptr(out))
+    return out
+
+
+def partition_request(B: int, C: int, n_q: int, K: int) -> np.ndarray:
+    out = np.empty(C, dtype=np.int64)
+    _load().avsg_ref_partition_request(B, C, n_q, K, _ptr(out))
+    return out
+
+
+def partition_position(n_positions: int, C: int) -> np.ndarray:
+    out = np.empty(C + 1, dtype=np.int64)
+    _load().avsg_ref_partition_position(n_positions, C, _ptr(out))
+    return out
