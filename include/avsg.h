@@ -1,0 +1,195 @@
+/* avsg.h — C ABI of the MI355X (gfx950) implementation of AVSG's per-decode-step
+ * sparse-gather operator (Accelerated Vectorized Sparse Gather, arXiv 2609.37538).
+ *
+ * Per decode step, for every request r of a batch of B requests and every one
+ * of its N_q query tokens (the initial token plus N_mtp speculative ones,
+ * Section 3.2 "Problem formulation"), the operator takes the K token indices the
+ * sparse-attention indexer selected and
+ *   1. matches them against the request's persistent S-slot Hash-State table
+ *      (Section 3.2, Eq. 1-4; Probe, Eq. 8-11),
+ *   2. reserves slots for the misses with lifetime-based eviction
+ *      (Section 3.3 Algorithm 1, Section 3.5, CollectDead Eq. 12, Algorithms 2-3),
+ *   3. shares those reservations across the N_q tokens of the step
+ *      (Section 3.6, Algorithm 4), and
+ *   4. copies only the missed rows from host memory into the reserved slots of
+ *      the device buffer, with the miss list split evenly over all workers
+ *      (Section 3.4, Eq. 5-6).
+ * At the end of the step every cached index >= the verified context length N
+ * is cleared (speculative invalidation, Section 3.6 and Algorithm 4).
+ *
+ * Conventions for every entry point:
+ *   - Memory is owned by the caller: pinned host rows, the device workspace,
+ *     the device buffers and the step outputs.  The handle owns host-side
+ *     bookkeeping and HIP events only.
+ *   - "device" pointers are HIP device memory of the current device; "host"
+ *     pointers are ordinary host memory unless stated otherwise.
+ *   - Calls return an avsg_status; they never throw and never abort.  A
+ *     negative status leaves the handle usable; avsg_last_error() gives detail.
+ *   - avsg_step is asynchronous on the given stream.  Calls on one handle are
+ *     not thread-safe and must be ordered by the caller.
+ *   - Nothing here allocates device memory except avsg_host_alloc (pinned host
+ *     memory) and the HIP events/staging kept by a handle.
+ */
+#ifndef AVSG_H
+#define AVSG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t avsg_status;
+
+#define AVSG_OK 0
+#define AVSG_E_INVAL (-1)       /* null pointer, non-positive size, bad mode */
+#define AVSG_E_NOTPOW2 (-2)     /* S is not a power of two in [2, 2^23] */
+#define AVSG_E_CAPACITY (-3)    /* S < N_q * K (Eq. 7), or S/K beyond what one workgroup's LDS holds */
+#define AVSG_E_RANGE (-4)       /* R < 0, L outside [1, 127], a1/a2 not distinct primes, row size */
+#define AVSG_E_BADINDEX (-5)    /* a selected index outside [0, rows of its request) */
+#define AVSG_E_HIP (-6)         /* a HIP runtime call failed */
+#define AVSG_E_INTERNAL (-7)    /* broken internal invariant */
+#define AVSG_E_UNSUPPORTED (-8) /* valid but unsupported combination (e.g. dual-pointer with N_q > 1) */
+
+/* Stage One matching algorithm. */
+#define AVSG_MATCH_HASH 0     /* vectorized open-addressing hash matching (Section 3.3) */
+#define AVSG_MATCH_DUALPTR 1  /* scalar dual-pointer sort-merge baseline, needs S == K (Appendix C) */
+
+/* Stage Two work assignment (Appendix D). */
+#define AVSG_GATHER_BALANCED 0 /* S3: the miss list split into floor/ceil(N_miss/C) consecutive misses per worker (Eq. 6) */
+#define AVSG_GATHER_REQUEST 1  /* S1: one worker per request (Eq. 13) */
+#define AVSG_GATHER_SDMA 2     /* comparator: the miss list is read back and every missed row is one hipMemcpyAsync on the copy engines */
+#define AVSG_GATHER_NONE 3     /* Stage One only (matching measured alone) */
+
+#define AVSG_MAX_STREAMS 2
+
+typedef struct avsg_config {
+    int32_t batch;      /* B >= 1 */
+    int32_t topk;       /* K >= 1, selected indices per query token */
+    int32_t n_q;        /* N_q = N_mtp + 1 >= 1 query tokens per request per step */
+    int32_t slots;      /* S = 2^m, 2 <= S <= 2^23, S >= N_q*K (Eq. 7) */
+    int32_t retry;      /* R >= 0; probes examine R+1 buckets (default 3) */
+    int32_t max_life;   /* L in [1, 127]; lifetime of a hit or new slot (default 16) */
+    uint32_t a1, a2;    /* distinct primes setting initial bucket and stride (Eq. 9) */
+    int32_t n_streams;  /* 1 (KV rows) or 2 (KV rows + indexer-key rows) */
+    int32_t gather_workers; /* C, workgroups of the balanced gather; 0 = 4 per CU */
+    int64_t row_bytes[AVSG_MAX_STREAMS]; /* bytes per row of each stream, multiple of 4 */
+    int32_t match_mode;  /* AVSG_MATCH_* */
+    int32_t gather_mode; /* AVSG_GATHER_* */
+} avsg_config;
+
+/* Cumulative counters since create (or the last avsg_reset_stats). */
+typedef struct avsg_stats_t {
+    uint64_t steps;           /* avsg_step calls */
+    uint64_t lookups;         /* selected indices looked up: steps * B * N_q * K */
+    uint64_t hits;            /* lookups that found their index resident */
+    uint64_t misses;          /* lookups that reserved a slot and caused a copy */
+    uint64_t bytes_moved;     /* host -> device payload bytes, all streams */
+    uint64_t lost_exhausted;  /* misses whose R+1 install probes found no reusable bucket */
+    uint64_t lost_collision;  /* misses whose bucket install lost to a larger miss rank */
+    uint64_t alloc_decays;    /* unit decays done by the allocation loop (Algorithm 1) */
+    uint64_t revivals;        /* hits on a slot whose lifetime was negative */
+    uint64_t invalidations;   /* cached indices cleared by speculative invalidation */
+    uint64_t bad_indices;     /* selected indices outside [0, rows) (skipped by the copy) */
+    int32_t max_step_alloc_decays; /* largest allocation-decay count of one request-step */
+    int32_t reserved;
+} avsg_stats_t;
+
+typedef struct avsg_handle avsg_handle;
+
+/* Size in bytes of the device workspace that avsg_create needs for cfg
+ * (per-request tables of 8*S bytes, transfer lists of 8*N_q*K bytes,
+ * counters and pointer tables).  Returns 0 for an invalid cfg. */
+size_t avsg_workspace_bytes(const avsg_config *cfg);
+
+/* Create a handle and reset every table to empty (c_j = -1, lifetime -1, every
+ * bucket invalid) on `stream`.
+ *   host_rows        [n_streams*B] host row arrays, entry s*B + r is row 0 of
+ *                    request r in stream s; each row is row_bytes[s] long.  The
+ *                    memory must be pinned and mapped for the device
+ *                    (avsg_host_alloc or hipHostMalloc), 16-byte aligned when
+ *                    row_bytes[s] is a multiple of 16.  Row x of request r is
+ *                    the KV (or indexer-key) entry of token position x.
+ *   rows_per_request [B] host array: number of rows of each request (ids must
+ *                    lie in [0, rows)).
+ *   d_workspace      device memory of avsg_workspace_bytes(cfg) bytes, 256-byte
+ *                    aligned; owned by the caller and used exclusively by this
+ *                    handle until avsg_destroy.
+ *   d_buffers        [n_streams*B] device buffers, entry s*B + r holds S rows of
+ *                    row_bytes[s] bytes (slot o at offset o*row_bytes[s]).
+ *   stream           hipStream_t (NULL = default stream).
+ * Errors: AVSG_E_INVAL, AVSG_E_NOTPOW2, AVSG_E_CAPACITY, AVSG_E_RANGE,
+ * AVSG_E_UNSUPPORTED, AVSG_E_HIP.  On error *out is NULL. */
+avsg_status avsg_create(const avsg_config *cfg, const void *const *host_rows,
+                        const int64_t *rows_per_request, void *d_workspace, size_t workspace_bytes,
+                        void *const *d_buffers, void *stream, avsg_handle **out);
+
+/* One decode step (Algorithm 4) for the whole batch, enqueued on `stream`.
+ *   d_topk          device int32 [B][N_q][K]: selected indices; the indices of
+ *                   one token must be distinct (a DSA top-K list is).
+ *   d_verified_len  device int64 [B]: verified context length N of each
+ *                   request; cached indices >= N are cleared at the end of the
+ *                   step.  NULL disables the invalidation.
+ *   d_slots         device int32 [B][N_q][K] out: buffer slot of every index
+ *                   (the matrix O of Algorithm 4).
+ *   d_miss_counts   device int32 [B][N_q] out: miss count n_g of every token.
+ * When the step's kernels finish, every slot named in d_slots holds the row of
+ * its index in every stream.  Indices outside [0, rows) are counted in
+ * bad_indices and not copied.  Errors: AVSG_E_INVAL, AVSG_E_HIP. */
+avsg_status avsg_step(avsg_handle *h, const int32_t *d_topk, const int64_t *d_verified_len,
+                      int32_t *d_slots, int32_t *d_miss_counts, void *stream);
+
+/* Cumulative counters.  Synchronizes with the handle's last stream. */
+avsg_status avsg_stats(avsg_handle *h, avsg_stats_t *out);
+avsg_status avsg_reset_stats(avsg_handle *h, void *stream);
+
+/* Return request r's table to the initial empty state (a new request takes
+ * over the batch position), enqueued on `stream`.  The buffers are untouched. */
+avsg_status avsg_reset_request(avsg_handle *h, int32_t r, void *stream);
+
+/* Canonical table view of request r, copied to host memory (synchronous):
+ * c_out[S] cached indices, q_out[S] metadata words in the layout of Eq. 2
+ * (lifetime byte | invalid bit | fingerprint | slot).  Hash mode only. */
+avsg_status avsg_export_state(avsg_handle *h, int32_t r, int32_t *c_out, uint32_t *q_out);
+
+/* Transfer list of request r from the last step, copied to host memory
+ * (synchronous): n_out receives the request's miss total, x_out/o_out
+ * (capacity N_q*K each) the index and slot of every miss, ordered by token,
+ * then by position inside the token (increasing index order for dual-pointer). */
+avsg_status avsg_export_misses(avsg_handle *h, int32_t r, int32_t *n_out, int32_t *x_out,
+                               int32_t *o_out);
+
+/* Per-step kernel timing with HIP events recorded on the step's stream.
+ * avsg_set_timing(h, 1) starts recording (and clears the record);
+ * avsg_timing copies up to `cap` recorded steps (synchronizing):
+ * match_ms[i] and gather_ms[i] are the durations of step i's matching kernel
+ * and of its Stage Two (kernel or copies). */
+avsg_status avsg_set_timing(avsg_handle *h, int32_t enable);
+avsg_status avsg_timing(avsg_handle *h, float *match_ms, float *gather_ms, int32_t cap,
+                        int32_t *n_out);
+
+avsg_status avsg_destroy(avsg_handle *h);
+
+const char *avsg_strerror(avsg_status s);
+const char *avsg_last_error(const avsg_handle *h);
+
+/* Pinned, device-mapped host memory for the host rows (hipHostMalloc with
+ * hipHostMallocMapped, plus hipHostMallocNonCoherent when coherent == 0 so the
+ * device may cache reads).  Free with avsg_host_free. */
+avsg_status avsg_host_alloc(size_t bytes, int32_t coherent, void **out);
+avsg_status avsg_host_free(void *p);
+
+/* Measured hipMemcpyAsync host-to-device bandwidth from pinned `host` to
+ * `device` (`bytes` each), median of `iters` timed copies after one warm-up,
+ * in GB/s (1e9 B/s).  Synchronous. */
+avsg_status avsg_h2d_peak(const void *host, void *device, size_t bytes, int32_t iters,
+                          void *stream, double *gbps);
+
+/* Number of compute units of the current device (the default C is 4x this). */
+int32_t avsg_device_cus(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AVSG_H */

@@ -1,0 +1,554 @@
+// Host side of libavsg: the C ABI declared in include/avsg.h.
+//
+// Validates configurations, lays out the caller's device workspace, records
+// device-visible addresses of the caller's pinned host rows, and enqueues the
+// Stage One / Stage Two kernels of each decode step on the caller's stream.
+#include "avsg.h"
+
+#include <algorithm>
+#include <array>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "avsg_internal.h"
+
+using namespace avsg;
+
+struct avsg_handle {
+  avsg_config cfg{};
+  int device = 0;
+  int m = 0;
+  size_t lds = 0;
+  int workers = 0;
+  // workspace sections
+  int32_t* table_c = nullptr;
+  uint32_t* table_q = nullptr;
+  int2* dp_state = nullptr;
+  int2* miss_list = nullptr;
+  unsigned long long* stats = nullptr;
+  uint64_t* host_ptrs = nullptr;
+  uint64_t* buf_ptrs = nullptr;
+  int64_t* rows_dev = nullptr;
+  // host copies
+  std::vector<int64_t> rows;
+  std::vector<uint64_t> host_dev, bufs;
+  uint64_t steps = 0;
+  hipStream_t last_stream = nullptr;
+  int32_t* last_counts = nullptr;
+  // timing
+  bool timing = false;
+  std::vector<std::array<hipEvent_t, 3>> events;
+  size_t n_timed = 0;
+  // SDMA comparator staging (pinned host)
+  int32_t* h_counts = nullptr;
+  int2* h_list = nullptr;
+  std::vector<void*> dsts, srcs;
+  std::vector<size_t> sizes;
+  std::string err;
+};
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int kMaxBatch = 1024;
+constexpr size_t kMaxTimedSteps = 16384;
+
+size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+bool is_prime_u32(uint32_t v) {
+  if (v < 2) return false;
+  if (v % 2 == 0) return v == 2;
+  for (uint64_t d = 3; d * d <= v; d += 2)
+    if (v % d == 0) return false;
+  return true;
+}
+
+struct Layout {
+  size_t table_c, table_q, miss_list, stats, host_ptrs, buf_ptrs, rows, total;
+};
+
+Layout layout_of(const avsg_config& c) {
+  Layout L{};
+  const size_t B = static_cast<size_t>(c.batch), S = static_cast<size_t>(c.slots);
+  size_t off = 0;
+  L.table_c = off; off += up(B * S * 4);
+  L.table_q = off; off += up(B * S * 4);
+  L.miss_list = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk * 8);
+  L.stats = off; off += up(B * kNumStats * 8);
+  L.host_ptrs = off; off += up(static_cast<size_t>(c.n_streams) * B * 8);
+  L.buf_ptrs = off; off += up(static_cast<size_t>(c.n_streams) * B * 8);
+  L.rows = off; off += up(B * 8);
+  L.total = off;
+  return L;
+}
+
+int log2_exact(int32_t s) {
+  int m = 0;
+  while ((1 << m) < s) ++m;
+  return m;
+}
+
+avsg_status check_config(const avsg_config* c, std::string* why) {
+  auto fail = [&](avsg_status s, const char* msg) {
+    if (why) *why = msg;
+    return s;
+  };
+  if (!c) return fail(AVSG_E_INVAL, "null config");
+  if (c->batch < 1 || c->batch > kMaxBatch) return fail(AVSG_E_INVAL, "batch must be in [1, 1024]");
+  if (c->topk < 1 || c->n_q < 1) return fail(AVSG_E_INVAL, "topk and n_q must be positive");
+  if (c->slots < 2 || (c->slots & (c->slots - 1)) != 0 || c->slots > (1 << 23))
+    return fail(AVSG_E_NOTPOW2, "slots must be a power of two in [2, 2^23]");
+  if (static_cast<int64_t>(c->slots) < static_cast<int64_t>(c->n_q) * c->topk)
+    return fail(AVSG_E_CAPACITY, "slots < n_q * topk (buffer capacity rule)");
+  if (c->retry < 0) return fail(AVSG_E_RANGE, "retry must be >= 0");
+  if (c->max_life < 1 || c->max_life > 127) return fail(AVSG_E_RANGE, "max_life must be in [1, 127]");
+  if (c->a1 == c->a2 || !is_prime_u32(c->a1) || !is_prime_u32(c->a2))
+    return fail(AVSG_E_RANGE, "a1 and a2 must be distinct primes");
+  if (c->n_streams < 1 || c->n_streams > AVSG_MAX_STREAMS)
+    return fail(AVSG_E_INVAL, "n_streams must be 1 or 2");
+  for (int s = 0; s < c->n_streams; ++s)
+    if (c->row_bytes[s] <= 0 || (c->row_bytes[s] & 3) != 0)
+      return fail(AVSG_E_RANGE, "row_bytes must be a positive multiple of 4");
+  if (c->gather_workers < 0) return fail(AVSG_E_INVAL, "gather_workers must be >= 0");
+  if (c->match_mode != AVSG_MATCH_HASH && c->match_mode != AVSG_MATCH_DUALPTR)
+    return fail(AVSG_E_INVAL, "unknown match_mode");
+  if (c->gather_mode < AVSG_GATHER_BALANCED || c->gather_mode > AVSG_GATHER_NONE)
+    return fail(AVSG_E_INVAL, "unknown gather_mode");
+  if (c->match_mode == AVSG_MATCH_DUALPTR) {
+    if (c->n_q != 1) return fail(AVSG_E_UNSUPPORTED, "dual-pointer matching handles one token per step");
+    if (c->slots != c->topk) return fail(AVSG_E_UNSUPPORTED, "dual-pointer matching needs slots == topk");
+    if (c->topk > 4096) return fail(AVSG_E_CAPACITY, "dual-pointer matching supports topk <= 4096");
+  } else {
+    if (match_lds_bytes(c->slots, c->topk) == 0)
+      return fail(AVSG_E_CAPACITY, "topk beyond 4096 indices per token");
+  }
+  return AVSG_OK;
+}
+
+avsg_status hip_fail(avsg_handle* h, hipError_t e, const char* what) {
+  if (h) {
+    h->err = std::string(what) + ": " + hipGetErrorString(e);
+  }
+  return AVSG_E_HIP;
+}
+
+#define HIP_TRY(h, call)                                   \
+  do {                                                     \
+    hipError_t e_ = (call);                                \
+    if (e_ != hipSuccess) return hip_fail((h), e_, #call); \
+  } while (0)
+
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  return cus;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t avsg_workspace_bytes(const avsg_config* cfg) {
+  if (check_config(cfg, nullptr) != AVSG_OK) return 0;
+  return layout_of(*cfg).total;
+}
+
+const char* avsg_strerror(avsg_status s) {
+  switch (s) {
+    case AVSG_OK: return "ok";
+    case AVSG_E_INVAL: return "invalid argument";
+    case AVSG_E_NOTPOW2: return "slots is not a power of two in [2, 2^23]";
+    case AVSG_E_CAPACITY: return "capacity: slots < n_q*topk, or beyond the on-chip limit";
+    case AVSG_E_RANGE: return "parameter out of range";
+    case AVSG_E_BADINDEX: return "selected index out of range";
+    case AVSG_E_HIP: return "HIP runtime error";
+    case AVSG_E_INTERNAL: return "internal error";
+    case AVSG_E_UNSUPPORTED: return "unsupported combination";
+    default: return "unknown status";
+  }
+}
+
+const char* avsg_last_error(const avsg_handle* h) { return h ? h->err.c_str() : ""; }
+
+int32_t avsg_device_cus(void) { return device_cus(); }
+
+avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
+                        const int64_t* rows_per_request, void* d_workspace, size_t workspace_bytes,
+                        void* const* d_buffers, void* stream, avsg_handle** out) {
+  if (!out) return AVSG_E_INVAL;
+  *out = nullptr;
+  std::string why;
+  avsg_status st = check_config(cfg, &why);
+  if (st != AVSG_OK) {
+    std::fprintf(stderr, "avsg_create: %s\n", why.c_str());
+    return st;
+  }
+  const avsg_config c = *cfg;
+  if (!host_rows || !rows_per_request || !d_workspace || !d_buffers) return AVSG_E_INVAL;
+  const Layout L = layout_of(c);
+  if (workspace_bytes < L.total) return AVSG_E_INVAL;
+  if ((reinterpret_cast<uintptr_t>(d_workspace) & (kAlign - 1)) != 0) return AVSG_E_INVAL;
+  const int B = c.batch;
+  for (int r = 0; r < B; ++r)
+    if (rows_per_request[r] < 1) return AVSG_E_INVAL;
+  for (int i = 0; i < c.n_streams * B; ++i) {
+    if (!host_rows[i] || !d_buffers[i]) return AVSG_E_INVAL;
+    const int s = i / B;
+    if ((c.row_bytes[s] & 15) == 0 &&
+        ((reinterpret_cast<uintptr_t>(host_rows[i]) & 15) != 0 ||
+         (reinterpret_cast<uintptr_t>(d_buffers[i]) & 15) != 0))
+      return AVSG_E_INVAL;
+    if ((reinterpret_cast<uintptr_t>(host_rows[i]) & 3) != 0 ||
+        (reinterpret_cast<uintptr_t>(d_buffers[i]) & 3) != 0)
+      return AVSG_E_INVAL;
+  }
+
+  auto* h = new avsg_handle();
+  h->cfg = c;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  h->last_stream = s;
+  if (hipGetDevice(&h->device) != hipSuccess) {
+    delete h;
+    return AVSG_E_HIP;
+  }
+  h->m = log2_exact(c.slots);
+  unsigned char* ws = static_cast<unsigned char*>(d_workspace);
+  h->table_c = reinterpret_cast<int32_t*>(ws + L.table_c);
+  h->table_q = reinterpret_cast<uint32_t*>(ws + L.table_q);
+  h->dp_state = reinterpret_cast<int2*>(ws + L.table_c);  // S == K: the two table arrays hold [B][K] pairs
+  h->miss_list = reinterpret_cast<int2*>(ws + L.miss_list);
+  h->stats = reinterpret_cast<unsigned long long*>(ws + L.stats);
+  h->host_ptrs = reinterpret_cast<uint64_t*>(ws + L.host_ptrs);
+  h->buf_ptrs = reinterpret_cast<uint64_t*>(ws + L.buf_ptrs);
+  h->rows_dev = reinterpret_cast<int64_t*>(ws + L.rows);
+  h->rows.assign(rows_per_request, rows_per_request + B);
+  h->host_dev.resize(static_cast<size_t>(c.n_streams) * B);
+  h->bufs.resize(static_cast<size_t>(c.n_streams) * B);
+  for (int i = 0; i < c.n_streams * B; ++i) {
+    void* dptr = nullptr;
+    hipError_t e = hipHostGetDevicePointer(&dptr, const_cast<void*>(host_rows[i]), 0);
+    if (e != hipSuccess || !dptr) {
+      h->err = "host rows must be pinned, device-mapped memory (avsg_host_alloc / hipHostMalloc)";
+      std::fprintf(stderr, "avsg_create: %s (%s)\n", h->err.c_str(), hipGetErrorString(e));
+      delete h;
+      return AVSG_E_INVAL;
+    }
+    h->host_dev[i] = reinterpret_cast<uint64_t>(dptr);
+    h->bufs[i] = reinterpret_cast<uint64_t>(d_buffers[i]);
+  }
+  const int cus = device_cus();
+  h->workers = c.gather_workers > 0 ? c.gather_workers : std::max(1, 4 * cus);
+
+  auto cleanup = [&](avsg_status rc) {
+    delete h;
+    return rc;
+  };
+  hipError_t e;
+  if (c.match_mode == AVSG_MATCH_HASH) {
+    h->lds = match_lds_bytes(c.slots, c.topk);
+    int max_lds = 0;
+    hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device);
+    if (max_lds > 0 && h->lds > static_cast<size_t>(max_lds)) {
+      std::fprintf(stderr, "avsg_create: table of %d slots needs %zu B of LDS, limit %d\n",
+                   c.slots, h->lds, max_lds);
+      return cleanup(AVSG_E_CAPACITY);
+    }
+    if ((e = prepare_match_hash(h->lds)) != hipSuccess) return cleanup(hip_fail(nullptr, e, ""));
+    if ((e = launch_reset_tables(h->table_c, h->table_q,
+                                 static_cast<size_t>(B) * c.slots, s)) != hipSuccess)
+      return cleanup(AVSG_E_HIP);
+  } else {
+    h->lds = dualptr_lds_bytes(c.topk);
+    if ((e = prepare_match_dualptr(h->lds)) != hipSuccess) return cleanup(AVSG_E_HIP);
+    if ((e = launch_reset_dualptr(h->dp_state, B, c.topk, s)) != hipSuccess) return cleanup(AVSG_E_HIP);
+  }
+  if (launch_zero_u64(h->stats, static_cast<size_t>(B) * kNumStats, s) != hipSuccess)
+    return cleanup(AVSG_E_HIP);
+  if (hipMemcpyAsync(h->host_ptrs, h->host_dev.data(), h->host_dev.size() * 8,
+                     hipMemcpyHostToDevice, s) != hipSuccess ||
+      hipMemcpyAsync(h->buf_ptrs, h->bufs.data(), h->bufs.size() * 8, hipMemcpyHostToDevice, s) !=
+          hipSuccess ||
+      hipMemcpyAsync(h->rows_dev, h->rows.data(), h->rows.size() * 8, hipMemcpyHostToDevice, s) !=
+          hipSuccess)
+    return cleanup(AVSG_E_HIP);
+  if (c.gather_mode == AVSG_GATHER_SDMA) {
+    const size_t nl = static_cast<size_t>(B) * c.n_q * c.topk;
+    if (hipHostMalloc(reinterpret_cast<void**>(&h->h_counts), static_cast<size_t>(B) * c.n_q * 4, 0) != hipSuccess ||
+        hipHostMalloc(reinterpret_cast<void**>(&h->h_list), nl * 8, 0) != hipSuccess)
+      return cleanup(AVSG_E_HIP);
+    h->dsts.reserve(nl * c.n_streams);
+    h->srcs.reserve(nl * c.n_streams);
+    h->sizes.reserve(nl * c.n_streams);
+  }
+  if (hipStreamSynchronize(s) != hipSuccess) return cleanup(AVSG_E_HIP);
+  *out = h;
+  return AVSG_OK;
+}
+
+static avsg_status record(avsg_handle* h, int which, hipStream_t s) {
+  if (!h->timing || h->n_timed >= kMaxTimedSteps) return AVSG_OK;
+  if (h->events.size() <= h->n_timed) {
+    std::array<hipEvent_t, 3> ev{};
+    for (auto& x : ev) HIP_TRY(h, hipEventCreate(&x));
+    h->events.push_back(ev);
+  }
+  HIP_TRY(h, hipEventRecord(h->events[h->n_timed][which], s));
+  return AVSG_OK;
+}
+
+static avsg_status sdma_gather(avsg_handle* h, const int32_t* d_counts, hipStream_t s) {
+  const avsg_config& c = h->cfg;
+  const int B = c.batch;
+  const size_t per_req = static_cast<size_t>(c.n_q) * c.topk;
+  HIP_TRY(h, hipMemcpyAsync(h->h_counts, d_counts, static_cast<size_t>(B) * c.n_q * 4,
+                            hipMemcpyDeviceToHost, s));
+  HIP_TRY(h, hipMemcpyAsync(h->h_list, h->miss_list, static_cast<size_t>(B) * per_req * 8,
+                            hipMemcpyDeviceToHost, s));
+  HIP_TRY(h, hipStreamSynchronize(s));
+  h->dsts.clear();
+  h->srcs.clear();
+  h->sizes.clear();
+  for (int r = 0; r < B; ++r) {
+    int64_t tot = 0;
+    for (int g = 0; g < c.n_q; ++g) tot += h->h_counts[static_cast<size_t>(r) * c.n_q + g];
+    for (int64_t k = 0; k < tot; ++k) {
+      const int2 e = h->h_list[static_cast<size_t>(r) * per_req + k];
+      if (e.x < 0 || e.x >= h->rows[r] || e.y < 0 || e.y >= c.slots) continue;
+      for (int st = 0; st < c.n_streams; ++st) {
+        const uint64_t rb = static_cast<uint64_t>(c.row_bytes[st]);
+        h->srcs.push_back(reinterpret_cast<void*>(h->host_dev[static_cast<size_t>(st) * B + r] +
+                                                  static_cast<uint64_t>(e.x) * rb));
+        h->dsts.push_back(reinterpret_cast<void*>(h->bufs[static_cast<size_t>(st) * B + r] +
+                                                  static_cast<uint64_t>(e.y) * rb));
+        h->sizes.push_back(static_cast<size_t>(rb));
+      }
+    }
+  }
+  // one copy-engine command per missed row and stream
+  for (size_t i = 0; i < h->sizes.size(); ++i)
+    HIP_TRY(h, hipMemcpyAsync(h->dsts[i], h->srcs[i], h->sizes[i], hipMemcpyHostToDevice, s));
+  return AVSG_OK;
+}
+
+avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_verified_len,
+                      int32_t* d_slots, int32_t* d_miss_counts, void* stream) {
+  if (!h || !d_topk || !d_slots || !d_miss_counts) return AVSG_E_INVAL;
+  const avsg_config& c = h->cfg;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  h->last_stream = s;
+  h->last_counts = d_miss_counts;
+  avsg_status rc;
+  if ((rc = record(h, 0, s)) != AVSG_OK) return rc;
+  if (c.match_mode == AVSG_MATCH_HASH) {
+    MatchParams p{};
+    p.B = c.batch; p.K = c.topk; p.n_q = c.n_q; p.S = c.slots; p.m = h->m;
+    p.R = c.retry; p.L = c.max_life; p.a1 = c.a1; p.a2 = c.a2;
+    p.f_mask = static_cast<uint32_t>((1u << (23 - h->m)) - 1u);
+    p.topk = d_topk; p.verified = d_verified_len; p.rows = h->rows_dev;
+    p.table_c = h->table_c; p.table_q = h->table_q;
+    p.slots_out = d_slots; p.miss_counts = d_miss_counts; p.miss_list = h->miss_list;
+    p.stats = h->stats;
+    HIP_TRY(h, launch_match_hash(p, h->lds, s));
+  } else {
+    DualPtrParams p{};
+    p.B = c.batch; p.K = c.topk; p.topk = d_topk; p.rows = h->rows_dev; p.state = h->dp_state;
+    p.slots_out = d_slots; p.miss_counts = d_miss_counts; p.miss_list = h->miss_list;
+    p.stats = h->stats;
+    HIP_TRY(h, launch_match_dualptr(p, h->lds, s));
+  }
+  if ((rc = record(h, 1, s)) != AVSG_OK) return rc;
+  GatherParams g{};
+  g.B = c.batch; g.n_q = c.n_q; g.K = c.topk; g.S = c.slots;
+  g.miss_counts = d_miss_counts; g.miss_list = h->miss_list; g.rows = h->rows_dev;
+  g.n_streams = c.n_streams; g.host_ptrs = h->host_ptrs; g.buf_ptrs = h->buf_ptrs;
+  g.row_bytes0 = c.row_bytes[0];
+  g.row_bytes1 = c.n_streams > 1 ? c.row_bytes[1] : 0;
+  switch (c.gather_mode) {
+    case AVSG_GATHER_BALANCED: HIP_TRY(h, launch_gather_balanced(g, h->workers, s)); break;
+    case AVSG_GATHER_REQUEST: HIP_TRY(h, launch_gather_request(g, s)); break;
+    case AVSG_GATHER_SDMA:
+      if ((rc = sdma_gather(h, d_miss_counts, s)) != AVSG_OK) return rc;
+      break;
+    default: break;
+  }
+  if ((rc = record(h, 2, s)) != AVSG_OK) return rc;
+  if (h->timing && h->n_timed < kMaxTimedSteps) h->n_timed++;
+  h->steps++;
+  return AVSG_OK;
+}
+
+avsg_status avsg_stats(avsg_handle* h, avsg_stats_t* out) {
+  if (!h || !out) return AVSG_E_INVAL;
+  const avsg_config& c = h->cfg;
+  HIP_TRY(h, hipStreamSynchronize(h->last_stream));
+  std::vector<unsigned long long> st(static_cast<size_t>(c.batch) * kNumStats);
+  HIP_TRY(h, hipMemcpy(st.data(), h->stats, st.size() * 8, hipMemcpyDeviceToHost));
+  std::memset(out, 0, sizeof(*out));
+  out->steps = h->steps;
+  out->lookups = h->steps * static_cast<uint64_t>(c.batch) * c.n_q * c.topk;
+  uint64_t max_dec = 0;
+  for (int r = 0; r < c.batch; ++r) {
+    const unsigned long long* s = &st[static_cast<size_t>(r) * kNumStats];
+    out->hits += s[kStatHits];
+    out->misses += s[kStatMisses];
+    out->lost_exhausted += s[kStatLostExhausted];
+    out->lost_collision += s[kStatLostCollision];
+    out->alloc_decays += s[kStatAllocDecays];
+    out->revivals += s[kStatRevivals];
+    out->invalidations += s[kStatInvalidations];
+    out->bad_indices += s[kStatBadIndices];
+    max_dec = std::max<uint64_t>(max_dec, s[kStatMaxStepDecays]);
+  }
+  out->max_step_alloc_decays = static_cast<int32_t>(max_dec);
+  uint64_t rb = 0;
+  for (int s = 0; s < c.n_streams; ++s) rb += static_cast<uint64_t>(c.row_bytes[s]);
+  out->bytes_moved = c.gather_mode == AVSG_GATHER_NONE ? 0 : out->misses * rb;
+  return AVSG_OK;
+}
+
+avsg_status avsg_reset_stats(avsg_handle* h, void* stream) {
+  if (!h) return AVSG_E_INVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIP_TRY(h, launch_zero_u64(h->stats, static_cast<size_t>(h->cfg.batch) * kNumStats, s));
+  h->steps = 0;
+  h->last_stream = s;
+  return AVSG_OK;
+}
+
+avsg_status avsg_reset_request(avsg_handle* h, int32_t r, void* stream) {
+  if (!h || r < 0 || r >= h->cfg.batch) return AVSG_E_INVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t S = static_cast<size_t>(h->cfg.slots);
+  if (h->cfg.match_mode == AVSG_MATCH_HASH) {
+    HIP_TRY(h, launch_reset_tables(h->table_c + r * S, h->table_q + r * S, S, s));
+  } else {
+    // a one-request reset of the dual-pointer list: (-1, j) for j = 0..K-1
+    HIP_TRY(h, launch_reset_dualptr(h->dp_state + r * S, 1, h->cfg.topk, s));
+  }
+  h->last_stream = s;
+  return AVSG_OK;
+}
+
+avsg_status avsg_export_state(avsg_handle* h, int32_t r, int32_t* c_out, uint32_t* q_out) {
+  if (!h || !c_out || !q_out || r < 0 || r >= h->cfg.batch) return AVSG_E_INVAL;
+  if (h->cfg.match_mode != AVSG_MATCH_HASH) return AVSG_E_UNSUPPORTED;
+  const size_t S = static_cast<size_t>(h->cfg.slots);
+  HIP_TRY(h, hipStreamSynchronize(h->last_stream));
+  HIP_TRY(h, hipMemcpy(c_out, h->table_c + r * S, S * 4, hipMemcpyDeviceToHost));
+  HIP_TRY(h, hipMemcpy(q_out, h->table_q + r * S, S * 4, hipMemcpyDeviceToHost));
+  return AVSG_OK;
+}
+
+avsg_status avsg_export_misses(avsg_handle* h, int32_t r, int32_t* n_out, int32_t* x_out,
+                               int32_t* o_out) {
+  if (!h || !n_out || !x_out || !o_out || r < 0 || r >= h->cfg.batch) return AVSG_E_INVAL;
+  const avsg_config& c = h->cfg;
+  if (!h->last_counts) {
+    *n_out = 0;
+    return AVSG_OK;
+  }
+  HIP_TRY(h, hipStreamSynchronize(h->last_stream));
+  std::vector<int32_t> cnt(c.n_q);
+  HIP_TRY(h, hipMemcpy(cnt.data(), h->last_counts + static_cast<size_t>(r) * c.n_q, c.n_q * 4,
+                       hipMemcpyDeviceToHost));
+  int64_t tot = 0;
+  for (int g = 0; g < c.n_q; ++g) tot += cnt[g];
+  if (tot < 0 || tot > static_cast<int64_t>(c.n_q) * c.topk) return AVSG_E_INTERNAL;
+  std::vector<int2> ml(static_cast<size_t>(tot));
+  if (tot > 0)
+    HIP_TRY(h, hipMemcpy(ml.data(), h->miss_list + static_cast<size_t>(r) * c.n_q * c.topk,
+                         static_cast<size_t>(tot) * 8, hipMemcpyDeviceToHost));
+  for (int64_t k = 0; k < tot; ++k) {
+    x_out[k] = ml[k].x;
+    o_out[k] = ml[k].y;
+  }
+  *n_out = static_cast<int32_t>(tot);
+  return AVSG_OK;
+}
+
+avsg_status avsg_set_timing(avsg_handle* h, int32_t enable) {
+  if (!h) return AVSG_E_INVAL;
+  h->timing = enable != 0;
+  h->n_timed = 0;
+  return AVSG_OK;
+}
+
+avsg_status avsg_timing(avsg_handle* h, float* match_ms, float* gather_ms, int32_t cap,
+                        int32_t* n_out) {
+  if (!h || !n_out || cap < 0) return AVSG_E_INVAL;
+  HIP_TRY(h, hipStreamSynchronize(h->last_stream));
+  const size_t n = std::min<size_t>(h->n_timed, static_cast<size_t>(cap));
+  for (size_t i = 0; i < n; ++i) {
+    float a = 0.f, b = 0.f;
+    HIP_TRY(h, hipEventElapsedTime(&a, h->events[i][0], h->events[i][1]));
+    HIP_TRY(h, hipEventElapsedTime(&b, h->events[i][1], h->events[i][2]));
+    if (match_ms) match_ms[i] = a;
+    if (gather_ms) gather_ms[i] = b;
+  }
+  *n_out = static_cast<int32_t>(n);
+  return AVSG_OK;
+}
+
+avsg_status avsg_destroy(avsg_handle* h) {
+  if (!h) return AVSG_E_INVAL;
+  (void)hipStreamSynchronize(h->last_stream);
+  for (auto& ev : h->events)
+    for (auto& x : ev) (void)hipEventDestroy(x);
+  if (h->h_counts) (void)hipHostFree(h->h_counts);
+  if (h->h_list) (void)hipHostFree(h->h_list);
+  delete h;
+  return AVSG_OK;
+}
+
+avsg_status avsg_host_alloc(size_t bytes, int32_t coherent, void** out) {
+  if (!out || bytes == 0) return AVSG_E_INVAL;
+  *out = nullptr;
+  unsigned flags = hipHostMallocMapped | (coherent ? hipHostMallocCoherent : hipHostMallocNonCoherent);
+  if (hipHostMalloc(out, bytes, flags) != hipSuccess) {
+    *out = nullptr;
+    return AVSG_E_HIP;
+  }
+  return AVSG_OK;
+}
+
+avsg_status avsg_host_free(void* p) {
+  if (!p) return AVSG_E_INVAL;
+  return hipHostFree(p) == hipSuccess ? AVSG_OK : AVSG_E_HIP;
+}
+
+avsg_status avsg_h2d_peak(const void* host, void* device, size_t bytes, int32_t iters, void* stream,
+                          double* gbps) {
+  if (!host || !device || !gbps || bytes == 0 || iters < 1) return AVSG_E_INVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipEvent_t a, b;
+  if (hipEventCreate(&a) != hipSuccess) return AVSG_E_HIP;
+  if (hipEventCreate(&b) != hipSuccess) {
+    (void)hipEventDestroy(a);
+    return AVSG_E_HIP;
+  }
+  std::vector<float> ms;
+  avsg_status rc = AVSG_OK;
+  for (int i = 0; i <= iters && rc == AVSG_OK; ++i) {
+    if (hipEventRecord(a, s) != hipSuccess ||
+        hipMemcpyAsync(device, host, bytes, hipMemcpyHostToDevice, s) != hipSuccess ||
+        hipEventRecord(b, s) != hipSuccess || hipEventSynchronize(b) != hipSuccess) {
+      rc = AVSG_E_HIP;
+      break;
+    }
+    float t = 0.f;
+    if (hipEventElapsedTime(&t, a, b) != hipSuccess) rc = AVSG_E_HIP;
+    if (i > 0) ms.push_back(t);
+  }
+  (void)hipEventDestroy(a);
+  (void)hipEventDestroy(b);
+  if (rc != AVSG_OK) return rc;
+  std::sort(ms.begin(), ms.end());
+  const double med = ms[ms.size() / 2];
+  *gbps = static_cast<double>(bytes) / (med * 1e-3) / 1e9;
+  return AVSG_OK;
+}
+
+}  // extern "C"

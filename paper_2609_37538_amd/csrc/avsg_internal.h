@@ -1,0 +1,85 @@
+// Internal declarations shared by the translation units of libavsg (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace avsg {
+
+// Threads of one matching workgroup (one request per workgroup).
+constexpr int kMatchThreads = 1024;
+// Threads of one gather workgroup.
+constexpr int kGatherThreads = 256;
+// Misses staged per gather tile.
+constexpr int kGatherTile = 64;
+
+// Per-request device counters (uint64 each, cumulative).
+enum StatIndex : int {
+  kStatHits = 0,
+  kStatMisses,
+  kStatLostExhausted,
+  kStatLostCollision,
+  kStatAllocDecays,
+  kStatRevivals,
+  kStatInvalidations,
+  kStatBadIndices,
+  kStatMaxStepDecays,
+  kNumStats
+};
+
+// Word written to every bucket/slot by a reset: lifetime -1, invalid, fp 0, slot 0.
+constexpr uint32_t kEmptyWord = 0xFF800000u;
+
+struct MatchParams {
+  int32_t B, K, n_q, S, m, R, L;
+  uint32_t a1, a2;
+  uint32_t f_mask;              // F - 1, F = 2^(23-m)
+  const int32_t* topk;          // [B][n_q][K]
+  const int64_t* verified;      // [B] or nullptr
+  const int64_t* rows;          // [B]
+  int32_t* table_c;             // [B][S]
+  uint32_t* table_q;            // [B][S]
+  int32_t* slots_out;           // [B][n_q][K]
+  int32_t* miss_counts;         // [B][n_q]
+  int2* miss_list;              // [B][n_q*K]  (index, slot)
+  unsigned long long* stats;    // [B][kNumStats]
+};
+
+struct GatherParams {
+  int32_t B, n_q, K, S;
+  const int32_t* miss_counts;   // [B][n_q]
+  const int2* miss_list;        // [B][n_q*K]
+  const int64_t* rows;          // [B]
+  int32_t n_streams;
+  const uint64_t* host_ptrs;    // [n_streams][B] device-visible addresses of host row 0
+  const uint64_t* buf_ptrs;     // [n_streams][B] device buffer base addresses
+  int64_t row_bytes0, row_bytes1;
+};
+
+struct DualPtrParams {
+  int32_t B, K;
+  const int32_t* topk;          // [B][K]
+  const int64_t* rows;          // [B]
+  int2* state;                  // [B][K] (cached id, slot) sorted by id
+  int32_t* slots_out;           // [B][K]
+  int32_t* miss_counts;         // [B]
+  int2* miss_list;              // [B][K]
+  unsigned long long* stats;    // [B][kNumStats]
+};
+
+// LDS bytes of the matching kernel for (S, K); 0 if K exceeds the supported
+// indices per thread.
+size_t match_lds_bytes(int S, int K);
+size_t dualptr_lds_bytes(int K);
+
+hipError_t launch_match_hash(const MatchParams& p, size_t lds, hipStream_t s);
+hipError_t prepare_match_hash(size_t lds);
+hipError_t launch_reset_tables(int32_t* c, uint32_t* q, size_t n, hipStream_t s);
+hipError_t launch_zero_u64(unsigned long long* p, size_t n, hipStream_t s);
+hipError_t launch_gather_balanced(const GatherParams& p, int workers, hipStream_t s);
+hipError_t launch_gather_request(const GatherParams& p, hipStream_t s);
+hipError_t launch_match_dualptr(const DualPtrParams& p, size_t lds, hipStream_t s);
+hipError_t prepare_match_dualptr(size_t lds);
+hipError_t launch_reset_dualptr(int2* state, int B, int K, hipStream_t s);
+
+}  // namespace avsg

@@ -1,0 +1,181 @@
+"""Test harness: one seeded workload driven through the CPU oracle and the GPU
+operator on the same pinned host rows, compared element by element.
+
+Only tests, the smoke check and the benchmark's CPU-baseline leg import this.
+"""
+from __future__ import annotations
+
+import sys
+import time
+from typing import Optional
+
+import numpy as np
+
+import oracle as ORC
+import workload as W
+
+
+def log(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+class HostRows:
+    """Per-stream pinned host regions holding every request's rows."""
+
+    def __init__(self, wl: W.Workload, coherent: bool = False):
+        from paper_2609_37538_amd import avsg as A
+        self.wl = wl
+        spec = wl.spec
+        self.regions = []
+        self.ptrs = []           # ordered s*B + r
+        offs = wl.request_row_offsets()
+        for s, rb in enumerate(spec.row_bytes):
+            reg = A.HostRegion(wl.host_rows_total() * rb, coherent=coherent)
+            W.fill_host(wl, s, reg.ptr)
+            self.regions.append(reg)
+            self.ptrs += [reg.ptr + int(offs[r]) * rb for r in range(spec.batch)]
+
+    def stream_ptrs(self):
+        return [reg.ptr for reg in self.regions]
+
+    def row_view(self, s: int, r: int) -> np.ndarray:
+        spec = self.wl.spec
+        rb = spec.row_bytes[s]
+        offs = self.wl.request_row_offsets()
+        full = self.regions[s].view()
+        start = int(offs[r]) * rb
+        return full[start:start + int(self.wl.ctx[r]) * rb].reshape(-1, rb)
+
+    def free(self):
+        for reg in self.regions:
+            reg.free()
+        self.regions = []
+
+
+class OracleSide:
+    def __init__(self, wl: W.Workload, host: HostRows, retry=3, max_life=16, nthreads=None,
+                 images=True):
+        spec = wl.spec
+        self.wl = wl
+        self.o = ORC.Oracle(spec.batch, spec.topk, spec.n_q, spec.slots, retry=retry,
+                            max_life=max_life, nthreads=nthreads)
+        self.host = host
+        self.images = None
+        if images:
+            self.images = [np.zeros((spec.batch, spec.slots, rb), dtype=np.uint8)
+                           for rb in spec.row_bytes]
+            self.buf_ptrs = [self.images[s][r].ctypes.data for s in range(len(spec.row_bytes))
+                             for r in range(spec.batch)]
+
+    def step(self, X, N):
+        spec = self.wl.spec
+        if self.images is None:
+            return self.o.step(X, N, rows=self.wl.ctx)
+        return self.o.step(X, N, host=self.host.ptrs, buf=self.buf_ptrs, row_bytes=list(spec.row_bytes),
+                           rows=self.wl.ctx)
+
+
+class GpuSide:
+    def __init__(self, wl: W.Workload, host: HostRows, retry=3, max_life=16, gather_mode=0,
+                 match_mode=0, gather_workers=0, device="cuda"):
+        import torch
+        from paper_2609_37538_amd import avsg as A
+        spec = wl.spec
+        self.torch = torch
+        self.cfg = A.make_config(spec.batch, spec.topk, spec.n_q, spec.slots, retry=retry,
+                                 max_life=max_life, row_bytes=spec.row_bytes,
+                                 gather_workers=gather_workers, match_mode=match_mode,
+                                 gather_mode=gather_mode)
+        self.op = A.Operator(self.cfg, host.ptrs, wl.ctx, device=device)
+        self.device = device
+
+    def step(self, X, N):
+        t = self.torch
+        Xd = t.from_numpy(np.ascontiguousarray(X, dtype=np.int32)).to(self.device)
+        Nd = None if N is None else t.from_numpy(np.ascontiguousarray(N, dtype=np.int64)).to(self.device)
+        O, n = self.op.step(Xd, Nd)
+        t.cuda.synchronize()
+        return O.cpu().numpy(), n.cpu().numpy()
+
+    def buffers(self):
+        return [b.cpu().numpy() for b in self.op.buffers]
+
+    def close(self):
+        self.op.close()
+
+
+def compare_step(t, O_ref, n_ref, O_gpu, n_gpu):
+    if not np.array_equal(n_ref, n_gpu):
+        bad = np.argwhere(n_ref != n_gpu)
+        raise AssertionError(f"step {t}: miss counts differ at {bad[:5].tolist()} "
+                             f"(oracle {n_ref[tuple(bad[0])]}, gpu {n_gpu[tuple(bad[0])]})")
+    if not np.array_equal(O_ref, O_gpu):
+        bad = np.argwhere(O_ref != O_gpu)
+        raise AssertionError(f"step {t}: slots differ at {len(bad)} positions, first {bad[:5].tolist()}")
+
+
+def content_check(host: HostRows, wl: W.Workload, bufs, X, O):
+    """Every selected index's slot holds exactly its host row, every stream."""
+    spec = wl.spec
+    for s in range(len(spec.row_bytes)):
+        for r in range(spec.batch):
+            rows = host.row_view(s, r)
+            got = bufs[s][r][O[r].ravel()]
+            want = rows[X[r].ravel()]
+            if not np.array_equal(got, want):
+                bad = np.nonzero(np.any(got != want, axis=1))[0]
+                raise AssertionError(f"stream {s} request {r}: {len(bad)} slots hold wrong bytes")
+
+
+def run_parity(spec: W.Spec, steps: Optional[int] = None, table_every: int = 16,
+               buffers_every: int = 64, miss_list_requests: int = 2, gather_mode: int = 0,
+               retry=3, max_life=16, coherent=False):
+    """Drive `steps` decode steps through both sides; raise on any mismatch.
+    Returns (oracle totals, gpu stats)."""
+    wl = W.Workload(spec)
+    T = spec.steps if steps is None else steps
+    log(f"[parity] {spec.name}: B={spec.batch} K={spec.topk} n_q={spec.n_q} S={spec.slots} T={T} "
+        f"gather_mode={gather_mode}")
+    host = HostRows(wl, coherent=coherent)
+    orc = OracleSide(wl, host, retry=retry, max_life=max_life)
+    gpu = GpuSide(wl, host, retry=retry, max_life=max_life, gather_mode=gather_mode)
+    t0 = time.time()
+    try:
+        for t in range(T):
+            X = wl.topk(t)
+            N = wl.verified_len(t)
+            W.refresh_speculative(wl, t, host.stream_ptrs())
+            O_ref, n_ref = orc.step(X, N)
+            O_gpu, n_gpu = gpu.step(X, N)
+            compare_step(t, O_ref, n_ref, O_gpu, n_gpu)
+            for r in range(min(miss_list_requests, spec.batch)):
+                rr = (r * 7 + t) % spec.batch
+                mx, mo = orc.o.misses(rr, n_ref[rr])
+                gx, go = gpu.op.export_misses(rr)
+                assert np.array_equal(mx, gx) and np.array_equal(mo, go), f"step {t} request {rr} miss list"
+            last = t == T - 1
+            if last or (table_every and t % table_every == 0):
+                for r in range(spec.batch):
+                    c_ref, q_ref = orc.o.export(r)
+                    c_gpu, q_gpu = gpu.op.export_state(r)
+                    assert np.array_equal(c_ref, c_gpu), f"step {t} request {r}: cached ids differ"
+                    assert np.array_equal(q_ref, q_gpu), f"step {t} request {r}: metadata words differ"
+            if gather_mode != 3 and (last or (buffers_every and t % buffers_every == 0)):
+                bufs = gpu.buffers()
+                for s in range(len(spec.row_bytes)):
+                    assert np.array_equal(bufs[s], orc.images[s]), f"step {t} stream {s}: buffers differ"
+                content_check(host, wl, bufs, X, O_gpu)
+            if t % 32 == 0:
+                log(f"[parity] {spec.name} step {t} ok ({time.time() - t0:.1f}s)")
+        ref = orc.o.total_stats()
+        got = gpu.op.stats()
+        for k in ("hits", "misses", "lost_exhausted", "lost_collision", "alloc_decays", "revivals",
+                  "invalidations", "max_step_alloc_decays"):
+            assert ref[k] == got[k], f"counter {k}: oracle {ref[k]} gpu {got[k]}"
+        log(f"[parity] {spec.name} done in {time.time() - t0:.1f}s: hit rate "
+            f"{got['hits'] / max(1, got['lookups']):.4f}")
+        return ref, got
+    finally:
+        gpu.close()
+        host.free()

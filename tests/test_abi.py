@@ -1,0 +1,76 @@
+"""The C-ABI library loads and exports every entry point include/avsg.h declares,
+and host-side validation behaves as documented (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_37538_amd.avsg as A
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "avsg.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"\b(avsg_[a-z0-9_]+)\s*\(", text)
+    return sorted(set(names))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(A.LIB_PATH):
+        from paper_2609_37538_amd import _build
+        _build.build()
+    return A.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in avsg.h but not exported"
+
+
+def test_binding_has_same_names(lib):
+    for n in declared_functions():
+        assert hasattr(A, n), f"binding lacks {n}"
+
+
+def test_struct_sizes_match_header(lib):
+    # avsg_config: 10 int32 + 2 int64 + 2 int32 = 64 bytes; stats: 11 u64 + 2 i32
+    assert ctypes.sizeof(A.AvsgConfig) == 64
+    assert ctypes.sizeof(A.AvsgStats) == 96
+
+
+def test_strerror(lib):
+    assert A.avsg_strerror(0) == "ok"
+    assert "capacity" in A.avsg_strerror(A.AVSG_E_CAPACITY)
+    assert A.avsg_strerror(12345) == "unknown status"
+
+
+def ws(**kw):
+    base = dict(batch=64, topk=2048, n_q=2, slots=8192, row_bytes=(1152, 132))
+    base.update(kw)
+    return A.avsg_workspace_bytes(A.make_config(**base))
+
+
+def test_workspace_size_and_validation(lib):
+    n = ws()
+    B, S, K, nq = 64, 8192, 2048, 2
+    assert n >= 8 * B * S + 8 * B * nq * K
+    assert n % 256 == 0
+    assert ws(slots=12288) == 0                 # not a power of two
+    assert ws(slots=2048) == 0                  # S < N_q K (Eq. 7)
+    assert ws(max_life=0) == 0 and ws(max_life=128) == 0
+    assert ws(a1=7, a2=7) == 0                  # primes must differ
+    assert ws(a1=9) == 0                        # 9 is not prime
+    assert ws(retry=-1) == 0
+    assert ws(row_bytes=(1150,)) == 0           # not a multiple of 4
+    assert ws(batch=0) == 0 and ws(batch=1025) == 0
+    assert ws(topk=8192, n_q=1, slots=8192) == 0   # beyond 4096 indices per token
+    assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=1, slots=2048) > 0
+    assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=2) == 0
+    assert ws(gather_mode=7) == 0
+    assert ws(n_q=1, slots=2, topk=1, batch=1, row_bytes=(4,)) > 0

@@ -1,0 +1,251 @@
+"""GPU parity: the HIP operator (through the C ABI) against the CPU oracle on the
+same seeded inputs and the same pinned host rows, bit-exact: slot map, miss
+counts, transfer lists, table state (c_j and q_j), counters and buffer bytes.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle as ORC
+import workload as W
+from harness import GpuSide, HostRows, OracleSide, compare_step, content_check, log, run_parity
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    from paper_2609_37538_amd import avsg as A
+    A.load()            # fails loudly when the HIP library is missing
+    W.build(force=False)
+    ORC.build(force=False)
+
+
+def test_hand_trace_on_gpu():
+    """The hand-traced S = 8 example through the GPU path."""
+    from paper_2609_37538_amd import avsg as A
+    import torch
+    g = json.load(open(os.path.join(GOLDEN, "hand_trace_s8.json")))
+    c = g["config"]
+    log("[gpu] hand trace S=8")
+    host = A.HostRegion(64 * 16)
+    host.view()[:] = np.arange(64 * 16, dtype=np.uint32).astype(np.uint8)
+    cfg = A.make_config(1, c["topk"], c["n_q"], c["slots"], retry=c["retry"], max_life=c["max_life"],
+                        a1=c["a1"], a2=c["a2"], row_bytes=(16,))
+    op = A.Operator(cfg, [host.ptr], [64])
+    try:
+        for k, s in enumerate(g["steps"]):
+            X = torch.tensor([s["X"]], dtype=torch.int32, device="cuda")
+            N = torch.tensor([s["N"]], dtype=torch.int64, device="cuda")
+            O, n = op.step(X, N)
+            torch.cuda.synchronize()
+            assert O[0].cpu().tolist() == s["O"], f"step {k}"
+            assert n[0].cpu().tolist() == s["n"], f"step {k}"
+            mx, mo = op.export_misses(0)
+            assert mx.tolist() == s["miss_x"] and mo.tolist() == s["miss_o"]
+        cc, q = op.export_state(0)
+        assert cc.tolist() == g["final_c"]
+        life = ((q >> 24).astype(np.uint8)).astype(np.int8).tolist()
+        assert life == g["final_life"]
+        for j, (b, fp, slot) in enumerate(g["final_buckets"]):
+            w = int(q[j]) & 0xFFFFFF
+            assert (w >> 23, (w >> 3) & 0xFFFFF, w & 7) == (b, fp, slot), f"bucket {j}"
+        st = op.stats()
+        for k, v in g["counters"].items():
+            assert st[k] == v, k
+        buf = op.buffers[0].cpu().numpy()[0]
+        rows = host.view().reshape(64, 16)
+        for s in g["steps"][-1:]:
+            for gi, row in enumerate(s["X"]):
+                for i, x in enumerate(row):
+                    assert np.array_equal(buf[s["O"][gi][i]], rows[x])
+    finally:
+        op.close()
+        host.free()
+
+
+def test_parity_tiny():
+    """1 request, context 8192, K = 256, S = 1024: every step, every table."""
+    run_parity(W.get_spec("tiny"), table_every=1, buffers_every=8, miss_list_requests=1)
+
+
+EDGE_CASES = [
+    # name, kwargs of workload.custom_spec
+    ("ragged_k", dict(batch=3, topk=100, slots=256, n_q=1, steps=20, ctx=3000)),
+    ("k_1000_mtp3", dict(batch=2, topk=1000, slots=4096, n_q=3, steps=12, ctx=50000)),
+    ("capacity_exact", dict(batch=2, topk=512, slots=2048, n_q=4, steps=16, ctx=20000)),
+    ("k_one", dict(batch=5, topk=1, slots=2, n_q=1, steps=40, ctx=6)),
+    ("k_3000", dict(batch=2, topk=3000, slots=8192, n_q=2, steps=8, ctx=100000)),
+    ("k_4096_max", dict(batch=1, topk=4096, slots=8192, n_q=2, steps=6, ctx=200000)),
+    ("s_16384_max", dict(batch=2, topk=2048, slots=16384, n_q=2, steps=8, ctx=300000)),
+    ("tiny_context", dict(batch=4, topk=64, slots=128, n_q=2, steps=30, ctx=200, retention=0.5)),
+    ("all_hits", dict(batch=2, topk=256, slots=1024, n_q=2, steps=10, ctx=256, retention=1.0, overlap=1.0)),
+    ("row_132_only", dict(batch=2, topk=128, slots=512, n_q=1, steps=10, ctx=4000, row_bytes=(132,))),
+    ("two_streams_odd", dict(batch=3, topk=200, slots=512, n_q=2, steps=10, ctx=9000, row_bytes=(1152, 132))),
+    ("spec_window", dict(batch=2, topk=256, slots=2048, n_q=3, steps=20, ctx=4096, mode="zipf_window",
+                         window=64, retention=0.8)),
+    ("batch_200", dict(batch=200, topk=128, slots=256, n_q=2, steps=6, ctx=2000)),
+]
+
+
+@pytest.mark.parametrize("name,kw", EDGE_CASES, ids=[e[0] for e in EDGE_CASES])
+def test_parity_edge_cases(name, kw):
+    spec = W.custom_spec(name=name, **kw)
+    run_parity(spec, table_every=1, buffers_every=1, miss_list_requests=3)
+
+
+@pytest.mark.parametrize("retry,max_life", [(0, 1), (1, 2), (7, 4), (3, 127)])
+def test_parity_parameters(retry, max_life):
+    """Probe budgets and lifetimes at and near their limits."""
+    spec = W.custom_spec(name=f"params_{retry}_{max_life}", batch=3, topk=256, slots=1024, n_q=2,
+                         steps=24, ctx=6000, retention=0.7)
+    run_parity(spec, table_every=4, buffers_every=8, retry=retry, max_life=max_life)
+
+
+@pytest.mark.parametrize("mode", [1, 2], ids=["request_level", "sdma_batch"])
+def test_gather_modes_match_balanced(mode):
+    """Request-level (S1) and copy-engine transfers move the same bytes."""
+    spec = W.custom_spec(name=f"mode{mode}", batch=6, topk=512, slots=2048, n_q=2, steps=12,
+                         ctx=30000, row_bytes=(1152, 132))
+    run_parity(spec, table_every=0, buffers_every=4, gather_mode=mode)
+
+
+def test_lds_capacity_error():
+    """A table larger than one workgroup's LDS is refused at create time."""
+    from paper_2609_37538_amd import avsg as A
+    host = A.HostRegion(1 << 20)
+    cfg = A.make_config(1, 2048, 1, 32768, row_bytes=(16,))
+    try:
+        with pytest.raises(A.AvsgError) as e:
+            A.Operator(cfg, [host.ptr], [65536])
+        assert e.value.status == A.AVSG_E_CAPACITY
+    finally:
+        host.free()
+
+
+def test_match_only_leaves_buffers():
+    spec = W.custom_spec(name="match_only", batch=2, topk=128, slots=512, n_q=1, steps=5, ctx=2000)
+    wl = W.Workload(spec)
+    host = HostRows(wl)
+    orc = OracleSide(wl, host, images=False)
+    gpu = GpuSide(wl, host, gather_mode=3)
+    try:
+        for t in range(spec.steps):
+            X, N = wl.topk(t), wl.verified_len(t)
+            O_ref, n_ref = orc.step(X, N)
+            O_gpu, n_gpu = gpu.step(X, N)
+            compare_step(t, O_ref, n_ref, O_gpu, n_gpu)
+        assert all(not b.any() for b in gpu.buffers())
+    finally:
+        gpu.close()
+        host.free()
+
+
+def test_dual_pointer_parity():
+    """Scalar dual-pointer baseline (S = K) against its oracle."""
+    from paper_2609_37538_amd import avsg as A
+    spec = W.custom_spec(name="dualptr", batch=4, topk=512, slots=512, n_q=1, steps=20, ctx=4000,
+                         retention=0.8)
+    wl = W.Workload(spec)
+    host = HostRows(wl)
+    dp = ORC.DualPointerOracle(spec.batch, spec.topk)
+    images = [np.zeros((spec.batch, spec.slots, spec.row_bytes[0]), dtype=np.uint8)]
+    bptr = [images[0][r].ctypes.data for r in range(spec.batch)]
+    gpu = GpuSide(wl, host, match_mode=A.AVSG_MATCH_DUALPTR)
+    try:
+        for t in range(spec.steps):
+            X = wl.topk(t)
+            O_ref, n_ref = dp.step(X, host=host.ptrs, buf=bptr, row_bytes=list(spec.row_bytes))
+            O_gpu, n_gpu = gpu.step(X, None)
+            compare_step(t, O_ref, n_ref, O_gpu, n_gpu)
+            for r in range(spec.batch):
+                gx, go = gpu.op.export_misses(r)
+                assert np.array_equal(gx, dp.miss_x[r, :n_ref[r, 0]])
+                assert np.array_equal(go, dp.miss_o[r, :n_ref[r, 0]])
+        bufs = gpu.buffers()
+        assert np.array_equal(bufs[0], images[0])
+        content_check(host, wl, bufs, X, O_gpu)
+    finally:
+        gpu.close()
+        host.free()
+
+
+def test_reset_request_and_determinism():
+    """A reset request starts cold (token 0 all misses); two runs of the same
+    inputs give identical outputs."""
+    spec = W.custom_spec(name="reset", batch=3, topk=256, slots=1024, n_q=2, steps=6, ctx=5000)
+    outs = []
+    for run in range(2):
+        wl = W.Workload(spec)
+        host = HostRows(wl)
+        gpu = GpuSide(wl, host)
+        try:
+            res = []
+            for t in range(spec.steps):
+                X = wl.topk(t)
+                if t == 4:
+                    from paper_2609_37538_amd import avsg as A
+                    A.avsg_reset_request(gpu.op.h, 1, gpu.op.stream.cuda_stream)
+                O, n = gpu.step(X, wl.verified_len(t))
+                res.append((O, n))
+                if t == 4:
+                    assert n[1, 0] == spec.topk
+                    c, q = gpu.op.export_state(1)
+                    assert c.max() < spec.ctx
+            outs.append(res)
+        finally:
+            gpu.close()
+            host.free()
+    for (a, b), (c, d) in zip(outs[0], outs[1]):
+        assert np.array_equal(a, c) and np.array_equal(b, d)
+
+
+def test_bad_indices_are_counted_not_copied():
+    """An index outside [0, rows) is counted; its row is not read."""
+    from paper_2609_37538_amd import avsg as A
+    import torch
+    host = A.HostRegion(100 * 16)
+    host.view()[:] = 7
+    cfg = A.make_config(1, 4, 1, 16, row_bytes=(16,))
+    op = A.Operator(cfg, [host.ptr], [100])
+    try:
+        X = torch.tensor([[[1, 2, 100, 3]]], dtype=torch.int32, device="cuda")
+        O, n = op.step(X)
+        torch.cuda.synchronize()
+        st = op.stats()
+        assert st["bad_indices"] == 1 and n.item() == 4
+        buf = op.buffers[0].cpu().numpy()[0]
+        o = O.cpu().numpy()[0, 0]
+        assert np.all(buf[o[[0, 1, 3]]] == 7) and np.all(buf[o[2]] == 0)
+    finally:
+        op.close()
+        host.free()
+
+
+# ---- the five benchmark workloads at full size ----------------------------
+@pytest.mark.timeout(900)
+def test_parity_batch16_full():
+    run_parity(W.get_spec("batch16"))
+
+
+@pytest.mark.timeout(900)
+def test_parity_batch64_mtp2_full():
+    run_parity(W.get_spec("batch64_mtp2"))
+
+
+@pytest.mark.timeout(900)
+def test_parity_imbalance_full():
+    ref, got = run_parity(W.get_spec("imbalance"))
+
+
+@pytest.mark.timeout(1200)
+def test_parity_stress_full():
+    ref, got = run_parity(W.get_spec("stress"), buffers_every=128)
+    assert got["invalidations"] > 0

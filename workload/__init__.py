@@ -138,7 +138,8 @@ class Workload:
             self.p = np.array([lo + (hi - lo) * _rng(spec, r, 0, 0, _P_RET).random() for r in range(B)])
         else:
             self.p = np.full(B, spec.retention, dtype=np.float64)
-        if np.any(self.ctx < spec.n_q * spec.topk):
+        extra = spec.topk - int(round(spec.overlap * spec.topk)) if spec.n_q > 1 else 0
+        if np.any(self.ctx < spec.topk + extra):
             raise ValueError("context shorter than the selection")
         self._prev = [None] * B   # token-0 selection (non-window part) of the last step
         self._next_t = 0

@@ -23,13 +23,11 @@ static inline uint64_t splitmix64(uint64_t z) {
 }
 
 static inline uint16_t bf16_from_u16(uint16_t u) {
-    /* u / 65536 * 2 - 1 lies in [-1, 1) and is exact in fp32; round to bf16
-     * with round-to-nearest-even on the dropped 16 mantissa bits. */
+    /* u / 65536 * 2 - 1 lies in [-1, 1) and is exact in fp32; truncating to
+     * bf16 rounds toward zero, which keeps the value inside [-1, 1). */
     float f = (float)u * (1.0f / 32768.0f) - 1.0f;
     uint32_t b;
     memcpy(&b, &f, 4);
-    uint32_t lsb = (b >> 16) & 1u;
-    b += 0x7FFFu + lsb;
     return (uint16_t)(b >> 16);
 }
 
