@@ -1,0 +1,231 @@
+#!/usr/bin/env python3
+"""Benchmark of the AVSG decode-step operator on one MI355X.
+
+A step is one avsg_step over the whole batch: Stage One (hash matching, slot
+reservation, MTP sharing, invalidation) and Stage Two (miss-only copy of host
+rows into the reserved HBM slots).  The default workload is batch 64, top-K
+2048, 8192 slots per request, two query tokens per step (MTP), 1,152-byte KV
+rows plus 132-byte indexer-key rows in pinned host memory, step-to-step
+retention 0.9.  Inputs for every step are generated and copied to HBM before
+the timed region; the host rows stay in pinned host memory (they are what the
+operator transfers).
+
+Prints one JSON line.  `value` is microseconds per decode step (lower is
+better); the line also carries the effective host-to-device bandwidth, the hit
+rate, the roofline of the dominant kernel (the gather, bound by the host link)
+and the CPU oracle timed on a sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PCIE_GEN5_X16_GBPS = 63.0   # 32 GT/s x 16 lanes x 128/130 / 8, one direction
+METRIC = "µs per decode step for match+gather; effective H2D GB/s vs PCIe peak; hit rate"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=240)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--config", default="batch64_mtp2",
+                    choices=["tiny", "batch16", "batch64_mtp2", "imbalance", "stress"])
+    ap.add_argument("--gather", default="balanced", choices=["balanced", "request", "sdma", "none"])
+    ap.add_argument("--match", default="hash", choices=["hash", "dualptr"])
+    ap.add_argument("--workers", type=int, default=0, help="gather workgroups (0 = 4 per CU)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-steps", type=int, default=0,
+                    help="oracle steps timed for the CPU baseline (0 = all warmup+timed steps)")
+    ap.add_argument("--coherent", action="store_true", help="coherent (uncached) host rows")
+    ap.add_argument("--report", default="", help="also write a detailed JSON report here")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this operator runs on one GPU; --gpus {args.gpus} is not supported "
+              "(requests shard across GPUs with no communication, see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import workload as W
+    from paper_2609_37538_amd import avsg as A
+
+    gather_mode = {"balanced": A.AVSG_GATHER_BALANCED, "request": A.AVSG_GATHER_REQUEST,
+                   "sdma": A.AVSG_GATHER_SDMA, "none": A.AVSG_GATHER_NONE}[args.gather]
+    match_mode = {"hash": A.AVSG_MATCH_HASH, "dualptr": A.AVSG_MATCH_DUALPTR}[args.match]
+    spec = W.get_spec(args.config)
+    if match_mode == A.AVSG_MATCH_DUALPTR:
+        import dataclasses
+        spec = dataclasses.replace(spec, slots=spec.topk)
+    T = args.warmup + args.steps
+    if spec.mode == "zipf_window" and T > spec.steps:
+        raise SystemExit(f"{spec.name} defines {spec.steps} steps; warmup+steps = {T}")
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    A.load()
+
+    # ---- inputs: generated up front, copied to HBM before timing ----
+    t_gen = time.time()
+    wl = W.Workload(spec)
+    X_host = wl.all_steps(T)                                   # [T][B][n_q][K] int32
+    N_host = np.stack([wl.verified_len(t) for t in range(T)])  # [T][B] int64
+    X_dev = torch.from_numpy(X_host).to(dev)
+    N_dev = torch.from_numpy(N_host).to(dev)
+    offs = wl.request_row_offsets()
+    regions = []
+    host_ptrs = []
+    for s, rb in enumerate(spec.row_bytes):
+        reg = A.HostRegion(wl.host_rows_total() * rb, coherent=args.coherent)
+        W.fill_host(wl, s, reg.ptr)
+        regions.append(reg)
+        host_ptrs += [reg.ptr + int(offs[r]) * rb for r in range(spec.batch)]
+    gen_s = time.time() - t_gen
+
+    cfg = A.make_config(spec.batch, spec.topk, spec.n_q, spec.slots, row_bytes=spec.row_bytes,
+                        gather_workers=args.workers, match_mode=match_mode, gather_mode=gather_mode)
+    stream = torch.cuda.current_stream(dev)
+    op = A.Operator(cfg, host_ptrs, wl.ctx, device=dev, stream=stream)
+
+    # ---- measured hipMemcpy H2D peak (pinned host -> HBM, 512 MiB) ----
+    peak_bytes = min(512 << 20, regions[0].nbytes)
+    tmp = torch.empty(peak_bytes, dtype=torch.uint8, device=dev)
+    memcpy_peak = A.avsg_h2d_peak(regions[0].ptr, tmp.data_ptr(), peak_bytes, 20, stream.cuda_stream)
+    del tmp
+
+    # ---- warmup, then the timed region ----
+    for t in range(args.warmup):
+        op.step(X_dev[t], N_dev[t] if spec.speculative else None)
+    torch.cuda.synchronize()
+    before = op.stats()
+    A.avsg_set_timing(op.h, True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(args.warmup, T):
+        op.step(X_dev[t], N_dev[t] if spec.speculative else None)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    match_ms, gather_ms = A.avsg_timing(op.h, args.steps)
+    A.avsg_set_timing(op.h, False)
+    after = op.stats()
+
+    K = args.steps
+    us_per_step = wall / K * 1e6
+    lookups = after["lookups"] - before["lookups"]
+    hits = after["hits"] - before["hits"]
+    misses = after["misses"] - before["misses"]
+    row_total = sum(spec.row_bytes)
+    moved = misses * row_total if gather_mode != A.AVSG_GATHER_NONE else 0
+    gather_s = float(np.sum(gather_ms)) * 1e-3
+    match_s = float(np.sum(match_ms)) * 1e-3
+    gather_gbps = moved / gather_s / 1e9 if gather_s > 0 and moved else 0.0
+    eff_gbps = moved / wall / 1e9 if moved else 0.0
+
+    # ---- CPU baseline: the oracle on the same inputs ----
+    cpu = None
+    if not args.no_cpu_baseline and match_mode == A.AVSG_MATCH_HASH:
+        cpu = cpu_baseline(spec, wl, X_host, N_host, host_ptrs, args, gather_mode)
+
+    out = {
+        "metric": METRIC,
+        "value": round(us_per_step, 2),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(us_per_step / 1e3, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {
+            "workload": spec.name, "batch": spec.batch, "topk": spec.topk, "slots": spec.slots,
+            "n_q": spec.n_q, "context": int(wl.ctx.max()), "row_bytes": list(spec.row_bytes),
+            "retention": spec.retention, "match": args.match, "gather": args.gather,
+            "steps_timed": f"{args.warmup}..{T - 1}",
+        },
+        "hit_rate": round(hits / max(1, lookups), 5),
+        "misses_per_step": round(misses / K, 1),
+        "h2d_gbps_effective": round(eff_gbps, 3),
+        "h2d_gbps_gather_kernel": round(gather_gbps, 3),
+        "hipmemcpy_h2d_peak_gbps": round(memcpy_peak, 3),
+        "frac_of_hipmemcpy_peak": round(gather_gbps / memcpy_peak, 4) if memcpy_peak else None,
+        "frac_of_pcie_gen5_x16": round(gather_gbps / PCIE_GEN5_X16_GBPS, 4),
+        "match_us_median": round(float(np.median(match_ms)) * 1e3, 2) if len(match_ms) else None,
+        "gather_us_median": round(float(np.median(gather_ms)) * 1e3, 2) if len(gather_ms) else None,
+        "match_frac_of_step": round(match_s / wall, 4),
+        "roofline": {
+            "bound": "pcie",
+            "kernel": "gather_balanced_kernel" if args.gather == "balanced" else args.gather,
+            "achieved": round(gather_gbps, 3),
+            "peak": PCIE_GEN5_X16_GBPS,
+            "unit": "GB/s",
+            "frac": round(gather_gbps / PCIE_GEN5_X16_GBPS, 4),
+            "traffic": None,
+            "measured_hipmemcpy_peak": round(memcpy_peak, 3),
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    if args.report:
+        rep = dict(out)
+        rep["gen_seconds"] = round(gen_s, 1)
+        rep["match_ms"] = [round(float(x), 4) for x in match_ms]
+        rep["gather_ms"] = [round(float(x), 4) for x in gather_ms]
+        rep["stats"] = after
+        with open(args.report, "w") as f:
+            json.dump(rep, f, indent=1)
+    op.close()
+    for reg in regions:
+        reg.free()
+
+
+def cpu_baseline(spec, wl, X_host, N_host, host_ptrs, args, gather_mode):
+    """Time the oracle (match + Stage Two copy into host images of the buffers)
+    on the warmup+timed steps of the same workload, from the same cold start;
+    report µs per timed step."""
+    import oracle as ORC
+    threads = ORC.default_threads()
+    o = ORC.Oracle(spec.batch, spec.topk, spec.n_q, spec.slots, nthreads=threads)
+    images = [np.zeros((spec.batch, spec.slots, rb), dtype=np.uint8) for rb in spec.row_bytes]
+    bptr = [images[s][r].ctypes.data for s in range(len(spec.row_bytes)) for r in range(spec.batch)]
+    T = X_host.shape[0]
+    n_run = T if args.cpu_sample_steps <= 0 else min(T, args.cpu_sample_steps)
+    first_timed = min(args.warmup, n_run - 1)
+    timed = 0.0
+    n_timed = 0
+    gather = gather_mode != 3
+    for t in range(n_run):
+        N = N_host[t] if spec.speculative else None
+        t0 = time.perf_counter()
+        if gather:
+            o.step(X_host[t], N, host=host_ptrs, buf=bptr, row_bytes=list(spec.row_bytes))
+        else:
+            o.step(X_host[t], N)
+        dt = time.perf_counter() - t0
+        if t >= first_timed:
+            timed += dt
+            n_timed += 1
+    return {
+        "value": round(timed / max(1, n_timed) * 1e6, 1),
+        "unit": "us/step",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{spec.name} steps {first_timed}..{n_run - 1} ({n_timed} steps) after a cold start "
+                  f"at step 0, match + Stage Two copy into host images, {threads} OpenMP threads",
+    }
+
+
+if __name__ == "__main__":
+    main()
