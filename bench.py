@@ -41,12 +41,14 @@ def parse():
                     choices=["tiny", "batch16", "batch64_mtp2", "imbalance", "stress"])
     ap.add_argument("--gather", default="balanced", choices=["balanced", "request", "sdma", "none"])
     ap.add_argument("--match", default="hash", choices=["hash", "dualptr"])
-    ap.add_argument("--workers", type=int, default=0, help="gather workgroups (0 = 4 per CU)")
+    ap.add_argument("--workers", type=int, default=0, help="gather workgroups (0 = one per CU)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-steps", type=int, default=0,
                     help="oracle steps timed for the CPU baseline (0 = all warmup+timed steps)")
     ap.add_argument("--coherent", action="store_true", help="coherent (uncached) host rows")
     ap.add_argument("--report", default="", help="also write a detailed JSON report here")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="run one device-to-device copy of this many MiB first (counter calibration)")
     return ap.parse_args()
 
 
@@ -103,6 +105,13 @@ def main():
     memcpy_peak = A.avsg_h2d_peak(regions[0].ptr, tmp.data_ptr(), peak_bytes, 20, stream.cuda_stream)
     del tmp
 
+    if args.copy_probe_mib > 0:
+        a = torch.ones(args.copy_probe_mib << 20, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
     # ---- warmup, then the timed region ----
     for t in range(args.warmup):
         op.step(X_dev[t], N_dev[t] if spec.speculative else None)
@@ -136,6 +145,7 @@ def main():
     if not args.no_cpu_baseline and match_mode == A.AVSG_MATCH_HASH:
         cpu = cpu_baseline(spec, wl, X_host, N_host, host_ptrs, args, gather_mode)
 
+    traffic = measured_traffic(args)
     out = {
         "metric": METRIC,
         "value": round(us_per_step, 2),
@@ -172,7 +182,9 @@ def main():
             "peak": PCIE_GEN5_X16_GBPS,
             "unit": "GB/s",
             "frac": round(gather_gbps / PCIE_GEN5_X16_GBPS, 4),
-            "traffic": None,
+            "traffic": traffic["traffic_bytes_per_launch"] if traffic else None,
+            "traffic_source": TRAFFIC_SUMMARY if traffic else None,
+            "algorithmic_bytes_per_launch": round(moved / K) if moved else 0,
             "measured_hipmemcpy_peak": round(memcpy_peak, 3),
         },
         "cpu_baseline": cpu,
@@ -189,6 +201,35 @@ def main():
     op.close()
     for reg in regions:
         reg.free()
+
+
+GATHER_SOURCES = ("paper_2609_37538_amd/csrc/gather.hip", "paper_2609_37538_amd/csrc/avsg_internal.h")
+TRAFFIC_SUMMARY = "profiles/gather_traffic_batch64_mtp2.md"
+
+
+def measured_traffic(args):
+    """HBM + host-link bytes per gather launch from the committed rocprofv3
+    counter summary (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0, copy-calibrated), or
+    None when this run is not the profiled configuration or the gather source
+    has changed since the counters were taken."""
+    import hashlib
+    import re
+    if (args.config, args.warmup, args.steps, args.workers, args.gather, args.match) != \
+            ("batch64_mtp2", 16, 240, 0, "balanced", "hash"):
+        return None
+    path = os.path.join(ROOT, TRAFFIC_SUMMARY)
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"```json\n(.*?)\n```", open(path).read(), re.S)
+    if not m:
+        return None
+    block = json.loads(m.group(1))
+    h = hashlib.sha256()
+    for p in GATHER_SOURCES:
+        h.update(open(os.path.join(ROOT, p), "rb").read())
+    if h.hexdigest()[:16] != block.get("source_sha256_16"):
+        return None
+    return block
 
 
 def cpu_baseline(spec, wl, X_host, N_host, host_ptrs, args, gather_mode):

@@ -73,7 +73,7 @@ typedef struct avsg_config {
     int32_t max_life;   /* L in [1, 127]; lifetime of a hit or new slot (default 16) */
     uint32_t a1, a2;    /* distinct primes setting initial bucket and stride (Eq. 9) */
     int32_t n_streams;  /* 1 (KV rows) or 2 (KV rows + indexer-key rows) */
-    int32_t gather_workers; /* C, workgroups of the balanced gather; 0 = 4 per CU */
+    int32_t gather_workers; /* C, workgroups of the balanced gather; 0 = one per CU */
     int64_t row_bytes[AVSG_MAX_STREAMS]; /* bytes per row of each stream, multiple of 4 */
     int32_t match_mode;  /* AVSG_MATCH_* */
     int32_t gather_mode; /* AVSG_GATHER_* */
@@ -186,7 +186,7 @@ avsg_status avsg_host_free(void *p);
 avsg_status avsg_h2d_peak(const void *host, void *device, size_t bytes, int32_t iters,
                           void *stream, double *gbps);
 
-/* Number of compute units of the current device (the default C is 4x this). */
+/* Number of compute units of the current device (the default C). */
 int32_t avsg_device_cus(void);
 
 #ifdef __cplusplus

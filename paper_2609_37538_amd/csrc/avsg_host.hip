@@ -240,7 +240,7 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
     h->bufs[i] = reinterpret_cast<uint64_t>(d_buffers[i]);
   }
   const int cus = device_cus();
-  h->workers = c.gather_workers > 0 ? c.gather_workers : std::max(1, 4 * cus);
+  h->workers = c.gather_workers > 0 ? c.gather_workers : std::max(1, cus);
 
   auto cleanup = [&](avsg_status rc) {
     delete h;
