@@ -39,7 +39,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--config", default="batch64_mtp2",
                     choices=["tiny", "batch16", "batch64_mtp2", "imbalance", "stress"])
-    ap.add_argument("--gather", default="balanced", choices=["balanced", "request", "sdma", "none"])
+    ap.add_argument("--gather", default="balanced",
+                    choices=["balanced", "request", "position", "sdma", "none"])
     ap.add_argument("--match", default="hash", choices=["hash", "dualptr"])
     ap.add_argument("--workers", type=int, default=0, help="gather workgroups (0 = one per CU)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -47,6 +48,8 @@ def parse():
                     help="oracle steps timed for the CPU baseline (0 = all warmup+timed steps)")
     ap.add_argument("--coherent", action="store_true", help="coherent (uncached) host rows")
     ap.add_argument("--report", default="", help="also write a detailed JSON report here")
+    ap.add_argument("--appendix-d-sweep", default="",
+                    help="run the S1/S2/S3 transfer sweep (batch x reuse) and write it here")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one device-to-device copy of this many MiB first (counter calibration)")
     return ap.parse_args()
@@ -62,9 +65,13 @@ def main():
     import torch
     import workload as W
     from paper_2609_37538_amd import avsg as A
+    if args.appendix_d_sweep:
+        appendix_d_sweep(args.appendix_d_sweep)
+        return
 
     gather_mode = {"balanced": A.AVSG_GATHER_BALANCED, "request": A.AVSG_GATHER_REQUEST,
-                   "sdma": A.AVSG_GATHER_SDMA, "none": A.AVSG_GATHER_NONE}[args.gather]
+                   "sdma": A.AVSG_GATHER_SDMA, "none": A.AVSG_GATHER_NONE,
+                   "position": A.AVSG_GATHER_POSITION}[args.gather]
     match_mode = {"hash": A.AVSG_MATCH_HASH, "dualptr": A.AVSG_MATCH_DUALPTR}[args.match]
     spec = W.get_spec(args.config)
     if match_mode == A.AVSG_MATCH_DUALPTR:
@@ -201,6 +208,62 @@ def main():
     op.close()
     for reg in regions:
         reg.free()
+
+
+def appendix_d_sweep(out_path):
+    """Transfer efficiency of the three core-binding strategies (request-level
+    S1, equal top-K positions S2, balanced miss list S3) over batch sizes
+    {1,2,4,8,16,32} and reuse {0, .25, .5, .75, 1}, K = 2048, one query token,
+    1,152-byte rows.  Reuse is controlled by a fixed hot set selected every step
+    plus never-seen ids; each point runs 8 warm-up steps then times 16 steps.
+    Effective bandwidth = moved bytes / summed Stage Two kernel time."""
+    import torch
+    import workload as W
+    from paper_2609_37538_amd import avsg as A
+    Bs, reuses = [1, 2, 4, 8, 16, 32], [0.0, 0.25, 0.5, 0.75, 1.0]
+    modes = [("S1", A.AVSG_GATHER_REQUEST), ("S2", A.AVSG_GATHER_POSITION),
+             ("S3", A.AVSG_GATHER_BALANCED)]
+    K, S, ctx, warm, timed = 2048, 8192, 65536, 8, 16
+    dev = torch.device("cuda:0")
+    base = W.custom_spec(name="appendix_d", cfg_id=10, batch=max(Bs), topk=K, slots=S, n_q=1,
+                         steps=warm + timed, ctx=ctx, mode="controlled")
+    host = A.HostRegion(max(Bs) * ctx * W.KV_ROW_BYTES)
+    W.fill_host(W.Workload(base), 0, host.ptr)
+    results = []
+    for B in Bs:
+        for reuse in reuses:
+            import dataclasses
+            spec = dataclasses.replace(base, batch=B, retention=reuse)
+            wl = W.Workload(spec)
+            X = torch.from_numpy(wl.all_steps(warm + timed)).to(dev)
+            ptrs = [host.ptr + r * ctx * W.KV_ROW_BYTES for r in range(B)]
+            for name, mode in modes:
+                cfg = A.make_config(B, K, 1, S, row_bytes=(W.KV_ROW_BYTES,), gather_mode=mode)
+                op = A.Operator(cfg, ptrs, wl.ctx, device=dev)
+                for t in range(warm):
+                    op.step(X[t])
+                torch.cuda.synchronize()
+                before = op.stats()
+                A.avsg_set_timing(op.h, True)
+                for t in range(warm, warm + timed):
+                    op.step(X[t])
+                _, gather_ms = A.avsg_timing(op.h, timed)
+                after = op.stats()
+                op.close()
+                misses = after["misses"] - before["misses"]
+                moved = misses * W.KV_ROW_BYTES
+                gsec = float(np.sum(gather_ms)) * 1e-3
+                row = {"batch": B, "reuse_target": reuse, "strategy": name,
+                       "hit_rate": round((after["hits"] - before["hits"]) /
+                                         max(1, after["lookups"] - before["lookups"]), 4),
+                       "misses_per_step": round(misses / timed, 1),
+                       "gather_us": round(gsec / timed * 1e6, 2),
+                       "gbps": round(moved / gsec / 1e9, 3) if gsec > 0 else 0.0}
+                results.append(row)
+                print(json.dumps(row), flush=True)
+    host.free()
+    with open(out_path, "w") as f:
+        json.dump(results, f, indent=1)
 
 
 GATHER_SOURCES = ("paper_2609_37538_amd/csrc/gather.hip", "paper_2609_37538_amd/csrc/avsg_internal.h")

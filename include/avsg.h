@@ -61,6 +61,7 @@ typedef int32_t avsg_status;
 #define AVSG_GATHER_REQUEST 1  /* S1: one worker per request (Eq. 13) */
 #define AVSG_GATHER_SDMA 2     /* comparator: the miss list is read back and every missed row is one hipMemcpyAsync on the copy engines */
 #define AVSG_GATHER_NONE 3     /* Stage One only (matching measured alone) */
+#define AVSG_GATHER_POSITION 4 /* S2: the N_g*K selected positions split into C near-equal ranges, hits issue nothing (Eq. 14) */
 
 #define AVSG_MAX_STREAMS 2
 
@@ -99,8 +100,8 @@ typedef struct avsg_stats_t {
 typedef struct avsg_handle avsg_handle;
 
 /* Size in bytes of the device workspace that avsg_create needs for cfg
- * (per-request tables of 8*S bytes, transfer lists of 8*N_q*K bytes,
- * counters and pointer tables).  Returns 0 for an invalid cfg. */
+ * (per-request tables of 8*S bytes, transfer lists of 8*N_q*K bytes, a hit
+ * mask of N_q*K bytes, counters and pointer tables).  Returns 0 for an invalid cfg. */
 size_t avsg_workspace_bytes(const avsg_config *cfg);
 
 /* Create a handle and reset every table to empty (c_j = -1, lifetime -1, every

@@ -34,6 +34,7 @@ AVSG_GATHER_BALANCED = 0
 AVSG_GATHER_REQUEST = 1
 AVSG_GATHER_SDMA = 2
 AVSG_GATHER_NONE = 3
+AVSG_GATHER_POSITION = 4
 AVSG_MAX_STREAMS = 2
 
 A1_DEFAULT = 2654435761

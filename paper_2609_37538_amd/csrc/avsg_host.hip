@@ -27,6 +27,7 @@ struct avsg_handle {
   uint32_t* table_q = nullptr;
   int2* dp_state = nullptr;
   int2* miss_list = nullptr;
+  uint8_t* hit_mask = nullptr;
   unsigned long long* stats = nullptr;
   uint64_t* host_ptrs = nullptr;
   uint64_t* buf_ptrs = nullptr;
@@ -66,7 +67,7 @@ bool is_prime_u32(uint32_t v) {
 }
 
 struct Layout {
-  size_t table_c, table_q, miss_list, stats, host_ptrs, buf_ptrs, rows, total;
+  size_t table_c, table_q, miss_list, hit_mask, stats, host_ptrs, buf_ptrs, rows, total;
 };
 
 Layout layout_of(const avsg_config& c) {
@@ -76,6 +77,7 @@ Layout layout_of(const avsg_config& c) {
   L.table_c = off; off += up(B * S * 4);
   L.table_q = off; off += up(B * S * 4);
   L.miss_list = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk * 8);
+  L.hit_mask = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk);
   L.stats = off; off += up(B * kNumStats * 8);
   L.host_ptrs = off; off += up(static_cast<size_t>(c.n_streams) * B * 8);
   L.buf_ptrs = off; off += up(static_cast<size_t>(c.n_streams) * B * 8);
@@ -114,12 +116,14 @@ avsg_status check_config(const avsg_config* c, std::string* why) {
   if (c->gather_workers < 0) return fail(AVSG_E_INVAL, "gather_workers must be >= 0");
   if (c->match_mode != AVSG_MATCH_HASH && c->match_mode != AVSG_MATCH_DUALPTR)
     return fail(AVSG_E_INVAL, "unknown match_mode");
-  if (c->gather_mode < AVSG_GATHER_BALANCED || c->gather_mode > AVSG_GATHER_NONE)
+  if (c->gather_mode < AVSG_GATHER_BALANCED || c->gather_mode > AVSG_GATHER_POSITION)
     return fail(AVSG_E_INVAL, "unknown gather_mode");
   if (c->match_mode == AVSG_MATCH_DUALPTR) {
     if (c->n_q != 1) return fail(AVSG_E_UNSUPPORTED, "dual-pointer matching handles one token per step");
     if (c->slots != c->topk) return fail(AVSG_E_UNSUPPORTED, "dual-pointer matching needs slots == topk");
     if (c->topk > 4096) return fail(AVSG_E_CAPACITY, "dual-pointer matching supports topk <= 4096");
+    if (c->gather_mode == AVSG_GATHER_POSITION)
+      return fail(AVSG_E_UNSUPPORTED, "position-level transfer needs hash matching");
   } else {
     if (match_lds_bytes(c->slots, c->topk) == 0)
       return fail(AVSG_E_CAPACITY, "topk beyond 4096 indices per token");
@@ -220,6 +224,7 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
   h->table_q = reinterpret_cast<uint32_t*>(ws + L.table_q);
   h->dp_state = reinterpret_cast<int2*>(ws + L.table_c);  // S == K: the two table arrays hold [B][K] pairs
   h->miss_list = reinterpret_cast<int2*>(ws + L.miss_list);
+  h->hit_mask = ws + L.hit_mask;
   h->stats = reinterpret_cast<unsigned long long*>(ws + L.stats);
   h->host_ptrs = reinterpret_cast<uint64_t*>(ws + L.host_ptrs);
   h->buf_ptrs = reinterpret_cast<uint64_t*>(ws + L.buf_ptrs);
@@ -351,6 +356,7 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
     p.table_c = h->table_c; p.table_q = h->table_q;
     p.slots_out = d_slots; p.miss_counts = d_miss_counts; p.miss_list = h->miss_list;
     p.stats = h->stats;
+    p.hit_mask = c.gather_mode == AVSG_GATHER_POSITION ? h->hit_mask : nullptr;
     HIP_TRY(h, launch_match_hash(p, h->lds, s));
   } else {
     DualPtrParams p{};
@@ -366,9 +372,11 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
   g.n_streams = c.n_streams; g.host_ptrs = h->host_ptrs; g.buf_ptrs = h->buf_ptrs;
   g.row_bytes0 = c.row_bytes[0];
   g.row_bytes1 = c.n_streams > 1 ? c.row_bytes[1] : 0;
+  g.topk = d_topk; g.slots = d_slots; g.hit_mask = h->hit_mask;
   switch (c.gather_mode) {
     case AVSG_GATHER_BALANCED: HIP_TRY(h, launch_gather_balanced(g, h->workers, s)); break;
     case AVSG_GATHER_REQUEST: HIP_TRY(h, launch_gather_request(g, s)); break;
+    case AVSG_GATHER_POSITION: HIP_TRY(h, launch_gather_position(g, h->workers, s)); break;
     case AVSG_GATHER_SDMA:
       if ((rc = sdma_gather(h, d_miss_counts, s)) != AVSG_OK) return rc;
       break;

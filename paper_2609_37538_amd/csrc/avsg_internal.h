@@ -43,6 +43,7 @@ struct MatchParams {
   int32_t* miss_counts;         // [B][n_q]
   int2* miss_list;              // [B][n_q*K]  (index, slot)
   unsigned long long* stats;    // [B][kNumStats]
+  uint8_t* hit_mask;            // [B][n_q][K] 1 = hit, or nullptr (not written)
 };
 
 struct GatherParams {
@@ -54,6 +55,10 @@ struct GatherParams {
   const uint64_t* host_ptrs;    // [n_streams][B] device-visible addresses of host row 0
   const uint64_t* buf_ptrs;     // [n_streams][B] device buffer base addresses
   int64_t row_bytes0, row_bytes1;
+  // position-level assignment only
+  const int32_t* topk;          // [B][n_q][K]
+  const int32_t* slots;         // [B][n_q][K]
+  const uint8_t* hit_mask;      // [B][n_q][K]
 };
 
 struct DualPtrParams {
@@ -78,6 +83,7 @@ hipError_t launch_reset_tables(int32_t* c, uint32_t* q, size_t n, hipStream_t s)
 hipError_t launch_zero_u64(unsigned long long* p, size_t n, hipStream_t s);
 hipError_t launch_gather_balanced(const GatherParams& p, int workers, hipStream_t s);
 hipError_t launch_gather_request(const GatherParams& p, hipStream_t s);
+hipError_t launch_gather_position(const GatherParams& p, int workers, hipStream_t s);
 hipError_t launch_match_dualptr(const DualPtrParams& p, size_t lds, hipStream_t s);
 hipError_t prepare_match_dualptr(size_t lds);
 hipError_t launch_reset_dualptr(int2* state, int B, int K, hipStream_t s);

@@ -8,7 +8,10 @@
 // tile of misses is staged in LDS as (source, destination) address pairs, and
 // the lanes copy the rows with 16-byte loads from pinned, device-mapped host
 // memory (4-byte loads for rows that are not a multiple of 16 bytes, such as
-// the 132-byte indexer-key rows), several loads in flight per lane.
+// the 132-byte indexer-key rows), several loads in flight per lane.  The
+// position kernel (S2, Eq. 14) splits the flattened N_g*K selected positions
+// into C near-equal contiguous ranges; hit positions issue no copy but still
+// occupy their worker's share.
 #include "avsg_internal.h"
 
 namespace avsg {
@@ -97,6 +100,22 @@ __device__ __forceinline__ void copy_rows(const uint64_t* src, const uint64_t* d
   }
 }
 
+__device__ void copy_tile_rows(const GatherParams& p, int tn, uint64_t* src0, uint64_t* dst0,
+                               uint64_t* src1, uint64_t* dst1) {
+  __syncthreads();
+  if ((p.row_bytes0 & 15) == 0)
+    copy_rows<uint4>(src0, dst0, tn, static_cast<int>(p.row_bytes0 / 16));
+  else
+    copy_rows<uint32_t>(src0, dst0, tn, static_cast<int>(p.row_bytes0 / 4));
+  if (p.n_streams > 1) {
+    if ((p.row_bytes1 & 15) == 0)
+      copy_rows<uint4>(src1, dst1, tn, static_cast<int>(p.row_bytes1 / 16));
+    else
+      copy_rows<uint32_t>(src1, dst1, tn, static_cast<int>(p.row_bytes1 / 4));
+  }
+  __syncthreads();
+}
+
 // Copy misses [a, b) of the batch-wide list.
 __device__ void copy_range(const GatherParams& p, const long long* pre, long long a, long long b,
                            uint64_t* src0, uint64_t* dst0, uint64_t* src1, uint64_t* dst1) {
@@ -142,6 +161,33 @@ __global__ __launch_bounds__(NT) void gather_balanced_kernel(GatherParams p) {
   copy_range(p, pre, a, b, src0, dst0, src1, dst1);
 }
 
+__global__ __launch_bounds__(NT) void gather_position_kernel(GatherParams p) {
+  __shared__ uint64_t src0[TILE], dst0[TILE], src1[TILE], dst1[TILE];
+  const long long per_req = static_cast<long long>(p.n_q) * p.K;
+  const long long P = per_req * p.B;
+  const long long C = gridDim.x, w = blockIdx.x;
+  const long long a = (w * P) / C;          // Eq. 14: near-equal ranges of positions
+  const long long b = ((w + 1) * P) / C;
+  for (long long t0 = a; t0 < b; t0 += TILE) {
+    const int tn = static_cast<int>((b - t0) < TILE ? (b - t0) : TILE);
+    for (int i = threadIdx.x; i < tn; i += NT) {
+      const long long pos = t0 + i;
+      const int r = static_cast<int>(pos / per_req);
+      const int32_t x = p.topk[pos];
+      const int32_t o = p.slots[pos];
+      const bool miss = p.hit_mask[pos] == 0;
+      const bool ok = miss && x >= 0 && static_cast<int64_t>(x) < p.rows[r] && o >= 0 && o < p.S;
+      src0[i] = ok ? p.host_ptrs[r] + static_cast<uint64_t>(x) * p.row_bytes0 : 0;
+      dst0[i] = p.buf_ptrs[r] + static_cast<uint64_t>(o) * p.row_bytes0;
+      if (p.n_streams > 1) {
+        src1[i] = ok ? p.host_ptrs[p.B + r] + static_cast<uint64_t>(x) * p.row_bytes1 : 0;
+        dst1[i] = p.buf_ptrs[p.B + r] + static_cast<uint64_t>(o) * p.row_bytes1;
+      }
+    }
+    copy_tile_rows(p, tn, src0, dst0, src1, dst1);
+  }
+}
+
 __global__ __launch_bounds__(NT) void gather_request_kernel(GatherParams p) {
   __shared__ long long pre[kMaxBatch + 1];
   __shared__ long long wtot[NT / 64];
@@ -156,6 +202,12 @@ __global__ __launch_bounds__(NT) void gather_request_kernel(GatherParams p) {
 hipError_t launch_gather_balanced(const GatherParams& p, int workers, hipStream_t s) {
   if (p.B > kMaxBatch || workers < 1) return hipErrorInvalidValue;
   hipLaunchKernelGGL(gather_balanced_kernel, dim3(workers), dim3(NT), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_position(const GatherParams& p, int workers, hipStream_t s) {
+  if (workers < 1 || !p.hit_mask || !p.topk || !p.slots) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gather_position_kernel, dim3(workers), dim3(NT), 0, s, p);
   return hipGetLastError();
 }
 

@@ -142,6 +142,7 @@ __global__ __launch_bounds__(NT) void match_hash_kernel(MatchParams p) {
         }
       }
       hit[u] = h_ok;
+      if (p.hit_mask && act[u]) p.hit_mask[row * K + i] = h_ok ? 1 : 0;
       const uint64_t mm = __ballot(act[u] && !h_ok);
       if (lane == 0) wc[u * NW + wave] = __popcll(mm);
       rank[u] = bits_below(mm);

@@ -73,4 +73,6 @@ def test_workspace_size_and_validation(lib):
     assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=1, slots=2048) > 0
     assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=2) == 0
     assert ws(gather_mode=7) == 0
+    assert ws(gather_mode=A.AVSG_GATHER_POSITION) > ws() - 1
+    assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=1, slots=2048, gather_mode=A.AVSG_GATHER_POSITION) == 0
     assert ws(n_q=1, slots=2, topk=1, batch=1, row_bytes=(4,)) > 0

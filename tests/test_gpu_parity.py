@@ -109,9 +109,10 @@ def test_parity_parameters(retry, max_life):
     run_parity(spec, table_every=4, buffers_every=8, retry=retry, max_life=max_life)
 
 
-@pytest.mark.parametrize("mode", [1, 2], ids=["request_level", "sdma_batch"])
+@pytest.mark.parametrize("mode", [1, 2, 4], ids=["request_level", "copy_engine", "position_level"])
 def test_gather_modes_match_balanced(mode):
-    """Request-level (S1) and copy-engine transfers move the same bytes."""
+    """Request-level (S1), position-level (S2) and copy-engine transfers move
+    the same bytes as the balanced miss-list transfer (S3)."""
     spec = W.custom_spec(name=f"mode{mode}", batch=6, topk=512, slots=2048, n_q=2, steps=12,
                          ctx=30000, row_bytes=(1152, 132))
     run_parity(spec, table_every=0, buffers_every=4, gather_mode=mode)

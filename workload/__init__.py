@@ -49,7 +49,7 @@ class Spec:
     retention: float = 0.9                # step-to-step keep probability
     retention_range: Optional[tuple] = None  # (lo, hi): per-request U[lo, hi]
     overlap: float = 0.95                 # tokens g >= 1 share this fraction with token 0
-    mode: str = "uniform"                 # "uniform" | "zipf_window"
+    mode: str = "uniform"                 # "uniform" | "zipf_window" | "controlled"
     zipf_s: float = 1.1
     window: int = 512
     row_bytes: tuple = (KV_ROW_BYTES,)
@@ -143,6 +143,8 @@ class Workload:
             raise ValueError("context shorter than the selection")
         self._prev = [None] * B   # token-0 selection (non-window part) of the last step
         self._next_t = 0
+        self._hot = None          # controlled-reuse mode: hot set and fresh stream per request
+        self._fresh = None
         if spec.mode == "zipf_window":
             # base verified length: the last step's speculative tokens end at ctx
             self._n0 = int(spec.ctx) - spec.n_q + 1 - (spec.steps - 1)
@@ -191,8 +193,34 @@ class Workload:
             out = np.concatenate([out, pos[: need - out.size]])
         return out
 
+    def _controlled_step(self, r: int, t: int) -> np.ndarray:
+        """Controlled reuse: a fixed hot set of round(p*K) ids is selected at
+        every step and the remaining ids are fresh (never selected before by
+        this request), so once the hot set is resident the adjacent-step
+        reuse is p."""
+        s = self.spec
+        K, ctx = s.topk, int(self.ctx[r])
+        if self._hot is None:
+            self._hot = [None] * s.batch
+            self._fresh = [None] * s.batch
+        if self._hot[r] is None:
+            g = _rng(s, r, 0, 0, _P_INIT)
+            n_hot = int(round(self.p[r] * K))
+            perm = g.permutation(ctx).astype(np.int64)
+            self._hot[r] = perm[:n_hot]
+            self._fresh[r] = perm[n_hot:]
+        hot = self._hot[r]
+        m = K - hot.size
+        if (t + 1) * m > self._fresh[r].size:
+            raise ValueError("context too short for this many fresh selections")
+        fresh = self._fresh[r][t * m:(t + 1) * m]
+        sel = _rng(s, r, t, 0, _P_PERM).permutation(np.concatenate([hot, fresh]))
+        return np.tile(sel, (s.n_q, 1))
+
     def _request_step(self, r: int, t: int) -> np.ndarray:
         s = self.spec
+        if s.mode == "controlled":
+            return self._controlled_step(r, t)
         K, ctx = s.topk, int(self.ctx[r])
         out = np.empty((s.n_q, K), dtype=np.int64)
         if s.mode == "uniform":
