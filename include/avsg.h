@@ -45,7 +45,7 @@ typedef int32_t avsg_status;
 #define AVSG_OK 0
 #define AVSG_E_INVAL (-1)       /* null pointer, non-positive size, bad mode */
 #define AVSG_E_NOTPOW2 (-2)     /* S is not a power of two in [2, 2^23] */
-#define AVSG_E_CAPACITY (-3)    /* S < N_q * K (Eq. 7), or S/K beyond what one workgroup's LDS holds */
+#define AVSG_E_CAPACITY (-3)    /* S < N_q * K (Eq. 7), or 9*S + 12*K bytes beyond one workgroup's LDS */
 #define AVSG_E_RANGE (-4)       /* R < 0, L outside [1, 127], a1/a2 not distinct primes, row size */
 #define AVSG_E_BADINDEX (-5)    /* a selected index outside [0, rows of its request) */
 #define AVSG_E_HIP (-6)         /* a HIP runtime call failed */
@@ -68,7 +68,7 @@ typedef int32_t avsg_status;
 typedef struct avsg_config {
     int32_t batch;      /* B >= 1 */
     int32_t topk;       /* K >= 1, selected indices per query token */
-    int32_t n_q;        /* N_q = N_mtp + 1 >= 1 query tokens per request per step */
+    int32_t n_q;        /* N_q = N_mtp + 1 in [1, 127] query tokens per request per step */
     int32_t slots;      /* S = 2^m, 2 <= S <= 2^23, S >= N_q*K (Eq. 7) */
     int32_t retry;      /* R >= 0; probes examine R+1 buckets (default 3) */
     int32_t max_life;   /* L in [1, 127]; lifetime of a hit or new slot (default 16) */
@@ -98,6 +98,11 @@ typedef struct avsg_stats_t {
 } avsg_stats_t;
 
 typedef struct avsg_handle avsg_handle;
+
+/* Validate a configuration without touching the device: AVSG_OK or the status
+ * avsg_create would return for it (AVSG_E_INVAL, AVSG_E_NOTPOW2,
+ * AVSG_E_CAPACITY, AVSG_E_RANGE, AVSG_E_UNSUPPORTED). */
+avsg_status avsg_check_config(const avsg_config *cfg);
 
 /* Size in bytes of the device workspace that avsg_create needs for cfg
  * (per-request tables of 8*S bytes, transfer lists of 8*N_q*K bytes, a hit

@@ -85,6 +85,8 @@ def load():
                           "(the operator has no other implementation)")
     lib = ctypes.CDLL(LIB_PATH)
     i32, i64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    lib.avsg_check_config.restype = i32
+    lib.avsg_check_config.argtypes = [ctypes.POINTER(AvsgConfig)]
     lib.avsg_workspace_bytes.restype = sz
     lib.avsg_workspace_bytes.argtypes = [ctypes.POINTER(AvsgConfig)]
     lib.avsg_create.restype = i32
@@ -158,6 +160,10 @@ def make_config(batch, topk, n_q, slots, retry=3, max_life=16, a1=A1_DEFAULT, a2
 # ---------------------------------------------------------------------------
 # entry points, same names as the C ABI
 # ---------------------------------------------------------------------------
+def avsg_check_config(cfg: AvsgConfig) -> int:
+    return int(load().avsg_check_config(ctypes.byref(cfg)))
+
+
 def avsg_workspace_bytes(cfg: AvsgConfig) -> int:
     return int(load().avsg_workspace_bytes(ctypes.byref(cfg)))
 
@@ -295,9 +301,8 @@ class Operator:
         self.device = dev
         self.stream = stream or torch.cuda.current_stream(dev)
         B, K, n_q, S = cfg.batch, cfg.topk, cfg.n_q, cfg.slots
+        _check(avsg_check_config(cfg), "avsg_check_config")
         ws = avsg_workspace_bytes(cfg)
-        if ws == 0:
-            raise AvsgError(AVSG_E_INVAL, "avsg_workspace_bytes", "invalid configuration")
         self.workspace = torch.empty(ws, dtype=torch.uint8, device=dev)
         self.buffers = [torch.zeros((B, S, int(cfg.row_bytes[s])), dtype=torch.uint8, device=dev)
                         for s in range(cfg.n_streams)]

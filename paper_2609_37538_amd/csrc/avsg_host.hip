@@ -55,6 +55,7 @@ namespace {
 constexpr size_t kAlign = 256;
 constexpr int kMaxBatch = 1024;
 constexpr size_t kMaxTimedSteps = 16384;
+constexpr size_t kLdsPerWorkgroup = 160 * 1024;   // gfx950
 
 size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
@@ -100,6 +101,7 @@ avsg_status check_config(const avsg_config* c, std::string* why) {
   if (!c) return fail(AVSG_E_INVAL, "null config");
   if (c->batch < 1 || c->batch > kMaxBatch) return fail(AVSG_E_INVAL, "batch must be in [1, 1024]");
   if (c->topk < 1 || c->n_q < 1) return fail(AVSG_E_INVAL, "topk and n_q must be positive");
+  if (c->n_q > 127) return fail(AVSG_E_RANGE, "n_q must be at most 127");
   if (c->slots < 2 || (c->slots & (c->slots - 1)) != 0 || c->slots > (1 << 23))
     return fail(AVSG_E_NOTPOW2, "slots must be a power of two in [2, 2^23]");
   if (static_cast<int64_t>(c->slots) < static_cast<int64_t>(c->n_q) * c->topk)
@@ -125,8 +127,9 @@ avsg_status check_config(const avsg_config* c, std::string* why) {
     if (c->gather_mode == AVSG_GATHER_POSITION)
       return fail(AVSG_E_UNSUPPORTED, "position-level transfer needs hash matching");
   } else {
-    if (match_lds_bytes(c->slots, c->topk) == 0)
-      return fail(AVSG_E_CAPACITY, "topk beyond 4096 indices per token");
+    const size_t lds = match_lds_bytes(c->slots, c->topk);
+    if (lds == 0 || lds > kLdsPerWorkgroup)
+      return fail(AVSG_E_CAPACITY, "table and selection exceed one workgroup's LDS (9*S + 12*K bytes)");
   }
   return AVSG_OK;
 }
@@ -154,6 +157,8 @@ int device_cus() {
 }  // namespace
 
 extern "C" {
+
+avsg_status avsg_check_config(const avsg_config* cfg) { return check_config(cfg, nullptr); }
 
 size_t avsg_workspace_bytes(const avsg_config* cfg) {
   if (check_config(cfg, nullptr) != AVSG_OK) return 0;

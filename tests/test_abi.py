@@ -56,6 +56,22 @@ def ws(**kw):
     return A.avsg_workspace_bytes(A.make_config(**base))
 
 
+def test_check_config_statuses(lib):
+    def chk(**kw):
+        base = dict(batch=64, topk=2048, n_q=2, slots=8192, row_bytes=(1152, 132))
+        base.update(kw)
+        return A.avsg_check_config(A.make_config(**base))
+    assert chk() == A.AVSG_OK
+    assert chk(slots=12288) == A.AVSG_E_NOTPOW2
+    assert chk(slots=2048) == A.AVSG_E_CAPACITY
+    assert chk(slots=32768, n_q=1) == A.AVSG_E_CAPACITY      # beyond one workgroup's LDS
+    assert chk(slots=16384, topk=1024) == A.AVSG_OK           # 9*16384 + 12*1024 bytes fit
+    assert chk(slots=16384, topk=2048) == A.AVSG_E_CAPACITY
+    assert chk(max_life=0) == A.AVSG_E_RANGE
+    assert chk(batch=0) == A.AVSG_E_INVAL
+    assert chk(match_mode=A.AVSG_MATCH_DUALPTR) == A.AVSG_E_UNSUPPORTED
+
+
 def test_workspace_size_and_validation(lib):
     n = ws()
     B, S, K, nq = 64, 8192, 2048, 2
@@ -76,3 +92,5 @@ def test_workspace_size_and_validation(lib):
     assert ws(gather_mode=A.AVSG_GATHER_POSITION) > ws() - 1
     assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=1, slots=2048, gather_mode=A.AVSG_GATHER_POSITION) == 0
     assert ws(n_q=1, slots=2, topk=1, batch=1, row_bytes=(4,)) > 0
+    assert ws(n_q=127, topk=64, slots=8192, row_bytes=(4,)) > 0
+    assert ws(n_q=128, topk=64, slots=8192, row_bytes=(4,)) == 0

@@ -84,7 +84,8 @@ EDGE_CASES = [
     ("k_one", dict(batch=5, topk=1, slots=2, n_q=1, steps=40, ctx=6)),
     ("k_3000", dict(batch=2, topk=3000, slots=8192, n_q=2, steps=8, ctx=100000)),
     ("k_4096_max", dict(batch=1, topk=4096, slots=8192, n_q=2, steps=6, ctx=200000)),
-    ("s_16384_max", dict(batch=2, topk=2048, slots=16384, n_q=2, steps=8, ctx=300000)),
+    ("s_16384_max", dict(batch=2, topk=1024, slots=16384, n_q=3, steps=8, ctx=300000)),
+    ("mtp_8_tokens", dict(batch=2, topk=128, slots=1024, n_q=8, steps=10, ctx=5000)),
     ("tiny_context", dict(batch=4, topk=64, slots=128, n_q=2, steps=30, ctx=200, retention=0.5)),
     ("all_hits", dict(batch=2, topk=256, slots=1024, n_q=2, steps=10, ctx=256, retention=1.0, overlap=1.0)),
     ("row_132_only", dict(batch=2, topk=128, slots=512, n_q=1, steps=10, ctx=4000, row_bytes=(132,))),
