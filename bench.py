@@ -40,7 +40,7 @@ def parse():
     ap.add_argument("--config", default="batch64_mtp2",
                     choices=["tiny", "batch16", "batch64_mtp2", "imbalance", "stress"])
     ap.add_argument("--gather", default="balanced",
-                    choices=["balanced", "request", "position", "sdma", "none"])
+                    choices=["balanced", "request", "position", "sdma", "none", "pipelined"])
     ap.add_argument("--match", default="hash", choices=["hash", "dualptr"])
     ap.add_argument("--workers", type=int, default=0, help="gather workgroups (0 = one per CU)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -50,6 +50,10 @@ def parse():
     ap.add_argument("--report", default="", help="also write a detailed JSON report here")
     ap.add_argument("--appendix-d-sweep", default="",
                     help="run the S1/S2/S3 transfer sweep (batch x reuse) and write it here")
+    ap.add_argument("--matching-sweep", default="",
+                    help="run the Stage One latency sweeps (S=K=N, K at S=4096, S at K=512) and write them here")
+    ap.add_argument("--lifetime-sweep", default="",
+                    help="run the maximum-lifetime sweep (L = 1..32) and write it here")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one device-to-device copy of this many MiB first (counter calibration)")
     return ap.parse_args()
@@ -68,10 +72,17 @@ def main():
     if args.appendix_d_sweep:
         appendix_d_sweep(args.appendix_d_sweep)
         return
+    if args.matching_sweep:
+        matching_sweep(args.matching_sweep)
+        return
+    if args.lifetime_sweep:
+        lifetime_sweep(args.lifetime_sweep)
+        return
 
     gather_mode = {"balanced": A.AVSG_GATHER_BALANCED, "request": A.AVSG_GATHER_REQUEST,
                    "sdma": A.AVSG_GATHER_SDMA, "none": A.AVSG_GATHER_NONE,
-                   "position": A.AVSG_GATHER_POSITION}[args.gather]
+                   "position": A.AVSG_GATHER_POSITION,
+                   "pipelined": A.AVSG_GATHER_PIPELINED}[args.gather]
     match_mode = {"hash": A.AVSG_MATCH_HASH, "dualptr": A.AVSG_MATCH_DUALPTR}[args.match]
     spec = W.get_spec(args.config)
     if match_mode == A.AVSG_MATCH_DUALPTR:
@@ -142,6 +153,10 @@ def main():
     misses = after["misses"] - before["misses"]
     row_total = sum(spec.row_bytes)
     moved = misses * row_total if gather_mode != A.AVSG_GATHER_NONE else 0
+    pipelined = gather_mode == A.AVSG_GATHER_PIPELINED
+    if pipelined:
+        # one fused launch: its duration is recorded in the matching slot
+        gather_ms, match_ms = match_ms, np.zeros_like(match_ms)
     gather_s = float(np.sum(gather_ms)) * 1e-3
     match_s = float(np.sum(match_ms)) * 1e-3
     gather_gbps = moved / gather_s / 1e9 if gather_s > 0 and moved else 0.0
@@ -179,12 +194,14 @@ def main():
         "hipmemcpy_h2d_peak_gbps": round(memcpy_peak, 3),
         "frac_of_hipmemcpy_peak": round(gather_gbps / memcpy_peak, 4) if memcpy_peak else None,
         "frac_of_pcie_gen5_x16": round(gather_gbps / PCIE_GEN5_X16_GBPS, 4),
-        "match_us_median": round(float(np.median(match_ms)) * 1e3, 2) if len(match_ms) else None,
+        "match_us_median": (round(float(np.median(match_ms)) * 1e3, 2)
+                            if len(match_ms) and not pipelined else None),
         "gather_us_median": round(float(np.median(gather_ms)) * 1e3, 2) if len(gather_ms) else None,
         "match_frac_of_step": round(match_s / wall, 4),
         "roofline": {
             "bound": "pcie",
-            "kernel": "gather_balanced_kernel" if args.gather == "balanced" else args.gather,
+            "kernel": {"balanced": "gather_balanced_kernel",
+                       "pipelined": "step_pipelined_kernel"}.get(args.gather, args.gather),
             "achieved": round(gather_gbps, 3),
             "peak": PCIE_GEN5_X16_GBPS,
             "unit": "GB/s",
@@ -266,7 +283,112 @@ def appendix_d_sweep(out_path):
         json.dump(results, f, indent=1)
 
 
-GATHER_SOURCES = ("paper_2609_37538_amd/csrc/gather.hip", "paper_2609_37538_amd/csrc/avsg_internal.h")
+def _timed_run(spec, cfg_kw, warm, timed, host_ptrs, dev, verified=False):
+    """Run warm + timed steps of `spec` through one operator; return
+    (match_ms[], gather_ms[], stats delta)."""
+    import torch
+    import workload as W
+    from paper_2609_37538_amd import avsg as A
+    wl = W.Workload(spec)
+    X = torch.from_numpy(wl.all_steps(warm + timed)).to(dev)
+    N = torch.from_numpy(np.stack([wl.verified_len(t) for t in range(warm + timed)])).to(dev)
+    cfg = A.make_config(spec.batch, spec.topk, spec.n_q, spec.slots, **cfg_kw)
+    op = A.Operator(cfg, host_ptrs, wl.ctx, device=dev)
+    try:
+        for t in range(warm):
+            op.step(X[t], N[t] if verified else None)
+        torch.cuda.synchronize()
+        before = op.stats()
+        A.avsg_set_timing(op.h, True)
+        for t in range(warm, warm + timed):
+            op.step(X[t], N[t] if verified else None)
+        match_ms, gather_ms = A.avsg_timing(op.h, timed)
+        after = op.stats()
+    finally:
+        op.close()
+    delta = {k: after[k] - before[k] for k in after if k != "max_step_alloc_decays"}
+    return match_ms, gather_ms, delta
+
+
+def matching_sweep(out_path):
+    """Stage One latency (matching kernel only, Stage Two off), median over 32
+    timed steps after 8 warm-up steps, uniform retention 0.9, one query token:
+    (a) hash vs dual-pointer at S = K = N; (b) hash, S = 4096, K = 512..4096;
+    (c) hash, K = 512, S = 512..8192.  Batch 1 (one request, one workgroup)
+    and batch 64."""
+    import dataclasses
+    import torch
+    import workload as W
+    from paper_2609_37538_amd import avsg as A
+    dev = torch.device("cuda:0")
+    ctx, rb, warm, timed = 65536, 16, 8, 32
+    host = A.HostRegion(64 * ctx * rb)
+    ptrs = [host.ptr + r * ctx * rb for r in range(64)]
+    points = []
+    for n in (256, 512, 1024, 2048):
+        points += [("a", "hash", n, n), ("a", "dualptr", n, n)]
+    for k in (512, 1024, 2048, 4096):
+        points.append(("b", "hash", 4096, k))
+    for sl in (512, 1024, 2048, 4096, 8192):
+        points.append(("c", "hash", sl, 512))
+    results = []
+    for B in (1, 64):
+        for panel, method, S, K in points:
+            spec = W.custom_spec(name="match_sweep", cfg_id=11, batch=B, topk=K, slots=S, n_q=1,
+                                 steps=warm + timed, ctx=ctx, retention=0.9)
+            mm = A.AVSG_MATCH_DUALPTR if method == "dualptr" else A.AVSG_MATCH_HASH
+            match_ms, _, d = _timed_run(spec, dict(row_bytes=(rb,), match_mode=mm,
+                                                   gather_mode=A.AVSG_GATHER_NONE),
+                                        warm, timed, ptrs[:B], dev)
+            row = {"panel": panel, "method": method, "batch": B, "S": S, "K": K,
+                   "match_us_median": round(float(np.median(match_ms)) * 1e3, 2),
+                   "hit_rate": round(d["hits"] / max(1, d["lookups"]), 4)}
+            results.append(row)
+            print(json.dumps(row), flush=True)
+    host.free()
+    with open(out_path, "w") as f:
+        json.dump(results, f, indent=1)
+
+
+def lifetime_sweep(out_path):
+    """Hit rate and Stage One / Stage Two time versus the maximum lifetime L
+    on a workload with reuse beyond adjacent steps: 16 requests, K = 2048,
+    S = 8192, one query token, a 512-position recency window plus 1,536
+    Zipf(1.1) hot positions kept step to step with p = 0.8 (16 warm-up
+    steps, 48 timed).  The adjacent-step reuse of the selections is reported
+    for reference."""
+    import torch
+    import workload as W
+    from paper_2609_37538_amd import avsg as A
+    dev = torch.device("cuda:0")
+    B, K, S, ctx, warm, timed = 16, 2048, 8192, 1 << 20, 16, 48
+    spec = W.custom_spec(name="lifetime_sweep", cfg_id=12, batch=B, topk=K, slots=S, n_q=1,
+                         steps=warm + timed, ctx=ctx, mode="zipf_window", retention=0.8)
+    wl = W.Workload(spec)
+    X = wl.all_steps(warm + timed)
+    adj = np.mean([len(np.intersect1d(X[t, r, 0], X[t - 1, r, 0])) / K
+                   for t in range(warm, warm + timed) for r in range(B)])
+    host = A.HostRegion(B * ctx * W.KV_ROW_BYTES)
+    W.fill_host(wl, 0, host.ptr)
+    ptrs = [host.ptr + r * ctx * W.KV_ROW_BYTES for r in range(B)]
+    results = []
+    for L in (1, 2, 4, 8, 16, 32):
+        match_ms, gather_ms, d = _timed_run(spec, dict(row_bytes=(W.KV_ROW_BYTES,), max_life=L),
+                                            warm, timed, ptrs, dev, verified=True)
+        row = {"L": L, "hit_rate": round(d["hits"] / max(1, d["lookups"]), 4),
+               "adjacent_step_reuse": round(float(adj), 4),
+               "match_us_median": round(float(np.median(match_ms)) * 1e3, 2),
+               "gather_us_median": round(float(np.median(gather_ms)) * 1e3, 2),
+               "lost_installs_per_step": round((d["lost_exhausted"] + d["lost_collision"]) / timed, 1)}
+        results.append(row)
+        print(json.dumps(row), flush=True)
+    host.free()
+    with open(out_path, "w") as f:
+        json.dump(results, f, indent=1)
+
+
+GATHER_SOURCES = ("paper_2609_37538_amd/csrc/gather.hip", "paper_2609_37538_amd/csrc/gather_body.h",
+                  "paper_2609_37538_amd/csrc/avsg_internal.h")
 TRAFFIC_SUMMARY = "profiles/gather_traffic_batch64_mtp2.md"
 
 

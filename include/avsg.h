@@ -62,6 +62,9 @@ typedef int32_t avsg_status;
 #define AVSG_GATHER_SDMA 2     /* comparator: the miss list is read back and every missed row is one hipMemcpyAsync on the copy engines */
 #define AVSG_GATHER_NONE 3     /* Stage One only (matching measured alone) */
 #define AVSG_GATHER_POSITION 4 /* S2: the N_g*K selected positions split into C near-equal ranges, hits issue nothing (Eq. 14) */
+#define AVSG_GATHER_PIPELINED 5 /* Stage One and Stage Two in one launch: each token's misses are queued in
+                                   chunks as soon as they are reserved and copied by every CU (hash matching,
+                                   batch <= CU count) */
 
 #define AVSG_MAX_STREAMS 2
 
@@ -94,7 +97,7 @@ typedef struct avsg_stats_t {
     uint64_t invalidations;   /* cached indices cleared by speculative invalidation */
     uint64_t bad_indices;     /* selected indices outside [0, rows) (skipped by the copy) */
     int32_t max_step_alloc_decays; /* largest allocation-decay count of one request-step */
-    int32_t reserved;
+    int32_t queue_timeouts;   /* pipelined step: consumers that gave up waiting (0 in correct operation) */
 } avsg_stats_t;
 
 typedef struct avsg_handle avsg_handle;

@@ -4,7 +4,8 @@ The operator lives in the HIP library ``libavsg.so`` (C ABI in
 ``include/avsg.h``); :mod:`paper_2609_37538_amd.avsg` is its ctypes binding.
 """
 from .avsg import (  # noqa: F401
-    AVSG_GATHER_BALANCED, AVSG_GATHER_NONE, AVSG_GATHER_POSITION, AVSG_GATHER_REQUEST,
+    AVSG_GATHER_BALANCED, AVSG_GATHER_NONE, AVSG_GATHER_PIPELINED, AVSG_GATHER_POSITION,
+    AVSG_GATHER_REQUEST,
     AVSG_GATHER_SDMA,
     AVSG_MATCH_DUALPTR, AVSG_MATCH_HASH, AvsgConfig, AvsgError, HostRegion, Operator,
     avsg_check_config, avsg_create, avsg_destroy, avsg_device_cus, avsg_export_misses, avsg_export_state,

@@ -35,6 +35,7 @@ AVSG_GATHER_REQUEST = 1
 AVSG_GATHER_SDMA = 2
 AVSG_GATHER_NONE = 3
 AVSG_GATHER_POSITION = 4
+AVSG_GATHER_PIPELINED = 5
 AVSG_MAX_STREAMS = 2
 
 A1_DEFAULT = 2654435761
@@ -56,10 +57,10 @@ class AvsgStats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in (
         "steps", "lookups", "hits", "misses", "bytes_moved", "lost_exhausted", "lost_collision",
         "alloc_decays", "revivals", "invalidations", "bad_indices")] + [
-        ("max_step_alloc_decays", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+        ("max_step_alloc_decays", ctypes.c_int32), ("queue_timeouts", ctypes.c_int32)]
 
     def as_dict(self):
-        return {f: int(getattr(self, f)) for f, _ in self._fields_ if f != "reserved"}
+        return {f: int(getattr(self, f)) for f, _ in self._fields_}
 
 
 class AvsgError(RuntimeError):

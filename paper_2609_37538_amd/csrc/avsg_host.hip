@@ -28,6 +28,11 @@ struct avsg_handle {
   int2* dp_state = nullptr;
   int2* miss_list = nullptr;
   uint8_t* hit_mask = nullptr;
+  int* pipe_ctl = nullptr;      // head, tail, done, exit_count, error
+  int4* pipe_chunks = nullptr;
+  int pipe_max_chunks = 0;
+  int pipe_epoch = 0;
+  int cus = 0;
   unsigned long long* stats = nullptr;
   uint64_t* host_ptrs = nullptr;
   uint64_t* buf_ptrs = nullptr;
@@ -67,8 +72,10 @@ bool is_prime_u32(uint32_t v) {
   return true;
 }
 
+size_t pipe_chunks_for(const avsg_config& c);
+
 struct Layout {
-  size_t table_c, table_q, miss_list, hit_mask, stats, host_ptrs, buf_ptrs, rows, total;
+  size_t table_c, table_q, miss_list, hit_mask, pipe, pipe_bytes, stats, host_ptrs, buf_ptrs, rows, total;
 };
 
 Layout layout_of(const avsg_config& c) {
@@ -79,12 +86,20 @@ Layout layout_of(const avsg_config& c) {
   L.table_q = off; off += up(B * S * 4);
   L.miss_list = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk * 8);
   L.hit_mask = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk);
+  L.pipe = off;
+  L.pipe_bytes = up(kAlign + 16 * pipe_chunks_for(c));
+  off += L.pipe_bytes;
   L.stats = off; off += up(B * kNumStats * 8);
   L.host_ptrs = off; off += up(static_cast<size_t>(c.n_streams) * B * 8);
   L.buf_ptrs = off; off += up(static_cast<size_t>(c.n_streams) * B * 8);
   L.rows = off; off += up(B * 8);
   L.total = off;
   return L;
+}
+
+size_t pipe_chunks_for(const avsg_config& c) {
+  const int ch = pipelined_chunk_misses();
+  return static_cast<size_t>(c.batch) * c.n_q * ((c.topk + ch - 1) / ch);
 }
 
 int log2_exact(int32_t s) {
@@ -118,17 +133,19 @@ avsg_status check_config(const avsg_config* c, std::string* why) {
   if (c->gather_workers < 0) return fail(AVSG_E_INVAL, "gather_workers must be >= 0");
   if (c->match_mode != AVSG_MATCH_HASH && c->match_mode != AVSG_MATCH_DUALPTR)
     return fail(AVSG_E_INVAL, "unknown match_mode");
-  if (c->gather_mode < AVSG_GATHER_BALANCED || c->gather_mode > AVSG_GATHER_POSITION)
+  if (c->gather_mode < AVSG_GATHER_BALANCED || c->gather_mode > AVSG_GATHER_PIPELINED)
     return fail(AVSG_E_INVAL, "unknown gather_mode");
   if (c->match_mode == AVSG_MATCH_DUALPTR) {
     if (c->n_q != 1) return fail(AVSG_E_UNSUPPORTED, "dual-pointer matching handles one token per step");
     if (c->slots != c->topk) return fail(AVSG_E_UNSUPPORTED, "dual-pointer matching needs slots == topk");
     if (c->topk > 4096) return fail(AVSG_E_CAPACITY, "dual-pointer matching supports topk <= 4096");
-    if (c->gather_mode == AVSG_GATHER_POSITION)
-      return fail(AVSG_E_UNSUPPORTED, "position-level transfer needs hash matching");
+    if (c->gather_mode == AVSG_GATHER_POSITION || c->gather_mode == AVSG_GATHER_PIPELINED)
+      return fail(AVSG_E_UNSUPPORTED, "position-level and pipelined transfer need hash matching");
   } else {
-    const size_t lds = match_lds_bytes(c->slots, c->topk);
-    if (lds == 0 || lds > kLdsPerWorkgroup)
+    const size_t lds = c->gather_mode == AVSG_GATHER_PIPELINED
+                           ? pipelined_lds_bytes(c->slots, c->topk)
+                           : match_lds_bytes(c->slots, c->topk);
+    if (match_lds_bytes(c->slots, c->topk) == 0 || lds > kLdsPerWorkgroup)
       return fail(AVSG_E_CAPACITY, "table and selection exceed one workgroup's LDS (9*S + 12*K bytes)");
   }
   return AVSG_OK;
@@ -230,6 +247,9 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
   h->dp_state = reinterpret_cast<int2*>(ws + L.table_c);  // S == K: the two table arrays hold [B][K] pairs
   h->miss_list = reinterpret_cast<int2*>(ws + L.miss_list);
   h->hit_mask = ws + L.hit_mask;
+  h->pipe_ctl = reinterpret_cast<int*>(ws + L.pipe);
+  h->pipe_chunks = reinterpret_cast<int4*>(ws + L.pipe + kAlign);
+  h->pipe_max_chunks = static_cast<int>(pipe_chunks_for(c));
   h->stats = reinterpret_cast<unsigned long long*>(ws + L.stats);
   h->host_ptrs = reinterpret_cast<uint64_t*>(ws + L.host_ptrs);
   h->buf_ptrs = reinterpret_cast<uint64_t*>(ws + L.buf_ptrs);
@@ -250,6 +270,7 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
     h->bufs[i] = reinterpret_cast<uint64_t>(d_buffers[i]);
   }
   const int cus = device_cus();
+  h->cus = cus;
   h->workers = c.gather_workers > 0 ? c.gather_workers : std::max(1, cus);
 
   auto cleanup = [&](avsg_status rc) {
@@ -267,6 +288,18 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
       return cleanup(AVSG_E_CAPACITY);
     }
     if ((e = prepare_match_hash(h->lds)) != hipSuccess) return cleanup(hip_fail(nullptr, e, ""));
+    if (c.gather_mode == AVSG_GATHER_PIPELINED) {
+      // producers (one per request) must all be resident beside the consumers
+      if (c.batch > cus) {
+        std::fprintf(stderr, "avsg_create: pipelined step needs batch <= %d (one workgroup per CU)\n", cus);
+        return cleanup(AVSG_E_UNSUPPORTED);
+      }
+      h->lds = pipelined_lds_bytes(c.slots, c.topk);
+      if ((e = prepare_step_pipelined(h->lds)) != hipSuccess) return cleanup(AVSG_E_HIP);
+      if (launch_zero_u64(reinterpret_cast<unsigned long long*>(h->pipe_ctl), L.pipe_bytes / 8, s) !=
+          hipSuccess)
+        return cleanup(AVSG_E_HIP);
+    }
     if ((e = launch_reset_tables(h->table_c, h->table_q,
                                  static_cast<size_t>(B) * c.slots, s)) != hipSuccess)
       return cleanup(AVSG_E_HIP);
@@ -352,6 +385,35 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
   h->last_counts = d_miss_counts;
   avsg_status rc;
   if ((rc = record(h, 0, s)) != AVSG_OK) return rc;
+  if (c.gather_mode == AVSG_GATHER_PIPELINED) {
+    MatchParams p{};
+    p.B = c.batch; p.K = c.topk; p.n_q = c.n_q; p.S = c.slots; p.m = h->m;
+    p.R = c.retry; p.L = c.max_life; p.a1 = c.a1; p.a2 = c.a2;
+    p.f_mask = static_cast<uint32_t>((1u << (23 - h->m)) - 1u);
+    p.topk = d_topk; p.verified = d_verified_len; p.rows = h->rows_dev;
+    p.table_c = h->table_c; p.table_q = h->table_q;
+    p.slots_out = d_slots; p.miss_counts = d_miss_counts; p.miss_list = h->miss_list;
+    p.stats = h->stats; p.hit_mask = nullptr;
+    GatherParams g{};
+    g.B = c.batch; g.n_q = c.n_q; g.K = c.topk; g.S = c.slots;
+    g.miss_counts = d_miss_counts; g.miss_list = h->miss_list; g.rows = h->rows_dev;
+    g.n_streams = c.n_streams; g.host_ptrs = h->host_ptrs; g.buf_ptrs = h->buf_ptrs;
+    g.row_bytes0 = c.row_bytes[0];
+    g.row_bytes1 = c.n_streams > 1 ? c.row_bytes[1] : 0;
+    PipeParams q{};
+    q.head = h->pipe_ctl; q.tail = h->pipe_ctl + 1; q.done = h->pipe_ctl + 2;
+    q.exit_count = h->pipe_ctl + 3; q.error = h->pipe_ctl + 4;
+    q.chunks = h->pipe_chunks; q.max_chunks = h->pipe_max_chunks;
+    if (++h->pipe_epoch <= 0) h->pipe_epoch = 1;
+    q.epoch = h->pipe_epoch;
+    const int wgs = std::max(c.batch, c.gather_workers > 0 ? c.gather_workers : h->cus);
+    HIP_TRY(h, launch_step_pipelined(p, g, q, wgs, h->lds, s));
+    if ((rc = record(h, 1, s)) != AVSG_OK) return rc;
+    if ((rc = record(h, 2, s)) != AVSG_OK) return rc;
+    if (h->timing && h->n_timed < kMaxTimedSteps) h->n_timed++;
+    h->steps++;
+    return AVSG_OK;
+  }
   if (c.match_mode == AVSG_MATCH_HASH) {
     MatchParams p{};
     p.B = c.batch; p.K = c.topk; p.n_q = c.n_q; p.S = c.slots; p.m = h->m;
@@ -416,6 +478,15 @@ avsg_status avsg_stats(avsg_handle* h, avsg_stats_t* out) {
     max_dec = std::max<uint64_t>(max_dec, s[kStatMaxStepDecays]);
   }
   out->max_step_alloc_decays = static_cast<int32_t>(max_dec);
+  if (c.gather_mode == AVSG_GATHER_PIPELINED) {
+    int ctl[5] = {0, 0, 0, 0, 0};
+    HIP_TRY(h, hipMemcpy(ctl, h->pipe_ctl, sizeof(ctl), hipMemcpyDeviceToHost));
+    out->queue_timeouts = ctl[4];
+    if (ctl[4]) {
+      h->err = "pipelined step: a consumer timed out waiting for the chunk queue";
+      return AVSG_E_INTERNAL;
+    }
+  }
   uint64_t rb = 0;
   for (int s = 0; s < c.n_streams; ++s) rb += static_cast<uint64_t>(c.row_bytes[s]);
   out->bytes_moved = c.gather_mode == AVSG_GATHER_NONE ? 0 : out->misses * rb;

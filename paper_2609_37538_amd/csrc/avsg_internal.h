@@ -61,6 +61,18 @@ struct GatherParams {
   const uint8_t* hit_mask;      // [B][n_q][K]
 };
 
+// Device-wide chunk queue of the pipelined step (workspace resident).
+struct PipeParams {
+  int* head;          // next queue entry to claim
+  int* tail;          // queue entries reserved by producers
+  int* done;          // requests whose Stage One has finished
+  int* exit_count;    // workgroups that have left
+  int* error;         // set when a consumer gave up waiting
+  int4* chunks;       // [max_chunks] (request, first miss, count, epoch)
+  int max_chunks;
+  int epoch;          // step stamp, never 0
+};
+
 struct DualPtrParams {
   int32_t B, K;
   const int32_t* topk;          // [B][K]
@@ -84,6 +96,11 @@ hipError_t launch_zero_u64(unsigned long long* p, size_t n, hipStream_t s);
 hipError_t launch_gather_balanced(const GatherParams& p, int workers, hipStream_t s);
 hipError_t launch_gather_request(const GatherParams& p, hipStream_t s);
 hipError_t launch_gather_position(const GatherParams& p, int workers, hipStream_t s);
+int pipelined_chunk_misses();
+size_t pipelined_lds_bytes(int S, int K);
+hipError_t prepare_step_pipelined(size_t lds);
+hipError_t launch_step_pipelined(const MatchParams& mp, const GatherParams& gp, const PipeParams& q,
+                                 int workgroups, size_t lds, hipStream_t s);
 hipError_t launch_match_dualptr(const DualPtrParams& p, size_t lds, hipStream_t s);
 hipError_t prepare_match_dualptr(size_t lds);
 hipError_t launch_reset_dualptr(int2* state, int B, int K, hipStream_t s);

@@ -1,0 +1,150 @@
+// Device code of Stage Two shared by the gather kernels and the pipelined
+// step kernel (see gather.hip for the work assignments).
+#pragma once
+
+#include "avsg_internal.h"
+
+namespace avsg {
+namespace {
+
+
+constexpr int GT = kGatherThreads;
+constexpr int TILE = kGatherTile;
+constexpr int kMaxBatch = 1024;
+constexpr int kUnroll = 4;
+
+__device__ __forceinline__ int lane_index() {
+  return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+}
+
+// Exclusive prefix of the per-request miss totals into pre[0..B] (pre[B] = N).
+__device__ void request_prefix(const GatherParams& p, long long* pre, long long* wtot) {
+  const int tid = threadIdx.x, lane = lane_index(), wave = tid >> 6;
+  const int per = (p.B + GT - 1) / GT;
+  const int r0 = tid * per;
+  long long local = 0;
+  for (int k = 0; k < per; ++k) {
+    const int r = r0 + k;
+    if (r < p.B) {
+      long long t = 0;
+      for (int g = 0; g < p.n_q; ++g) t += p.miss_counts[static_cast<size_t>(r) * p.n_q + g];
+      pre[r + 1] = t;
+      local += t;
+    }
+  }
+  long long incl = local;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    long long t = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += t;
+  }
+  if (lane == 63) wtot[wave] = incl;
+  __syncthreads();
+  long long base = incl - local;
+  for (int w = 0; w < wave; ++w) base += wtot[w];
+  for (int k = 0; k < per; ++k) {
+    const int r = r0 + k;
+    if (r < p.B) {
+      const long long t = pre[r + 1];
+      base += t;
+      pre[r + 1] = base;
+    }
+  }
+  if (tid == 0) pre[0] = 0;
+  __syncthreads();
+}
+
+__device__ __forceinline__ int find_request(const long long* pre, int B, long long j) {
+  int lo = 0, hi = B;  // pre[lo] <= j < pre[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (pre[mid] <= j) lo = mid;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// A 16-byte vector as a clang vector type: arrays of it stay in registers
+// (HIP's uint4 is a union-based struct that is kept in scratch memory here).
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Rows i < tn: copy chunks * sizeof(V) bytes from src[i] to dst[i] (src[i] == 0
+// skips the row), with NT threads each keeping U loads in flight.
+template <typename V, int U = kUnroll, int NT = GT>
+__device__ __forceinline__ void copy_rows(const uint64_t* src, const uint64_t* dst, int tn,
+                                          int chunks) {
+  const int total = tn * chunks;
+  for (int q0 = threadIdx.x; q0 < total; q0 += NT * U) {
+    V v[U];
+    uint64_t da[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int q = q0 + u * NT;
+      da[u] = 0;
+      if (q < total) {
+        const int i = q / chunks;
+        const int ch = q - i * chunks;
+        const uint64_t s = src[i];
+        if (s) {
+          v[u] = *reinterpret_cast<const V*>(s + static_cast<uint64_t>(ch) * sizeof(V));
+          da[u] = dst[i] + static_cast<uint64_t>(ch) * sizeof(V);
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (da[u]) *reinterpret_cast<V*>(da[u]) = v[u];
+  }
+}
+
+__device__ void copy_tile_rows(const GatherParams& p, int tn, uint64_t* src0, uint64_t* dst0,
+                               uint64_t* src1, uint64_t* dst1) {
+  __syncthreads();
+  if ((p.row_bytes0 & 15) == 0)
+    copy_rows<u32x4>(src0, dst0, tn, static_cast<int>(p.row_bytes0 / 16));
+  else
+    copy_rows<uint32_t>(src0, dst0, tn, static_cast<int>(p.row_bytes0 / 4));
+  if (p.n_streams > 1) {
+    if ((p.row_bytes1 & 15) == 0)
+      copy_rows<u32x4>(src1, dst1, tn, static_cast<int>(p.row_bytes1 / 16));
+    else
+      copy_rows<uint32_t>(src1, dst1, tn, static_cast<int>(p.row_bytes1 / 4));
+  }
+  __syncthreads();
+}
+
+// Copy misses [a, b) of the batch-wide list.
+__device__ void copy_range(const GatherParams& p, const long long* pre, long long a, long long b,
+                           uint64_t* src0, uint64_t* dst0, uint64_t* src1, uint64_t* dst1) {
+  const size_t per_req = static_cast<size_t>(p.n_q) * p.K;
+  for (long long t0 = a; t0 < b; t0 += TILE) {
+    const int tn = static_cast<int>((b - t0) < TILE ? (b - t0) : TILE);
+    for (int i = threadIdx.x; i < tn; i += GT) {
+      const long long j = t0 + i;
+      const int r = find_request(pre, p.B, j);
+      const int2 e = p.miss_list[static_cast<size_t>(r) * per_req + static_cast<size_t>(j - pre[r])];
+      const bool ok = e.x >= 0 && static_cast<int64_t>(e.x) < p.rows[r] && e.y >= 0 && e.y < p.S;
+      src0[i] = ok ? p.host_ptrs[r] + static_cast<uint64_t>(e.x) * p.row_bytes0 : 0;
+      dst0[i] = p.buf_ptrs[r] + static_cast<uint64_t>(e.y) * p.row_bytes0;
+      if (p.n_streams > 1) {
+        src1[i] = ok ? p.host_ptrs[p.B + r] + static_cast<uint64_t>(e.x) * p.row_bytes1 : 0;
+        dst1[i] = p.buf_ptrs[p.B + r] + static_cast<uint64_t>(e.y) * p.row_bytes1;
+      }
+    }
+    __syncthreads();
+    if ((p.row_bytes0 & 15) == 0)
+      copy_rows<u32x4>(src0, dst0, tn, static_cast<int>(p.row_bytes0 / 16));
+    else
+      copy_rows<uint32_t>(src0, dst0, tn, static_cast<int>(p.row_bytes0 / 4));
+    if (p.n_streams > 1) {
+      if ((p.row_bytes1 & 15) == 0)
+        copy_rows<u32x4>(src1, dst1, tn, static_cast<int>(p.row_bytes1 / 16));
+      else
+        copy_rows<uint32_t>(src1, dst1, tn, static_cast<int>(p.row_bytes1 / 4));
+    }
+    __syncthreads();
+  }
+}
+
+}  // namespace
+}  // namespace avsg

@@ -1,0 +1,452 @@
+// Device code of Stage One shared by the matching kernel and the pipelined
+// step kernel (see match_hash.hip for the phases).
+#pragma once
+
+#include "avsg_internal.h"
+
+namespace avsg {
+namespace {
+
+
+constexpr int MT = kMatchThreads;
+constexpr int MW = MT / 64;
+constexpr int kMaxIPT = 4;                 // up to K = 4096 indices per token
+constexpr int kMaxSPT = 16;                // up to S = 16384 slots
+constexpr int kScratchInts = 2 * kMaxIPT * MW + MW + 4 + 8;
+constexpr uint32_t kBid = 0x80000000u;     // marks a bucket written by an install bid
+
+__device__ __forceinline__ int lane_id() {
+  return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+}
+// number of set bits of `mask` at lanes below this lane
+__device__ __forceinline__ int bits_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+}
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+__device__ __forceinline__ int wave_inclusive_scan(int v, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    int t = __shfl_up(v, off, 64);
+    if (lane >= off) v += t;
+  }
+  return v;
+}
+
+__host__ __device__ constexpr size_t align16(size_t v) { return (v + 15) & ~size_t(15); }
+
+// Bucket words in LDS hold either the canonical low 24 bits of Eq. 3
+// (invalid | fingerprint | slot) or an install bid
+// (kBid | token << 24 | slot << (23 - m) | fingerprint), always a valid mapping.
+struct Word {
+  uint32_t m, smask, fmask;
+  __device__ __forceinline__ uint32_t slot(uint32_t w) const {
+    return ((w & kBid) ? (w >> (23 - m)) : w) & smask;
+  }
+  __device__ __forceinline__ bool invalid(uint32_t w) const {
+    return !(w & kBid) && ((w >> 23) & 1u);
+  }
+  __device__ __forceinline__ uint32_t fp(uint32_t w) const {
+    return ((w & kBid) ? w : (w >> m)) & fmask;
+  }
+  __device__ __forceinline__ uint32_t canonical(uint32_t w) const {
+    return (w & kBid) ? ((fp(w) << m) | slot(w)) : (w & 0xFFFFFFu);
+  }
+};
+
+// The lifetimes a thread owns, packed four to a register.
+struct Own {
+  uint32_t w[kMaxSPT / 4];
+  __device__ __forceinline__ int get(int e) const {
+    return static_cast<int>(static_cast<int8_t>(w[e >> 2] >> (8 * (e & 3))));
+  }
+  __device__ __forceinline__ void set(int e, int v) {
+    const uint32_t sh = 8 * (e & 3);
+    w[e >> 2] = (w[e >> 2] & ~(0xFFu << sh)) | (static_cast<uint32_t>(static_cast<uint8_t>(v)) << sh);
+  }
+  __device__ __forceinline__ void load(const int8_t* slife, int j0, int spt) {
+#pragma unroll
+    for (int k = 0; k < kMaxSPT / 4; ++k) w[k] = 0u;
+    if (spt >= 4) {
+      const uint32_t* p = reinterpret_cast<const uint32_t*>(slife + j0);
+#pragma unroll
+      for (int k = 0; k < kMaxSPT / 4; ++k)
+        if (k < spt / 4) w[k] = p[k];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 3; ++e)
+        if (e < spt) set(e, slife[j0 + e]);
+    }
+  }
+  __device__ __forceinline__ void store(int8_t* slife, int j0, int spt) const {
+    if (spt >= 4) {
+      uint32_t* p = reinterpret_cast<uint32_t*>(slife + j0);
+#pragma unroll
+      for (int k = 0; k < kMaxSPT / 4; ++k)
+        if (k < spt / 4) p[k] = w[k];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 3; ++e)
+        if (e < spt) slife[j0 + e] = static_cast<int8_t>(get(e));
+    }
+  }
+  // number of owned lifetimes below k
+  __device__ __forceinline__ int count_below(int k, int spt) const {
+    int c = 0;
+#pragma unroll
+    for (int e = 0; e < kMaxSPT; ++e) c += (e < spt && get(e) < k) ? 1 : 0;
+    return c;
+  }
+  // decay by k, never below -1
+  __device__ __forceinline__ void decay(int k, int spt) {
+#pragma unroll
+    for (int e = 0; e < kMaxSPT; ++e)
+      if (e < spt) {
+        const int l = get(e) - k;
+        set(e, l < -1 ? -1 : l);
+      }
+  }
+};
+
+// Stage One for request r (Algorithm 4's token loop) in workgroup-owned LDS.
+// After each token with misses, publish(r, first, count) is called by every
+// thread once the token's transfer-list entries are written (a no-op for the
+// plain matching kernel).
+template <int IPT, typename Publish>
+__device__ __forceinline__ void match_request(const MatchParams& p, const int r, unsigned char* lds,
+                              Publish& publish) {
+  const int S = p.S, K = p.K, R = p.R;
+  const uint32_t smask = static_cast<uint32_t>(S - 1);
+  const Word W{static_cast<uint32_t>(p.m), smask, p.f_mask};
+  int32_t* sc = reinterpret_cast<int32_t*>(lds);
+  uint32_t* smap = reinterpret_cast<uint32_t*>(lds + 4 * static_cast<size_t>(S));
+  int8_t* slife = reinterpret_cast<int8_t*>(lds + 8 * static_cast<size_t>(S));
+  int32_t* somiss = reinterpret_cast<int32_t*>(lds + 8 * static_cast<size_t>(S) + align16(S));
+  int32_t* smx = somiss + K;                 // [K] dense miss indices
+  int32_t* smp = smx + K;                    // [K] dense miss positions
+  int32_t* swc = smp + K;                    // [2][IPT][MW] miss counts per wave
+  int32_t* sdead = swc + 2 * kMaxIPT * MW;   // [MW] dead counts per wave
+  int32_t* sred = sdead + MW;                // [4] rotating reduction slots
+  int32_t* sstat = sred + 4;                 // [8] counter reduction
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const int lane = lane_id();
+
+  int32_t* gc = p.table_c + static_cast<size_t>(r) * S;
+  uint32_t* gq = p.table_q + static_cast<size_t>(r) * S;
+  for (int j = tid; j < S; j += MT) {
+    const uint32_t q = gq[j];
+    sc[j] = gc[j];
+    smap[j] = q & 0xFFFFFFu;
+    slife[j] = static_cast<int8_t>(q >> 24);
+  }
+  if (tid < 4) sred[tid] = 0;
+  if (tid < 8) sstat[tid] = 0;
+
+  const int spt = S >= MT ? S / MT : 1;   // lifetimes owned by this thread: [j0, j0 + spt)
+  const int own_n = tid < S ? spt : 0;
+  const int j0 = tid < S ? tid * spt : 0;
+  const int64_t rows_r = p.rows[r];
+  const int64_t n_verified = p.verified ? p.verified[r] : INT64_MAX;
+  const uint32_t a1 = p.a1, a2 = p.a2, fmask = p.f_mask;
+  const int m = p.m, L = p.L;
+
+  int st_hits = 0, st_miss = 0, st_exh = 0, st_col = 0, st_rev = 0, st_bad = 0;
+  int step_decays = 0;
+  int listed = 0;
+  int red_it = 0;
+  // bids of the previous token, checked after the next barrier
+  uint32_t bid_h[IPT], bid_v[IPT];
+#pragma unroll
+  for (int u = 0; u < IPT; ++u) {
+    bid_v[u] = 0u;
+    bid_h[u] = 0u;
+  }
+
+  int32_t xv[IPT];
+  {
+    const int32_t* xg = p.topk + static_cast<size_t>(r) * p.n_q * K;
+#pragma unroll
+    for (int u = 0; u < IPT; ++u) {
+      const int i = u * MT + tid;
+      xv[u] = i < K ? xg[i] : 0;
+    }
+  }
+  __syncthreads();
+
+  for (int g = 0; g < p.n_q; ++g) {
+    // Pass 1 (refresh): the first token decays every lifetime by one.
+    if (g == 0) {
+      Own o;
+      o.load(slife, j0, own_n);
+      o.decay(1, own_n);
+      o.store(slife, j0, own_n);
+      __syncthreads();
+    }
+    const size_t row = static_cast<size_t>(r) * p.n_q + g;
+    int32_t* og = p.slots_out + row * K;
+    int32_t* wc = swc + (g & 1) * kMaxIPT * MW;
+
+    // ---- A: probe, refresh hits, rank misses ------------------------------
+    uint32_t hh[IPT], dd[IPT];
+    int oo[IPT];
+    bool act[IPT], found[IPT];
+#pragma unroll
+    for (int u = 0; u < IPT; ++u) {
+      act[u] = u * MT + tid < K;
+      const uint32_t ux = static_cast<uint32_t>(xv[u]);
+      hh[u] = (a1 * ux) & smask;              // initial bucket (Eq. 9)
+      dd[u] = ((a2 * ux) & smask) | 1u;       // odd stride (Eq. 9)
+      found[u] = false;
+      oo[u] = 0;
+      if (act[u] && (xv[u] < 0 || static_cast<int64_t>(xv[u]) >= rows_r)) st_bad++;
+    }
+    for (int rd = 0; rd <= R; ++rd) {
+      bool pending = false;
+      uint32_t qw[IPT];
+#pragma unroll
+      for (int u = 0; u < IPT; ++u)
+        if (act[u] && !found[u]) qw[u] = smap[hh[u]];
+#pragma unroll
+      for (int u = 0; u < IPT; ++u)
+        if (act[u] && !found[u]) oo[u] = static_cast<int>(W.slot(qw[u]));   // Eq. 10
+      int32_t cv[IPT];
+#pragma unroll
+      for (int u = 0; u < IPT; ++u)
+        if (act[u] && !found[u]) cv[u] = sc[oo[u]];
+#pragma unroll
+      for (int u = 0; u < IPT; ++u)
+        if (act[u] && !found[u]) {
+          if (cv[u] == xv[u]) {
+            found[u] = true;
+          } else {
+            hh[u] = (hh[u] + dd[u]) & smask;  // unresolved probes advance (Eq. 11)
+            pending = true;
+          }
+        }
+      if (!__ballot(pending)) break;
+    }
+    int rank[IPT];
+#pragma unroll
+    for (int u = 0; u < IPT; ++u) {
+      const int i = u * MT + tid;
+      if (found[u]) {
+        if (slife[oo[u]] < 0) st_rev++;
+        slife[oo[u]] = static_cast<int8_t>(L);   // refresh the hit slot
+        og[i] = oo[u];                           // Pass 2: o[m] = o^match
+        st_hits++;
+      }
+      if (p.hit_mask && act[u]) p.hit_mask[row * K + i] = found[u] ? 1 : 0;
+      const uint64_t mm = __ballot(act[u] && !found[u]);
+      if (lane == 0) wc[u * MW + wave] = __popcll(mm);
+      rank[u] = bits_below(mm);
+    }
+    // installs of the previous token that lost their bucket
+#pragma unroll
+    for (int u = 0; u < IPT; ++u)
+      if (bid_v[u]) {
+        if (smap[bid_h[u]] != bid_v[u]) st_col++;
+        bid_v[u] = 0u;
+      }
+    __syncthreads();
+
+    // ---- B: classify, compact misses, count dead slots ---------------------
+    int n_g = 0;
+#pragma unroll
+    for (int u = 0; u < IPT; ++u) {
+      int tot = 0, before = 0;
+      for (int w = 0; w < MW; ++w) {
+        const int c = wc[u * MW + w];
+        tot += c;
+        before += (w < wave) ? c : 0;
+      }
+      rank[u] += n_g + before;
+      n_g += tot;
+    }
+    if (tid == 0) {
+      p.miss_counts[row] = n_g;
+      st_miss += n_g;
+    }
+#pragma unroll
+    for (int u = 0; u < IPT; ++u)
+      if (act[u] && !found[u]) {
+        smx[rank[u]] = xv[u];
+        smp[rank[u]] = u * MT + tid;
+      }
+    Own own;
+    own.load(slife, j0, own_n);
+    int dcnt = own.count_below(0, own_n);
+    int incl = wave_inclusive_scan(dcnt, lane);
+    if (lane == 63) sdead[wave] = incl;
+    // prefetch the next token's indices
+    if (g + 1 < p.n_q) {
+      const int32_t* xg = p.topk + (row + 1) * K;
+#pragma unroll
+      for (int u = 0; u < IPT; ++u) {
+        const int i = u * MT + tid;
+        xv[u] = i < K ? xg[i] : 0;
+      }
+    }
+    __syncthreads();
+
+    if (n_g > 0) {
+      // ---- C: enough dead slots (decay loop of Algorithm 1), CollectDead --
+      int dead = 0, wbase = 0;
+      for (int w = 0; w < MW; ++w) {
+        const int c = sdead[w];
+        dead += c;
+        wbase += (w < wave) ? c : 0;
+      }
+      if (dead < n_g) {
+        // smallest k with #{lifetime_j < k} >= n_g; k = L + 1 always suffices
+        int kstar = 1;
+        for (int k = 1;; ++k) {
+          const int cnt = wave_sum(own.count_below(k, own_n));
+          const int slot = red_it % 3;
+          if (lane == 0 && cnt) atomicAdd(&sred[slot], cnt);
+          if (tid == 0) sred[(red_it + 1) % 3] = 0;
+          red_it++;
+          __syncthreads();
+          if (sred[slot] >= n_g || k > L) {
+            kstar = k;
+            break;
+          }
+        }
+        own.decay(kstar, own_n);
+        own.store(slife, j0, own_n);
+        step_decays += kstar;
+        dcnt = own.count_below(0, own_n);
+        incl = wave_inclusive_scan(dcnt, lane);
+        if (lane == 63) sdead[wave] = incl;   // every wave read sdead before the loop's barrier
+        __syncthreads();
+        wbase = 0;
+        for (int w = 0; w < wave; ++w) wbase += sdead[w];
+      }
+      int drank = wbase + incl - dcnt;
+      if (drank < n_g) {
+#pragma unroll
+        for (int e = 0; e < kMaxSPT; ++e)
+          if (e < own_n && own.get(e) < 0 && drank < n_g) somiss[drank++] = j0 + e;
+      }
+      __syncthreads();
+
+      // ---- D: reusable chains on the pre-write table (Algorithm 2) ---------
+      int32_t mt[IPT], mo[IPT], mp[IPT];
+      uint32_t mh[IPT], md[IPT];
+      bool mact[IPT], mv[IPT];
+#pragma unroll
+      for (int u = 0; u < IPT; ++u) {
+        const int k = u * MT + tid;
+        mact[u] = k < n_g;
+        mv[u] = false;
+        mt[u] = mact[u] ? smx[k] : 0;
+        mp[u] = mact[u] ? smp[k] : 0;
+        mo[u] = mact[u] ? (somiss[k] & static_cast<int>(smask)) : 0;
+        const uint32_t ux = static_cast<uint32_t>(mt[u]);
+        mh[u] = (a1 * ux) & smask;
+        md[u] = ((a2 * ux) & smask) | 1u;
+      }
+      for (int rd = 0; rd <= R; ++rd) {
+        bool pending = false;
+        uint32_t qw[IPT];
+#pragma unroll
+        for (int u = 0; u < IPT; ++u)
+          if (mact[u] && !mv[u]) qw[u] = smap[mh[u]];
+        int lf[IPT];
+        int32_t cv[IPT];
+#pragma unroll
+        for (int u = 0; u < IPT; ++u)
+          if (mact[u] && !mv[u]) {
+            const uint32_t o2 = W.slot(qw[u]);
+            lf[u] = slife[o2];
+            cv[u] = sc[o2];
+          }
+#pragma unroll
+        for (int u = 0; u < IPT; ++u)
+          if (mact[u] && !mv[u]) {
+            // reusable (Eq. 4): invalid, pointed slot inactive, or stale fingerprint
+            if (W.invalid(qw[u]) || lf[u] < 0 ||
+                W.fp(qw[u]) != (static_cast<uint32_t>(cv[u]) & fmask)) {
+              mv[u] = true;
+            } else if (rd < R) {
+              mh[u] = (mh[u] + md[u]) & smask;
+              pending = true;
+            }
+          }
+        if (!__ballot(pending)) break;
+      }
+      __syncthreads();
+
+      // ---- E: take the slots, bid for buckets, emit outputs ---------------
+      const size_t lbase = static_cast<size_t>(r) * p.n_q * K + listed;
+#pragma unroll
+      for (int u = 0; u < IPT; ++u) {
+        if (!mact[u]) continue;
+        const int k = u * MT + tid;
+        sc[mo[u]] = mt[u];
+        slife[mo[u]] = static_cast<int8_t>(L);
+        og[mp[u]] = mo[u];                                   // o[not m] = o^miss
+        p.miss_list[lbase + k] = make_int2(mt[u], mo[u]);
+        if (mv[u]) {
+          const uint32_t bid = kBid | (static_cast<uint32_t>(g) << 24) |
+                               (static_cast<uint32_t>(mo[u]) << (23 - m)) |
+                               (static_cast<uint32_t>(mt[u]) & fmask);
+          atomicMax(&smap[mh[u]], bid);
+          bid_h[u] = mh[u];
+          bid_v[u] = bid;
+        } else {
+          st_exh++;
+        }
+      }
+      publish(r, listed, n_g);
+      listed += n_g;
+      __syncthreads();
+    }
+  }
+
+  // installs of the last token that lost their bucket
+#pragma unroll
+  for (int u = 0; u < IPT; ++u)
+    if (bid_v[u] && smap[bid_h[u]] != bid_v[u]) st_col++;
+
+  // End of step: speculative invalidation fused into the write back.
+  int st_inv = 0;
+  for (int j = tid; j < S; j += MT) {
+    int32_t c = sc[j];
+    if (static_cast<int64_t>(c) >= n_verified) {
+      c = -1;
+      st_inv++;
+    }
+    gc[j] = c;
+    gq[j] = (static_cast<uint32_t>(static_cast<uint8_t>(slife[j])) << 24) | W.canonical(smap[j]);
+  }
+
+  int vals[7] = {st_hits, st_miss, st_exh, st_col, st_rev, st_inv, st_bad};
+#pragma unroll
+  for (int k = 0; k < 7; ++k) {
+    const int v = wave_sum(vals[k]);
+    if (lane == 0 && v) atomicAdd(&sstat[k], v);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    unsigned long long* st = p.stats + static_cast<size_t>(r) * kNumStats;
+    st[kStatHits] += static_cast<unsigned long long>(sstat[0]);
+    st[kStatMisses] += static_cast<unsigned long long>(sstat[1]);
+    st[kStatLostExhausted] += static_cast<unsigned long long>(sstat[2]);
+    st[kStatLostCollision] += static_cast<unsigned long long>(sstat[3]);
+    st[kStatRevivals] += static_cast<unsigned long long>(sstat[4]);
+    st[kStatInvalidations] += static_cast<unsigned long long>(sstat[5]);
+    st[kStatBadIndices] += static_cast<unsigned long long>(sstat[6]);
+    st[kStatAllocDecays] += static_cast<unsigned long long>(step_decays);
+    if (static_cast<unsigned long long>(step_decays) > st[kStatMaxStepDecays])
+      st[kStatMaxStepDecays] = static_cast<unsigned long long>(step_decays);
+  }
+}
+
+}  // namespace
+}  // namespace avsg

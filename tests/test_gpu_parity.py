@@ -110,10 +110,11 @@ def test_parity_parameters(retry, max_life):
     run_parity(spec, table_every=4, buffers_every=8, retry=retry, max_life=max_life)
 
 
-@pytest.mark.parametrize("mode", [1, 2, 4], ids=["request_level", "copy_engine", "position_level"])
+@pytest.mark.parametrize("mode", [1, 2, 4, 5],
+                         ids=["request_level", "copy_engine", "position_level", "pipelined"])
 def test_gather_modes_match_balanced(mode):
-    """Request-level (S1), position-level (S2) and copy-engine transfers move
-    the same bytes as the balanced miss-list transfer (S3)."""
+    """Request-level (S1), position-level (S2), copy-engine and pipelined
+    transfers move the same bytes as the balanced miss-list transfer (S3)."""
     spec = W.custom_spec(name=f"mode{mode}", batch=6, topk=512, slots=2048, n_q=2, steps=12,
                          ctx=30000, row_bytes=(1152, 132))
     run_parity(spec, table_every=0, buffers_every=4, gather_mode=mode)
@@ -231,6 +232,40 @@ def test_bad_indices_are_counted_not_copied():
         host.free()
 
 
+PIPELINED_CASES = [
+    ("tiny", None),
+    ("mtp3_ragged", dict(batch=5, topk=300, slots=1024, n_q=3, steps=12, ctx=8000, row_bytes=(1152, 132))),
+    ("all_hits", dict(batch=2, topk=256, slots=1024, n_q=2, steps=8, ctx=256, retention=1.0, overlap=1.0)),
+    ("spec_window", dict(batch=3, topk=256, slots=2048, n_q=3, steps=16, ctx=4096, mode="zipf_window",
+                         window=64, retention=0.8)),
+]
+
+
+@pytest.mark.parametrize("name,kw", PIPELINED_CASES, ids=[c[0] for c in PIPELINED_CASES])
+def test_pipelined_step_parity(name, kw):
+    """Stage One and Stage Two in one launch (chunk queue): same outputs,
+    tables, counters and buffers as the oracle, and no queue time-outs."""
+    spec = W.get_spec("tiny") if kw is None else W.custom_spec(name=name, **kw)
+    ref, got = run_parity(spec, table_every=2, buffers_every=2, miss_list_requests=2, gather_mode=5)
+    assert got["queue_timeouts"] == 0
+
+
+def test_pipelined_batch_limit():
+    """The pipelined step needs every request's producer resident: batch above
+    the CU count is refused at create time."""
+    from paper_2609_37538_amd import avsg as A
+    cus = A.avsg_device_cus()
+    B = cus + 1
+    host = A.HostRegion(B * 64 * 16)
+    cfg = A.make_config(B, 16, 1, 64, row_bytes=(16,), gather_mode=A.AVSG_GATHER_PIPELINED)
+    try:
+        with pytest.raises(A.AvsgError) as e:
+            A.Operator(cfg, [host.ptr + r * 64 * 16 for r in range(B)], [64] * B)
+        assert e.value.status == A.AVSG_E_UNSUPPORTED
+    finally:
+        host.free()
+
+
 # ---- the five benchmark workloads at full size ----------------------------
 @pytest.mark.timeout(900)
 def test_parity_batch16_full():
@@ -240,6 +275,12 @@ def test_parity_batch16_full():
 @pytest.mark.timeout(900)
 def test_parity_batch64_mtp2_full():
     run_parity(W.get_spec("batch64_mtp2"))
+
+
+@pytest.mark.timeout(900)
+def test_parity_batch64_mtp2_full_pipelined():
+    ref, got = run_parity(W.get_spec("batch64_mtp2"), gather_mode=5)
+    assert got["queue_timeouts"] == 0
 
 
 @pytest.mark.timeout(900)
