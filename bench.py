@@ -40,7 +40,7 @@ def parse():
     ap.add_argument("--config", default="batch64_mtp2",
                     choices=["tiny", "batch16", "batch64_mtp2", "imbalance", "stress"])
     ap.add_argument("--gather", default="balanced",
-                    choices=["balanced", "request", "position", "sdma", "none", "pipelined"])
+                    choices=["balanced", "request", "position", "sdma", "none", "pipelined", "resident"])
     ap.add_argument("--match", default="hash", choices=["hash", "dualptr"])
     ap.add_argument("--workers", type=int, default=0, help="gather workgroups (0 = one per CU)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -54,6 +54,9 @@ def parse():
                     help="run the Stage One latency sweeps (S=K=N, K at S=4096, S at K=512) and write them here")
     ap.add_argument("--lifetime-sweep", default="",
                     help="run the maximum-lifetime sweep (L = 1..32) and write it here")
+    ap.add_argument("--config-table", default="",
+                    help="run every workload under every Stage Two strategy (and the dual-pointer "
+                         "ablation where it applies); write JSON rows here")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one device-to-device copy of this many MiB first (counter calibration)")
     return ap.parse_args()
@@ -78,11 +81,15 @@ def main():
     if args.lifetime_sweep:
         lifetime_sweep(args.lifetime_sweep)
         return
+    if args.config_table:
+        config_table(args.config_table)
+        return
 
     gather_mode = {"balanced": A.AVSG_GATHER_BALANCED, "request": A.AVSG_GATHER_REQUEST,
                    "sdma": A.AVSG_GATHER_SDMA, "none": A.AVSG_GATHER_NONE,
                    "position": A.AVSG_GATHER_POSITION,
-                   "pipelined": A.AVSG_GATHER_PIPELINED}[args.gather]
+                   "pipelined": A.AVSG_GATHER_PIPELINED,
+                   "resident": A.AVSG_GATHER_RESIDENT}[args.gather]
     match_mode = {"hash": A.AVSG_MATCH_HASH, "dualptr": A.AVSG_MATCH_DUALPTR}[args.match]
     spec = W.get_spec(args.config)
     if match_mode == A.AVSG_MATCH_DUALPTR:
@@ -130,21 +137,23 @@ def main():
         torch.cuda.synchronize()
         del a, b
 
-    # ---- warmup, then the timed region ----
+    # ---- warmup, then the timed region (HIP events on the step stream from
+    # step 0, so the cold start is reported on its own) ----
+    A.avsg_set_timing(op.h, True)
     for t in range(args.warmup):
         op.step(X_dev[t], N_dev[t] if spec.speculative else None)
     torch.cuda.synchronize()
     before = op.stats()
-    A.avsg_set_timing(op.h, True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for t in range(args.warmup, T):
         op.step(X_dev[t], N_dev[t] if spec.speculative else None)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    match_ms, gather_ms = A.avsg_timing(op.h, args.steps)
+    match_all, gather_all = A.avsg_timing(op.h, T)
     A.avsg_set_timing(op.h, False)
     after = op.stats()
+    match_ms, gather_ms = match_all[args.warmup:], gather_all[args.warmup:]
 
     K = args.steps
     us_per_step = wall / K * 1e6
@@ -153,14 +162,16 @@ def main():
     misses = after["misses"] - before["misses"]
     row_total = sum(spec.row_bytes)
     moved = misses * row_total if gather_mode != A.AVSG_GATHER_NONE else 0
+    host_moved = after["host_bytes"] - before["host_bytes"]
     pipelined = gather_mode == A.AVSG_GATHER_PIPELINED
     if pipelined:
         # one fused launch: its duration is recorded in the matching slot
         gather_ms, match_ms = match_ms, np.zeros_like(match_ms)
+        gather_all, match_all = match_all, np.zeros_like(match_all)
     gather_s = float(np.sum(gather_ms)) * 1e-3
     match_s = float(np.sum(match_ms)) * 1e-3
-    gather_gbps = moved / gather_s / 1e9 if gather_s > 0 and moved else 0.0
-    eff_gbps = moved / wall / 1e9 if moved else 0.0
+    gather_gbps = host_moved / gather_s / 1e9 if gather_s > 0 and host_moved else 0.0
+    eff_gbps = host_moved / wall / 1e9 if host_moved else 0.0
 
     # ---- CPU baseline: the oracle on the same inputs ----
     cpu = None
@@ -189,6 +200,8 @@ def main():
         },
         "hit_rate": round(hits / max(1, lookups), 5),
         "misses_per_step": round(misses / K, 1),
+        "host_rows_per_step": round(host_moved / row_total / K, 1) if row_total else 0.0,
+        "delivered_gbps": round(moved / wall / 1e9, 3) if moved else 0.0,
         "h2d_gbps_effective": round(eff_gbps, 3),
         "h2d_gbps_gather_kernel": round(gather_gbps, 3),
         "hipmemcpy_h2d_peak_gbps": round(memcpy_peak, 3),
@@ -197,10 +210,16 @@ def main():
         "match_us_median": (round(float(np.median(match_ms)) * 1e3, 2)
                             if len(match_ms) and not pipelined else None),
         "gather_us_median": round(float(np.median(gather_ms)) * 1e3, 2) if len(gather_ms) else None,
+        "match_us_p99": (round(float(np.percentile(match_ms, 99)) * 1e3, 2)
+                         if len(match_ms) and not pipelined else None),
+        "gather_us_p99": round(float(np.percentile(gather_ms, 99)) * 1e3, 2) if len(gather_ms) else None,
+        "cold_start_step0_us": ({"match": None if pipelined else round(float(match_all[0]) * 1e3, 2),
+                                 "gather": round(float(gather_all[0]) * 1e3, 2)}
+                                if len(gather_all) == T else None),
         "match_frac_of_step": round(match_s / wall, 4),
         "roofline": {
             "bound": "pcie",
-            "kernel": {"balanced": "gather_balanced_kernel",
+            "kernel": {"balanced": "gather_balanced_kernel", "resident": "gather_balanced_kernel",
                        "pipelined": "step_pipelined_kernel"}.get(args.gather, args.gather),
             "achieved": round(gather_gbps, 3),
             "peak": PCIE_GEN5_X16_GBPS,
@@ -208,7 +227,7 @@ def main():
             "frac": round(gather_gbps / PCIE_GEN5_X16_GBPS, 4),
             "traffic": traffic["traffic_bytes_per_launch"] if traffic else None,
             "traffic_source": TRAFFIC_SUMMARY if traffic else None,
-            "algorithmic_bytes_per_launch": round(moved / K) if moved else 0,
+            "algorithmic_bytes_per_launch": round(host_moved / K) if host_moved else 0,
             "measured_hipmemcpy_peak": round(memcpy_peak, 3),
         },
         "cpu_baseline": cpu,
@@ -387,6 +406,73 @@ def lifetime_sweep(out_path):
         json.dump(results, f, indent=1)
 
 
+def config_table(out_path):
+    """Every workload (tiny, batch16, batch64_mtp2, imbalance, stress) under the
+    balanced (S3), request-level (S1), position-level (S2), pipelined and
+    resident-reuse Stage Two, plus the dual-pointer matching ablation (S = K)
+    on the single-token workloads: 16 warm-up steps from a cold start, then 64
+    timed steps; medians and sums from HIP events on the step stream.
+    gather_gbps = bytes read over the host link / Stage Two time."""
+    import dataclasses
+    import torch
+    import workload as W
+    from paper_2609_37538_amd import avsg as A
+    dev = torch.device("cuda:0")
+    cus = A.avsg_device_cus()
+    warm, timed = 16, 64
+    strategies = [("S3 balanced", A.AVSG_MATCH_HASH, A.AVSG_GATHER_BALANCED),
+                  ("S1 request", A.AVSG_MATCH_HASH, A.AVSG_GATHER_REQUEST),
+                  ("S2 position", A.AVSG_MATCH_HASH, A.AVSG_GATHER_POSITION),
+                  ("pipelined", A.AVSG_MATCH_HASH, A.AVSG_GATHER_PIPELINED),
+                  ("resident reuse + S3", A.AVSG_MATCH_HASH, A.AVSG_GATHER_RESIDENT),
+                  ("dual-pointer + S3", A.AVSG_MATCH_DUALPTR, A.AVSG_GATHER_BALANCED)]
+    results = []
+    for name in ("tiny", "batch16", "batch64_mtp2", "imbalance", "stress"):
+        spec = W.get_spec(name)
+        wl = W.Workload(spec)
+        offs = wl.request_row_offsets()
+        regions, ptrs = [], []
+        for st, rb in enumerate(spec.row_bytes):
+            reg = A.HostRegion(wl.host_rows_total() * rb)
+            W.fill_host(wl, st, reg.ptr)
+            regions.append(reg)
+            ptrs += [reg.ptr + int(offs[r]) * rb for r in range(spec.batch)]
+        for label, mm, gm in strategies:
+            run_spec = spec
+            if mm == A.AVSG_MATCH_DUALPTR:
+                if spec.n_q != 1:
+                    continue
+                run_spec = dataclasses.replace(spec, slots=spec.topk)
+            if gm == A.AVSG_GATHER_PIPELINED and spec.batch > cus:
+                continue
+            match_ms, gather_ms, d = _timed_run(
+                run_spec, dict(row_bytes=spec.row_bytes, match_mode=mm, gather_mode=gm),
+                warm, timed, ptrs, dev, verified=spec.speculative)
+            if gm == A.AVSG_GATHER_PIPELINED:
+                gather_ms, match_ms = match_ms, None
+            moved = d["host_bytes"]
+            gsec = float(np.sum(gather_ms)) * 1e-3
+            row = {"workload": name, "strategy": label, "batch": spec.batch, "topk": spec.topk,
+                   "slots": run_spec.slots, "n_q": spec.n_q,
+                   "hit_rate": round(d["hits"] / max(1, d["lookups"]), 4),
+                   "misses_per_step": round(d["misses"] / timed, 1),
+                   "host_rows_per_step": round(d["host_bytes"] / sum(spec.row_bytes) / timed, 1),
+                   "match_us_median": (round(float(np.median(match_ms)) * 1e3, 2)
+                                       if match_ms is not None else None),
+                   "gather_us_median": round(float(np.median(gather_ms)) * 1e3, 2),
+                   "kernel_us_per_step": round((gsec + (float(np.sum(match_ms)) * 1e-3
+                                                        if match_ms is not None else 0.0))
+                                               / timed * 1e6, 2),
+                   "gather_gbps": round(moved / gsec / 1e9, 3) if gsec > 0 else 0.0,
+                   "lost_installs_per_step": round((d["lost_exhausted"] + d["lost_collision"]) / timed, 1)}
+            results.append(row)
+            print(json.dumps(row), flush=True)
+        for reg in regions:
+            reg.free()
+    with open(out_path, "w") as f:
+        json.dump(results, f, indent=1)
+
+
 GATHER_SOURCES = ("paper_2609_37538_amd/csrc/gather.hip", "paper_2609_37538_amd/csrc/gather_body.h",
                   "paper_2609_37538_amd/csrc/avsg_internal.h")
 TRAFFIC_SUMMARY = "profiles/gather_traffic_batch64_mtp2.md"
@@ -443,6 +529,19 @@ def cpu_baseline(spec, wl, X_host, N_host, host_ptrs, args, gather_mode):
         if t >= first_timed:
             timed += dt
             n_timed += 1
+    # the same oracle on one thread, over a shorter run (cold start + warmup + 8 timed steps)
+    o1 = ORC.Oracle(spec.batch, spec.topk, spec.n_q, spec.slots, nthreads=1)
+    n1 = min(n_run, first_timed + 8)
+    t1 = 0.0
+    for t in range(n1):
+        N = N_host[t] if spec.speculative else None
+        t0 = time.perf_counter()
+        if gather:
+            o1.step(X_host[t], N, host=host_ptrs, buf=bptr, row_bytes=list(spec.row_bytes))
+        else:
+            o1.step(X_host[t], N)
+        if t >= first_timed:
+            t1 += time.perf_counter() - t0
     return {
         "value": round(timed / max(1, n_timed) * 1e6, 1),
         "unit": "us/step",
@@ -450,7 +549,20 @@ def cpu_baseline(spec, wl, X_host, N_host, host_ptrs, args, gather_mode):
         "kind": "oracle",
         "sample": f"{spec.name} steps {first_timed}..{n_run - 1} ({n_timed} steps) after a cold start "
                   f"at step 0, match + Stage Two copy into host images, {threads} OpenMP threads",
+        "single_thread_us_per_step": round(t1 / max(1, n1 - first_timed) * 1e6, 1),
+        "single_thread_sample": f"steps {first_timed}..{n1 - 1} of the same run",
+        "cpu_model": _cpu_model(),
     }
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 if __name__ == "__main__":

@@ -65,6 +65,16 @@ typedef int32_t avsg_status;
 #define AVSG_GATHER_PIPELINED 5 /* Stage One and Stage Two in one launch: each token's misses are queued in
                                    chunks as soon as they are reserved and copied by every CU (hash matching,
                                    batch <= CU count) */
+#define AVSG_GATHER_RESIDENT 6  /* S3 over the misses whose row is not yet on the device, then device-to-device
+                                   copies for the rest (hash matching only).  A miss whose index is still cached
+                                   by a slot of the same request outside this step's reservations (its mapping
+                                   was lost to an exhausted probe chain or a bucket collision, so the probe of
+                                   Eq. 8-11 cannot find it) is filled from that slot; a miss that repeats an
+                                   earlier miss of the same step (same index, a later token) is filled from the
+                                   slot that step's host copy writes.  Slots, counts, tables and buffer contents
+                                   are identical to AVSG_GATHER_BALANCED; only fewer rows cross the host link.
+                                   Relies on the same property as a hit: a cached row below the verified length
+                                   does not change on the host. */
 
 #define AVSG_MAX_STREAMS 2
 
@@ -89,13 +99,16 @@ typedef struct avsg_stats_t {
     uint64_t lookups;         /* selected indices looked up: steps * B * N_q * K */
     uint64_t hits;            /* lookups that found their index resident */
     uint64_t misses;          /* lookups that reserved a slot and caused a copy */
-    uint64_t bytes_moved;     /* host -> device payload bytes, all streams */
+    uint64_t bytes_moved;     /* payload bytes written into the buffers: misses * row bytes, all streams */
     uint64_t lost_exhausted;  /* misses whose R+1 install probes found no reusable bucket */
     uint64_t lost_collision;  /* misses whose bucket install lost to a larger miss rank */
     uint64_t alloc_decays;    /* unit decays done by the allocation loop (Algorithm 1) */
     uint64_t revivals;        /* hits on a slot whose lifetime was negative */
     uint64_t invalidations;   /* cached indices cleared by speculative invalidation */
     uint64_t bad_indices;     /* selected indices outside [0, rows) (skipped by the copy) */
+    uint64_t resident_rows;   /* AVSG_GATHER_RESIDENT: misses filled from a slot that already held the row */
+    uint64_t duplicate_rows;  /* AVSG_GATHER_RESIDENT: misses filled from a same-step miss of the same index */
+    uint64_t host_bytes;      /* payload bytes read over the host link, all streams */
     int32_t max_step_alloc_decays; /* largest allocation-decay count of one request-step */
     int32_t queue_timeouts;   /* pipelined step: consumers that gave up waiting (0 in correct operation) */
 } avsg_stats_t;
@@ -168,6 +181,19 @@ avsg_status avsg_export_state(avsg_handle *h, int32_t r, int32_t *c_out, uint32_
  * then by position inside the token (increasing index order for dual-pointer). */
 avsg_status avsg_export_misses(avsg_handle *h, int32_t r, int32_t *n_out, int32_t *x_out,
                                int32_t *o_out);
+
+/* Stage Two plan of request r from the last step (AVSG_GATHER_RESIDENT only),
+ * copied to host memory (synchronous), each list in transfer-list order:
+ *   n_host, host_x[k], host_o[k]  misses copied from host row host_x[k] into
+ *                                 slot host_o[k] (capacity N_q*K each);
+ *   n_dev, dev_src[k], dev_dst[k] misses filled by copying slot dev_src[k] into
+ *                                 slot dev_dst[k] after the host copies.
+ * The source of a device copy is the largest slot outside this step's
+ * reservations that caches the index (a valid verified row), else the largest
+ * slot this step reserved for the index.  Errors: AVSG_E_INVAL,
+ * AVSG_E_UNSUPPORTED (another gather mode), AVSG_E_HIP. */
+avsg_status avsg_export_plan(avsg_handle *h, int32_t r, int32_t *n_host, int32_t *host_x,
+                             int32_t *host_o, int32_t *n_dev, int32_t *dev_src, int32_t *dev_dst);
 
 /* Per-step kernel timing with HIP events recorded on the step's stream.
  * avsg_set_timing(h, 1) starts recording (and clears the record);

@@ -279,6 +279,54 @@ def phi(m, x) -> int:
     return int(_load().avsg_ref_phi(m, x))
 
 
+def transfer_plan(miss_x, miss_o, c_after, rows_r: int):
+    """Resident-reuse plan of one request-step: which misses must cross the host
+    link.  This is a property of the transfer, not of the paper's method, whose
+    Stage Two copies every miss from the host (Section 3.4); filling a slot from
+    another slot that holds the same row leaves the buffer unchanged.
+
+    Plain definition, for each miss (x, o) of the step's transfer list in order:
+      - x outside [0, rows_r): a host entry (the copy skips it);
+      - else, if some slot j outside this step's reservations caches x after the
+        step (c_after[j] == x; invalidated entries are already -1), a device
+        copy from the largest such j (its row arrived in an earlier step);
+      - else, if the largest slot reserved this step for x is not o, a device
+        copy from that slot (x missed again in a later token of the step);
+      - else a host entry.
+    Returns (host_x, host_o, dev_src, dev_dst, n_resident, n_duplicate).
+    """
+    miss_x = [int(v) for v in miss_x]
+    miss_o = [int(v) for v in miss_o]
+    c_after = np.asarray(c_after)
+    reserved = set(miss_o)
+    wanted = {x for x in miss_x if 0 <= x < rows_r}
+    resident = {}
+    for j in range(len(c_after)):          # ascending, so the largest slot stays
+        x = int(c_after[j])
+        if x in wanted and j not in reserved:
+            resident[x] = j
+    rep = {}
+    for x, o in zip(miss_x, miss_o):
+        if 0 <= x < rows_r:
+            rep[x] = max(rep.get(x, -1), o)
+    host_x, host_o, dev_src, dev_dst = [], [], [], []
+    n_res = n_dup = 0
+    for x, o in zip(miss_x, miss_o):
+        if 0 <= x < rows_r and x in resident:
+            dev_src.append(resident[x])
+            dev_dst.append(o)
+            n_res += 1
+        elif 0 <= x < rows_r and rep[x] != o:
+            dev_src.append(rep[x])
+            dev_dst.append(o)
+            n_dup += 1
+        else:
+            host_x.append(x)
+            host_o.append(o)
+    as32 = lambda v: np.asarray(v, dtype=np.int32)
+    return as32(host_x), as32(host_o), as32(dev_src), as32(dev_dst), n_res, n_dup
+
+
 def partition_balanced(n_miss: int, C: int) -> np.ndarray:
     out = np.empty(C + 1, dtype=np.int64)
     _load().avsg_ref_partition_balanced(n_miss, C, _ptr(out))

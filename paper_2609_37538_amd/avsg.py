@@ -36,6 +36,7 @@ AVSG_GATHER_SDMA = 2
 AVSG_GATHER_NONE = 3
 AVSG_GATHER_POSITION = 4
 AVSG_GATHER_PIPELINED = 5
+AVSG_GATHER_RESIDENT = 6
 AVSG_MAX_STREAMS = 2
 
 A1_DEFAULT = 2654435761
@@ -56,7 +57,8 @@ class AvsgConfig(ctypes.Structure):
 class AvsgStats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_uint64) for n in (
         "steps", "lookups", "hits", "misses", "bytes_moved", "lost_exhausted", "lost_collision",
-        "alloc_decays", "revivals", "invalidations", "bad_indices")] + [
+        "alloc_decays", "revivals", "invalidations", "bad_indices", "resident_rows",
+        "duplicate_rows", "host_bytes")] + [
         ("max_step_alloc_decays", ctypes.c_int32), ("queue_timeouts", ctypes.c_int32)]
 
     def as_dict(self):
@@ -105,6 +107,8 @@ def load():
     lib.avsg_export_state.argtypes = [_P, i32, _P, _P]
     lib.avsg_export_misses.restype = i32
     lib.avsg_export_misses.argtypes = [_P, i32, _P, _P, _P]
+    lib.avsg_export_plan.restype = i32
+    lib.avsg_export_plan.argtypes = [_P, i32, _P, _P, _P, _P, _P, _P]
     lib.avsg_set_timing.restype = i32
     lib.avsg_set_timing.argtypes = [_P, i32]
     lib.avsg_timing.restype = i32
@@ -206,6 +210,17 @@ def avsg_export_state(h, r: int, slots: int):
     _check(load().avsg_export_state(h, r, c.ctypes.data_as(_P), q.ctypes.data_as(_P)),
            "avsg_export_state", h)
     return c, q
+
+
+def avsg_export_plan(h, r: int, capacity: int):
+    """(host_x, host_o, dev_src, dev_dst) of request r's last Stage Two plan."""
+    nh = ctypes.c_int32(0)
+    nd = ctypes.c_int32(0)
+    hx, ho, ds, dd = (np.empty(capacity, dtype=np.int32) for _ in range(4))
+    _check(load().avsg_export_plan(h, r, ctypes.byref(nh), hx.ctypes.data_as(_P), ho.ctypes.data_as(_P),
+                                   ctypes.byref(nd), ds.ctypes.data_as(_P), dd.ctypes.data_as(_P)),
+           "avsg_export_plan", h)
+    return hx[: nh.value].copy(), ho[: nh.value].copy(), ds[: nd.value].copy(), dd[: nd.value].copy()
 
 
 def avsg_export_misses(h, r: int, capacity: int):
@@ -334,6 +349,9 @@ class Operator:
 
     def export_misses(self, r: int):
         return avsg_export_misses(self.h, r, self.cfg.n_q * self.cfg.topk)
+
+    def export_plan(self, r: int):
+        return avsg_export_plan(self.h, r, self.cfg.n_q * self.cfg.topk)
 
     def close(self):
         if getattr(self, "h", None):

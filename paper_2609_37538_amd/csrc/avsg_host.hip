@@ -28,6 +28,10 @@ struct avsg_handle {
   int2* dp_state = nullptr;
   int2* miss_list = nullptr;
   uint8_t* hit_mask = nullptr;
+  int2* host_list = nullptr;    // resident-reuse plan (AVSG_GATHER_RESIDENT)
+  int2* dev_list = nullptr;
+  int32_t* plan_counts = nullptr;
+  int plan_words = 0;
   int* pipe_ctl = nullptr;      // head, tail, done, exit_count, error
   int4* pipe_chunks = nullptr;
   int pipe_max_chunks = 0;
@@ -75,7 +79,8 @@ bool is_prime_u32(uint32_t v) {
 size_t pipe_chunks_for(const avsg_config& c);
 
 struct Layout {
-  size_t table_c, table_q, miss_list, hit_mask, pipe, pipe_bytes, stats, host_ptrs, buf_ptrs, rows, total;
+  size_t table_c, table_q, miss_list, hit_mask, plan, pipe, pipe_bytes, stats, host_ptrs, buf_ptrs, rows,
+      total;
 };
 
 Layout layout_of(const avsg_config& c) {
@@ -86,6 +91,9 @@ Layout layout_of(const avsg_config& c) {
   L.table_q = off; off += up(B * S * 4);
   L.miss_list = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk * 8);
   L.hit_mask = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk);
+  L.plan = off;
+  if (c.gather_mode == AVSG_GATHER_RESIDENT)   // host list, device list, counts
+    off += 2 * up(B * static_cast<size_t>(c.n_q) * c.topk * 8) + up(B * 8);
   L.pipe = off;
   L.pipe_bytes = up(kAlign + 16 * pipe_chunks_for(c));
   off += L.pipe_bytes;
@@ -133,20 +141,23 @@ avsg_status check_config(const avsg_config* c, std::string* why) {
   if (c->gather_workers < 0) return fail(AVSG_E_INVAL, "gather_workers must be >= 0");
   if (c->match_mode != AVSG_MATCH_HASH && c->match_mode != AVSG_MATCH_DUALPTR)
     return fail(AVSG_E_INVAL, "unknown match_mode");
-  if (c->gather_mode < AVSG_GATHER_BALANCED || c->gather_mode > AVSG_GATHER_PIPELINED)
+  if (c->gather_mode < AVSG_GATHER_BALANCED || c->gather_mode > AVSG_GATHER_RESIDENT)
     return fail(AVSG_E_INVAL, "unknown gather_mode");
   if (c->match_mode == AVSG_MATCH_DUALPTR) {
     if (c->n_q != 1) return fail(AVSG_E_UNSUPPORTED, "dual-pointer matching handles one token per step");
     if (c->slots != c->topk) return fail(AVSG_E_UNSUPPORTED, "dual-pointer matching needs slots == topk");
     if (c->topk > 4096) return fail(AVSG_E_CAPACITY, "dual-pointer matching supports topk <= 4096");
-    if (c->gather_mode == AVSG_GATHER_POSITION || c->gather_mode == AVSG_GATHER_PIPELINED)
-      return fail(AVSG_E_UNSUPPORTED, "position-level and pipelined transfer need hash matching");
+    if (c->gather_mode == AVSG_GATHER_POSITION || c->gather_mode == AVSG_GATHER_PIPELINED ||
+        c->gather_mode == AVSG_GATHER_RESIDENT)
+      return fail(AVSG_E_UNSUPPORTED, "position-level, pipelined and resident-reuse transfer need hash matching");
   } else {
     const size_t lds = c->gather_mode == AVSG_GATHER_PIPELINED
                            ? pipelined_lds_bytes(c->slots, c->topk)
                            : match_lds_bytes(c->slots, c->topk);
     if (match_lds_bytes(c->slots, c->topk) == 0 || lds > kLdsPerWorkgroup)
       return fail(AVSG_E_CAPACITY, "table and selection exceed one workgroup's LDS (9*S + 12*K bytes)");
+    if (c->gather_mode == AVSG_GATHER_RESIDENT && plan_map_words(c->slots, c->topk, c->n_q) == 0)
+      return fail(AVSG_E_CAPACITY, "resident-reuse plan: the index map of 1.5*n_q*topk words does not fit in LDS");
   }
   return AVSG_OK;
 }
@@ -247,6 +258,13 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
   h->dp_state = reinterpret_cast<int2*>(ws + L.table_c);  // S == K: the two table arrays hold [B][K] pairs
   h->miss_list = reinterpret_cast<int2*>(ws + L.miss_list);
   h->hit_mask = ws + L.hit_mask;
+  if (c.gather_mode == AVSG_GATHER_RESIDENT) {
+    const size_t list = up(static_cast<size_t>(B) * c.n_q * c.topk * 8);
+    h->host_list = reinterpret_cast<int2*>(ws + L.plan);
+    h->dev_list = reinterpret_cast<int2*>(ws + L.plan + list);
+    h->plan_counts = reinterpret_cast<int32_t*>(ws + L.plan + 2 * list);
+    h->plan_words = plan_map_words(c.slots, c.topk, c.n_q);
+  }
   h->pipe_ctl = reinterpret_cast<int*>(ws + L.pipe);
   h->pipe_chunks = reinterpret_cast<int4*>(ws + L.pipe + kAlign);
   h->pipe_max_chunks = static_cast<int>(pipe_chunks_for(c));
@@ -335,7 +353,8 @@ static avsg_status record(avsg_handle* h, int which, hipStream_t s) {
   if (!h->timing || h->n_timed >= kMaxTimedSteps) return AVSG_OK;
   if (h->events.size() <= h->n_timed) {
     std::array<hipEvent_t, 3> ev{};
-    for (auto& x : ev) HIP_TRY(h, hipEventCreate(&x));
+    // timing-only events: no system-scope cache write-back/invalidate at record
+    for (auto& x : ev) HIP_TRY(h, hipEventCreateWithFlags(&x, hipEventDisableSystemFence));
     h->events.push_back(ev);
   }
   HIP_TRY(h, hipEventRecord(h->events[h->n_timed][which], s));
@@ -396,7 +415,8 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
     p.stats = h->stats; p.hit_mask = nullptr;
     GatherParams g{};
     g.B = c.batch; g.n_q = c.n_q; g.K = c.topk; g.S = c.slots;
-    g.miss_counts = d_miss_counts; g.miss_list = h->miss_list; g.rows = h->rows_dev;
+    g.miss_counts = d_miss_counts; g.counts_per_req = c.n_q; g.count_stride = c.n_q;
+    g.miss_list = h->miss_list; g.rows = h->rows_dev;
     g.n_streams = c.n_streams; g.host_ptrs = h->host_ptrs; g.buf_ptrs = h->buf_ptrs;
     g.row_bytes0 = c.row_bytes[0];
     g.row_bytes1 = c.n_streams > 1 ? c.row_bytes[1] : 0;
@@ -424,6 +444,12 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
     p.slots_out = d_slots; p.miss_counts = d_miss_counts; p.miss_list = h->miss_list;
     p.stats = h->stats;
     p.hit_mask = c.gather_mode == AVSG_GATHER_POSITION ? h->hit_mask : nullptr;
+    if (c.gather_mode == AVSG_GATHER_RESIDENT) {
+      p.plan_words = h->plan_words;
+      p.host_list = h->host_list;
+      p.dev_list = h->dev_list;
+      p.plan_counts = h->plan_counts;
+    }
     HIP_TRY(h, launch_match_hash(p, h->lds, s));
   } else {
     DualPtrParams p{};
@@ -435,7 +461,8 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
   if ((rc = record(h, 1, s)) != AVSG_OK) return rc;
   GatherParams g{};
   g.B = c.batch; g.n_q = c.n_q; g.K = c.topk; g.S = c.slots;
-  g.miss_counts = d_miss_counts; g.miss_list = h->miss_list; g.rows = h->rows_dev;
+  g.miss_counts = d_miss_counts; g.counts_per_req = c.n_q; g.count_stride = c.n_q;
+  g.miss_list = h->miss_list; g.rows = h->rows_dev;
   g.n_streams = c.n_streams; g.host_ptrs = h->host_ptrs; g.buf_ptrs = h->buf_ptrs;
   g.row_bytes0 = c.row_bytes[0];
   g.row_bytes1 = c.n_streams > 1 ? c.row_bytes[1] : 0;
@@ -444,6 +471,16 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
     case AVSG_GATHER_BALANCED: HIP_TRY(h, launch_gather_balanced(g, h->workers, s)); break;
     case AVSG_GATHER_REQUEST: HIP_TRY(h, launch_gather_request(g, s)); break;
     case AVSG_GATHER_POSITION: HIP_TRY(h, launch_gather_position(g, h->workers, s)); break;
+    case AVSG_GATHER_RESIDENT: {
+      // host rows first (balanced over the host list), then the device copies
+      g.miss_counts = h->plan_counts; g.counts_per_req = 1; g.count_stride = 2;
+      g.miss_list = h->host_list;
+      HIP_TRY(h, launch_gather_balanced(g, h->workers, s));
+      g.miss_counts = h->plan_counts + 1;
+      g.miss_list = h->dev_list;
+      HIP_TRY(h, launch_copy_device(g, h->workers, s));
+      break;
+    }
     case AVSG_GATHER_SDMA:
       if ((rc = sdma_gather(h, d_miss_counts, s)) != AVSG_OK) return rc;
       break;
@@ -475,6 +512,8 @@ avsg_status avsg_stats(avsg_handle* h, avsg_stats_t* out) {
     out->revivals += s[kStatRevivals];
     out->invalidations += s[kStatInvalidations];
     out->bad_indices += s[kStatBadIndices];
+    out->resident_rows += s[kStatResident];
+    out->duplicate_rows += s[kStatDuplicate];
     max_dec = std::max<uint64_t>(max_dec, s[kStatMaxStepDecays]);
   }
   out->max_step_alloc_decays = static_cast<int32_t>(max_dec);
@@ -490,6 +529,9 @@ avsg_status avsg_stats(avsg_handle* h, avsg_stats_t* out) {
   uint64_t rb = 0;
   for (int s = 0; s < c.n_streams; ++s) rb += static_cast<uint64_t>(c.row_bytes[s]);
   out->bytes_moved = c.gather_mode == AVSG_GATHER_NONE ? 0 : out->misses * rb;
+  out->host_bytes = c.gather_mode == AVSG_GATHER_NONE
+                        ? 0
+                        : (out->misses - out->resident_rows - out->duplicate_rows) * rb;
   return AVSG_OK;
 }
 
@@ -550,6 +592,43 @@ avsg_status avsg_export_misses(avsg_handle* h, int32_t r, int32_t* n_out, int32_
     o_out[k] = ml[k].y;
   }
   *n_out = static_cast<int32_t>(tot);
+  return AVSG_OK;
+}
+
+avsg_status avsg_export_plan(avsg_handle* h, int32_t r, int32_t* n_host, int32_t* host_x,
+                             int32_t* host_o, int32_t* n_dev, int32_t* dev_src, int32_t* dev_dst) {
+  if (!h || !n_host || !host_x || !host_o || !n_dev || !dev_src || !dev_dst || r < 0 ||
+      r >= h->cfg.batch)
+    return AVSG_E_INVAL;
+  const avsg_config& c = h->cfg;
+  if (c.gather_mode != AVSG_GATHER_RESIDENT) return AVSG_E_UNSUPPORTED;
+  *n_host = 0;
+  *n_dev = 0;
+  if (!h->last_counts) return AVSG_OK;
+  HIP_TRY(h, hipStreamSynchronize(h->last_stream));
+  int32_t cnt[2] = {0, 0};
+  HIP_TRY(h, hipMemcpy(cnt, h->plan_counts + 2 * static_cast<size_t>(r), sizeof(cnt),
+                       hipMemcpyDeviceToHost));
+  const int64_t cap = static_cast<int64_t>(c.n_q) * c.topk;
+  if (cnt[0] < 0 || cnt[1] < 0 || cnt[0] + static_cast<int64_t>(cnt[1]) > cap) return AVSG_E_INTERNAL;
+  const size_t base = static_cast<size_t>(r) * c.n_q * c.topk;
+  std::vector<int2> v(static_cast<size_t>(std::max(cnt[0], cnt[1])));
+  if (cnt[0] > 0)
+    HIP_TRY(h, hipMemcpy(v.data(), h->host_list + base, static_cast<size_t>(cnt[0]) * 8,
+                         hipMemcpyDeviceToHost));
+  for (int k = 0; k < cnt[0]; ++k) {
+    host_x[k] = v[k].x;
+    host_o[k] = v[k].y;
+  }
+  if (cnt[1] > 0)
+    HIP_TRY(h, hipMemcpy(v.data(), h->dev_list + base, static_cast<size_t>(cnt[1]) * 8,
+                         hipMemcpyDeviceToHost));
+  for (int k = 0; k < cnt[1]; ++k) {
+    dev_src[k] = v[k].x;
+    dev_dst[k] = v[k].y;
+  }
+  *n_host = cnt[0];
+  *n_dev = cnt[1];
   return AVSG_OK;
 }
 

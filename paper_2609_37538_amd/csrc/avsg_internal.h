@@ -24,6 +24,8 @@ enum StatIndex : int {
   kStatInvalidations,
   kStatBadIndices,
   kStatMaxStepDecays,
+  kStatResident,
+  kStatDuplicate,
   kNumStats
 };
 
@@ -44,12 +46,19 @@ struct MatchParams {
   int2* miss_list;              // [B][n_q*K]  (index, slot)
   unsigned long long* stats;    // [B][kNumStats]
   uint8_t* hit_mask;            // [B][n_q][K] 1 = hit, or nullptr (not written)
+  // Stage Two plan of the resident-reuse gather (written when plan_words > 0)
+  int32_t plan_words;           // words of the end-of-step index map in LDS
+  int2* host_list;              // [B][n_q*K] (index, slot) copied from the host
+  int2* dev_list;               // [B][n_q*K] (source slot, slot) copied on the device
+  int32_t* plan_counts;         // [B][2] host entries, device entries
 };
 
 struct GatherParams {
   int32_t B, n_q, K, S;
-  const int32_t* miss_counts;   // [B][n_q]
-  const int2* miss_list;        // [B][n_q*K]
+  // entry counts of request r: miss_counts[r * count_stride + g], g < counts_per_req
+  const int32_t* miss_counts;
+  int32_t counts_per_req, count_stride;
+  const int2* miss_list;        // [B][n_q*K] (index or source slot, slot)
   const int64_t* rows;          // [B]
   int32_t n_streams;
   const uint64_t* host_ptrs;    // [n_streams][B] device-visible addresses of host row 0
@@ -96,6 +105,11 @@ hipError_t launch_zero_u64(unsigned long long* p, size_t n, hipStream_t s);
 hipError_t launch_gather_balanced(const GatherParams& p, int workers, hipStream_t s);
 hipError_t launch_gather_request(const GatherParams& p, hipStream_t s);
 hipError_t launch_gather_position(const GatherParams& p, int workers, hipStream_t s);
+// device-to-device row copies: miss_list entries are (source slot, slot)
+hipError_t launch_copy_device(const GatherParams& p, int workers, hipStream_t s);
+// words of the end-of-step index map the matching kernel can hold for (S, K, n_q);
+// 0 when the plan does not fit in the kernel's LDS
+int plan_map_words(int S, int K, int n_q);
 int pipelined_chunk_misses();
 size_t pipelined_lds_bytes(int S, int K);
 hipError_t prepare_step_pipelined(size_t lds);

@@ -11,7 +11,9 @@
 // the 132-byte indexer-key rows), several loads in flight per lane.  The
 // position kernel (S2, Eq. 14) splits the flattened N_g*K selected positions
 // into C near-equal contiguous ranges; hit positions issue no copy but still
-// occupy their worker's share.
+// occupy their worker's share.  The device-copy kernel fills the misses whose
+// row is already in the request's buffer (resident-reuse plan of the matching
+// kernel) with the same balanced split, after the host copies.
 #include "gather_body.h"
 
 namespace avsg {
@@ -26,7 +28,21 @@ __global__ __launch_bounds__(GT) void gather_balanced_kernel(GatherParams p) {
   const long long C = gridDim.x, w = blockIdx.x;
   const long long a = (w * N) / C;          // Eq. 6: consecutive, floor/ceil(N/C) each
   const long long b = ((w + 1) * N) / C;
-  copy_range(p, pre, a, b, src0, dst0, src1, dst1);
+  copy_range<false>(p, pre, a, b, src0, dst0, src1, dst1);
+}
+
+// Device-to-device row copies (source slot -> slot) over the same balanced
+// split; runs after the host copies of the step, so every source holds its row.
+__global__ __launch_bounds__(GT) void copy_device_kernel(GatherParams p) {
+  __shared__ long long pre[kMaxBatch + 1];
+  __shared__ long long wtot[GT / 64];
+  __shared__ uint64_t src0[TILE], dst0[TILE], src1[TILE], dst1[TILE];
+  request_prefix(p, pre, wtot);
+  const long long N = pre[p.B];
+  const long long C = gridDim.x, w = blockIdx.x;
+  const long long a = (w * N) / C;
+  const long long b = ((w + 1) * N) / C;
+  copy_range<true>(p, pre, a, b, src0, dst0, src1, dst1);
 }
 
 __global__ __launch_bounds__(GT) void gather_position_kernel(GatherParams p) {
@@ -62,7 +78,7 @@ __global__ __launch_bounds__(GT) void gather_request_kernel(GatherParams p) {
   __shared__ uint64_t src0[TILE], dst0[TILE], src1[TILE], dst1[TILE];
   request_prefix(p, pre, wtot);
   const int r = blockIdx.x;                 // Eq. 13: one worker per request
-  copy_range(p, pre, pre[r], pre[r + 1], src0, dst0, src1, dst1);
+  copy_range<false>(p, pre, pre[r], pre[r + 1], src0, dst0, src1, dst1);
 }
 
 }  // namespace
@@ -70,6 +86,12 @@ __global__ __launch_bounds__(GT) void gather_request_kernel(GatherParams p) {
 hipError_t launch_gather_balanced(const GatherParams& p, int workers, hipStream_t s) {
   if (p.B > kMaxBatch || workers < 1) return hipErrorInvalidValue;
   hipLaunchKernelGGL(gather_balanced_kernel, dim3(workers), dim3(GT), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_device(const GatherParams& p, int workers, hipStream_t s) {
+  if (workers < 1 || p.B > kMaxBatch) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(copy_device_kernel, dim3(workers), dim3(GT), 0, s, p);
   return hipGetLastError();
 }
 

@@ -27,7 +27,8 @@ __device__ void request_prefix(const GatherParams& p, long long* pre, long long*
     const int r = r0 + k;
     if (r < p.B) {
       long long t = 0;
-      for (int g = 0; g < p.n_q; ++g) t += p.miss_counts[static_cast<size_t>(r) * p.n_q + g];
+      for (int g = 0; g < p.counts_per_req; ++g)
+        t += p.miss_counts[static_cast<size_t>(r) * p.count_stride + g];
       pre[r + 1] = t;
       local += t;
     }
@@ -113,7 +114,9 @@ __device__ void copy_tile_rows(const GatherParams& p, int tn, uint64_t* src0, ui
   __syncthreads();
 }
 
-// Copy misses [a, b) of the batch-wide list.
+// Copy entries [a, b) of the batch-wide list.  kDevice: an entry is (source
+// slot, slot) of the request's own buffers; otherwise (host row, slot).
+template <bool kDevice>
 __device__ void copy_range(const GatherParams& p, const long long* pre, long long a, long long b,
                            uint64_t* src0, uint64_t* dst0, uint64_t* src1, uint64_t* dst1) {
   const size_t per_req = static_cast<size_t>(p.n_q) * p.K;
@@ -123,11 +126,14 @@ __device__ void copy_range(const GatherParams& p, const long long* pre, long lon
       const long long j = t0 + i;
       const int r = find_request(pre, p.B, j);
       const int2 e = p.miss_list[static_cast<size_t>(r) * per_req + static_cast<size_t>(j - pre[r])];
-      const bool ok = e.x >= 0 && static_cast<int64_t>(e.x) < p.rows[r] && e.y >= 0 && e.y < p.S;
-      src0[i] = ok ? p.host_ptrs[r] + static_cast<uint64_t>(e.x) * p.row_bytes0 : 0;
+      const bool ok = e.x >= 0 && e.y >= 0 && e.y < p.S &&
+                      (kDevice ? e.x < p.S : static_cast<int64_t>(e.x) < p.rows[r]);
+      const uint64_t base0 = kDevice ? p.buf_ptrs[r] : p.host_ptrs[r];
+      src0[i] = ok ? base0 + static_cast<uint64_t>(e.x) * p.row_bytes0 : 0;
       dst0[i] = p.buf_ptrs[r] + static_cast<uint64_t>(e.y) * p.row_bytes0;
       if (p.n_streams > 1) {
-        src1[i] = ok ? p.host_ptrs[p.B + r] + static_cast<uint64_t>(e.x) * p.row_bytes1 : 0;
+        const uint64_t base1 = kDevice ? p.buf_ptrs[p.B + r] : p.host_ptrs[p.B + r];
+        src1[i] = ok ? base1 + static_cast<uint64_t>(e.x) * p.row_bytes1 : 0;
         dst1[i] = p.buf_ptrs[p.B + r] + static_cast<uint64_t>(e.y) * p.row_bytes1;
       }
     }

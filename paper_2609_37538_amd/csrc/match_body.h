@@ -112,6 +112,152 @@ struct Own {
   }
 };
 
+// Words of LDS bookkeeping of the end-of-step plan besides the reservation
+// bitmap and the index map: per-wave counts of two compaction rounds + totals.
+constexpr int kPlanMiscWords = 4 * MW + 4;
+constexpr uint32_t kPlanResident = 0x80000000u;   // map word names a slot outside this step's reservations
+
+// Home word of index x in the plan's map of P words (multiplicative hash).
+__device__ __forceinline__ uint32_t plan_home(int32_t x, uint32_t P) {
+  return static_cast<uint32_t>((static_cast<uint64_t>(static_cast<uint32_t>(x) * 0x9E3779B1u) * P) >> 32);
+}
+
+// Stage Two plan of the resident-reuse gather, after the step's table write
+// back (every LDS array but c[] is free).  Each of the step's listed misses
+// (index x, slot o) becomes
+//   a host copy, unless
+//   a device copy from the largest slot outside this step's reservations that
+//   still caches x below the verified length (its row arrived in an earlier
+//   step and cannot have changed), or else
+//   a device copy from the largest slot this step reserved for x, when that is
+//   not o (a later token missed x again after its install was lost).
+// LDS map: P words, open addressing with linear probing keyed by the index a
+// word names through c[]; a word is (resident bit | slot + 1), 0 = empty, and
+// atomicMax makes the choice deterministic.  The map holds at most N_q * K keys
+// and P >= 1.5 N_q K, so every probe sequence ends at an empty word.
+__device__ __forceinline__ void plan_request(const MatchParams& p, const int r, unsigned char* lds,
+                                          const int listed, const int64_t rows_r,
+                                          const int64_t n_verified) {
+  const int S = p.S;
+  const int32_t* sc = reinterpret_cast<const int32_t*>(lds);
+  uint32_t* sres = reinterpret_cast<uint32_t*>(lds + 4 * static_cast<size_t>(S));  // reserved-slot bitmap
+  const int nb = (S + 31) >> 5;
+  const uint32_t P = static_cast<uint32_t>(p.plan_words);
+  uint32_t* smp = sres + nb;                                        // [P] index map
+  int* scnt = reinterpret_cast<int*>(smp + P);                      // [kPlanMiscWords]
+  const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
+  const size_t lb = static_cast<size_t>(r) * p.n_q * p.K;
+  const int2* ml = p.miss_list + lb;
+
+  for (int j = tid; j < nb + static_cast<int>(P) + kPlanMiscWords; j += MT) sres[j] = 0u;
+  __syncthreads();
+
+  // (1) mark this step's reservations; one map word per distinct valid index
+  for (int e = tid; e < listed; e += MT) {
+    const int2 v = ml[e];
+    if (v.y < 0 || v.y >= S) continue;
+    atomicOr(&sres[v.y >> 5], 1u << (v.y & 31));
+    if (v.x < 0 || static_cast<int64_t>(v.x) >= rows_r) continue;
+    const uint32_t val = static_cast<uint32_t>(v.y) + 1u;
+    uint32_t h = plan_home(v.x, P);
+    for (uint32_t t = 0; t < P; ++t) {
+      const uint32_t w = atomicCAS(&smp[h], 0u, val);
+      if (w == 0u) break;
+      if (sc[(w & ~kPlanResident) - 1u] == v.x) {
+        atomicMax(&smp[h], val);
+        break;
+      }
+      h = (h + 1u == P) ? 0u : h + 1u;
+    }
+  }
+  __syncthreads();
+
+  // (2) slots outside the reservations that cache one of those indices
+  for (int j = tid; j < S; j += MT) {
+    const int32_t x = sc[j];
+    if (x < 0 || static_cast<int64_t>(x) >= rows_r || static_cast<int64_t>(x) >= n_verified) continue;
+    if ((sres[j >> 5] >> (j & 31)) & 1u) continue;
+    uint32_t h = plan_home(x, P);
+    for (uint32_t t = 0; t < P; ++t) {
+      const uint32_t w = smp[h];
+      if (w == 0u) break;
+      if (sc[(w & ~kPlanResident) - 1u] == x) {
+        atomicMax(&smp[h], kPlanResident | (static_cast<uint32_t>(j) + 1u));
+        break;
+      }
+      h = (h + 1u == P) ? 0u : h + 1u;
+    }
+  }
+  __syncthreads();
+
+  // (3) classify in transfer-list order and compact the two lists
+  int n_host = 0, n_dev = 0, my_res = 0, my_dup = 0;
+  for (int e0 = 0, it = 0; e0 < listed; e0 += MT, ++it) {
+    const int e = e0 + tid;
+    int kind = -1;                 // 0 host, 1 resident slot, 2 same-step slot
+    int2 v = make_int2(0, 0);
+    int src = 0;
+    if (e < listed) {
+      v = ml[e];
+      kind = 0;
+      if (v.x >= 0 && static_cast<int64_t>(v.x) < rows_r) {
+        uint32_t h = plan_home(v.x, P);
+        for (uint32_t t = 0; t < P; ++t) {
+          const uint32_t w = smp[h];
+          if (w == 0u) break;
+          const int o = static_cast<int>(w & ~kPlanResident) - 1;
+          if (sc[o] == v.x) {
+            if (w & kPlanResident) {
+              kind = 1;
+              src = o;
+            } else if (o != v.y) {
+              kind = 2;
+              src = o;
+            }
+            break;
+          }
+          h = (h + 1u == P) ? 0u : h + 1u;
+        }
+      }
+    }
+    my_res += kind == 1 ? 1 : 0;
+    my_dup += kind == 2 ? 1 : 0;
+    const uint64_t mh = __ballot(kind == 0), md = __ballot(kind > 0);
+    int* wc = scnt + (it & 1) * 2 * MW;
+    if (lane == 0) {
+      wc[wave] = __popcll(mh);
+      wc[MW + wave] = __popcll(md);
+    }
+    __syncthreads();
+    int bh = 0, bd = 0, th = 0, td = 0;
+    for (int w = 0; w < MW; ++w) {
+      const int ch = wc[w], cd = wc[MW + w];
+      th += ch;
+      td += cd;
+      bh += (w < wave) ? ch : 0;
+      bd += (w < wave) ? cd : 0;
+    }
+    if (kind == 0) p.host_list[lb + n_host + bh + bits_below(mh)] = v;
+    else if (kind > 0) p.dev_list[lb + n_dev + bd + bits_below(md)] = make_int2(src, v.y);
+    n_host += th;
+    n_dev += td;
+  }
+  my_res = wave_sum(my_res);
+  my_dup = wave_sum(my_dup);
+  if (lane == 0) {
+    if (my_res) atomicAdd(&scnt[4 * MW], my_res);
+    if (my_dup) atomicAdd(&scnt[4 * MW + 1], my_dup);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    p.plan_counts[2 * static_cast<size_t>(r)] = n_host;
+    p.plan_counts[2 * static_cast<size_t>(r) + 1] = n_dev;
+    unsigned long long* st = p.stats + static_cast<size_t>(r) * kNumStats;
+    st[kStatResident] += static_cast<unsigned long long>(scnt[4 * MW]);
+    st[kStatDuplicate] += static_cast<unsigned long long>(scnt[4 * MW + 1]);
+  }
+}
+
 // Stage One for request r (Algorithm 4's token loop) in workgroup-owned LDS.
 // After each token with misses, publish(r, first, count) is called by every
 // thread once the token's transfer-list entries are written (a no-op for the
@@ -445,6 +591,10 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
     st[kStatAllocDecays] += static_cast<unsigned long long>(step_decays);
     if (static_cast<unsigned long long>(step_decays) > st[kStatMaxStepDecays])
       st[kStatMaxStepDecays] = static_cast<unsigned long long>(step_decays);
+  }
+  if (p.plan_words > 0) {
+    __syncthreads();   // the counter reduction above is read before its LDS is reused
+    plan_request(p, r, lds, listed, rows_r, n_verified);
   }
 }
 

@@ -28,7 +28,9 @@
 //      mapping by every later reader and is rewritten in the canonical Eq. 3
 //      layout when the table goes back to HBM.
 // After the last token, speculative invalidation (c_j >= N -> -1) is fused
-// into the write back.
+// into the write back.  With the resident-reuse gather the workgroup then
+// plans Stage Two (plan_request): which misses need the host link and which
+// can be filled from a slot that already holds their row.
 #include "match_body.h"
 
 namespace avsg {
@@ -68,6 +70,18 @@ size_t match_lds_bytes(int S, int K) {
   if (ipt < 1 || ipt > kMaxIPT || S > kMaxSPT * MT) return 0;
   return 8 * static_cast<size_t>(S) + align16(S) + 12 * static_cast<size_t>(K) +
          4 * static_cast<size_t>(kScratchInts);
+}
+
+int plan_map_words(int S, int K, int n_q) {
+  const size_t lds = match_lds_bytes(S, K);
+  if (lds == 0 || n_q < 1) return 0;
+  // every array but c[] (4 S bytes) is free once the table is written back
+  const long long words = static_cast<long long>((lds - 4 * static_cast<size_t>(S)) / 4) -
+                          (S + 31) / 32 - kPlanMiscWords;
+  const long long keys = static_cast<long long>(n_q) * K;
+  long long P = words < 4 * keys ? words : 4 * keys;
+  if (P < (3 * keys + 1) / 2) return 0;   // keep the map at most two-thirds full
+  return static_cast<int>(P);
 }
 
 hipError_t prepare_match_hash(size_t lds) {

@@ -140,6 +140,9 @@ def run_parity(spec: W.Spec, steps: Optional[int] = None, table_every: int = 16,
     host = HostRows(wl, coherent=coherent)
     orc = OracleSide(wl, host, retry=retry, max_life=max_life)
     gpu = GpuSide(wl, host, retry=retry, max_life=max_life, gather_mode=gather_mode)
+    from paper_2609_37538_amd import avsg as A
+    resident = gather_mode == A.AVSG_GATHER_RESIDENT
+    want_res = want_dup = 0
     t0 = time.time()
     try:
         for t in range(T):
@@ -154,6 +157,20 @@ def run_parity(spec: W.Spec, steps: Optional[int] = None, table_every: int = 16,
                 mx, mo = orc.o.misses(rr, n_ref[rr])
                 gx, go = gpu.op.export_misses(rr)
                 assert np.array_equal(mx, gx) and np.array_equal(mo, go), f"step {t} request {rr} miss list"
+            if resident:
+                sampled = {(r * 7 + t) % spec.batch for r in range(min(miss_list_requests, spec.batch))}
+                for r in range(spec.batch):
+                    mx, mo = orc.o.misses(r, n_ref[r])
+                    c_ref, _ = orc.o.export(r)
+                    plan = ORC.transfer_plan(mx, mo, c_ref, int(wl.ctx[r]))
+                    want_res += plan[4]
+                    want_dup += plan[5]
+                    if r in sampled:
+                        got = gpu.op.export_plan(r)
+                        for k, name in enumerate(("host index", "host slot", "device source",
+                                                  "device slot")):
+                            assert np.array_equal(plan[k], got[k]), \
+                                f"step {t} request {r}: plan {name} list differs"
             last = t == T - 1
             if last or (table_every and t % table_every == 0):
                 for r in range(spec.batch):
@@ -173,6 +190,12 @@ def run_parity(spec: W.Spec, steps: Optional[int] = None, table_every: int = 16,
         for k in ("hits", "misses", "lost_exhausted", "lost_collision", "alloc_decays", "revivals",
                   "invalidations", "max_step_alloc_decays"):
             assert ref[k] == got[k], f"counter {k}: oracle {ref[k]} gpu {got[k]}"
+        if resident:
+            assert (got["resident_rows"], got["duplicate_rows"]) == (want_res, want_dup), \
+                f"plan counters: oracle ({want_res}, {want_dup}) gpu " \
+                f"({got['resident_rows']}, {got['duplicate_rows']})"
+            log(f"[parity] {spec.name}: {want_res} resident + {want_dup} repeated of "
+                f"{got['misses']} misses filled on the device")
         log(f"[parity] {spec.name} done in {time.time() - t0:.1f}s: hit rate "
             f"{got['hits'] / max(1, got['lookups']):.4f}")
         return ref, got

@@ -39,9 +39,9 @@ def test_binding_has_same_names(lib):
 
 
 def test_struct_sizes_match_header(lib):
-    # avsg_config: 10 int32 + 2 int64 + 2 int32 = 64 bytes; stats: 11 u64 + 2 i32
+    # avsg_config: 10 int32 + 2 int64 + 2 int32 = 64 bytes; stats: 14 u64 + 2 i32
     assert ctypes.sizeof(A.AvsgConfig) == 64
-    assert ctypes.sizeof(A.AvsgStats) == 96
+    assert ctypes.sizeof(A.AvsgStats) == 120
 
 
 def test_strerror(lib):

@@ -110,11 +110,12 @@ def test_parity_parameters(retry, max_life):
     run_parity(spec, table_every=4, buffers_every=8, retry=retry, max_life=max_life)
 
 
-@pytest.mark.parametrize("mode", [1, 2, 4, 5],
-                         ids=["request_level", "copy_engine", "position_level", "pipelined"])
+@pytest.mark.parametrize("mode", [1, 2, 4, 5, 6],
+                         ids=["request_level", "copy_engine", "position_level", "pipelined", "resident"])
 def test_gather_modes_match_balanced(mode):
-    """Request-level (S1), position-level (S2), copy-engine and pipelined
-    transfers move the same bytes as the balanced miss-list transfer (S3)."""
+    """Request-level (S1), position-level (S2), copy-engine, pipelined and
+    resident-reuse transfers leave the same bytes as the balanced miss-list
+    transfer (S3)."""
     spec = W.custom_spec(name=f"mode{mode}", batch=6, topk=512, slots=2048, n_q=2, steps=12,
                          ctx=30000, row_bytes=(1152, 132))
     run_parity(spec, table_every=0, buffers_every=4, gather_mode=mode)
@@ -232,6 +233,79 @@ def test_bad_indices_are_counted_not_copied():
         host.free()
 
 
+RESIDENT_CASES = [
+    # name, kwargs of workload.custom_spec, retry R (R = 0 loses many installs)
+    ("lost_installs", dict(batch=4, topk=256, slots=512, n_q=2, steps=24, ctx=3000, retention=0.8), 0),
+    ("mtp4_exact_capacity", dict(batch=2, topk=512, slots=2048, n_q=4, steps=16, ctx=20000), 3),
+    ("two_streams_odd", dict(batch=3, topk=200, slots=512, n_q=2, steps=12, ctx=9000,
+                             row_bytes=(1152, 132)), 1),
+    ("spec_window", dict(batch=2, topk=256, slots=2048, n_q=3, steps=20, ctx=4096, mode="zipf_window",
+                         window=64, retention=0.8), 3),
+    ("k_one", dict(batch=5, topk=1, slots=2, n_q=1, steps=40, ctx=6), 0),
+    ("s_16384_max", dict(batch=2, topk=1024, slots=16384, n_q=3, steps=8, ctx=300000), 3),
+    ("batch_200", dict(batch=200, topk=128, slots=256, n_q=2, steps=6, ctx=2000), 0),
+]
+
+
+@pytest.mark.parametrize("name,kw,retry", RESIDENT_CASES, ids=[c[0] for c in RESIDENT_CASES])
+def test_resident_reuse_parity(name, kw, retry):
+    """Resident-reuse transfer: the plan (host list, device list) equals the
+    oracle's transfer_plan bit for bit, and slots, tables, counters and every
+    buffer byte equal the oracle's paper-order Stage Two."""
+    from paper_2609_37538_amd import avsg as A
+    spec = W.custom_spec(name=f"res_{name}", **kw)
+    ref, got = run_parity(spec, table_every=4, buffers_every=1, miss_list_requests=3,
+                          gather_mode=A.AVSG_GATHER_RESIDENT, retry=retry)
+    moved_on_device = (got["resident_rows"] + got["duplicate_rows"]) * sum(spec.row_bytes)
+    assert got["host_bytes"] + moved_on_device == got["bytes_moved"]
+
+
+def test_resident_reuse_with_bad_indices():
+    """Indices outside [0, rows) stay host entries that the copy skips, and the
+    buffers match the balanced transfer's step by step."""
+    from paper_2609_37538_amd import avsg as A
+    import torch
+    rows, S, K = 40, 16, 4
+    host = A.HostRegion(rows * 16)
+    host.view()[:] = np.repeat(np.arange(rows, dtype=np.uint8), 16)
+    ops = [A.Operator(A.make_config(1, K, 2, S, retry=0, max_life=2, row_bytes=(16,), gather_mode=gm),
+                      [host.ptr], [rows])
+           for gm in (A.AVSG_GATHER_BALANCED, A.AVSG_GATHER_RESIDENT)]
+    rng = np.random.default_rng(5)
+    try:
+        for t in range(12):
+            X = np.stack([rng.choice(rows + 8, size=K, replace=False) for _ in range(2)])
+            X[1, :2] = X[0, :2]                  # repeats across the two tokens
+            Xd = torch.tensor(X[None], dtype=torch.int32, device="cuda")
+            outs = [op.step(Xd) for op in ops]
+            torch.cuda.synchronize()
+            assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+            assert torch.equal(ops[0].buffers[0], ops[1].buffers[0]), f"step {t}"
+            hx, ho, ds, dd = ops[1].export_plan(0)
+            mx, _ = ops[1].export_misses(0)
+            assert sorted(hx[hx >= rows].tolist()) == sorted(mx[mx >= rows].tolist())
+        st = ops[1].stats()
+        assert st["bad_indices"] > 0 and st["resident_rows"] + st["duplicate_rows"] > 0
+    finally:
+        for op in ops:
+            op.close()
+        host.free()
+
+
+def test_resident_reuse_refused_without_room():
+    """The plan's index map must fit beside the table in LDS, and the mode
+    needs hash matching."""
+    from paper_2609_37538_amd import avsg as A
+    chk = lambda **kw: A.avsg_check_config(A.make_config(**kw))
+    assert chk(batch=1, topk=128, n_q=100, slots=16384, row_bytes=(16,),
+               gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_OK
+    assert chk(batch=1, topk=128, n_q=110, slots=16384, row_bytes=(16,),
+               gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_E_CAPACITY
+    assert chk(batch=1, topk=128, n_q=110, slots=16384, row_bytes=(16,)) == A.AVSG_OK
+    assert chk(batch=1, topk=64, n_q=1, slots=64, row_bytes=(16,), match_mode=A.AVSG_MATCH_DUALPTR,
+               gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_E_UNSUPPORTED
+
+
 PIPELINED_CASES = [
     ("tiny", None),
     ("mtp3_ragged", dict(batch=5, topk=300, slots=1024, n_q=3, steps=12, ctx=8000, row_bytes=(1152, 132))),
@@ -284,6 +358,13 @@ def test_parity_batch64_mtp2_full_pipelined():
 
 
 @pytest.mark.timeout(900)
+def test_parity_batch64_mtp2_full_resident():
+    from paper_2609_37538_amd import avsg as A
+    ref, got = run_parity(W.get_spec("batch64_mtp2"), gather_mode=A.AVSG_GATHER_RESIDENT)
+    assert got["host_bytes"] < 0.8 * got["bytes_moved"]
+
+
+@pytest.mark.timeout(900)
 def test_parity_imbalance_full():
     ref, got = run_parity(W.get_spec("imbalance"))
 
@@ -292,3 +373,12 @@ def test_parity_imbalance_full():
 def test_parity_stress_full():
     ref, got = run_parity(W.get_spec("stress"), buffers_every=128)
     assert got["invalidations"] > 0
+
+
+@pytest.mark.timeout(1200)
+def test_parity_stress_full_resident():
+    """Speculative rows are rewritten every step: the plan must never reuse a
+    slot whose cached index was invalidated."""
+    from paper_2609_37538_amd import avsg as A
+    ref, got = run_parity(W.get_spec("stress"), buffers_every=64, gather_mode=A.AVSG_GATHER_RESIDENT)
+    assert got["invalidations"] > 0 and got["resident_rows"] > 0

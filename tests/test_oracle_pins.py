@@ -451,3 +451,100 @@ def test_config_errors(oracle_lib):
     assert O.Oracle.create_status(**ok, a1=7, a2=7) == -4
     assert O.Oracle.create_status(**ok, a1=9, a2=7) == -4   # not prime
     assert O.Oracle.create_status(**ok, retry=-1) == -4
+
+
+# ---------------------------------------------------------------------------
+# resident-reuse transfer plan (a property of the transfer: every slot must end
+# up with the bytes the paper's Stage Two writes)
+# ---------------------------------------------------------------------------
+def _replay_plan(buf, plan, rows):
+    """Apply a plan to a buffer of row ids: host entries first (ids outside
+    [0, rows) are skipped, as by the copy), then device copies."""
+    hx, ho, ds, dd, _, _ = plan
+    for x, o in zip(hx.tolist(), ho.tolist()):
+        if 0 <= x < rows:
+            buf[o] = x
+    src = buf[ds].copy()
+    for s, o in zip(src.tolist(), dd.tolist()):
+        buf[o] = s
+
+
+@pytest.mark.parametrize("K,n_q,S,R,L,U,T,bad", [
+    (16, 2, 32, 0, 4, 60, 40, False),
+    (8, 3, 32, 1, 2, 40, 40, False),
+    (16, 4, 64, 0, 16, 120, 30, False),
+    (16, 2, 32, 0, 4, 60, 30, True),
+])
+def test_transfer_plan_replays_stage_two(oracle_lib, K, n_q, S, R, L, U, T, bad):
+    """Replaying the plan on a buffer of row ids gives, step after step, the
+    buffer of the paper's Stage Two (every miss copied from the host in list
+    order), and device copies actually occur (R = 0 loses many installs)."""
+    rng = np.random.default_rng(K * 100 + n_q)
+    B = 2
+    rows = U
+    orc = O.Oracle(B, K, n_q, S, retry=R, max_life=L, nthreads=1)
+    paper = [np.full(S, -1, dtype=np.int64) for _ in range(B)]
+    plan_buf = [np.full(S, -1, dtype=np.int64) for _ in range(B)]
+    n_res = n_dup = 0
+    for t in range(T):
+        X = np.stack([np.stack([rng.choice(U, size=K, replace=False) for _ in range(n_q)])
+                      for _ in range(B)]).astype(np.int32)
+        if bad:
+            X[0, 0, 0] = U + 5               # outside [0, rows): never copied
+        _, n = orc.step(X)                   # no index validation: a bad id takes a slot
+        for r in range(B):
+            mx, mo = orc.misses(r, n[r])
+            for x, o in zip(mx.tolist(), mo.tolist()):
+                if 0 <= x < rows:
+                    paper[r][o] = x
+            c, _ = orc.export(r)
+            plan = O.transfer_plan(mx, mo, c, rows)
+            hx, ho, ds, dd, nr, nd = plan
+            assert len(hx) + len(ds) == len(mx) and nr + nd == len(ds)
+            # host entries read distinct valid rows
+            valid = [x for x in hx.tolist() if 0 <= x < rows]
+            assert len(valid) == len(set(valid))
+            _replay_plan(plan_buf[r], plan, rows)
+            assert np.array_equal(plan_buf[r], paper[r]), f"step {t} request {r}"
+            n_res += nr
+            n_dup += nd
+    assert n_res > 0 and (n_q == 1 or n_dup > 0)
+
+
+def test_transfer_plan_finds_an_orphaned_slot(oracle_lib):
+    """Hand case: slot 5 caches id 42 but no bucket maps to it (every bucket is
+    invalid), so 42 misses, takes a dead slot, and the plan fills that slot from
+    slot 5 instead of the host."""
+    S, m = 8, 3
+    orc = O.Oracle(1, 1, 1, S, retry=S - 1, max_life=4, nthreads=1)
+    c = np.full(S, -1, dtype=np.int32)
+    c[5] = 42
+    q = np.full(S, O.pack(m, -1, 1, 0, 0), dtype=np.uint32)   # all buckets invalid, lifetimes -1
+    q[5] = O.pack(m, 3, 1, 0, 0)                              # slot 5 alive (lifetime 3)
+    orc.import_table(0, c, q)
+    O_t, n = orc.step(np.array([[[42]]], dtype=np.int32), rows=np.array([100], dtype=np.int64))
+    assert n[0, 0] == 1
+    mx, mo = orc.misses(0, n[0])
+    new = int(mo[0])
+    assert new != 5
+    cc, _ = orc.export(0)
+    hx, ho, ds, dd, nr, nd = O.transfer_plan(mx, mo, cc, 100)
+    assert len(hx) == 0 and ds.tolist() == [5] and dd.tolist() == [new] and (nr, nd) == (1, 0)
+    # with the orphan invalidated (c = -1) the row must come from the host
+    cc2 = cc.copy()
+    cc2[5] = -1
+    hx, ho, ds, dd, nr, nd = O.transfer_plan(mx, mo, cc2, 100)
+    assert hx.tolist() == [42] and ho.tolist() == [new] and len(ds) == 0
+
+
+def test_transfer_plan_same_step_repeat(oracle_lib):
+    """Hand case: the same id listed by two tokens of one step (its first
+    install lost) is copied from the host once, into the larger slot, and the
+    other slot is filled from it."""
+    mx = np.array([7, 9, 7], dtype=np.int32)
+    mo = np.array([2, 3, 6], dtype=np.int32)
+    c = np.full(8, -1, dtype=np.int32)
+    c[2], c[3], c[6] = 7, 9, 7
+    hx, ho, ds, dd, nr, nd = O.transfer_plan(mx, mo, c, 10)
+    assert hx.tolist() == [9, 7] and ho.tolist() == [3, 6]
+    assert ds.tolist() == [6] and dd.tolist() == [2] and (nr, nd) == (0, 1)
