@@ -39,11 +39,13 @@ def parse():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--config", default="batch64_mtp2",
                     choices=["tiny", "batch16", "batch64_mtp2", "imbalance", "stress"])
-    ap.add_argument("--gather", default="balanced",
+    ap.add_argument("--gather", default="resident",
                     choices=["balanced", "request", "position", "sdma", "none", "pipelined", "resident"])
     ap.add_argument("--match", default="hash", choices=["hash", "dualptr"])
     ap.add_argument("--workers", type=int, default=0, help="gather workgroups (0 = one per CU)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-reference", action="store_true",
+                    help="skip the reference run of the paper's Stage Two (every miss from the host)")
     ap.add_argument("--cpu-sample-steps", type=int, default=0,
                     help="oracle steps timed for the CPU baseline (0 = all warmup+timed steps)")
     ap.add_argument("--coherent", action="store_true", help="coherent (uncached) host rows")
@@ -150,10 +152,32 @@ def main():
         op.step(X_dev[t], N_dev[t] if spec.speculative else None)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    match_all, gather_all = A.avsg_timing(op.h, T)
+    match_all, gather_all, tail_all = A.avsg_timing(op.h, T)
     A.avsg_set_timing(op.h, False)
     after = op.stats()
     match_ms, gather_ms = match_all[args.warmup:], gather_all[args.warmup:]
+    tail_ms = tail_all[args.warmup:]
+
+    # ---- reference: the paper's Stage Two (S3, every miss copied from the
+    # host) on the same steps, same host rows, same stream ----
+    reference = None
+    if gather_mode == A.AVSG_GATHER_RESIDENT and not args.no_reference:
+        cfg_ref = A.make_config(spec.batch, spec.topk, spec.n_q, spec.slots, row_bytes=spec.row_bytes,
+                                gather_workers=args.workers, match_mode=match_mode,
+                                gather_mode=A.AVSG_GATHER_BALANCED)
+        op_ref = A.Operator(cfg_ref, host_ptrs, wl.ctx, device=dev, stream=stream)
+        for t in range(args.warmup):
+            op_ref.step(X_dev[t], N_dev[t] if spec.speculative else None)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for t in range(args.warmup, T):
+            op_ref.step(X_dev[t], N_dev[t] if spec.speculative else None)
+        torch.cuda.synchronize()
+        wall_ref = time.perf_counter() - t1
+        op_ref.close()
+        reference = {"gather": "balanced", "value": round(wall_ref / args.steps * 1e6, 2),
+                     "unit": "us/step",
+                     "what": "the paper's Stage Two (S3, Eq. 6): every miss copied from the host"}
 
     K = args.steps
     us_per_step = wall / K * 1e6
@@ -210,6 +234,8 @@ def main():
         "match_us_median": (round(float(np.median(match_ms)) * 1e3, 2)
                             if len(match_ms) and not pipelined else None),
         "gather_us_median": round(float(np.median(gather_ms)) * 1e3, 2) if len(gather_ms) else None,
+        "repeat_copy_us_median": (round(float(np.median(tail_ms)) * 1e3, 2)
+                                  if gather_mode == A.AVSG_GATHER_RESIDENT and len(tail_ms) else None),
         "match_us_p99": (round(float(np.percentile(match_ms, 99)) * 1e3, 2)
                          if len(match_ms) and not pipelined else None),
         "gather_us_p99": round(float(np.percentile(gather_ms, 99)) * 1e3, 2) if len(gather_ms) else None,
@@ -219,7 +245,7 @@ def main():
         "match_frac_of_step": round(match_s / wall, 4),
         "roofline": {
             "bound": "pcie",
-            "kernel": {"balanced": "gather_balanced_kernel", "resident": "gather_balanced_kernel",
+            "kernel": {"balanced": "gather_balanced_kernel", "resident": "gather_resident_kernel",
                        "pipelined": "step_pipelined_kernel"}.get(args.gather, args.gather),
             "achieved": round(gather_gbps, 3),
             "peak": PCIE_GEN5_X16_GBPS,
@@ -231,6 +257,7 @@ def main():
             "measured_hipmemcpy_peak": round(memcpy_peak, 3),
         },
         "cpu_baseline": cpu,
+        "reference_all_misses_from_host": reference,
     }
     print(json.dumps(out), flush=True)
     if args.report:
@@ -283,7 +310,7 @@ def appendix_d_sweep(out_path):
                 A.avsg_set_timing(op.h, True)
                 for t in range(warm, warm + timed):
                     op.step(X[t])
-                _, gather_ms = A.avsg_timing(op.h, timed)
+                _, gather_ms, _ = A.avsg_timing(op.h, timed)
                 after = op.stats()
                 op.close()
                 misses = after["misses"] - before["misses"]
@@ -321,7 +348,8 @@ def _timed_run(spec, cfg_kw, warm, timed, host_ptrs, dev, verified=False):
         A.avsg_set_timing(op.h, True)
         for t in range(warm, warm + timed):
             op.step(X[t], N[t] if verified else None)
-        match_ms, gather_ms = A.avsg_timing(op.h, timed)
+        match_ms, gather_ms, tail_ms = A.avsg_timing(op.h, timed)
+        gather_ms = gather_ms + tail_ms       # all of Stage Two
         after = op.stats()
     finally:
         op.close()
@@ -473,9 +501,11 @@ def config_table(out_path):
         json.dump(results, f, indent=1)
 
 
+# sources that decide the profiled kernel's traffic: the gather code and the
+# matching code that plans which rows it reads
 GATHER_SOURCES = ("paper_2609_37538_amd/csrc/gather.hip", "paper_2609_37538_amd/csrc/gather_body.h",
-                  "paper_2609_37538_amd/csrc/avsg_internal.h")
-TRAFFIC_SUMMARY = "profiles/gather_traffic_batch64_mtp2.md"
+                  "paper_2609_37538_amd/csrc/match_body.h", "paper_2609_37538_amd/csrc/avsg_internal.h")
+TRAFFIC_SUMMARY = "profiles/gather_resident_traffic_batch64_mtp2.md"
 
 
 def measured_traffic(args):
@@ -486,7 +516,7 @@ def measured_traffic(args):
     import hashlib
     import re
     if (args.config, args.warmup, args.steps, args.workers, args.gather, args.match) != \
-            ("batch64_mtp2", 16, 240, 0, "balanced", "hash"):
+            ("batch64_mtp2", 16, 240, 0, "resident", "hash"):
         return None
     path = os.path.join(ROOT, TRAFFIC_SUMMARY)
     if not os.path.exists(path):

@@ -183,26 +183,32 @@ avsg_status avsg_export_misses(avsg_handle *h, int32_t r, int32_t *n_out, int32_
                                int32_t *o_out);
 
 /* Stage Two plan of request r from the last step (AVSG_GATHER_RESIDENT only),
- * copied to host memory (synchronous), each list in transfer-list order:
- *   n_host, host_x[k], host_o[k]  misses copied from host row host_x[k] into
- *                                 slot host_o[k] (capacity N_q*K each);
- *   n_dev, dev_src[k], dev_dst[k] misses filled by copying slot dev_src[k] into
- *                                 slot dev_dst[k] after the host copies.
- * The source of a device copy is the largest slot outside this step's
- * reservations that caches the index (a valid verified row), else the largest
- * slot this step reserved for the index.  Errors: AVSG_E_INVAL,
- * AVSG_E_UNSUPPORTED (another gather mode), AVSG_E_HIP. */
+ * copied to host memory (synchronous); every list keeps transfer-list order
+ * and has capacity N_q*K:
+ *   n_host, host_x[k], host_o[k]   misses copied from host row host_x[k] into
+ *                                  slot host_o[k];
+ *   n_res, res_src[k], res_dst[k]  misses whose row is already in slot
+ *                                  res_src[k] (the largest slot outside this
+ *                                  step's reservations that caches the index
+ *                                  below the verified length): copied slot to
+ *                                  slot, alongside the host copies;
+ *   n_rep, rep_src[k], rep_dst[k]  repeats of an index missed twice in the
+ *                                  step: copied from the largest slot this step
+ *                                  reserved for it, after the host copies.
+ * Errors: AVSG_E_INVAL, AVSG_E_UNSUPPORTED (another gather mode), AVSG_E_HIP. */
 avsg_status avsg_export_plan(avsg_handle *h, int32_t r, int32_t *n_host, int32_t *host_x,
-                             int32_t *host_o, int32_t *n_dev, int32_t *dev_src, int32_t *dev_dst);
+                             int32_t *host_o, int32_t *n_res, int32_t *res_src, int32_t *res_dst,
+                             int32_t *n_rep, int32_t *rep_src, int32_t *rep_dst);
 
 /* Per-step kernel timing with HIP events recorded on the step's stream.
  * avsg_set_timing(h, 1) starts recording (and clears the record);
  * avsg_timing copies up to `cap` recorded steps (synchronizing):
- * match_ms[i] and gather_ms[i] are the durations of step i's matching kernel
- * and of its Stage Two (kernel or copies). */
+ * match_ms[i] is the duration of step i's matching kernel, gather_ms[i] that
+ * of its main Stage Two kernel (or copies), and tail_ms[i] (may be NULL) the
+ * rest of Stage Two: the repeat copies of AVSG_GATHER_RESIDENT, ~0 otherwise. */
 avsg_status avsg_set_timing(avsg_handle *h, int32_t enable);
-avsg_status avsg_timing(avsg_handle *h, float *match_ms, float *gather_ms, int32_t cap,
-                        int32_t *n_out);
+avsg_status avsg_timing(avsg_handle *h, float *match_ms, float *gather_ms, float *tail_ms,
+                        int32_t cap, int32_t *n_out);
 
 avsg_status avsg_destroy(avsg_handle *h);
 

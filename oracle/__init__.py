@@ -288,12 +288,13 @@ def transfer_plan(miss_x, miss_o, c_after, rows_r: int):
     Plain definition, for each miss (x, o) of the step's transfer list in order:
       - x outside [0, rows_r): a host entry (the copy skips it);
       - else, if some slot j outside this step's reservations caches x after the
-        step (c_after[j] == x; invalidated entries are already -1), a device
-        copy from the largest such j (its row arrived in an earlier step);
-      - else, if the largest slot reserved this step for x is not o, a device
+        step (c_after[j] == x; invalidated entries are already -1), a resident
+        copy j -> o from the largest such j (its row arrived in an earlier step);
+      - else, if the largest slot reserved this step for x is not o, a repeat
         copy from that slot (x missed again in a later token of the step);
       - else a host entry.
-    Returns (host_x, host_o, dev_src, dev_dst, n_resident, n_duplicate).
+    Each list keeps transfer-list order.  Returns
+    (host_x, host_o, res_src, res_dst, rep_src, rep_dst) as int32 arrays.
     """
     miss_x = [int(v) for v in miss_x]
     miss_o = [int(v) for v in miss_o]
@@ -305,26 +306,22 @@ def transfer_plan(miss_x, miss_o, c_after, rows_r: int):
         x = int(c_after[j])
         if x in wanted and j not in reserved:
             resident[x] = j
-    rep = {}
+    first = {}
     for x, o in zip(miss_x, miss_o):
         if 0 <= x < rows_r:
-            rep[x] = max(rep.get(x, -1), o)
-    host_x, host_o, dev_src, dev_dst = [], [], [], []
-    n_res = n_dup = 0
+            first[x] = max(first.get(x, -1), o)
+    lists = [[] for _ in range(6)]
     for x, o in zip(miss_x, miss_o):
         if 0 <= x < rows_r and x in resident:
-            dev_src.append(resident[x])
-            dev_dst.append(o)
-            n_res += 1
-        elif 0 <= x < rows_r and rep[x] != o:
-            dev_src.append(rep[x])
-            dev_dst.append(o)
-            n_dup += 1
+            lists[2].append(resident[x])
+            lists[3].append(o)
+        elif 0 <= x < rows_r and first[x] != o:
+            lists[4].append(first[x])
+            lists[5].append(o)
         else:
-            host_x.append(x)
-            host_o.append(o)
-    as32 = lambda v: np.asarray(v, dtype=np.int32)
-    return as32(host_x), as32(host_o), as32(dev_src), as32(dev_dst), n_res, n_dup
+            lists[0].append(x)
+            lists[1].append(o)
+    return tuple(np.asarray(v, dtype=np.int32) for v in lists)
 
 
 def partition_balanced(n_miss: int, C: int) -> np.ndarray:

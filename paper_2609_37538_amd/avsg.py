@@ -108,11 +108,11 @@ def load():
     lib.avsg_export_misses.restype = i32
     lib.avsg_export_misses.argtypes = [_P, i32, _P, _P, _P]
     lib.avsg_export_plan.restype = i32
-    lib.avsg_export_plan.argtypes = [_P, i32, _P, _P, _P, _P, _P, _P]
+    lib.avsg_export_plan.argtypes = [_P, i32, _P, _P, _P, _P, _P, _P, _P, _P, _P]
     lib.avsg_set_timing.restype = i32
     lib.avsg_set_timing.argtypes = [_P, i32]
     lib.avsg_timing.restype = i32
-    lib.avsg_timing.argtypes = [_P, _P, _P, i32, _P]
+    lib.avsg_timing.argtypes = [_P, _P, _P, _P, i32, _P]
     lib.avsg_destroy.restype = i32
     lib.avsg_destroy.argtypes = [_P]
     lib.avsg_strerror.restype = ctypes.c_char_p
@@ -213,14 +213,15 @@ def avsg_export_state(h, r: int, slots: int):
 
 
 def avsg_export_plan(h, r: int, capacity: int):
-    """(host_x, host_o, dev_src, dev_dst) of request r's last Stage Two plan."""
-    nh = ctypes.c_int32(0)
-    nd = ctypes.c_int32(0)
-    hx, ho, ds, dd = (np.empty(capacity, dtype=np.int32) for _ in range(4))
-    _check(load().avsg_export_plan(h, r, ctypes.byref(nh), hx.ctypes.data_as(_P), ho.ctypes.data_as(_P),
-                                   ctypes.byref(nd), ds.ctypes.data_as(_P), dd.ctypes.data_as(_P)),
+    """(host_x, host_o, res_src, res_dst, rep_src, rep_dst) of request r's last
+    Stage Two plan."""
+    n = [ctypes.c_int32(0) for _ in range(3)]
+    a = [np.empty(capacity, dtype=np.int32) for _ in range(6)]
+    _check(load().avsg_export_plan(h, r, ctypes.byref(n[0]), a[0].ctypes.data_as(_P), a[1].ctypes.data_as(_P),
+                                   ctypes.byref(n[1]), a[2].ctypes.data_as(_P), a[3].ctypes.data_as(_P),
+                                   ctypes.byref(n[2]), a[4].ctypes.data_as(_P), a[5].ctypes.data_as(_P)),
            "avsg_export_plan", h)
-    return hx[: nh.value].copy(), ho[: nh.value].copy(), ds[: nd.value].copy(), dd[: nd.value].copy()
+    return tuple(a[k][: n[k // 2].value].copy() for k in range(6))
 
 
 def avsg_export_misses(h, r: int, capacity: int):
@@ -237,12 +238,14 @@ def avsg_set_timing(h, enable: bool) -> None:
 
 
 def avsg_timing(h, cap: int):
+    """(match_ms, gather_ms, tail_ms) per recorded step."""
     a = np.zeros(cap, dtype=np.float32)
     b = np.zeros(cap, dtype=np.float32)
+    c = np.zeros(cap, dtype=np.float32)
     n = ctypes.c_int32(0)
-    _check(load().avsg_timing(h, a.ctypes.data_as(_P), b.ctypes.data_as(_P), cap, ctypes.byref(n)),
-           "avsg_timing", h)
-    return a[: n.value].copy(), b[: n.value].copy()
+    _check(load().avsg_timing(h, a.ctypes.data_as(_P), b.ctypes.data_as(_P), c.ctypes.data_as(_P), cap,
+                              ctypes.byref(n)), "avsg_timing", h)
+    return a[: n.value].copy(), b[: n.value].copy(), c[: n.value].copy()
 
 
 def avsg_destroy(h) -> None:

@@ -29,8 +29,10 @@ struct avsg_handle {
   int2* miss_list = nullptr;
   uint8_t* hit_mask = nullptr;
   int2* host_list = nullptr;    // resident-reuse plan (AVSG_GATHER_RESIDENT)
-  int2* dev_list = nullptr;
-  int32_t* plan_counts = nullptr;
+  int2* res_list = nullptr;
+  int2* rep_list = nullptr;
+  int32_t* plan_counts = nullptr;  // [B][3]
+  int32_t* plan_claim = nullptr;
   int plan_words = 0;
   int* pipe_ctl = nullptr;      // head, tail, done, exit_count, error
   int4* pipe_chunks = nullptr;
@@ -49,7 +51,8 @@ struct avsg_handle {
   int32_t* last_counts = nullptr;
   // timing
   bool timing = false;
-  std::vector<std::array<hipEvent_t, 3>> events;
+  std::vector<std::array<hipEvent_t, 4>> events;   // before Stage One, after it, after the
+                                                   // main Stage Two kernel, after Stage Two
   size_t n_timed = 0;
   // SDMA comparator staging (pinned host)
   int32_t* h_counts = nullptr;
@@ -92,8 +95,8 @@ Layout layout_of(const avsg_config& c) {
   L.miss_list = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk * 8);
   L.hit_mask = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk);
   L.plan = off;
-  if (c.gather_mode == AVSG_GATHER_RESIDENT)   // host list, device list, counts
-    off += 2 * up(B * static_cast<size_t>(c.n_q) * c.topk * 8) + up(B * 8);
+  if (c.gather_mode == AVSG_GATHER_RESIDENT)   // host, resident, repeat lists; counts; claim
+    off += 3 * up(B * static_cast<size_t>(c.n_q) * c.topk * 8) + up(B * 12) + up(4);
   L.pipe = off;
   L.pipe_bytes = up(kAlign + 16 * pipe_chunks_for(c));
   off += L.pipe_bytes;
@@ -261,8 +264,10 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
   if (c.gather_mode == AVSG_GATHER_RESIDENT) {
     const size_t list = up(static_cast<size_t>(B) * c.n_q * c.topk * 8);
     h->host_list = reinterpret_cast<int2*>(ws + L.plan);
-    h->dev_list = reinterpret_cast<int2*>(ws + L.plan + list);
-    h->plan_counts = reinterpret_cast<int32_t*>(ws + L.plan + 2 * list);
+    h->res_list = reinterpret_cast<int2*>(ws + L.plan + list);
+    h->rep_list = reinterpret_cast<int2*>(ws + L.plan + 2 * list);
+    h->plan_counts = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list);
+    h->plan_claim = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + up(static_cast<size_t>(B) * 12));
     h->plan_words = plan_map_words(c.slots, c.topk, c.n_q);
   }
   h->pipe_ctl = reinterpret_cast<int*>(ws + L.pipe);
@@ -352,7 +357,7 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
 static avsg_status record(avsg_handle* h, int which, hipStream_t s) {
   if (!h->timing || h->n_timed >= kMaxTimedSteps) return AVSG_OK;
   if (h->events.size() <= h->n_timed) {
-    std::array<hipEvent_t, 3> ev{};
+    std::array<hipEvent_t, 4> ev{};
     // timing-only events: no system-scope cache write-back/invalidate at record
     for (auto& x : ev) HIP_TRY(h, hipEventCreateWithFlags(&x, hipEventDisableSystemFence));
     h->events.push_back(ev);
@@ -430,6 +435,7 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
     HIP_TRY(h, launch_step_pipelined(p, g, q, wgs, h->lds, s));
     if ((rc = record(h, 1, s)) != AVSG_OK) return rc;
     if ((rc = record(h, 2, s)) != AVSG_OK) return rc;
+    if ((rc = record(h, 3, s)) != AVSG_OK) return rc;
     if (h->timing && h->n_timed < kMaxTimedSteps) h->n_timed++;
     h->steps++;
     return AVSG_OK;
@@ -447,8 +453,10 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
     if (c.gather_mode == AVSG_GATHER_RESIDENT) {
       p.plan_words = h->plan_words;
       p.host_list = h->host_list;
-      p.dev_list = h->dev_list;
+      p.res_list = h->res_list;
+      p.rep_list = h->rep_list;
       p.plan_counts = h->plan_counts;
+      p.plan_claim = h->plan_claim;
     }
     HIP_TRY(h, launch_match_hash(p, h->lds, s));
   } else {
@@ -472,12 +480,17 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
     case AVSG_GATHER_REQUEST: HIP_TRY(h, launch_gather_request(g, s)); break;
     case AVSG_GATHER_POSITION: HIP_TRY(h, launch_gather_position(g, h->workers, s)); break;
     case AVSG_GATHER_RESIDENT: {
-      // host rows first (balanced over the host list), then the device copies
-      g.miss_counts = h->plan_counts; g.counts_per_req = 1; g.count_stride = 2;
-      g.miss_list = h->host_list;
-      HIP_TRY(h, launch_gather_balanced(g, h->workers, s));
-      g.miss_counts = h->plan_counts + 1;
-      g.miss_list = h->dev_list;
+      // host list (balanced) and resident copies in one kernel, then the
+      // repeats of this step's host rows
+      GatherParams gh = g, gr = g;
+      gh.miss_counts = h->plan_counts; gh.counts_per_req = 1; gh.count_stride = 3;
+      gh.miss_list = h->host_list;
+      gr.miss_counts = h->plan_counts + 1; gr.counts_per_req = 1; gr.count_stride = 3;
+      gr.miss_list = h->res_list;
+      HIP_TRY(h, launch_gather_resident(gh, gr, h->plan_claim, h->workers, s));
+      if ((rc = record(h, 2, s)) != AVSG_OK) return rc;
+      g.miss_counts = h->plan_counts + 2; g.counts_per_req = 1; g.count_stride = 3;
+      g.miss_list = h->rep_list;
       HIP_TRY(h, launch_copy_device(g, h->workers, s));
       break;
     }
@@ -486,7 +499,8 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
       break;
     default: break;
   }
-  if ((rc = record(h, 2, s)) != AVSG_OK) return rc;
+  if (c.gather_mode != AVSG_GATHER_RESIDENT && (rc = record(h, 2, s)) != AVSG_OK) return rc;
+  if ((rc = record(h, 3, s)) != AVSG_OK) return rc;
   if (h->timing && h->n_timed < kMaxTimedSteps) h->n_timed++;
   h->steps++;
   return AVSG_OK;
@@ -596,39 +610,40 @@ avsg_status avsg_export_misses(avsg_handle* h, int32_t r, int32_t* n_out, int32_
 }
 
 avsg_status avsg_export_plan(avsg_handle* h, int32_t r, int32_t* n_host, int32_t* host_x,
-                             int32_t* host_o, int32_t* n_dev, int32_t* dev_src, int32_t* dev_dst) {
-  if (!h || !n_host || !host_x || !host_o || !n_dev || !dev_src || !dev_dst || r < 0 ||
-      r >= h->cfg.batch)
+                             int32_t* host_o, int32_t* n_res, int32_t* res_src, int32_t* res_dst,
+                             int32_t* n_rep, int32_t* rep_src, int32_t* rep_dst) {
+  if (!h || !n_host || !host_x || !host_o || !n_res || !res_src || !res_dst || !n_rep || !rep_src ||
+      !rep_dst || r < 0 || r >= h->cfg.batch)
     return AVSG_E_INVAL;
   const avsg_config& c = h->cfg;
   if (c.gather_mode != AVSG_GATHER_RESIDENT) return AVSG_E_UNSUPPORTED;
-  *n_host = 0;
-  *n_dev = 0;
+  *n_host = *n_res = *n_rep = 0;
   if (!h->last_counts) return AVSG_OK;
   HIP_TRY(h, hipStreamSynchronize(h->last_stream));
-  int32_t cnt[2] = {0, 0};
-  HIP_TRY(h, hipMemcpy(cnt, h->plan_counts + 2 * static_cast<size_t>(r), sizeof(cnt),
+  int32_t cnt[3] = {0, 0, 0};
+  HIP_TRY(h, hipMemcpy(cnt, h->plan_counts + 3 * static_cast<size_t>(r), sizeof(cnt),
                        hipMemcpyDeviceToHost));
   const int64_t cap = static_cast<int64_t>(c.n_q) * c.topk;
-  if (cnt[0] < 0 || cnt[1] < 0 || cnt[0] + static_cast<int64_t>(cnt[1]) > cap) return AVSG_E_INTERNAL;
+  if (cnt[0] < 0 || cnt[1] < 0 || cnt[2] < 0 ||
+      static_cast<int64_t>(cnt[0]) + cnt[1] + cnt[2] > cap)
+    return AVSG_E_INTERNAL;
   const size_t base = static_cast<size_t>(r) * c.n_q * c.topk;
-  std::vector<int2> v(static_cast<size_t>(std::max(cnt[0], cnt[1])));
-  if (cnt[0] > 0)
-    HIP_TRY(h, hipMemcpy(v.data(), h->host_list + base, static_cast<size_t>(cnt[0]) * 8,
-                         hipMemcpyDeviceToHost));
-  for (int k = 0; k < cnt[0]; ++k) {
-    host_x[k] = v[k].x;
-    host_o[k] = v[k].y;
-  }
-  if (cnt[1] > 0)
-    HIP_TRY(h, hipMemcpy(v.data(), h->dev_list + base, static_cast<size_t>(cnt[1]) * 8,
-                         hipMemcpyDeviceToHost));
-  for (int k = 0; k < cnt[1]; ++k) {
-    dev_src[k] = v[k].x;
-    dev_dst[k] = v[k].y;
+  const int2* lists[3] = {h->host_list, h->res_list, h->rep_list};
+  int32_t* outs[3][2] = {{host_x, host_o}, {res_src, res_dst}, {rep_src, rep_dst}};
+  std::vector<int2> v;
+  for (int k = 0; k < 3; ++k) {
+    v.resize(static_cast<size_t>(cnt[k]));
+    if (cnt[k] > 0)
+      HIP_TRY(h, hipMemcpy(v.data(), lists[k] + base, static_cast<size_t>(cnt[k]) * 8,
+                           hipMemcpyDeviceToHost));
+    for (int i = 0; i < cnt[k]; ++i) {
+      outs[k][0][i] = v[i].x;
+      outs[k][1][i] = v[i].y;
+    }
   }
   *n_host = cnt[0];
-  *n_dev = cnt[1];
+  *n_res = cnt[1];
+  *n_rep = cnt[2];
   return AVSG_OK;
 }
 
@@ -639,8 +654,8 @@ avsg_status avsg_set_timing(avsg_handle* h, int32_t enable) {
   return AVSG_OK;
 }
 
-avsg_status avsg_timing(avsg_handle* h, float* match_ms, float* gather_ms, int32_t cap,
-                        int32_t* n_out) {
+avsg_status avsg_timing(avsg_handle* h, float* match_ms, float* gather_ms, float* tail_ms,
+                        int32_t cap, int32_t* n_out) {
   if (!h || !n_out || cap < 0) return AVSG_E_INVAL;
   HIP_TRY(h, hipStreamSynchronize(h->last_stream));
   const size_t n = std::min<size_t>(h->n_timed, static_cast<size_t>(cap));
@@ -648,6 +663,11 @@ avsg_status avsg_timing(avsg_handle* h, float* match_ms, float* gather_ms, int32
     float a = 0.f, b = 0.f;
     HIP_TRY(h, hipEventElapsedTime(&a, h->events[i][0], h->events[i][1]));
     HIP_TRY(h, hipEventElapsedTime(&b, h->events[i][1], h->events[i][2]));
+    if (tail_ms) {
+      float c = 0.f;
+      HIP_TRY(h, hipEventElapsedTime(&c, h->events[i][2], h->events[i][3]));
+      tail_ms[i] = c;
+    }
     if (match_ms) match_ms[i] = a;
     if (gather_ms) gather_ms[i] = b;
   }

@@ -49,8 +49,10 @@ struct MatchParams {
   // Stage Two plan of the resident-reuse gather (written when plan_words > 0)
   int32_t plan_words;           // words of the end-of-step index map in LDS
   int2* host_list;              // [B][n_q*K] (index, slot) copied from the host
-  int2* dev_list;               // [B][n_q*K] (source slot, slot) copied on the device
-  int32_t* plan_counts;         // [B][2] host entries, device entries
+  int2* res_list;               // [B][n_q*K] (source slot, slot): row already resident
+  int2* rep_list;               // [B][n_q*K] (source slot, slot): repeat of a host entry
+  int32_t* plan_counts;         // [B][3] host, resident, repeat entries
+  int32_t* plan_claim;          // resident-copy tiles claimed by the gather (reset here)
 };
 
 struct GatherParams {
@@ -107,6 +109,10 @@ hipError_t launch_gather_request(const GatherParams& p, hipStream_t s);
 hipError_t launch_gather_position(const GatherParams& p, int workers, hipStream_t s);
 // device-to-device row copies: miss_list entries are (source slot, slot)
 hipError_t launch_copy_device(const GatherParams& p, int workers, hipStream_t s);
+// resident-reuse Stage Two: host entries (balanced), then resident copies
+// claimed tile by tile; `dev` describes the resident list, `claim` its counter
+hipError_t launch_gather_resident(const GatherParams& host, const GatherParams& dev, int* claim,
+                                  int workers, hipStream_t s);
 // words of the end-of-step index map the matching kernel can hold for (S, K, n_q);
 // 0 when the plan does not fit in the kernel's LDS
 int plan_map_words(int S, int K, int n_q);

@@ -11,9 +11,10 @@
 // the 132-byte indexer-key rows), several loads in flight per lane.  The
 // position kernel (S2, Eq. 14) splits the flattened N_g*K selected positions
 // into C near-equal contiguous ranges; hit positions issue no copy but still
-// occupy their worker's share.  The device-copy kernel fills the misses whose
-// row is already in the request's buffer (resident-reuse plan of the matching
-// kernel) with the same balanced split, after the host copies.
+// occupy their worker's share.  With the resident-reuse plan of the matching
+// kernel, the resident kernel copies the host list and the rows already in the
+// device buffer, and the device-copy kernel then fills repeats of this step's
+// host rows.
 #include "gather_body.h"
 
 namespace avsg {
@@ -29,6 +30,34 @@ __global__ __launch_bounds__(GT) void gather_balanced_kernel(GatherParams p) {
   const long long a = (w * N) / C;          // Eq. 6: consecutive, floor/ceil(N/C) each
   const long long b = ((w + 1) * N) / C;
   copy_range<false>(p, pre, a, b, src0, dst0, src1, dst1);
+}
+
+// Resident-reuse Stage Two: every workgroup copies its Eq. 6 share of the host
+// list, then claims tiles of the resident list (rows already in a slot of the
+// same request, not written this step) until none is left, so workgroups that
+// finish their host share early absorb the device copies.
+__global__ __launch_bounds__(GT) void gather_resident_kernel(GatherParams hp, GatherParams rp,
+                                                              int* claim) {
+  __shared__ long long pre[kMaxBatch + 1];
+  __shared__ long long wtot[GT / 64];
+  __shared__ uint64_t src0[TILE], dst0[TILE], src1[TILE], dst1[TILE];
+  __shared__ long long next;
+  request_prefix(hp, pre, wtot);
+  {
+    const long long N = pre[hp.B];
+    const long long C = gridDim.x, w = blockIdx.x;
+    copy_range<false>(hp, pre, (w * N) / C, ((w + 1) * N) / C, src0, dst0, src1, dst1);
+  }
+  __syncthreads();
+  request_prefix(rp, pre, wtot);
+  const long long R = pre[rp.B];
+  for (;;) {
+    if (threadIdx.x == 0) next = atomicAdd(claim, TILE);
+    __syncthreads();
+    const long long t0 = next;
+    if (t0 >= R) break;
+    copy_range<true>(rp, pre, t0, t0 + TILE < R ? t0 + TILE : R, src0, dst0, src1, dst1);
+  }
 }
 
 // Device-to-device row copies (source slot -> slot) over the same balanced
@@ -92,6 +121,13 @@ hipError_t launch_gather_balanced(const GatherParams& p, int workers, hipStream_
 hipError_t launch_copy_device(const GatherParams& p, int workers, hipStream_t s) {
   if (workers < 1 || p.B > kMaxBatch) return hipErrorInvalidValue;
   hipLaunchKernelGGL(copy_device_kernel, dim3(workers), dim3(GT), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_resident(const GatherParams& host, const GatherParams& dev, int* claim,
+                                  int workers, hipStream_t s) {
+  if (workers < 1 || host.B > kMaxBatch || !claim) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gather_resident_kernel, dim3(workers), dim3(GT), 0, s, host, dev, claim);
   return hipGetLastError();
 }
 

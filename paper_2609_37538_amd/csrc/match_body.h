@@ -113,8 +113,9 @@ struct Own {
 };
 
 // Words of LDS bookkeeping of the end-of-step plan besides the reservation
-// bitmap and the index map: per-wave counts of two compaction rounds + totals.
-constexpr int kPlanMiscWords = 4 * MW + 4;
+// bitmap and the index map: per-wave counts of the three lists for two
+// compaction rounds, plus totals.
+constexpr int kPlanMiscWords = 6 * MW + 4;
 constexpr uint32_t kPlanResident = 0x80000000u;   // map word names a slot outside this step's reservations
 
 // Home word of index x in the plan's map of P words (multiplicative hash).
@@ -125,19 +126,20 @@ __device__ __forceinline__ uint32_t plan_home(int32_t x, uint32_t P) {
 // Stage Two plan of the resident-reuse gather, after the step's table write
 // back (every LDS array but c[] is free).  Each of the step's listed misses
 // (index x, slot o) becomes
-//   a host copy, unless
-//   a device copy from the largest slot outside this step's reservations that
-//   still caches x below the verified length (its row arrived in an earlier
-//   step and cannot have changed), or else
-//   a device copy from the largest slot this step reserved for x, when that is
-//   not o (a later token missed x again after its install was lost).
-// LDS map: P words, open addressing with linear probing keyed by the index a
-// word names through c[]; a word is (resident bit | slot + 1), 0 = empty, and
-// atomicMax makes the choice deterministic.  The map holds at most N_q * K keys
-// and P >= 1.5 N_q K, so every probe sequence ends at an empty word.
+//   a resident copy from the largest slot outside this step's reservations
+//   that still caches x below the verified length (its row arrived in an
+//   earlier step and cannot have changed), or else
+//   a repeat copy from the largest slot this step reserved for x, when that is
+//   not o (a later token missed x again after its install was lost), or else
+//   a host copy.
+// The three lists keep transfer-list order.  LDS map: P words, open addressing
+// with linear probing keyed by the index a word names through c[]; a word is
+// (resident bit | slot + 1), 0 = empty, and atomicMax makes the choice
+// deterministic.  The map holds at most N_q * K keys and P >= 1.5 N_q K, so
+// every probe sequence ends at an empty word.
 __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, unsigned char* lds,
-                                          const int listed, const int64_t rows_r,
-                                          const int64_t n_verified) {
+                                             const int listed, const int64_t rows_r,
+                                             const int64_t n_verified) {
   const int S = p.S;
   const int32_t* sc = reinterpret_cast<const int32_t*>(lds);
   uint32_t* sres = reinterpret_cast<uint32_t*>(lds + 4 * static_cast<size_t>(S));  // reserved-slot bitmap
@@ -148,6 +150,7 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
   const size_t lb = static_cast<size_t>(r) * p.n_q * p.K;
   const int2* ml = p.miss_list + lb;
+  if (r == 0 && tid == 0) *p.plan_claim = 0;
 
   for (int j = tid; j < nb + static_cast<int>(P) + kPlanMiscWords; j += MT) sres[j] = 0u;
   __syncthreads();
@@ -190,11 +193,11 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   }
   __syncthreads();
 
-  // (3) classify in transfer-list order and compact the two lists
-  int n_host = 0, n_dev = 0, my_res = 0, my_dup = 0;
+  // (3) classify in transfer-list order and compact the three lists
+  int n_list[3] = {0, 0, 0};
   for (int e0 = 0, it = 0; e0 < listed; e0 += MT, ++it) {
     const int e = e0 + tid;
-    int kind = -1;                 // 0 host, 1 resident slot, 2 same-step slot
+    int kind = -1;                 // 0 host, 1 resident, 2 repeat
     int2 v = make_int2(0, 0);
     int src = 0;
     if (e < listed) {
@@ -220,41 +223,41 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
         }
       }
     }
-    my_res += kind == 1 ? 1 : 0;
-    my_dup += kind == 2 ? 1 : 0;
-    const uint64_t mh = __ballot(kind == 0), md = __ballot(kind > 0);
-    int* wc = scnt + (it & 1) * 2 * MW;
-    if (lane == 0) {
-      wc[wave] = __popcll(mh);
-      wc[MW + wave] = __popcll(md);
+    uint64_t mk[3];
+    int* wc = scnt + (it & 1) * 3 * MW;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      mk[k] = __ballot(kind == k);
+      if (lane == 0) wc[k * MW + wave] = __popcll(mk[k]);
     }
     __syncthreads();
-    int bh = 0, bd = 0, th = 0, td = 0;
+    int before[3] = {0, 0, 0}, total[3] = {0, 0, 0};
     for (int w = 0; w < MW; ++w) {
-      const int ch = wc[w], cd = wc[MW + w];
-      th += ch;
-      td += cd;
-      bh += (w < wave) ? ch : 0;
-      bd += (w < wave) ? cd : 0;
+#pragma unroll
+      for (int k = 0; k < 3; ++k) {
+        const int c = wc[k * MW + w];
+        total[k] += c;
+        before[k] += (w < wave) ? c : 0;
+      }
     }
-    if (kind == 0) p.host_list[lb + n_host + bh + bits_below(mh)] = v;
-    else if (kind > 0) p.dev_list[lb + n_dev + bd + bits_below(md)] = make_int2(src, v.y);
-    n_host += th;
-    n_dev += td;
+    if (kind == 0) {
+      p.host_list[lb + n_list[0] + before[0] + bits_below(mk[0])] = v;
+    } else if (kind == 1) {
+      p.res_list[lb + n_list[1] + before[1] + bits_below(mk[1])] = make_int2(src, v.y);
+    } else if (kind == 2) {
+      p.rep_list[lb + n_list[2] + before[2] + bits_below(mk[2])] = make_int2(src, v.y);
+    }
+#pragma unroll
+    for (int k = 0; k < 3; ++k) n_list[k] += total[k];
   }
-  my_res = wave_sum(my_res);
-  my_dup = wave_sum(my_dup);
-  if (lane == 0) {
-    if (my_res) atomicAdd(&scnt[4 * MW], my_res);
-    if (my_dup) atomicAdd(&scnt[4 * MW + 1], my_dup);
-  }
-  __syncthreads();
   if (tid == 0) {
-    p.plan_counts[2 * static_cast<size_t>(r)] = n_host;
-    p.plan_counts[2 * static_cast<size_t>(r) + 1] = n_dev;
+    int32_t* pc = p.plan_counts + 3 * static_cast<size_t>(r);
+    pc[0] = n_list[0];
+    pc[1] = n_list[1];
+    pc[2] = n_list[2];
     unsigned long long* st = p.stats + static_cast<size_t>(r) * kNumStats;
-    st[kStatResident] += static_cast<unsigned long long>(scnt[4 * MW]);
-    st[kStatDuplicate] += static_cast<unsigned long long>(scnt[4 * MW + 1]);
+    st[kStatResident] += static_cast<unsigned long long>(n_list[1]);
+    st[kStatDuplicate] += static_cast<unsigned long long>(n_list[2]);
   }
 }
 

@@ -281,7 +281,7 @@ def test_resident_reuse_with_bad_indices():
             torch.cuda.synchronize()
             assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
             assert torch.equal(ops[0].buffers[0], ops[1].buffers[0]), f"step {t}"
-            hx, ho, ds, dd = ops[1].export_plan(0)
+            hx, ho, rs, rd, ps, pd = ops[1].export_plan(0)
             mx, _ = ops[1].export_misses(0)
             assert sorted(hx[hx >= rows].tolist()) == sorted(mx[mx >= rows].tolist())
         st = ops[1].stats()

@@ -458,15 +458,19 @@ def test_config_errors(oracle_lib):
 # up with the bytes the paper's Stage Two writes)
 # ---------------------------------------------------------------------------
 def _replay_plan(buf, plan, rows):
-    """Apply a plan to a buffer of row ids: host entries first (ids outside
-    [0, rows) are skipped, as by the copy), then device copies."""
-    hx, ho, ds, dd, _, _ = plan
+    """Apply a plan to a buffer of row ids in the kernels' order: host entries
+    (ids outside [0, rows) are skipped, as by the copy) and resident copies,
+    then repeat copies."""
+    hx, ho, rs, rd, ps, pd = plan
+    res = buf[rs].copy()                    # resident sources are not written this step
     for x, o in zip(hx.tolist(), ho.tolist()):
         if 0 <= x < rows:
             buf[o] = x
-    src = buf[ds].copy()
-    for s, o in zip(src.tolist(), dd.tolist()):
-        buf[o] = s
+    for v, o in zip(res.tolist(), rd.tolist()):
+        buf[o] = v
+    rep = buf[ps].copy()
+    for v, o in zip(rep.tolist(), pd.tolist()):
+        buf[o] = v
 
 
 @pytest.mark.parametrize("K,n_q,S,R,L,U,T,bad", [
@@ -499,8 +503,11 @@ def test_transfer_plan_replays_stage_two(oracle_lib, K, n_q, S, R, L, U, T, bad)
                     paper[r][o] = x
             c, _ = orc.export(r)
             plan = O.transfer_plan(mx, mo, c, rows)
-            hx, ho, ds, dd, nr, nd = plan
-            assert len(hx) + len(ds) == len(mx) and nr + nd == len(ds)
+            hx, ho, rs, rd, ps, pd = plan
+            nr, nd = len(rs), len(ps)
+            assert len(hx) + nr + nd == len(mx)
+            assert not set(rs.tolist()) & set(mo.tolist())     # resident sources are not reserved
+            assert set(ps.tolist()) <= set(ho.tolist())        # repeat sources get a host copy
             # host entries read distinct valid rows
             valid = [x for x in hx.tolist() if 0 <= x < rows]
             assert len(valid) == len(set(valid))
@@ -528,13 +535,13 @@ def test_transfer_plan_finds_an_orphaned_slot(oracle_lib):
     new = int(mo[0])
     assert new != 5
     cc, _ = orc.export(0)
-    hx, ho, ds, dd, nr, nd = O.transfer_plan(mx, mo, cc, 100)
-    assert len(hx) == 0 and ds.tolist() == [5] and dd.tolist() == [new] and (nr, nd) == (1, 0)
+    hx, ho, rs, rd, ps, pd = O.transfer_plan(mx, mo, cc, 100)
+    assert len(hx) == 0 and rs.tolist() == [5] and rd.tolist() == [new] and len(ps) == 0
     # with the orphan invalidated (c = -1) the row must come from the host
     cc2 = cc.copy()
     cc2[5] = -1
-    hx, ho, ds, dd, nr, nd = O.transfer_plan(mx, mo, cc2, 100)
-    assert hx.tolist() == [42] and ho.tolist() == [new] and len(ds) == 0
+    hx, ho, rs, rd, ps, pd = O.transfer_plan(mx, mo, cc2, 100)
+    assert hx.tolist() == [42] and ho.tolist() == [new] and len(rs) == 0 and len(ps) == 0
 
 
 def test_transfer_plan_same_step_repeat(oracle_lib):
@@ -545,6 +552,6 @@ def test_transfer_plan_same_step_repeat(oracle_lib):
     mo = np.array([2, 3, 6], dtype=np.int32)
     c = np.full(8, -1, dtype=np.int32)
     c[2], c[3], c[6] = 7, 9, 7
-    hx, ho, ds, dd, nr, nd = O.transfer_plan(mx, mo, c, 10)
+    hx, ho, rs, rd, ps, pd = O.transfer_plan(mx, mo, c, 10)
     assert hx.tolist() == [9, 7] and ho.tolist() == [3, 6]
-    assert ds.tolist() == [6] and dd.tolist() == [2] and (nr, nd) == (0, 1)
+    assert ps.tolist() == [6] and pd.tolist() == [2] and len(rs) == 0
