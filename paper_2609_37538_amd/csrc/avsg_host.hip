@@ -68,6 +68,7 @@ constexpr size_t kAlign = 256;
 constexpr int kMaxBatch = 1024;
 constexpr size_t kMaxTimedSteps = 16384;
 constexpr size_t kLdsPerWorkgroup = 160 * 1024;   // gfx950
+constexpr int kRepeatWorkersPerCu = 4;
 
 size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
@@ -489,9 +490,13 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
       gr.miss_list = h->res_list;
       HIP_TRY(h, launch_gather_resident(gh, gr, h->plan_claim, h->workers, s));
       if ((rc = record(h, 2, s)) != AVSG_OK) return rc;
-      g.miss_counts = h->plan_counts + 2; g.counts_per_req = 1; g.count_stride = 3;
-      g.miss_list = h->rep_list;
-      HIP_TRY(h, launch_copy_device(g, h->workers, s));
+      // repeats need two tokens in a step; they are few and HBM-latency bound,
+      // so they get more, smaller workgroups
+      if (c.n_q > 1) {
+        g.miss_counts = h->plan_counts + 2; g.counts_per_req = 1; g.count_stride = 3;
+        g.miss_list = h->rep_list;
+        HIP_TRY(h, launch_copy_device(g, kRepeatWorkersPerCu * std::max(1, h->cus), s));
+      }
       break;
     }
     case AVSG_GATHER_SDMA:

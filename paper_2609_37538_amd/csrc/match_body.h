@@ -137,9 +137,11 @@ __device__ __forceinline__ uint32_t plan_home(int32_t x, uint32_t P) {
 // (resident bit | slot + 1), 0 = empty, and atomicMax makes the choice
 // deterministic.  The map holds at most N_q * K keys and P >= 1.5 N_q K, so
 // every probe sequence ends at an empty word.
+// v0: this thread's entry tid of the transfer list (loaded by the caller
+// before the table write-back, so its latency overlaps the write-back).
 __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, unsigned char* lds,
                                              const int listed, const int64_t rows_r,
-                                             const int64_t n_verified) {
+                                             const int64_t n_verified, const int2 v0) {
   const int S = p.S;
   const int32_t* sc = reinterpret_cast<const int32_t*>(lds);
   uint32_t* sres = reinterpret_cast<uint32_t*>(lds + 4 * static_cast<size_t>(S));  // reserved-slot bitmap
@@ -157,7 +159,7 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
 
   // (1) mark this step's reservations; one map word per distinct valid index
   for (int e = tid; e < listed; e += MT) {
-    const int2 v = ml[e];
+    const int2 v = e < MT ? v0 : ml[e];
     if (v.y < 0 || v.y >= S) continue;
     atomicOr(&sres[v.y >> 5], 1u << (v.y & 31));
     if (v.x < 0 || static_cast<int64_t>(v.x) >= rows_r) continue;
@@ -175,20 +177,39 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   }
   __syncthreads();
 
-  // (2) slots outside the reservations that cache one of those indices
-  for (int j = tid; j < S; j += MT) {
-    const int32_t x = sc[j];
-    if (x < 0 || static_cast<int64_t>(x) >= rows_r || static_cast<int64_t>(x) >= n_verified) continue;
-    if ((sres[j >> 5] >> (j & 31)) & 1u) continue;
-    uint32_t h = plan_home(x, P);
-    for (uint32_t t = 0; t < P; ++t) {
-      const uint32_t w = smp[h];
-      if (w == 0u) break;
-      if (sc[(w & ~kPlanResident) - 1u] == x) {
-        atomicMax(&smp[h], kPlanResident | (static_cast<uint32_t>(j) + 1u));
-        break;
+  // (2) slots outside the reservations that cache one of those indices; four
+  // slots per thread at a time so their LDS reads overlap (the map is sparse:
+  // most home words are empty and end the probe at once)
+  constexpr int kScanILP = 4;
+  for (int j0 = tid; j0 < S; j0 += kScanILP * MT) {
+    int32_t xs[kScanILP];
+    uint32_t hs[kScanILP], ws[kScanILP];
+#pragma unroll
+    for (int u = 0; u < kScanILP; ++u) {
+      const int j = j0 + u * MT;
+      xs[u] = j < S ? sc[j] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < kScanILP; ++u) {
+      const bool ok = xs[u] >= 0 && static_cast<int64_t>(xs[u]) < rows_r &&
+                      static_cast<int64_t>(xs[u]) < n_verified;
+      hs[u] = plan_home(xs[u], P);
+      ws[u] = ok ? smp[hs[u]] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kScanILP; ++u) {
+      const int j = j0 + u * MT;
+      // the reservation bitmap is read only for the few slots whose home word is taken
+      if (ws[u] != 0u && ((sres[j >> 5] >> (j & 31)) & 1u)) ws[u] = 0u;
+      uint32_t h = hs[u], w = ws[u];
+      for (uint32_t t = 0; w != 0u && t < P; ++t) {
+        if (sc[(w & ~kPlanResident) - 1u] == xs[u]) {
+          atomicMax(&smp[h], kPlanResident | (static_cast<uint32_t>(j0 + u * MT) + 1u));
+          break;
+        }
+        h = (h + 1u == P) ? 0u : h + 1u;
+        w = smp[h];
       }
-      h = (h + 1u == P) ? 0u : h + 1u;
     }
   }
   __syncthreads();
@@ -201,7 +222,7 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
     int2 v = make_int2(0, 0);
     int src = 0;
     if (e < listed) {
-      v = ml[e];
+      v = e < MT ? v0 : ml[e];
       kind = 0;
       if (v.x >= 0 && static_cast<int64_t>(v.x) < rows_r) {
         uint32_t h = plan_home(v.x, P);
@@ -563,6 +584,10 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   for (int u = 0; u < IPT; ++u)
     if (bid_v[u] && smap[bid_h[u]] != bid_v[u]) st_col++;
 
+  // the first transfer-list entry of this thread, for the Stage Two plan
+  int2 v0 = make_int2(-1, -1);
+  if (p.plan_words > 0 && tid < listed) v0 = p.miss_list[static_cast<size_t>(r) * p.n_q * K + tid];
+
   // End of step: speculative invalidation fused into the write back.
   int st_inv = 0;
   for (int j = tid; j < S; j += MT) {
@@ -597,7 +622,7 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   }
   if (p.plan_words > 0) {
     __syncthreads();   // the counter reduction above is read before its LDS is reused
-    plan_request(p, r, lds, listed, rows_r, n_verified);
+    plan_request(p, r, lds, listed, rows_r, n_verified, v0);
   }
 }
 

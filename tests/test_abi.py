@@ -70,6 +70,15 @@ def test_check_config_statuses(lib):
     assert chk(max_life=0) == A.AVSG_E_RANGE
     assert chk(batch=0) == A.AVSG_E_INVAL
     assert chk(match_mode=A.AVSG_MATCH_DUALPTR) == A.AVSG_E_UNSUPPORTED
+    # resident reuse: hash matching only; its index map must fit beside the table
+    assert chk(gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_OK
+    assert chk(n_q=1, slots=2048, match_mode=A.AVSG_MATCH_DUALPTR,
+               gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_E_UNSUPPORTED
+    assert chk(batch=1, topk=128, n_q=100, slots=16384, gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_OK
+    assert chk(batch=1, topk=128, n_q=110, slots=16384, gather_mode=A.AVSG_GATHER_RESIDENT) == \
+        A.AVSG_E_CAPACITY
+    assert chk(batch=1, topk=128, n_q=110, slots=16384) == A.AVSG_OK
+    assert chk(gather_mode=7) == A.AVSG_E_INVAL
 
 
 def test_workspace_size_and_validation(lib):
@@ -89,6 +98,9 @@ def test_workspace_size_and_validation(lib):
     assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=1, slots=2048) > 0
     assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=2) == 0
     assert ws(gather_mode=7) == 0
+    # the resident-reuse plan adds three transfer lists, counts and a claim counter
+    B, nq, K = 64, 2, 2048
+    assert ws(gather_mode=A.AVSG_GATHER_RESIDENT) >= ws() + 3 * 8 * B * nq * K + 12 * B
     assert ws(gather_mode=A.AVSG_GATHER_POSITION) > ws() - 1
     assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=1, slots=2048, gather_mode=A.AVSG_GATHER_POSITION) == 0
     assert ws(n_q=1, slots=2, topk=1, batch=1, row_bytes=(4,)) > 0
