@@ -382,3 +382,59 @@ def test_parity_stress_full_resident():
     from paper_2609_37538_amd import avsg as A
     ref, got = run_parity(W.get_spec("stress"), buffers_every=64, gather_mode=A.AVSG_GATHER_RESIDENT)
     assert got["invalidations"] > 0 and got["resident_rows"] > 0
+
+
+def test_resident_reuse_when_verified_length_shrinks():
+    """A verified length that moves back: slots caching an index at or above
+    the current verified length are never plan sources (the oracle sees them
+    invalidated), while the speculative rows beyond the largest length so far
+    are rewritten every step; plans, slots and buffers equal the oracle's, and
+    the case is exercised (such an index misses while a slot still caches it)."""
+    from paper_2609_37538_amd import avsg as A
+    spec = W.custom_spec(name="shrink_n", batch=2, topk=64, slots=512, n_q=2, steps=16, ctx=4096)
+    wl = W.Workload(spec)
+    host = HostRows(wl)
+    orc = OracleSide(wl, host, retry=0, max_life=8)
+    gpu = GpuSide(wl, host, retry=0, max_life=8, gather_mode=A.AVSG_GATHER_RESIDENT)
+    rng = np.random.default_rng(11)
+    n_max = 0
+    exercised = 0
+    try:
+        for t in range(spec.steps):
+            n_t = 2000 + 4 * t if t < 8 else 2000 + 32 - 8 * (t - 7)   # grows, then moves back
+            n_max = max(n_max, n_t)
+            N = np.full(spec.batch, n_t, dtype=np.int64)
+            for s in range(len(spec.row_bytes)):
+                for r in range(spec.batch):
+                    rows = host.row_view(s, r)[n_max:n_max + 16]    # never verified so far
+                    rows[:] = rng.integers(0, 256, size=rows.shape, dtype=np.uint8)
+            X = np.empty((spec.batch, spec.n_q, spec.topk), dtype=np.int32)
+            for r in range(spec.batch):
+                others = rng.choice(n_t - 24, size=spec.topk - 40, replace=False)
+                for g in range(spec.n_q):
+                    X[r, g] = np.concatenate([np.arange(n_t - 24, n_t + 16), others])
+            cached = [orc.o.export(r)[0] for r in range(spec.batch)]
+            O_ref, n_ref = orc.step(X, N)
+            O_gpu, n_gpu = gpu.step(X, N)
+            compare_step(t, O_ref, n_ref, O_gpu, n_gpu)
+            bufs = gpu.buffers()
+            for s in range(len(spec.row_bytes)):
+                assert np.array_equal(bufs[s], orc.images[s]), f"step {t} stream {s}: buffers differ"
+            content_check(host, wl, bufs, X, O_gpu)
+            for r in range(spec.batch):
+                mx, mo = orc.o.misses(r, n_ref[r])
+                c_ref, _ = orc.o.export(r)
+                want = ORC.transfer_plan(mx, mo, c_ref, int(wl.ctx[r]))
+                got = gpu.op.export_plan(r)
+                for k in range(6):
+                    assert np.array_equal(want[k], got[k]), f"step {t} request {r}: plan list {k}"
+                reserved = set(mo.tolist())
+                for x in mx.tolist():
+                    if x >= n_t and any(cached[r][j] == x and j not in reserved for j in range(spec.slots)):
+                        exercised += 1
+        st = gpu.op.stats()
+        assert exercised > 0 and st["invalidations"] > 0
+        assert st["resident_rows"] + st["duplicate_rows"] > 0
+    finally:
+        gpu.close()
+        host.free()
