@@ -45,7 +45,8 @@ typedef int32_t avsg_status;
 #define AVSG_OK 0
 #define AVSG_E_INVAL (-1)       /* null pointer, non-positive size, bad mode */
 #define AVSG_E_NOTPOW2 (-2)     /* S is not a power of two in [2, 2^23] */
-#define AVSG_E_CAPACITY (-3)    /* S < N_q * K (Eq. 7), or 9*S + 12*K bytes beyond one workgroup's LDS */
+#define AVSG_E_CAPACITY (-3)    /* S < N_q * K (Eq. 7), or 9*S + 12*K bytes beyond one workgroup's LDS
+                                   (or, resident reuse, no room beside the table for a map of 1.5*N_q*K words) */
 #define AVSG_E_RANGE (-4)       /* R < 0, L outside [1, 127], a1/a2 not distinct primes, row size */
 #define AVSG_E_BADINDEX (-5)    /* a selected index outside [0, rows of its request) */
 #define AVSG_E_HIP (-6)         /* a HIP runtime call failed */
@@ -122,7 +123,9 @@ avsg_status avsg_check_config(const avsg_config *cfg);
 
 /* Size in bytes of the device workspace that avsg_create needs for cfg
  * (per-request tables of 8*S bytes, transfer lists of 8*N_q*K bytes, a hit
- * mask of N_q*K bytes, counters and pointer tables).  Returns 0 for an invalid cfg. */
+ * mask of N_q*K bytes, counters and pointer tables; with AVSG_GATHER_RESIDENT
+ * three more lists of 8*N_q*K bytes per request; with AVSG_GATHER_PIPELINED a
+ * chunk queue of 16 bytes per 32 misses).  Returns 0 for an invalid cfg. */
 size_t avsg_workspace_bytes(const avsg_config *cfg);
 
 /* Create a handle and reset every table to empty (c_j = -1, lifetime -1, every
