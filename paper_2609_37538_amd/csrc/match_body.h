@@ -15,6 +15,10 @@ constexpr int kMaxSPT = 16;                // up to S = 16384 slots
 constexpr int kScratchInts = 2 * kMaxIPT * MW + MW + 4 + 8;
 constexpr uint32_t kBid = 0x80000000u;     // marks a bucket written by an install bid
 
+// 16-byte vectors as clang vector types (kept in registers)
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
 __device__ __forceinline__ int lane_id() {
   return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
 }
@@ -58,24 +62,37 @@ struct Word {
   }
 };
 
-// The lifetimes a thread owns, packed four to a register.
+// The lifetimes a thread owns (spt consecutive slots), four to a register as
+// biased bytes v = lifetime + 1 in [0, 128] (0 = dead); bytes past spt hold
+// 0xFF and never count as below any k <= 128.  Counting and decaying work on
+// two 16-bit lanes per word: (v + 256 - k) has bit 8 set exactly when v >= k.
 struct Own {
+  static constexpr uint32_t kLo = 0x00FF00FFu, kOne = 0x00010001u, kBias = 0x01000100u;
   uint32_t w[kMaxSPT / 4];
+  uint32_t pad;   // bytes of w[0] past spt (spt < 4), kept at 0xFF
   __device__ __forceinline__ int get(int e) const {
-    return static_cast<int>(static_cast<int8_t>(w[e >> 2] >> (8 * (e & 3))));
+    return static_cast<int>((w[e >> 2] >> (8 * (e & 3))) & 0xFFu) - 1;
   }
-  __device__ __forceinline__ void set(int e, int v) {
+  __device__ __forceinline__ void set(int e, int life) {
     const uint32_t sh = 8 * (e & 3);
-    w[e >> 2] = (w[e >> 2] & ~(0xFFu << sh)) | (static_cast<uint32_t>(static_cast<uint8_t>(v)) << sh);
+    w[e >> 2] = (w[e >> 2] & ~(0xFFu << sh)) | (static_cast<uint32_t>(life + 1) << sh);
+  }
+  // two's-complement lifetime bytes <-> biased bytes, four at a time
+  static __device__ __forceinline__ uint32_t bias(uint32_t raw) {
+    return ((raw & 0x7F7F7F7Fu) + 0x01010101u) ^ (raw & 0x80808080u);
+  }
+  static __device__ __forceinline__ uint32_t unbias(uint32_t b) {
+    return ((b | 0x80808080u) - 0x01010101u) ^ ((b ^ 0xFEFEFEFEu) & 0x80808080u);
   }
   __device__ __forceinline__ void load(const int8_t* slife, int j0, int spt) {
 #pragma unroll
-    for (int k = 0; k < kMaxSPT / 4; ++k) w[k] = 0u;
+    for (int k = 0; k < kMaxSPT / 4; ++k) w[k] = 0xFFFFFFFFu;
+    pad = spt >= 4 ? 0u : 0xFFFFFFFFu << (8 * spt);
     if (spt >= 4) {
       const uint32_t* p = reinterpret_cast<const uint32_t*>(slife + j0);
 #pragma unroll
       for (int k = 0; k < kMaxSPT / 4; ++k)
-        if (k < spt / 4) w[k] = p[k];
+        if (k < spt / 4) w[k] = bias(p[k]);
     } else {
 #pragma unroll
       for (int e = 0; e < 3; ++e)
@@ -87,28 +104,39 @@ struct Own {
       uint32_t* p = reinterpret_cast<uint32_t*>(slife + j0);
 #pragma unroll
       for (int k = 0; k < kMaxSPT / 4; ++k)
-        if (k < spt / 4) p[k] = w[k];
+        if (k < spt / 4) p[k] = unbias(w[k]);
     } else {
 #pragma unroll
       for (int e = 0; e < 3; ++e)
         if (e < spt) slife[j0 + e] = static_cast<int8_t>(get(e));
     }
   }
-  // number of owned lifetimes below k
+  // number of owned lifetimes below k (0 <= k <= 128)
   __device__ __forceinline__ int count_below(int k, int spt) const {
-    int c = 0;
+    const uint32_t kk = static_cast<uint32_t>(k + 1) * kOne;
+    int at_least = 0, n = 0;
 #pragma unroll
-    for (int e = 0; e < kMaxSPT; ++e) c += (e < spt && get(e) < k) ? 1 : 0;
-    return c;
-  }
-  // decay by k, never below -1
-  __device__ __forceinline__ void decay(int k, int spt) {
-#pragma unroll
-    for (int e = 0; e < kMaxSPT; ++e)
-      if (e < spt) {
-        const int l = get(e) - k;
-        set(e, l < -1 ? -1 : l);
+    for (int i = 0; i < kMaxSPT / 4; ++i)
+      if (i < (spt + 3) / 4) {
+        const uint32_t te = ((w[i] & kLo) + kBias) - kk;
+        const uint32_t to = (((w[i] >> 8) & kLo) + kBias) - kk;
+        at_least += __popc(((te >> 8) & kOne) | (((to >> 8) & kOne) << 1));
+        n += 4;
       }
+    return n - at_least;
+  }
+  // decay by k (1 <= k <= 128), never below -1
+  __device__ __forceinline__ void decay(int k, int spt) {
+    const uint32_t kk = static_cast<uint32_t>(k) * kOne;
+#pragma unroll
+    for (int i = 0; i < kMaxSPT / 4; ++i)
+      if (i < (spt + 3) / 4) {
+        const uint32_t te = ((w[i] & kLo) + kBias) - kk;
+        const uint32_t to = (((w[i] >> 8) & kLo) + kBias) - kk;
+        const uint32_t me = ((te >> 8) & kOne) * 0xFFu, mo = ((to >> 8) & kOne) * 0xFFu;
+        w[i] = (te & me) | ((to & mo) << 8);
+      }
+    w[0] |= pad;
   }
 };
 
@@ -277,8 +305,8 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
     pc[1] = n_list[1];
     pc[2] = n_list[2];
     unsigned long long* st = p.stats + static_cast<size_t>(r) * kNumStats;
-    st[kStatResident] += static_cast<unsigned long long>(n_list[1]);
-    st[kStatDuplicate] += static_cast<unsigned long long>(n_list[2]);
+    if (n_list[1]) atomicAdd(&st[kStatResident], static_cast<unsigned long long>(n_list[1]));
+    if (n_list[2]) atomicAdd(&st[kStatDuplicate], static_cast<unsigned long long>(n_list[2]));
   }
 }
 
@@ -307,20 +335,61 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   const int wave = tid >> 6;
   const int lane = lane_id();
 
+  // the first token's indices are requested before the table, so the two
+  // memory latencies overlap
+  int32_t xv[IPT];
+  {
+    const int32_t* xg = p.topk + static_cast<size_t>(r) * p.n_q * K;
+#pragma unroll
+    for (int u = 0; u < IPT; ++u) {
+      const int i = u * MT + tid;
+      xv[u] = i < K ? xg[i] : 0;
+    }
+  }
+
   int32_t* gc = p.table_c + static_cast<size_t>(r) * S;
   uint32_t* gq = p.table_q + static_cast<size_t>(r) * S;
-  for (int j = tid; j < S; j += MT) {
-    const uint32_t q = gq[j];
-    sc[j] = gc[j];
-    smap[j] = q & 0xFFFFFFu;
-    slife[j] = static_cast<int8_t>(q >> 24);
+  // stage-in: 16-byte loads of 4 entries, the loads of two blocks issued
+  // before their LDS stores
+  if ((S & (4 * MT - 1)) == 0) {
+    for (int b = tid; b < S / 4; b += 2 * MT) {
+      const i32x4 c0 = reinterpret_cast<const i32x4*>(gc)[b];
+      const u32x4 q0 = reinterpret_cast<const u32x4*>(gq)[b];
+      const bool two = b + MT < S / 4;
+      i32x4 c1 = 0;
+      u32x4 q1 = 0u;
+      if (two) {
+        c1 = reinterpret_cast<const i32x4*>(gc)[b + MT];
+        q1 = reinterpret_cast<const u32x4*>(gq)[b + MT];
+      }
+      reinterpret_cast<i32x4*>(sc)[b] = c0;
+      reinterpret_cast<u32x4*>(smap)[b] = q0 & 0xFFFFFFu;
+      reinterpret_cast<uint32_t*>(slife)[b] =
+          (q0.x >> 24) | ((q0.y >> 24) << 8) | ((q0.z >> 24) << 16) | (q0.w & 0xFF000000u);
+      if (two) {
+        reinterpret_cast<i32x4*>(sc)[b + MT] = c1;
+        reinterpret_cast<u32x4*>(smap)[b + MT] = q1 & 0xFFFFFFu;
+        reinterpret_cast<uint32_t*>(slife)[b + MT] =
+            (q1.x >> 24) | ((q1.y >> 24) << 8) | ((q1.z >> 24) << 16) | (q1.w & 0xFF000000u);
+      }
+    }
+  } else {
+    for (int j = tid; j < S; j += MT) {
+      const uint32_t q = gq[j];
+      sc[j] = gc[j];
+      smap[j] = q & 0xFFFFFFu;
+      slife[j] = static_cast<int8_t>(q >> 24);
+    }
   }
   if (tid < 4) sred[tid] = 0;
   if (tid < 8) sstat[tid] = 0;
 
-  const int spt = S >= MT ? S / MT : 1;   // lifetimes owned by this thread: [j0, j0 + spt)
-  const int own_n = tid < S ? spt : 0;
-  const int j0 = tid < S ? tid * spt : 0;
+  // lifetimes owned by this thread: [j0, j0 + spt) if it owns any (tid < S).
+  // spt is uniform, so the Own loops branch on scalars; only tables smaller
+  // than a workgroup leave threads without lifetimes.
+  const int spt = S >= MT ? S / MT : 1;
+  const bool owns = tid < S;
+  const int j0 = owns ? tid * spt : 0;
   const int64_t rows_r = p.rows[r];
   const int64_t n_verified = p.verified ? p.verified[r] : INT64_MAX;
   const uint32_t a1 = p.a1, a2 = p.a2, fmask = p.f_mask;
@@ -338,24 +407,17 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
     bid_h[u] = 0u;
   }
 
-  int32_t xv[IPT];
-  {
-    const int32_t* xg = p.topk + static_cast<size_t>(r) * p.n_q * K;
-#pragma unroll
-    for (int u = 0; u < IPT; ++u) {
-      const int i = u * MT + tid;
-      xv[u] = i < K ? xg[i] : 0;
-    }
-  }
   __syncthreads();
 
   for (int g = 0; g < p.n_q; ++g) {
     // Pass 1 (refresh): the first token decays every lifetime by one.
     if (g == 0) {
       Own o;
-      o.load(slife, j0, own_n);
-      o.decay(1, own_n);
-      o.store(slife, j0, own_n);
+      if (owns) {
+        o.load(slife, j0, spt);
+        o.decay(1, spt);
+        o.store(slife, j0, spt);
+      }
       __syncthreads();
     }
     const size_t row = static_cast<size_t>(r) * p.n_q + g;
@@ -449,8 +511,8 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
         smp[rank[u]] = u * MT + tid;
       }
     Own own;
-    own.load(slife, j0, own_n);
-    int dcnt = own.count_below(0, own_n);
+    if (owns) own.load(slife, j0, spt);
+    int dcnt = owns ? own.count_below(0, spt) : 0;
     int incl = wave_inclusive_scan(dcnt, lane);
     if (lane == 63) sdead[wave] = incl;
     // prefetch the next token's indices
@@ -476,7 +538,7 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
         // smallest k with #{lifetime_j < k} >= n_g; k = L + 1 always suffices
         int kstar = 1;
         for (int k = 1;; ++k) {
-          const int cnt = wave_sum(own.count_below(k, own_n));
+          const int cnt = wave_sum(owns ? own.count_below(k, spt) : 0);
           const int slot = red_it % 3;
           if (lane == 0 && cnt) atomicAdd(&sred[slot], cnt);
           if (tid == 0) sred[(red_it + 1) % 3] = 0;
@@ -487,10 +549,12 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
             break;
           }
         }
-        own.decay(kstar, own_n);
-        own.store(slife, j0, own_n);
+        if (owns) {
+          own.decay(kstar, spt);
+          own.store(slife, j0, spt);
+        }
         step_decays += kstar;
-        dcnt = own.count_below(0, own_n);
+        dcnt = owns ? own.count_below(0, spt) : 0;
         incl = wave_inclusive_scan(dcnt, lane);
         if (lane == 63) sdead[wave] = incl;   // every wave read sdead before the loop's barrier
         __syncthreads();
@@ -501,7 +565,7 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
       if (drank < n_g) {
 #pragma unroll
         for (int e = 0; e < kMaxSPT; ++e)
-          if (e < own_n && own.get(e) < 0 && drank < n_g) somiss[drank++] = j0 + e;
+          if (owns && e < spt && own.get(e) < 0 && drank < n_g) somiss[drank++] = j0 + e;
       }
       __syncthreads();
 
@@ -590,14 +654,36 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
 
   // End of step: speculative invalidation fused into the write back.
   int st_inv = 0;
-  for (int j = tid; j < S; j += MT) {
-    int32_t c = sc[j];
-    if (static_cast<int64_t>(c) >= n_verified) {
-      c = -1;
-      st_inv++;
+  if ((S & (4 * MT - 1)) == 0) {
+    // four entries per 16-byte store
+    for (int b = tid; b < S / 4; b += MT) {
+      i32x4 c = reinterpret_cast<const i32x4*>(sc)[b];
+      const u32x4 m = reinterpret_cast<const u32x4*>(smap)[b];
+      const uint32_t l = reinterpret_cast<const uint32_t*>(slife)[b];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (static_cast<int64_t>(c[e]) >= n_verified) {
+          c[e] = -1;
+          st_inv++;
+        }
+      u32x4 q;
+      q.x = (l << 24) | W.canonical(m.x);
+      q.y = ((l << 16) & 0xFF000000u) | W.canonical(m.y);
+      q.z = ((l << 8) & 0xFF000000u) | W.canonical(m.z);
+      q.w = (l & 0xFF000000u) | W.canonical(m.w);
+      reinterpret_cast<i32x4*>(gc)[b] = c;
+      reinterpret_cast<u32x4*>(gq)[b] = q;
     }
-    gc[j] = c;
-    gq[j] = (static_cast<uint32_t>(static_cast<uint8_t>(slife[j])) << 24) | W.canonical(smap[j]);
+  } else {
+    for (int j = tid; j < S; j += MT) {
+      int32_t c = sc[j];
+      if (static_cast<int64_t>(c) >= n_verified) {
+        c = -1;
+        st_inv++;
+      }
+      gc[j] = c;
+      gq[j] = (static_cast<uint32_t>(static_cast<uint8_t>(slife[j])) << 24) | W.canonical(smap[j]);
+    }
   }
 
   int vals[7] = {st_hits, st_miss, st_exh, st_col, st_rev, st_inv, st_bad};
@@ -608,17 +694,22 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   }
   __syncthreads();
   if (tid == 0) {
+    // atomics without a return value: thread 0 does not wait for the counters
     unsigned long long* st = p.stats + static_cast<size_t>(r) * kNumStats;
-    st[kStatHits] += static_cast<unsigned long long>(sstat[0]);
-    st[kStatMisses] += static_cast<unsigned long long>(sstat[1]);
-    st[kStatLostExhausted] += static_cast<unsigned long long>(sstat[2]);
-    st[kStatLostCollision] += static_cast<unsigned long long>(sstat[3]);
-    st[kStatRevivals] += static_cast<unsigned long long>(sstat[4]);
-    st[kStatInvalidations] += static_cast<unsigned long long>(sstat[5]);
-    st[kStatBadIndices] += static_cast<unsigned long long>(sstat[6]);
-    st[kStatAllocDecays] += static_cast<unsigned long long>(step_decays);
-    if (static_cast<unsigned long long>(step_decays) > st[kStatMaxStepDecays])
-      st[kStatMaxStepDecays] = static_cast<unsigned long long>(step_decays);
+    auto add = [&](StatIndex i, int v) {
+      if (v) atomicAdd(&st[i], static_cast<unsigned long long>(v));
+    };
+    add(kStatHits, sstat[0]);
+    add(kStatMisses, sstat[1]);
+    add(kStatLostExhausted, sstat[2]);
+    add(kStatLostCollision, sstat[3]);
+    add(kStatRevivals, sstat[4]);
+    add(kStatInvalidations, sstat[5]);
+    add(kStatBadIndices, sstat[6]);
+    if (step_decays) {
+      atomicAdd(&st[kStatAllocDecays], static_cast<unsigned long long>(step_decays));
+      atomicMax(&st[kStatMaxStepDecays], static_cast<unsigned long long>(step_decays));
+    }
   }
   if (p.plan_words > 0) {
     __syncthreads();   // the counter reduction above is read before its LDS is reused
