@@ -452,7 +452,7 @@ def config_table(out_path):
                   ("S1 request", A.AVSG_MATCH_HASH, A.AVSG_GATHER_REQUEST),
                   ("S2 position", A.AVSG_MATCH_HASH, A.AVSG_GATHER_POSITION),
                   ("pipelined", A.AVSG_MATCH_HASH, A.AVSG_GATHER_PIPELINED),
-                  ("resident reuse + S3", A.AVSG_MATCH_HASH, A.AVSG_GATHER_RESIDENT),
+                  ("resident reuse", A.AVSG_MATCH_HASH, A.AVSG_GATHER_RESIDENT),
                   ("dual-pointer + S3", A.AVSG_MATCH_DUALPTR, A.AVSG_GATHER_BALANCED)]
     results = []
     for name in ("tiny", "batch16", "batch64_mtp2", "imbalance", "stress"):

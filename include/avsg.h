@@ -66,8 +66,9 @@ typedef int32_t avsg_status;
 #define AVSG_GATHER_PIPELINED 5 /* Stage One and Stage Two in one launch: each token's misses are queued in
                                    chunks as soon as they are reserved and copied by every CU (hash matching,
                                    batch <= CU count) */
-#define AVSG_GATHER_RESIDENT 6  /* S3 over the misses whose row is not yet on the device, then device-to-device
-                                   copies for the rest (hash matching only).  A miss whose index is still cached
+#define AVSG_GATHER_RESIDENT 6  /* host copies of the misses whose row is not yet on the device (32-row tiles
+                                   claimed by every CU), then device-to-device copies for the rest (hash
+                                   matching only).  A miss whose index is still cached
                                    by a slot of the same request outside this step's reservations (its mapping
                                    was lost to an exhausted probe chain or a bucket collision, so the probe of
                                    Eq. 8-11 cannot find it) is filled from that slot; a miss that repeats an

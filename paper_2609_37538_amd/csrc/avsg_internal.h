@@ -52,7 +52,7 @@ struct MatchParams {
   int2* res_list;               // [B][n_q*K] (source slot, slot): row already resident
   int2* rep_list;               // [B][n_q*K] (source slot, slot): repeat of a host entry
   int32_t* plan_counts;         // [B][3] host, resident, repeat entries
-  int32_t* plan_claim;          // resident-copy tiles claimed by the gather (reset here)
+  int32_t* plan_claim;          // [2] resident and host rows claimed by the gather (reset here)
 };
 
 struct GatherParams {
@@ -109,8 +109,8 @@ hipError_t launch_gather_request(const GatherParams& p, hipStream_t s);
 hipError_t launch_gather_position(const GatherParams& p, int workers, hipStream_t s);
 // device-to-device row copies: miss_list entries are (source slot, slot)
 hipError_t launch_copy_device(const GatherParams& p, int workers, hipStream_t s);
-// resident-reuse Stage Two: host entries (balanced), then resident copies
-// claimed tile by tile; `dev` describes the resident list, `claim` its counter
+// resident-reuse Stage Two: host entries, then resident copies, both claimed
+// tile by tile; `dev` describes the resident list, `claim` the two counters
 hipError_t launch_gather_resident(const GatherParams& host, const GatherParams& dev, int* claim,
                                   int workers, hipStream_t s);
 // words of the end-of-step index map the matching kernel can hold for (S, K, n_q);

@@ -180,7 +180,10 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
   const size_t lb = static_cast<size_t>(r) * p.n_q * p.K;
   const int2* ml = p.miss_list + lb;
-  if (r == 0 && tid == 0) *p.plan_claim = 0;
+  if (r == 0 && tid == 0) {
+    p.plan_claim[0] = 0;
+    p.plan_claim[1] = 0;
+  }
 
   for (int j = tid; j < nb + static_cast<int>(P) + kPlanMiscWords; j += MT) sres[j] = 0u;
   __syncthreads();
