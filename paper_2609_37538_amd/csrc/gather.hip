@@ -32,39 +32,62 @@ __global__ __launch_bounds__(GT) void gather_balanced_kernel(GatherParams p) {
   copy_range<false>(p, pre, a, b, src0, dst0, src1, dst1);
 }
 
-// Resident-reuse Stage Two: workgroups claim 32-row tiles of the host list
-// with an atomic counter (the host-read rate of a CU varies up to 2x across
-// the chip, so claimed tiles end the kernel more evenly than a static Eq. 6
-// split: 0.6% faster at 64 requests), then 64-row tiles of the resident list
-// (rows already in a slot of the same request, not written this step) until
-// none is left.  claim[0] counts resident rows, claim[1] host rows; the
-// matching kernel resets both.
-constexpr int kHostClaim = 32;
+// Resident-reuse Stage Two over two lists: host rows, and rows already in a
+// slot of the same request (not written this step).  The last quarter of the
+// workgroups starts with the resident list and the others with the host list,
+// so the HBM copies run while the host link is busy (the link saturates with
+// far fewer workgroups); each group then moves to the other list.  Tile i of a
+// list first goes to the i-th workgroup of the group that starts with it (no
+// atomic: a step with few misses runs its host and device copies side by side
+// in one round), later tiles are claimed with an atomic counter, so the
+// workgroups that finish first take more (a CU's host-read rate varies up to
+// 2x across the chip; claimed tiles end the kernel more evenly than a static
+// Eq. 6 split).  claim[0] and claim[1] count the claimed resident and host
+// rows; the matching kernel resets both.
+constexpr int kHostTile = 32;
+
+// Copy tiles of T entries of a list of n entries: `first` (or none, -1) then
+// claimed tiles, which start at row `base`.
+template <bool kDevice, int T>
+__device__ void copy_tiles(const GatherParams& p, const long long* pre, long long n, long long first,
+                           long long base, int* counter, long long* next, uint64_t* src0,
+                           uint64_t* dst0, uint64_t* src1, uint64_t* dst1) {
+  long long t0 = first;
+  for (;;) {
+    if (t0 < 0) {
+      if (threadIdx.x == 0) *next = base + atomicAdd(counter, T);
+      __syncthreads();
+      t0 = *next;
+      __syncthreads();
+    }
+    if (t0 >= n) break;
+    copy_range<kDevice>(p, pre, t0, t0 + T < n ? t0 + T : n, src0, dst0, src1, dst1);
+    t0 = -1;
+  }
+}
 
 __global__ __launch_bounds__(GT) void gather_resident_kernel(GatherParams hp, GatherParams rp,
                                                               int* claim) {
-  __shared__ long long pre[kMaxBatch + 1];
+  __shared__ long long pre_h[kMaxBatch + 1], pre_r[kMaxBatch + 1];
   __shared__ long long wtot[GT / 64];
   __shared__ uint64_t src0[TILE], dst0[TILE], src1[TILE], dst1[TILE];
   __shared__ long long next;
-  request_prefix(hp, pre, wtot);
-  const long long N = pre[hp.B];
-  for (;;) {
-    if (threadIdx.x == 0) next = atomicAdd(claim + 1, kHostClaim);
-    __syncthreads();
-    const long long t0 = next;
-    if (t0 >= N) break;
-    copy_range<false>(hp, pre, t0, t0 + kHostClaim < N ? t0 + kHostClaim : N, src0, dst0, src1, dst1);
-  }
-  __syncthreads();
-  request_prefix(rp, pre, wtot);
-  const long long R = pre[rp.B];
-  for (;;) {
-    if (threadIdx.x == 0) next = atomicAdd(claim, TILE);
-    __syncthreads();
-    const long long t0 = next;
-    if (t0 >= R) break;
-    copy_range<true>(rp, pre, t0, t0 + TILE < R ? t0 + TILE : R, src0, dst0, src1, dst1);
+  request_prefix(hp, pre_h, wtot);
+  request_prefix(rp, pre_r, wtot);
+  const long long N = pre_h[hp.B], R = pre_r[rp.B];
+  const int C = static_cast<int>(gridDim.x), w = static_cast<int>(blockIdx.x);
+  const int cr = C / 4;                  // workgroups that start with the resident list
+  const int ch = C - cr;
+  const long long host_base = static_cast<long long>(ch) * kHostTile;
+  const long long res_base = static_cast<long long>(cr) * TILE;
+  if (w >= ch) {
+    const long long i = C - 1 - w;       // 0 .. cr-1
+    copy_tiles<true, TILE>(rp, pre_r, R, i * TILE, res_base, claim, &next, src0, dst0, src1, dst1);
+    copy_tiles<false, kHostTile>(hp, pre_h, N, -1, host_base, claim + 1, &next, src0, dst0, src1, dst1);
+  } else {
+    copy_tiles<false, kHostTile>(hp, pre_h, N, static_cast<long long>(w) * kHostTile, host_base, claim + 1,
+                                 &next, src0, dst0, src1, dst1);
+    copy_tiles<true, TILE>(rp, pre_r, R, -1, res_base, claim, &next, src0, dst0, src1, dst1);
   }
 }
 
