@@ -1,9 +1,11 @@
 """CPU oracle of the AVSG per-decode-step operator (test infrastructure only).
 
-The oracle is plain C (``avsg_oracle.c``), compiled with gcc into
-``liboracle_avsg.so`` and driven through ctypes with NumPy arrays.  Only the
-test suite, the smoke check and the benchmark's CPU-baseline leg use it; the
-product path never imports this package.
+The method's oracle is plain C (``avsg_oracle.c``), compiled with gcc into
+``liboracle_avsg.so`` and driven through ctypes with NumPy arrays;
+``transfer_plan`` (plain Python) defines which misses the resident-reuse
+transfer may fill from another slot.  Only the test suite, the smoke check and
+the benchmark's CPU-baseline leg use this package; the product path never
+imports it.
 """
 from __future__ import annotations
 
