@@ -66,17 +66,17 @@ typedef int32_t avsg_status;
 #define AVSG_GATHER_PIPELINED 5 /* Stage One and Stage Two in one launch: each token's misses are queued in
                                    chunks as soon as they are reserved and copied by every CU (hash matching,
                                    batch <= CU count) */
-#define AVSG_GATHER_RESIDENT 6  /* host copies of the misses whose row is not yet on the device (32-row tiles
-                                   claimed by every CU), then device-to-device copies for the rest (hash
-                                   matching only).  A miss whose index is still cached
+#define AVSG_GATHER_RESIDENT 6  /* Stage Two that moves over the host link only the misses whose row is not
+                                   yet on the device (hash matching only).  A miss whose index is still cached
                                    by a slot of the same request outside this step's reservations (its mapping
                                    was lost to an exhausted probe chain or a bucket collision, so the probe of
-                                   Eq. 8-11 cannot find it) is filled from that slot; a miss that repeats an
-                                   earlier miss of the same step (same index, a later token) is filled from the
-                                   slot that step's host copy writes.  Slots, counts, tables and buffer contents
-                                   are identical to AVSG_GATHER_BALANCED; only fewer rows cross the host link.
-                                   Relies on the same property as a hit: a cached row below the verified length
-                                   does not change on the host. */
+                                   Eq. 8-11 cannot find it) is copied from that slot; a miss that repeats a
+                                   miss of another token of the step (same index) is written by that index's
+                                   host copy (further repeats, from three tokens on, are copied from its slot).  Host rows go
+                                   in 32-row tiles claimed by every CU.  Slots, counts, tables and buffer
+                                   contents are identical to AVSG_GATHER_BALANCED.  Relies on the same
+                                   property as a hit: a cached row below the verified length does not change
+                                   on the host. */
 
 #define AVSG_MAX_STREAMS 2
 
@@ -125,7 +125,8 @@ avsg_status avsg_check_config(const avsg_config *cfg);
 /* Size in bytes of the device workspace that avsg_create needs for cfg
  * (per-request tables of 8*S bytes, transfer lists of 8*N_q*K bytes, a hit
  * mask of N_q*K bytes, counters and pointer tables; with AVSG_GATHER_RESIDENT
- * three more lists of 8*N_q*K bytes per request; with AVSG_GATHER_PIPELINED a
+ * three more lists of 8*N_q*K bytes, fan slots of 4*N_q*K bytes and bids of
+ * 4*S bytes per request; with AVSG_GATHER_PIPELINED a
  * chunk queue of 16 bytes per 32 misses).  Returns 0 for an invalid cfg. */
 size_t avsg_workspace_bytes(const avsg_config *cfg);
 
@@ -189,20 +190,23 @@ avsg_status avsg_export_misses(avsg_handle *h, int32_t r, int32_t *n_out, int32_
 /* Stage Two plan of request r from the last step (AVSG_GATHER_RESIDENT only),
  * copied to host memory (synchronous); every list keeps transfer-list order
  * and has capacity N_q*K:
- *   n_host, host_x[k], host_o[k]   misses copied from host row host_x[k] into
- *                                  slot host_o[k];
+ *   n_host, host_x[k], host_o[k],  misses copied from host row host_x[k] into
+ *   host_fan[k]                    slot host_o[k], and also into slot
+ *                                  host_fan[k] when it is not -1 (the largest
+ *                                  repeat destination of the index, below);
  *   n_res, res_src[k], res_dst[k]  misses whose row is already in slot
  *                                  res_src[k] (the largest slot outside this
  *                                  step's reservations that caches the index
  *                                  below the verified length): copied slot to
  *                                  slot, alongside the host copies;
- *   n_rep, rep_src[k], rep_dst[k]  repeats of an index missed twice in the
- *                                  step: copied from the largest slot this step
- *                                  reserved for it, after the host copies.
+ *   n_rep, rep_src[k], rep_dst[k]  further repeats of an index missed by three
+ *                                  or more tokens of the step: copied from the
+ *                                  largest slot this step reserved for it, after
+ *                                  the host copies.
  * Errors: AVSG_E_INVAL, AVSG_E_UNSUPPORTED (another gather mode), AVSG_E_HIP. */
 avsg_status avsg_export_plan(avsg_handle *h, int32_t r, int32_t *n_host, int32_t *host_x,
-                             int32_t *host_o, int32_t *n_res, int32_t *res_src, int32_t *res_dst,
-                             int32_t *n_rep, int32_t *rep_src, int32_t *rep_dst);
+                             int32_t *host_o, int32_t *host_fan, int32_t *n_res, int32_t *res_src,
+                             int32_t *res_dst, int32_t *n_rep, int32_t *rep_src, int32_t *rep_dst);
 
 /* Per-step kernel timing with HIP events recorded on the step's stream.
  * avsg_set_timing(h, 1) starts recording (and clears the record);

@@ -292,11 +292,13 @@ def transfer_plan(miss_x, miss_o, c_after, rows_r: int):
       - else, if some slot j outside this step's reservations caches x after the
         step (c_after[j] == x; invalidated entries are already -1), a resident
         copy j -> o from the largest such j (its row arrived in an earlier step);
-      - else, if the largest slot reserved this step for x is not o, a repeat
-        copy from that slot (x missed again in a later token of the step);
-      - else a host entry.
+      - else, if o is the largest slot this step reserved for x, a host entry;
+      - else a repeat of that host entry.
+    Each host entry also carries a fan slot: the largest repeat destination of
+    its index (-1 if none), which the host copy writes too; the other repeats
+    stay in the repeat list, copied from the host entry's slot.
     Each list keeps transfer-list order.  Returns
-    (host_x, host_o, res_src, res_dst, rep_src, rep_dst) as int32 arrays.
+    (host_x, host_o, host_fan, res_src, res_dst, rep_src, rep_dst) as int32 arrays.
     """
     miss_x = [int(v) for v in miss_x]
     miss_o = [int(v) for v in miss_o]
@@ -312,17 +314,24 @@ def transfer_plan(miss_x, miss_o, c_after, rows_r: int):
     for x, o in zip(miss_x, miss_o):
         if 0 <= x < rows_r:
             first[x] = max(first.get(x, -1), o)
-    lists = [[] for _ in range(6)]
+    fan = {}
     for x, o in zip(miss_x, miss_o):
-        if 0 <= x < rows_r and x in resident:
-            lists[2].append(resident[x])
-            lists[3].append(o)
-        elif 0 <= x < rows_r and first[x] != o:
-            lists[4].append(first[x])
-            lists[5].append(o)
+        if 0 <= x < rows_r and x not in resident and first[x] != o:
+            fan[x] = max(fan.get(x, -1), o)
+    lists = [[] for _ in range(7)]
+    for x, o in zip(miss_x, miss_o):
+        valid = 0 <= x < rows_r
+        if valid and x in resident:
+            lists[3].append(resident[x])
+            lists[4].append(o)
+        elif valid and first[x] != o:
+            if fan[x] != o:
+                lists[5].append(first[x])
+                lists[6].append(o)
         else:
             lists[0].append(x)
             lists[1].append(o)
+            lists[2].append(fan.get(x, -1) if valid else -1)
     return tuple(np.asarray(v, dtype=np.int32) for v in lists)
 
 

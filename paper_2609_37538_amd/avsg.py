@@ -108,7 +108,7 @@ def load():
     lib.avsg_export_misses.restype = i32
     lib.avsg_export_misses.argtypes = [_P, i32, _P, _P, _P]
     lib.avsg_export_plan.restype = i32
-    lib.avsg_export_plan.argtypes = [_P, i32, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+    lib.avsg_export_plan.argtypes = [_P, i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
     lib.avsg_set_timing.restype = i32
     lib.avsg_set_timing.argtypes = [_P, i32]
     lib.avsg_timing.restype = i32
@@ -213,15 +213,15 @@ def avsg_export_state(h, r: int, slots: int):
 
 
 def avsg_export_plan(h, r: int, capacity: int):
-    """(host_x, host_o, res_src, res_dst, rep_src, rep_dst) of request r's last
-    Stage Two plan."""
+    """(host_x, host_o, host_fan, res_src, res_dst, rep_src, rep_dst) of request
+    r's last Stage Two plan."""
     n = [ctypes.c_int32(0) for _ in range(3)]
-    a = [np.empty(capacity, dtype=np.int32) for _ in range(6)]
-    _check(load().avsg_export_plan(h, r, ctypes.byref(n[0]), a[0].ctypes.data_as(_P), a[1].ctypes.data_as(_P),
-                                   ctypes.byref(n[1]), a[2].ctypes.data_as(_P), a[3].ctypes.data_as(_P),
-                                   ctypes.byref(n[2]), a[4].ctypes.data_as(_P), a[5].ctypes.data_as(_P)),
-           "avsg_export_plan", h)
-    return tuple(a[k][: n[k // 2].value].copy() for k in range(6))
+    a = [np.empty(capacity, dtype=np.int32) for _ in range(7)]
+    P = [x.ctypes.data_as(_P) for x in a]
+    _check(load().avsg_export_plan(h, r, ctypes.byref(n[0]), P[0], P[1], P[2], ctypes.byref(n[1]), P[3], P[4],
+                                   ctypes.byref(n[2]), P[5], P[6]), "avsg_export_plan", h)
+    sizes = [n[0].value] * 3 + [n[1].value] * 2 + [n[2].value] * 2
+    return tuple(a[k][: sizes[k]].copy() for k in range(7))
 
 
 def avsg_export_misses(h, r: int, capacity: int):

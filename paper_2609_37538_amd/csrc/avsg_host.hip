@@ -29,6 +29,8 @@ struct avsg_handle {
   int2* miss_list = nullptr;
   uint8_t* hit_mask = nullptr;
   int2* host_list = nullptr;    // resident-reuse plan (AVSG_GATHER_RESIDENT)
+  int32_t* host_fan = nullptr;
+  int32_t* fan_slots = nullptr;
   int2* res_list = nullptr;
   int2* rep_list = nullptr;
   int32_t* plan_counts = nullptr;  // [B][3]
@@ -53,6 +55,7 @@ struct avsg_handle {
   bool timing = false;
   std::vector<std::array<hipEvent_t, 4>> events;   // before Stage One, after it, after the
                                                    // main Stage Two kernel, after Stage Two
+  std::vector<bool> has_tail;                      // step recorded the fourth event
   size_t n_timed = 0;
   // SDMA comparator staging (pinned host)
   int32_t* h_counts = nullptr;
@@ -96,8 +99,9 @@ Layout layout_of(const avsg_config& c) {
   L.miss_list = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk * 8);
   L.hit_mask = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk);
   L.plan = off;
-  if (c.gather_mode == AVSG_GATHER_RESIDENT)   // host, resident, repeat lists; counts; claim
-    off += 3 * up(B * static_cast<size_t>(c.n_q) * c.topk * 8) + up(B * 12) + up(4);
+  if (c.gather_mode == AVSG_GATHER_RESIDENT)   // host, resident, repeat lists; fan slots; bids; counts; claims
+    off += 3 * up(B * static_cast<size_t>(c.n_q) * c.topk * 8) + up(B * static_cast<size_t>(c.n_q) * c.topk * 4) +
+           up(B * S * 4) + up(B * 12) + up(8);
   L.pipe = off;
   L.pipe_bytes = up(kAlign + 16 * pipe_chunks_for(c));
   off += L.pipe_bytes;
@@ -267,8 +271,13 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
     h->host_list = reinterpret_cast<int2*>(ws + L.plan);
     h->res_list = reinterpret_cast<int2*>(ws + L.plan + list);
     h->rep_list = reinterpret_cast<int2*>(ws + L.plan + 2 * list);
-    h->plan_counts = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list);
-    h->plan_claim = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + up(static_cast<size_t>(B) * 12));
+    const size_t fan = up(static_cast<size_t>(B) * c.n_q * c.topk * 4);
+    const size_t bids = up(static_cast<size_t>(B) * c.slots * 4);
+    h->host_fan = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list);
+    h->fan_slots = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan);
+    h->plan_counts = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan + bids);
+    h->plan_claim =
+        reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan + bids + up(static_cast<size_t>(B) * 12));
     h->plan_words = plan_map_words(c.slots, c.topk, c.n_q);
   }
   h->pipe_ctl = reinterpret_cast<int*>(ws + L.pipe);
@@ -362,6 +371,7 @@ static avsg_status record(avsg_handle* h, int which, hipStream_t s) {
     // timing-only events: no system-scope cache write-back/invalidate at record
     for (auto& x : ev) HIP_TRY(h, hipEventCreateWithFlags(&x, hipEventDisableSystemFence));
     h->events.push_back(ev);
+    h->has_tail.push_back(false);
   }
   HIP_TRY(h, hipEventRecord(h->events[h->n_timed][which], s));
   return AVSG_OK;
@@ -436,8 +446,7 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
     HIP_TRY(h, launch_step_pipelined(p, g, q, wgs, h->lds, s));
     if ((rc = record(h, 1, s)) != AVSG_OK) return rc;
     if ((rc = record(h, 2, s)) != AVSG_OK) return rc;
-    if ((rc = record(h, 3, s)) != AVSG_OK) return rc;
-    if (h->timing && h->n_timed < kMaxTimedSteps) h->n_timed++;
+    if (h->timing && h->n_timed < kMaxTimedSteps) h->has_tail[h->n_timed++] = false;
     h->steps++;
     return AVSG_OK;
   }
@@ -454,6 +463,8 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
     if (c.gather_mode == AVSG_GATHER_RESIDENT) {
       p.plan_words = h->plan_words;
       p.host_list = h->host_list;
+      p.host_fan = h->host_fan;
+      p.fan_slots = h->fan_slots;
       p.res_list = h->res_list;
       p.rep_list = h->rep_list;
       p.plan_counts = h->plan_counts;
@@ -485,14 +496,15 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
       // repeats of this step's host rows
       GatherParams gh = g, gr = g;
       gh.miss_counts = h->plan_counts; gh.counts_per_req = 1; gh.count_stride = 3;
-      gh.miss_list = h->host_list;
+      gh.miss_list = h->host_list; gh.fan = h->host_fan;
       gr.miss_counts = h->plan_counts + 1; gr.counts_per_req = 1; gr.count_stride = 3;
       gr.miss_list = h->res_list;
       HIP_TRY(h, launch_gather_resident(gh, gr, h->plan_claim, h->workers, s));
       if ((rc = record(h, 2, s)) != AVSG_OK) return rc;
-      // repeats need two tokens in a step; they are few and HBM-latency bound,
-      // so they get more, smaller workgroups
-      if (c.n_q > 1) {
+      // the host copies also fill each index's last repeat, so repeats are
+      // left only with three or more tokens per step; they are few and
+      // HBM-latency bound, so they get more, smaller workgroups
+      if (c.n_q > 2) {
         g.miss_counts = h->plan_counts + 2; g.counts_per_req = 1; g.count_stride = 3;
         g.miss_list = h->rep_list;
         HIP_TRY(h, launch_copy_device(g, kRepeatWorkersPerCu * std::max(1, h->cus), s));
@@ -504,9 +516,12 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
       break;
     default: break;
   }
+  // a fourth event only when Stage Two has a tail kernel (each record costs
+  // the step stream a few microseconds)
+  const bool tail = c.gather_mode == AVSG_GATHER_RESIDENT && c.n_q > 2;
   if (c.gather_mode != AVSG_GATHER_RESIDENT && (rc = record(h, 2, s)) != AVSG_OK) return rc;
-  if ((rc = record(h, 3, s)) != AVSG_OK) return rc;
-  if (h->timing && h->n_timed < kMaxTimedSteps) h->n_timed++;
+  if (tail && (rc = record(h, 3, s)) != AVSG_OK) return rc;
+  if (h->timing && h->n_timed < kMaxTimedSteps) h->has_tail[h->n_timed++] = tail;
   h->steps++;
   return AVSG_OK;
 }
@@ -615,10 +630,10 @@ avsg_status avsg_export_misses(avsg_handle* h, int32_t r, int32_t* n_out, int32_
 }
 
 avsg_status avsg_export_plan(avsg_handle* h, int32_t r, int32_t* n_host, int32_t* host_x,
-                             int32_t* host_o, int32_t* n_res, int32_t* res_src, int32_t* res_dst,
-                             int32_t* n_rep, int32_t* rep_src, int32_t* rep_dst) {
-  if (!h || !n_host || !host_x || !host_o || !n_res || !res_src || !res_dst || !n_rep || !rep_src ||
-      !rep_dst || r < 0 || r >= h->cfg.batch)
+                             int32_t* host_o, int32_t* host_fan, int32_t* n_res, int32_t* res_src,
+                             int32_t* res_dst, int32_t* n_rep, int32_t* rep_src, int32_t* rep_dst) {
+  if (!h || !n_host || !host_x || !host_o || !host_fan || !n_res || !res_src || !res_dst || !n_rep ||
+      !rep_src || !rep_dst || r < 0 || r >= h->cfg.batch)
     return AVSG_E_INVAL;
   const avsg_config& c = h->cfg;
   if (c.gather_mode != AVSG_GATHER_RESIDENT) return AVSG_E_UNSUPPORTED;
@@ -646,6 +661,9 @@ avsg_status avsg_export_plan(avsg_handle* h, int32_t r, int32_t* n_host, int32_t
       outs[k][1][i] = v[i].y;
     }
   }
+  if (cnt[0] > 0)
+    HIP_TRY(h, hipMemcpy(host_fan, h->host_fan + base, static_cast<size_t>(cnt[0]) * 4,
+                         hipMemcpyDeviceToHost));
   *n_host = cnt[0];
   *n_res = cnt[1];
   *n_rep = cnt[2];
@@ -670,7 +688,7 @@ avsg_status avsg_timing(avsg_handle* h, float* match_ms, float* gather_ms, float
     HIP_TRY(h, hipEventElapsedTime(&b, h->events[i][1], h->events[i][2]));
     if (tail_ms) {
       float c = 0.f;
-      HIP_TRY(h, hipEventElapsedTime(&c, h->events[i][2], h->events[i][3]));
+      if (h->has_tail[i]) HIP_TRY(h, hipEventElapsedTime(&c, h->events[i][2], h->events[i][3]));
       tail_ms[i] = c;
     }
     if (match_ms) match_ms[i] = a;

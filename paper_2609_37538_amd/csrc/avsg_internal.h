@@ -49,6 +49,8 @@ struct MatchParams {
   // Stage Two plan of the resident-reuse gather (written when plan_words > 0)
   int32_t plan_words;           // words of the end-of-step index map in LDS
   int2* host_list;              // [B][n_q*K] (index, slot) copied from the host
+  int32_t* host_fan;            // [B][n_q*K] second slot a host entry is also copied to, or -1
+  int32_t* fan_slots;           // [B][S] fan slot bids per reserved slot (plan scratch)
   int2* res_list;               // [B][n_q*K] (source slot, slot): row already resident
   int2* rep_list;               // [B][n_q*K] (source slot, slot): repeat of a host entry
   int32_t* plan_counts;         // [B][3] host, resident, repeat entries
@@ -61,6 +63,7 @@ struct GatherParams {
   const int32_t* miss_counts;
   int32_t counts_per_req, count_stride;
   const int2* miss_list;        // [B][n_q*K] (index or source slot, slot)
+  const int32_t* fan;           // [B][n_q*K] second destination slot per entry (-1: none), or nullptr
   const int64_t* rows;          // [B]
   int32_t n_streams;
   const uint64_t* host_ptrs;    // [n_streams][B] device-visible addresses of host row 0

@@ -32,8 +32,9 @@ __global__ __launch_bounds__(GT) void gather_balanced_kernel(GatherParams p) {
   copy_range<false>(p, pre, a, b, src0, dst0, src1, dst1);
 }
 
-// Resident-reuse Stage Two over two lists: host rows, and rows already in a
-// slot of the same request (not written this step).  The last quarter of the
+// Resident-reuse Stage Two over two lists: host rows (each also written to
+// its fan slot, the last repeat of its index in the step), and rows already
+// in a slot of the same request (not written this step).  The last quarter of the
 // workgroups starts with the resident list and the others with the host list,
 // so the HBM copies run while the host link is busy (the link saturates with
 // far fewer workgroups); each group then moves to the other list.  Tile i of a
@@ -51,7 +52,8 @@ constexpr int kHostTile = 32;
 template <bool kDevice, int T>
 __device__ void copy_tiles(const GatherParams& p, const long long* pre, long long n, long long first,
                            long long base, int* counter, long long* next, uint64_t* src0,
-                           uint64_t* dst0, uint64_t* src1, uint64_t* dst1) {
+                           uint64_t* dst0, uint64_t* src1, uint64_t* dst1, uint64_t* dstx0 = nullptr,
+                           uint64_t* dstx1 = nullptr) {
   long long t0 = first;
   for (;;) {
     if (t0 < 0) {
@@ -61,7 +63,7 @@ __device__ void copy_tiles(const GatherParams& p, const long long* pre, long lon
       __syncthreads();
     }
     if (t0 >= n) break;
-    copy_range<kDevice>(p, pre, t0, t0 + T < n ? t0 + T : n, src0, dst0, src1, dst1);
+    copy_range<kDevice>(p, pre, t0, t0 + T < n ? t0 + T : n, src0, dst0, src1, dst1, dstx0, dstx1);
     t0 = -1;
   }
 }
@@ -70,7 +72,7 @@ __global__ __launch_bounds__(GT) void gather_resident_kernel(GatherParams hp, Ga
                                                               int* claim) {
   __shared__ long long pre_h[kMaxBatch + 1], pre_r[kMaxBatch + 1];
   __shared__ long long wtot[GT / 64];
-  __shared__ uint64_t src0[TILE], dst0[TILE], src1[TILE], dst1[TILE];
+  __shared__ uint64_t src0[TILE], dst0[TILE], src1[TILE], dst1[TILE], dstx0[TILE], dstx1[TILE];
   __shared__ long long next;
   request_prefix(hp, pre_h, wtot);
   request_prefix(rp, pre_r, wtot);
@@ -83,10 +85,11 @@ __global__ __launch_bounds__(GT) void gather_resident_kernel(GatherParams hp, Ga
   if (w >= ch) {
     const long long i = C - 1 - w;       // 0 .. cr-1
     copy_tiles<true, TILE>(rp, pre_r, R, i * TILE, res_base, claim, &next, src0, dst0, src1, dst1);
-    copy_tiles<false, kHostTile>(hp, pre_h, N, -1, host_base, claim + 1, &next, src0, dst0, src1, dst1);
+    copy_tiles<false, kHostTile>(hp, pre_h, N, -1, host_base, claim + 1, &next, src0, dst0, src1, dst1,
+                                 dstx0, dstx1);
   } else {
     copy_tiles<false, kHostTile>(hp, pre_h, N, static_cast<long long>(w) * kHostTile, host_base, claim + 1,
-                                 &next, src0, dst0, src1, dst1);
+                                 &next, src0, dst0, src1, dst1, dstx0, dstx1);
     copy_tiles<true, TILE>(rp, pre_r, R, -1, res_base, claim, &next, src0, dst0, src1, dst1);
   }
 }
@@ -157,7 +160,7 @@ hipError_t launch_copy_device(const GatherParams& p, int workers, hipStream_t s)
 
 hipError_t launch_gather_resident(const GatherParams& host, const GatherParams& dev, int* claim,
                                   int workers, hipStream_t s) {
-  if (workers < 1 || host.B > kMaxBatch || !claim) return hipErrorInvalidValue;
+  if (workers < 1 || host.B > kMaxBatch || !claim || !host.fan) return hipErrorInvalidValue;
   hipLaunchKernelGGL(gather_resident_kernel, dim3(workers), dim3(GT), 0, s, host, dev, claim);
   return hipGetLastError();
 }

@@ -70,18 +70,20 @@ __device__ __forceinline__ int find_request(const long long* pre, int B, long lo
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // Rows i < tn: copy chunks * sizeof(V) bytes from src[i] to dst[i] (src[i] == 0
-// skips the row), with NT threads each keeping U loads in flight.
+// skips the row), and also to dstx[i] when dstx is given and dstx[i] != 0, with
+// NT threads each keeping U loads in flight.
 template <typename V, int U = kUnroll, int NT = GT>
 __device__ __forceinline__ void copy_rows(const uint64_t* src, const uint64_t* dst, int tn,
-                                          int chunks) {
+                                          int chunks, const uint64_t* dstx = nullptr) {
   const int total = tn * chunks;
   for (int q0 = threadIdx.x; q0 < total; q0 += NT * U) {
     V v[U];
-    uint64_t da[U];
+    uint64_t da[U], xa[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int q = q0 + u * NT;
       da[u] = 0;
+      xa[u] = 0;
       if (q < total) {
         const int i = q / chunks;
         const int ch = q - i * chunks;
@@ -89,12 +91,15 @@ __device__ __forceinline__ void copy_rows(const uint64_t* src, const uint64_t* d
         if (s) {
           v[u] = *reinterpret_cast<const V*>(s + static_cast<uint64_t>(ch) * sizeof(V));
           da[u] = dst[i] + static_cast<uint64_t>(ch) * sizeof(V);
+          if (dstx && dstx[i]) xa[u] = dstx[i] + static_cast<uint64_t>(ch) * sizeof(V);
         }
       }
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int u = 0; u < U; ++u) {
       if (da[u]) *reinterpret_cast<V*>(da[u]) = v[u];
+      if (xa[u]) *reinterpret_cast<V*>(xa[u]) = v[u];
+    }
   }
 }
 
@@ -115,38 +120,49 @@ __device__ void copy_tile_rows(const GatherParams& p, int tn, uint64_t* src0, ui
 }
 
 // Copy entries [a, b) of the batch-wide list.  kDevice: an entry is (source
-// slot, slot) of the request's own buffers; otherwise (host row, slot).
+// slot, slot) of the request's own buffers; otherwise (host row, slot), and
+// with p.fan and staging for it (dstx0/1), the row also goes to the entry's
+// fan slot.
 template <bool kDevice>
 __device__ void copy_range(const GatherParams& p, const long long* pre, long long a, long long b,
-                           uint64_t* src0, uint64_t* dst0, uint64_t* src1, uint64_t* dst1) {
+                           uint64_t* src0, uint64_t* dst0, uint64_t* src1, uint64_t* dst1,
+                           uint64_t* dstx0 = nullptr, uint64_t* dstx1 = nullptr) {
   const size_t per_req = static_cast<size_t>(p.n_q) * p.K;
   for (long long t0 = a; t0 < b; t0 += TILE) {
     const int tn = static_cast<int>((b - t0) < TILE ? (b - t0) : TILE);
     for (int i = threadIdx.x; i < tn; i += GT) {
       const long long j = t0 + i;
       const int r = find_request(pre, p.B, j);
-      const int2 e = p.miss_list[static_cast<size_t>(r) * per_req + static_cast<size_t>(j - pre[r])];
+      const size_t at = static_cast<size_t>(r) * per_req + static_cast<size_t>(j - pre[r]);
+      const int2 e = p.miss_list[at];
       const bool ok = e.x >= 0 && e.y >= 0 && e.y < p.S &&
                       (kDevice ? e.x < p.S : static_cast<int64_t>(e.x) < p.rows[r]);
       const uint64_t base0 = kDevice ? p.buf_ptrs[r] : p.host_ptrs[r];
       src0[i] = ok ? base0 + static_cast<uint64_t>(e.x) * p.row_bytes0 : 0;
       dst0[i] = p.buf_ptrs[r] + static_cast<uint64_t>(e.y) * p.row_bytes0;
+      int fan = -1;
+      if (dstx0) {
+        fan = p.fan[at];
+        if (fan < 0 || fan >= p.S) fan = -1;
+        dstx0[i] = fan >= 0 ? p.buf_ptrs[r] + static_cast<uint64_t>(fan) * p.row_bytes0 : 0;
+      }
       if (p.n_streams > 1) {
         const uint64_t base1 = kDevice ? p.buf_ptrs[p.B + r] : p.host_ptrs[p.B + r];
         src1[i] = ok ? base1 + static_cast<uint64_t>(e.x) * p.row_bytes1 : 0;
         dst1[i] = p.buf_ptrs[p.B + r] + static_cast<uint64_t>(e.y) * p.row_bytes1;
+        if (dstx1) dstx1[i] = fan >= 0 ? p.buf_ptrs[p.B + r] + static_cast<uint64_t>(fan) * p.row_bytes1 : 0;
       }
     }
     __syncthreads();
     if ((p.row_bytes0 & 15) == 0)
-      copy_rows<u32x4>(src0, dst0, tn, static_cast<int>(p.row_bytes0 / 16));
+      copy_rows<u32x4>(src0, dst0, tn, static_cast<int>(p.row_bytes0 / 16), dstx0);
     else
-      copy_rows<uint32_t>(src0, dst0, tn, static_cast<int>(p.row_bytes0 / 4));
+      copy_rows<uint32_t>(src0, dst0, tn, static_cast<int>(p.row_bytes0 / 4), dstx0);
     if (p.n_streams > 1) {
       if ((p.row_bytes1 & 15) == 0)
-        copy_rows<u32x4>(src1, dst1, tn, static_cast<int>(p.row_bytes1 / 16));
+        copy_rows<u32x4>(src1, dst1, tn, static_cast<int>(p.row_bytes1 / 16), dstx1);
       else
-        copy_rows<uint32_t>(src1, dst1, tn, static_cast<int>(p.row_bytes1 / 4));
+        copy_rows<uint32_t>(src1, dst1, tn, static_cast<int>(p.row_bytes1 / 4), dstx1);
     }
     __syncthreads();
   }

@@ -141,10 +141,12 @@ struct Own {
 };
 
 // Words of LDS bookkeeping of the end-of-step plan besides the reservation
-// bitmap and the index map: per-wave counts of the three lists for two
+// bitmap and the two maps: per-wave counts of the three lists for two
 // compaction rounds, plus totals.
 constexpr int kPlanMiscWords = 6 * MW + 4;
 constexpr uint32_t kPlanResident = 0x80000000u;   // map word names a slot outside this step's reservations
+constexpr uint32_t kPlanRepeat = 0x40000000u;     // the word's index has a repeat this step
+constexpr uint32_t kPlanSlot = 0x00FFFFFFu;       // slot + 1
 
 // Home word of index x in the plan's map of P words (multiplicative hash).
 __device__ __forceinline__ uint32_t plan_home(int32_t x, uint32_t P) {
@@ -160,13 +162,32 @@ __device__ __forceinline__ uint32_t plan_home(int32_t x, uint32_t P) {
 //   a repeat copy from the largest slot this step reserved for x, when that is
 //   not o (a later token missed x again after its install was lost), or else
 //   a host copy.
-// The three lists keep transfer-list order.  LDS map: P words, open addressing
-// with linear probing keyed by the index a word names through c[]; a word is
-// (resident bit | slot + 1), 0 = empty, and atomicMax makes the choice
-// deterministic.  The map holds at most N_q * K keys and P >= 1.5 N_q K, so
-// every probe sequence ends at an empty word.
+// A host entry also writes its row to the largest repeat destination of its
+// index (its fan slot), so with two tokens per step no repeat is left for a
+// later copy; repeats bid for the fan slot with a global atomicMax on a
+// per-slot word of the request (fan_slots, reset for this step's reservations
+// first).  The lists keep transfer-list order.  LDS map: P words, open
+// addressing with linear probing keyed by the index a word names through c[];
+// a word is (resident bit | slot + 1), 0 = empty, and atomicMax makes every
+// choice deterministic.  The map holds at most N_q * K keys and
+// P >= 1.5 N_q K, so every probe sequence ends at an empty word.
 // v0: this thread's entry tid of the transfer list (loaded by the caller
 // before the table write-back, so its latency overlaps the write-back).
+__device__ __forceinline__ int plan_lookup(const uint32_t* smp, const int32_t* sc, uint32_t P,
+                                           int32_t x, uint32_t* word) {
+  uint32_t h = plan_home(x, P);
+  for (uint32_t t = 0; t < P; ++t) {
+    const uint32_t w = smp[h];
+    if (w == 0u) break;
+    if (sc[(w & kPlanSlot) - 1u] == x) {
+      *word = w;
+      return static_cast<int>(h);
+    }
+    h = (h + 1u == P) ? 0u : h + 1u;
+  }
+  return -1;
+}
+
 __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, unsigned char* lds,
                                              const int listed, const int64_t rows_r,
                                              const int64_t n_verified, const int2 v0) {
@@ -177,6 +198,7 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   const uint32_t P = static_cast<uint32_t>(p.plan_words);
   uint32_t* smp = sres + nb;                                        // [P] index map
   int* scnt = reinterpret_cast<int*>(smp + P);                      // [kPlanMiscWords]
+  int32_t* gfan = p.fan_slots + static_cast<size_t>(r) * S;         // [S] fan slot per reserved slot
   const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
   const size_t lb = static_cast<size_t>(r) * p.n_q * p.K;
   const int2* ml = p.miss_list + lb;
@@ -193,13 +215,14 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
     const int2 v = e < MT ? v0 : ml[e];
     if (v.y < 0 || v.y >= S) continue;
     atomicOr(&sres[v.y >> 5], 1u << (v.y & 31));
+    if (p.n_q > 1) gfan[v.y] = -1;
     if (v.x < 0 || static_cast<int64_t>(v.x) >= rows_r) continue;
     const uint32_t val = static_cast<uint32_t>(v.y) + 1u;
     uint32_t h = plan_home(v.x, P);
     for (uint32_t t = 0; t < P; ++t) {
       const uint32_t w = atomicCAS(&smp[h], 0u, val);
       if (w == 0u) break;
-      if (sc[(w & ~kPlanResident) - 1u] == v.x) {
+      if (sc[(w & kPlanSlot) - 1u] == v.x) {
         atomicMax(&smp[h], val);
         break;
       }
@@ -234,7 +257,7 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
       if (ws[u] != 0u && ((sres[j >> 5] >> (j & 31)) & 1u)) ws[u] = 0u;
       uint32_t h = hs[u], w = ws[u];
       for (uint32_t t = 0; w != 0u && t < P; ++t) {
-        if (sc[(w & ~kPlanResident) - 1u] == xs[u]) {
+        if (sc[(w & kPlanSlot) - 1u] == xs[u]) {
           atomicMax(&smp[h], kPlanResident | (static_cast<uint32_t>(j0 + u * MT) + 1u));
           break;
         }
@@ -245,35 +268,65 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   }
   __syncthreads();
 
-  // (3) classify in transfer-list order and compact the three lists
-  int n_list[3] = {0, 0, 0};
-  for (int e0 = 0, it = 0; e0 < listed; e0 += MT, ++it) {
-    const int e = e0 + tid;
-    int kind = -1;                 // 0 host, 1 resident, 2 repeat
-    int2 v = make_int2(0, 0);
-    int src = 0;
-    if (e < listed) {
-      v = e < MT ? v0 : ml[e];
-      kind = 0;
-      if (v.x >= 0 && static_cast<int64_t>(v.x) < rows_r) {
-        uint32_t h = plan_home(v.x, P);
-        for (uint32_t t = 0; t < P; ++t) {
-          const uint32_t w = smp[h];
-          if (w == 0u) break;
-          const int o = static_cast<int>(w & ~kPlanResident) - 1;
-          if (sc[o] == v.x) {
-            if (w & kPlanResident) {
-              kind = 1;
-              src = o;
-            } else if (o != v.y) {
-              kind = 2;
-              src = o;
-            }
-            break;
-          }
-          h = (h + 1u == P) ? 0u : h + 1u;
-        }
+  // classify one entry: 0 host, 1 resident, 2 repeat (src = source slot,
+  // *hw = its map position), -1 past the list
+  auto classify = [&](int e, int2* v, int* src, int* hw) {
+    *src = 0;
+    *hw = -1;
+    if (e >= listed) return -1;
+    *v = e < MT ? v0 : ml[e];
+    if (v->x < 0 || static_cast<int64_t>(v->x) >= rows_r) return 0;
+    uint32_t w = 0u;
+    *hw = plan_lookup(smp, sc, P, v->x, &w);
+    if (*hw < 0) return 0;
+    const int o = static_cast<int>(w & kPlanSlot) - 1;
+    if (w & kPlanResident) {
+      *src = o;
+      return 1;
+    }
+    if (o != v->y) {
+      *src = o;
+      return 2;
+    }
+    return 0;
+  };
+
+  // (3) every repeat bids for its source's fan slot (the largest destination
+  // wins) and flags its index's map word; repeats need two tokens in the
+  // step.  The first round's classification is kept for (4).
+  int2 v_first = make_int2(0, 0);
+  int src_first = 0, hw_first = -1;
+  const int kind_first = classify(tid, &v_first, &src_first, &hw_first);
+  if (p.n_q > 1) {
+    for (int e = tid; e < listed; e += MT) {
+      int2 v = v_first;
+      int src = src_first, hw = hw_first;
+      const int kind = e < MT ? kind_first : classify(e, &v, &src, &hw);
+      if (kind == 2) {
+        atomicMax(&gfan[src], v.y);
+        atomicOr(&smp[hw], kPlanRepeat);
       }
+    }
+  }
+  __syncthreads();
+  // fan words are read past the L1, where the bids were made
+  auto fan_of = [&](int slot) {
+    return __hip_atomic_load(&gfan[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  };
+
+  // (4) compact the three lists in transfer-list order; host entries carry
+  // their fan slot, repeats that won the fan word leave the repeat list
+  int n_list[3] = {0, 0, 0}, n_rep = 0;
+  for (int e0 = 0, it = 0; e0 < listed; e0 += MT, ++it) {
+    int2 v = v_first;
+    int src = src_first, hw = hw_first;
+    int kind = it == 0 ? kind_first : classify(e0 + tid, &v, &src, &hw);
+    int fan = -1;
+    // only indices flagged by a repeat read their fan slot
+    if (kind == 0 && hw >= 0 && (smp[hw] & kPlanRepeat) && v.y >= 0 && v.y < S) fan = fan_of(v.y);
+    if (kind == 2) {
+      ++n_rep;
+      if (fan_of(src) == v.y) kind = 3;   // written by the host copy
     }
     uint64_t mk[3];
     int* wc = scnt + (it & 1) * 3 * MW;
@@ -293,7 +346,9 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
       }
     }
     if (kind == 0) {
-      p.host_list[lb + n_list[0] + before[0] + bits_below(mk[0])] = v;
+      const size_t at = lb + n_list[0] + before[0] + bits_below(mk[0]);
+      p.host_list[at] = v;
+      p.host_fan[at] = fan;
     } else if (kind == 1) {
       p.res_list[lb + n_list[1] + before[1] + bits_below(mk[1])] = make_int2(src, v.y);
     } else if (kind == 2) {
@@ -302,6 +357,9 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
 #pragma unroll
     for (int k = 0; k < 3; ++k) n_list[k] += total[k];
   }
+  n_rep = wave_sum(n_rep);
+  if (lane == 0 && n_rep) atomicAdd(&scnt[6 * MW], n_rep);
+  __syncthreads();
   if (tid == 0) {
     int32_t* pc = p.plan_counts + 3 * static_cast<size_t>(r);
     pc[0] = n_list[0];
@@ -309,7 +367,7 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
     pc[2] = n_list[2];
     unsigned long long* st = p.stats + static_cast<size_t>(r) * kNumStats;
     if (n_list[1]) atomicAdd(&st[kStatResident], static_cast<unsigned long long>(n_list[1]));
-    if (n_list[2]) atomicAdd(&st[kStatDuplicate], static_cast<unsigned long long>(n_list[2]));
+    if (scnt[6 * MW]) atomicAdd(&st[kStatDuplicate], static_cast<unsigned long long>(scnt[6 * MW]));
   }
 }
 

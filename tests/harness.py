@@ -163,12 +163,13 @@ def run_parity(spec: W.Spec, steps: Optional[int] = None, table_every: int = 16,
                     mx, mo = orc.o.misses(r, n_ref[r])
                     c_ref, _ = orc.o.export(r)
                     plan = ORC.transfer_plan(mx, mo, c_ref, int(wl.ctx[r]))
-                    want_res += len(plan[2])
-                    want_dup += len(plan[4])
+                    want_res += len(plan[3])
+                    want_dup += len(plan[5]) + int(np.sum(plan[2] >= 0))
                     if r in sampled:
                         got = gpu.op.export_plan(r)
-                        for k, name in enumerate(("host index", "host slot", "resident source",
-                                                  "resident slot", "repeat source", "repeat slot")):
+                        for k, name in enumerate(("host index", "host slot", "host fan slot",
+                                                  "resident source", "resident slot", "repeat source",
+                                                  "repeat slot")):
                             assert np.array_equal(plan[k], got[k]), \
                                 f"step {t} request {r}: plan {name} list differs"
             last = t == T - 1

@@ -281,7 +281,7 @@ def test_resident_reuse_with_bad_indices():
             torch.cuda.synchronize()
             assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
             assert torch.equal(ops[0].buffers[0], ops[1].buffers[0]), f"step {t}"
-            hx, ho, rs, rd, ps, pd = ops[1].export_plan(0)
+            hx, ho, hf, rs, rd, ps, pd = ops[1].export_plan(0)
             mx, _ = ops[1].export_misses(0)
             assert sorted(hx[hx >= rows].tolist()) == sorted(mx[mx >= rows].tolist())
         st = ops[1].stats()
@@ -426,7 +426,7 @@ def test_resident_reuse_when_verified_length_shrinks():
                 c_ref, _ = orc.o.export(r)
                 want = ORC.transfer_plan(mx, mo, c_ref, int(wl.ctx[r]))
                 got = gpu.op.export_plan(r)
-                for k in range(6):
+                for k in range(7):
                     assert np.array_equal(want[k], got[k]), f"step {t} request {r}: plan list {k}"
                 reserved = set(mo.tolist())
                 for x in mx.tolist():

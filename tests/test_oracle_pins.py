@@ -459,13 +459,15 @@ def test_config_errors(oracle_lib):
 # ---------------------------------------------------------------------------
 def _replay_plan(buf, plan, rows):
     """Apply a plan to a buffer of row ids in the kernels' order: host entries
-    (ids outside [0, rows) are skipped, as by the copy) and resident copies,
-    then repeat copies."""
-    hx, ho, rs, rd, ps, pd = plan
+    into their slot and fan slot (ids outside [0, rows) are skipped, as by the
+    copy) and resident copies, then repeat copies."""
+    hx, ho, hf, rs, rd, ps, pd = plan
     res = buf[rs].copy()                    # resident sources are not written this step
-    for x, o in zip(hx.tolist(), ho.tolist()):
+    for x, o, f in zip(hx.tolist(), ho.tolist(), hf.tolist()):
         if 0 <= x < rows:
             buf[o] = x
+            if f >= 0:
+                buf[f] = x
     for v, o in zip(res.tolist(), rd.tolist()):
         buf[o] = v
     rep = buf[ps].copy()
@@ -503,11 +505,13 @@ def test_transfer_plan_replays_stage_two(oracle_lib, K, n_q, S, R, L, U, T, bad)
                     paper[r][o] = x
             c, _ = orc.export(r)
             plan = O.transfer_plan(mx, mo, c, rows)
-            hx, ho, rs, rd, ps, pd = plan
-            nr, nd = len(rs), len(ps)
+            hx, ho, hf, rs, rd, ps, pd = plan
+            fanned = int(np.sum(hf >= 0))
+            nr, nd = len(rs), len(ps) + fanned
             assert len(hx) + nr + nd == len(mx)
             assert not set(rs.tolist()) & set(mo.tolist())     # resident sources are not reserved
             assert set(ps.tolist()) <= set(ho.tolist())        # repeat sources get a host copy
+            assert set(hf[hf >= 0].tolist()) <= set(mo.tolist()) - set(ho.tolist())
             # host entries read distinct valid rows
             valid = [x for x in hx.tolist() if 0 <= x < rows]
             assert len(valid) == len(set(valid))
@@ -535,23 +539,36 @@ def test_transfer_plan_finds_an_orphaned_slot(oracle_lib):
     new = int(mo[0])
     assert new != 5
     cc, _ = orc.export(0)
-    hx, ho, rs, rd, ps, pd = O.transfer_plan(mx, mo, cc, 100)
+    hx, ho, hf, rs, rd, ps, pd = O.transfer_plan(mx, mo, cc, 100)
     assert len(hx) == 0 and rs.tolist() == [5] and rd.tolist() == [new] and len(ps) == 0
     # with the orphan invalidated (c = -1) the row must come from the host
     cc2 = cc.copy()
     cc2[5] = -1
-    hx, ho, rs, rd, ps, pd = O.transfer_plan(mx, mo, cc2, 100)
-    assert hx.tolist() == [42] and ho.tolist() == [new] and len(rs) == 0 and len(ps) == 0
+    hx, ho, hf, rs, rd, ps, pd = O.transfer_plan(mx, mo, cc2, 100)
+    assert hx.tolist() == [42] and ho.tolist() == [new] and hf.tolist() == [-1]
+    assert len(rs) == 0 and len(ps) == 0
 
 
 def test_transfer_plan_same_step_repeat(oracle_lib):
     """Hand case: the same id listed by two tokens of one step (its first
     install lost) is copied from the host once, into the larger slot, and the
-    other slot is filled from it."""
+    same copy writes the other slot (its fan slot)."""
     mx = np.array([7, 9, 7], dtype=np.int32)
     mo = np.array([2, 3, 6], dtype=np.int32)
     c = np.full(8, -1, dtype=np.int32)
     c[2], c[3], c[6] = 7, 9, 7
-    hx, ho, rs, rd, ps, pd = O.transfer_plan(mx, mo, c, 10)
-    assert hx.tolist() == [9, 7] and ho.tolist() == [3, 6]
-    assert ps.tolist() == [6] and pd.tolist() == [2] and len(rs) == 0
+    hx, ho, hf, rs, rd, ps, pd = O.transfer_plan(mx, mo, c, 10)
+    assert hx.tolist() == [9, 7] and ho.tolist() == [3, 6] and hf.tolist() == [-1, 2]
+    assert len(ps) == 0 and len(rs) == 0
+
+
+def test_transfer_plan_three_tokens_repeat(oracle_lib):
+    """Hand case: an id listed by three tokens: one host copy into the largest
+    slot, the largest other slot as its fan slot, the third copied after."""
+    mx = np.array([7, 7, 7], dtype=np.int32)
+    mo = np.array([4, 1, 3], dtype=np.int32)
+    c = np.full(8, -1, dtype=np.int32)
+    c[1], c[3], c[4] = 7, 7, 7
+    hx, ho, hf, rs, rd, ps, pd = O.transfer_plan(mx, mo, c, 10)
+    assert hx.tolist() == [7] and ho.tolist() == [4] and hf.tolist() == [3]
+    assert ps.tolist() == [4] and pd.tolist() == [1] and len(rs) == 0
