@@ -43,14 +43,23 @@ __global__ __launch_bounds__(GT) void gather_balanced_kernel(GatherParams p) {
 // in one round), later tiles are claimed with an atomic counter, so the
 // workgroups that finish first take more (a CU's host-read rate varies up to
 // 2x across the chip; claimed tiles end the kernel more evenly than a static
-// Eq. 6 split).  claim[0] and claim[1] count the claimed resident and host
-// rows; the matching kernel resets both.
+// Eq. 6 split).  A list shorter than one full tile per workgroup of its group
+// is cut into tiles of ceil(n / group) rows, so a step with few misses still
+// spreads them over many CUs (one workgroup reads ~2.5 GB/s from the host).
+// claim[0] and claim[1] count the claimed resident and host rows; the
+// matching kernel resets both.
 constexpr int kHostTile = 32;
+
+// Rows per tile of a list of n entries shared by `group` workgroups.
+__device__ __forceinline__ int tile_rows(long long n, int group, int max_rows) {
+  const long long t = (n + group - 1) / group;
+  return t < 1 ? 1 : (t > max_rows ? max_rows : static_cast<int>(t));
+}
 
 // Copy tiles of T entries of a list of n entries: `first` (or none, -1) then
 // claimed tiles, which start at row `base`.
-template <bool kDevice, int T>
-__device__ void copy_tiles(const GatherParams& p, const long long* pre, long long n, long long first,
+template <bool kDevice>
+__device__ void copy_tiles(const GatherParams& p, const long long* pre, long long n, int T, long long first,
                            long long base, int* counter, long long* next, uint64_t* src0,
                            uint64_t* dst0, uint64_t* src1, uint64_t* dst1, uint64_t* dstx0 = nullptr,
                            uint64_t* dstx1 = nullptr) {
@@ -78,19 +87,20 @@ __global__ __launch_bounds__(GT) void gather_resident_kernel(GatherParams hp, Ga
   request_prefix(rp, pre_r, wtot);
   const long long N = pre_h[hp.B], R = pre_r[rp.B];
   const int C = static_cast<int>(gridDim.x), w = static_cast<int>(blockIdx.x);
-  const int cr = C / 4;                  // workgroups that start with the resident list
-  const int ch = C - cr;
-  const long long host_base = static_cast<long long>(ch) * kHostTile;
-  const long long res_base = static_cast<long long>(cr) * TILE;
+  const int cr = C / 4;                  // workgroups that start with the resident list (may be 0)
+  const int ch = C - cr;                 // >= 1
+  const int th = tile_rows(N, ch, kHostTile), tr = tile_rows(R, cr > 0 ? cr : ch, TILE);
+  const long long host_base = static_cast<long long>(ch) * th;
+  const long long res_base = static_cast<long long>(cr) * tr;
   if (w >= ch) {
     const long long i = C - 1 - w;       // 0 .. cr-1
-    copy_tiles<true, TILE>(rp, pre_r, R, i * TILE, res_base, claim, &next, src0, dst0, src1, dst1);
-    copy_tiles<false, kHostTile>(hp, pre_h, N, -1, host_base, claim + 1, &next, src0, dst0, src1, dst1,
-                                 dstx0, dstx1);
+    copy_tiles<true>(rp, pre_r, R, tr, i * tr, res_base, claim, &next, src0, dst0, src1, dst1);
+    copy_tiles<false>(hp, pre_h, N, th, -1, host_base, claim + 1, &next, src0, dst0, src1, dst1,
+                      dstx0, dstx1);
   } else {
-    copy_tiles<false, kHostTile>(hp, pre_h, N, static_cast<long long>(w) * kHostTile, host_base, claim + 1,
-                                 &next, src0, dst0, src1, dst1, dstx0, dstx1);
-    copy_tiles<true, TILE>(rp, pre_r, R, -1, res_base, claim, &next, src0, dst0, src1, dst1);
+    copy_tiles<false>(hp, pre_h, N, th, static_cast<long long>(w) * th, host_base, claim + 1,
+                      &next, src0, dst0, src1, dst1, dstx0, dstx1);
+    copy_tiles<true>(rp, pre_r, R, tr, -1, res_base, claim, &next, src0, dst0, src1, dst1);
   }
 }
 

@@ -130,7 +130,7 @@ def content_check(host: HostRows, wl: W.Workload, bufs, X, O):
 
 def run_parity(spec: W.Spec, steps: Optional[int] = None, table_every: int = 16,
                buffers_every: int = 64, miss_list_requests: int = 2, gather_mode: int = 0,
-               retry=3, max_life=16, coherent=False):
+               retry=3, max_life=16, coherent=False, gather_workers=0):
     """Drive `steps` decode steps through both sides; raise on any mismatch.
     Returns (oracle totals, gpu stats)."""
     wl = W.Workload(spec)
@@ -139,7 +139,8 @@ def run_parity(spec: W.Spec, steps: Optional[int] = None, table_every: int = 16,
         f"gather_mode={gather_mode}")
     host = HostRows(wl, coherent=coherent)
     orc = OracleSide(wl, host, retry=retry, max_life=max_life)
-    gpu = GpuSide(wl, host, retry=retry, max_life=max_life, gather_mode=gather_mode)
+    gpu = GpuSide(wl, host, retry=retry, max_life=max_life, gather_mode=gather_mode,
+                  gather_workers=gather_workers)
     from paper_2609_37538_amd import avsg as A
     resident = gather_mode == A.AVSG_GATHER_RESIDENT
     want_res = want_dup = 0

@@ -260,6 +260,19 @@ def test_resident_reuse_parity(name, kw, retry):
     assert got["host_bytes"] + moved_on_device == got["bytes_moved"]
 
 
+@pytest.mark.parametrize("workers", [1, 3, 5, 9, 1000])
+def test_resident_reuse_worker_counts(workers):
+    """Resident-reuse transfer with grids from one workgroup (no workgroup
+    starts with the resident list) to more workgroups than rows: every host,
+    fan and resident row is still copied exactly once."""
+    from paper_2609_37538_amd import avsg as A
+    spec = W.custom_spec(name=f"res_workers_{workers}", batch=3, topk=256, slots=512, n_q=2, steps=12,
+                         ctx=3000, retention=0.8, row_bytes=(1152, 132))
+    ref, got = run_parity(spec, table_every=4, buffers_every=1, miss_list_requests=3,
+                          gather_mode=A.AVSG_GATHER_RESIDENT, retry=0, gather_workers=workers)
+    assert got["resident_rows"] > 0 and got["duplicate_rows"] > 0
+
+
 def test_resident_reuse_with_bad_indices():
     """Indices outside [0, rows) stay host entries that the copy skips, and the
     buffers match the balanced transfer's step by step."""
