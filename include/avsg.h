@@ -163,7 +163,9 @@ avsg_status avsg_create(const avsg_config *cfg, const void *const *host_rows,
  *   d_miss_counts   device int32 [B][N_q] out: miss count n_g of every token.
  * When the step's kernels finish, every slot named in d_slots holds the row of
  * its index in every stream.  Indices outside [0, rows) are counted in
- * bad_indices and not copied.  Errors: AVSG_E_INVAL, AVSG_E_HIP. */
+ * bad_indices and not copied.  The current HIP device must be the one that
+ * was current at avsg_create.  Errors: AVSG_E_INVAL (null pointer, other
+ * device), AVSG_E_HIP. */
 avsg_status avsg_step(avsg_handle *h, const int32_t *d_topk, const int64_t *d_verified_len,
                       int32_t *d_slots, int32_t *d_miss_counts, void *stream);
 

@@ -334,11 +334,16 @@ class Operator:
     def step(self, topk, verified_len=None):
         """topk: cuda int32 [B][n_q][K]; verified_len: cuda int64 [B] or None."""
         t = self.torch
-        assert topk.dtype == t.int32 and topk.is_cuda and topk.is_contiguous()
-        assert tuple(topk.shape) == (self.cfg.batch, self.cfg.n_q, self.cfg.topk)
+        want = (self.cfg.batch, self.cfg.n_q, self.cfg.topk)
+        if (topk.dtype != t.int32 or topk.device != self.slots.device or not topk.is_contiguous()
+                or tuple(topk.shape) != want):
+            raise ValueError(f"topk must be a contiguous int32 tensor of shape {want} on {self.slots.device}")
         vp = None
         if verified_len is not None:
-            assert verified_len.dtype == t.int64 and verified_len.is_cuda
+            if (verified_len.dtype != t.int64 or verified_len.device != self.slots.device
+                    or not verified_len.is_contiguous() or verified_len.numel() != self.cfg.batch):
+                raise ValueError(f"verified_len must be a contiguous int64 tensor of {self.cfg.batch} "
+                                 f"values on {self.slots.device}")
             vp = verified_len.data_ptr()
         avsg_step(self.h, topk.data_ptr(), vp, self.slots.data_ptr(), self.miss_counts.data_ptr(),
                   self.stream.cuda_stream)

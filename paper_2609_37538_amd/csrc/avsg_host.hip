@@ -307,6 +307,8 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
   h->workers = c.gather_workers > 0 ? c.gather_workers : std::max(1, cus);
 
   auto cleanup = [&](avsg_status rc) {
+    if (h->h_counts) (void)hipHostFree(h->h_counts);
+    if (h->h_list) (void)hipHostFree(h->h_list);
     delete h;
     return rc;
   };
@@ -369,7 +371,13 @@ static avsg_status record(avsg_handle* h, int which, hipStream_t s) {
   if (h->events.size() <= h->n_timed) {
     std::array<hipEvent_t, 4> ev{};
     // timing-only events: no system-scope cache write-back/invalidate at record
-    for (auto& x : ev) HIP_TRY(h, hipEventCreateWithFlags(&x, hipEventDisableSystemFence));
+    for (size_t i = 0; i < ev.size(); ++i) {
+      const hipError_t e = hipEventCreateWithFlags(&ev[i], hipEventDisableSystemFence);
+      if (e != hipSuccess) {
+        for (size_t j = 0; j < i; ++j) (void)hipEventDestroy(ev[j]);
+        return hip_fail(h, e, "hipEventCreateWithFlags");
+      }
+    }
     h->events.push_back(ev);
     h->has_tail.push_back(false);
   }
@@ -415,6 +423,11 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
                       int32_t* d_slots, int32_t* d_miss_counts, void* stream) {
   if (!h || !d_topk || !d_slots || !d_miss_counts) return AVSG_E_INVAL;
   const avsg_config& c = h->cfg;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != h->device) {
+    h->err = "avsg_step: the current device is not the one the handle was created on";
+    return AVSG_E_INVAL;
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
   h->last_stream = s;
   h->last_counts = d_miss_counts;
