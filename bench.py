@@ -352,7 +352,7 @@ def appendix_d_sweep(out_path):
 
 def _timed_run(spec, cfg_kw, warm, timed, host_ptrs, dev, verified=False):
     """Run warm + timed steps of `spec` through one operator; return
-    (match_ms[], gather_ms[], stats delta)."""
+    (match_ms[], gather_ms[], stats delta, wall seconds of the timed steps)."""
     import torch
     import workload as W
     from paper_2609_37538_amd import avsg as A
@@ -367,15 +367,39 @@ def _timed_run(spec, cfg_kw, warm, timed, host_ptrs, dev, verified=False):
         torch.cuda.synchronize()
         before = op.stats()
         A.avsg_set_timing(op.h, True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
         for t in range(warm, warm + timed):
             op.step(X[t], N[t] if verified else None)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
         match_ms, gather_ms, tail_ms = A.avsg_timing(op.h, timed)
         gather_ms = gather_ms + tail_ms       # all of Stage Two
         after = op.stats()
     finally:
         op.close()
     delta = {k: after[k] - before[k] for k in after if k != "max_step_alloc_decays"}
-    return match_ms, gather_ms, delta
+    return match_ms, gather_ms, delta, wall
+
+
+def _oracle_us_per_step(spec, wl, host_ptrs, warm, timed):
+    """The CPU oracle (match + Stage Two copy into host images of the buffers)
+    on the same warm + timed steps from a cold start: µs per timed step and
+    the threads it used."""
+    import oracle as ORC
+    threads = ORC.default_threads()
+    o = ORC.Oracle(spec.batch, spec.topk, spec.n_q, spec.slots, nthreads=threads)
+    images = [np.zeros((spec.batch, spec.slots, rb), dtype=np.uint8) for rb in spec.row_bytes]
+    bptr = [images[s][r].ctypes.data for s in range(len(spec.row_bytes)) for r in range(spec.batch)]
+    X = wl.all_steps(warm + timed)
+    spent = 0.0
+    for t in range(warm + timed):
+        N = wl.verified_len(t) if spec.speculative else None
+        t0 = time.perf_counter()
+        o.step(X[t], N, host=host_ptrs, buf=bptr, row_bytes=list(spec.row_bytes))
+        if t >= warm:
+            spent += time.perf_counter() - t0
+    return spent / timed * 1e6, threads
 
 
 def matching_sweep(out_path):
@@ -405,9 +429,9 @@ def matching_sweep(out_path):
             spec = W.custom_spec(name="match_sweep", cfg_id=11, batch=B, topk=K, slots=S, n_q=1,
                                  steps=warm + timed, ctx=ctx, retention=0.9)
             mm = A.AVSG_MATCH_DUALPTR if method == "dualptr" else A.AVSG_MATCH_HASH
-            match_ms, _, d = _timed_run(spec, dict(row_bytes=(rb,), match_mode=mm,
-                                                   gather_mode=A.AVSG_GATHER_NONE),
-                                        warm, timed, ptrs[:B], dev)
+            match_ms, _, d, _ = _timed_run(spec, dict(row_bytes=(rb,), match_mode=mm,
+                                                      gather_mode=A.AVSG_GATHER_NONE),
+                                           warm, timed, ptrs[:B], dev)
             row = {"panel": panel, "method": method, "batch": B, "S": S, "K": K,
                    "match_us_median": round(float(np.median(match_ms)) * 1e3, 2),
                    "hit_rate": round(d["hits"] / max(1, d["lookups"]), 4)}
@@ -441,8 +465,8 @@ def lifetime_sweep(out_path):
     ptrs = [host.ptr + r * ctx * W.KV_ROW_BYTES for r in range(B)]
     results = []
     for L in (1, 2, 4, 8, 16, 32):
-        match_ms, gather_ms, d = _timed_run(spec, dict(row_bytes=(W.KV_ROW_BYTES,), max_life=L),
-                                            warm, timed, ptrs, dev, verified=True)
+        match_ms, gather_ms, d, _ = _timed_run(spec, dict(row_bytes=(W.KV_ROW_BYTES,), max_life=L),
+                                               warm, timed, ptrs, dev, verified=True)
         row = {"L": L, "hit_rate": round(d["hits"] / max(1, d["lookups"]), 4),
                "adjacent_step_reuse": round(float(adj), 4),
                "match_us_median": round(float(np.median(match_ms)) * 1e3, 2),
@@ -457,21 +481,34 @@ def lifetime_sweep(out_path):
 
 def config_table(out_path):
     """Every workload (tiny, batch16, batch64_mtp2, imbalance, stress) under the
-    balanced (S3), request-level (S1), position-level (S2), pipelined and
-    resident-reuse Stage Two, plus the dual-pointer matching ablation (S = K)
-    on the single-token workloads: 16 warm-up steps from a cold start, then 64
-    timed steps; medians and sums from HIP events on the step stream.
-    gather_gbps = bytes read over the host link / Stage Two time."""
+    balanced (S3), request-level (S1), position-level (S2), copy-engine,
+    pipelined and resident-reuse Stage Two, plus the dual-pointer matching
+    ablation (S = K) on the single-token workloads: 16 warm-up steps from a
+    cold start, then 64 timed steps; medians and sums from HIP events on the
+    step stream, wall time between two synchronizations around the timed
+    steps (with the events).  gather_gbps = bytes read over the host link /
+    Stage Two time, also as fractions of the measured hipMemcpy H2D peak and
+    of PCIe Gen5 x16.  Each workload also times the CPU oracle on the same
+    steps."""
     import dataclasses
     import torch
     import workload as W
     from paper_2609_37538_amd import avsg as A
     dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
     cus = A.avsg_device_cus()
     warm, timed = 16, 64
+    probe = A.HostRegion(512 << 20)
+    tmp = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    peak = A.avsg_h2d_peak(probe.ptr, tmp.data_ptr(), 512 << 20, 20,
+                           torch.cuda.current_stream(dev).cuda_stream)
+    del tmp
+    probe.free()
+    print(json.dumps({"hipmemcpy_h2d_peak_gbps": round(peak, 3)}), flush=True)
     strategies = [("S3 balanced", A.AVSG_MATCH_HASH, A.AVSG_GATHER_BALANCED),
                   ("S1 request", A.AVSG_MATCH_HASH, A.AVSG_GATHER_REQUEST),
                   ("S2 position", A.AVSG_MATCH_HASH, A.AVSG_GATHER_POSITION),
+                  ("copy engines", A.AVSG_MATCH_HASH, A.AVSG_GATHER_SDMA),
                   ("pipelined", A.AVSG_MATCH_HASH, A.AVSG_GATHER_PIPELINED),
                   ("resident reuse", A.AVSG_MATCH_HASH, A.AVSG_GATHER_RESIDENT),
                   ("dual-pointer + S3", A.AVSG_MATCH_DUALPTR, A.AVSG_GATHER_BALANCED)]
@@ -494,7 +531,7 @@ def config_table(out_path):
                 run_spec = dataclasses.replace(spec, slots=spec.topk)
             if gm == A.AVSG_GATHER_PIPELINED and spec.batch > cus:
                 continue
-            match_ms, gather_ms, d = _timed_run(
+            match_ms, gather_ms, d, wall = _timed_run(
                 run_spec, dict(row_bytes=spec.row_bytes, match_mode=mm, gather_mode=gm),
                 warm, timed, ptrs, dev, verified=spec.speculative)
             if gm == A.AVSG_GATHER_PIPELINED:
@@ -512,10 +549,19 @@ def config_table(out_path):
                    "kernel_us_per_step": round((gsec + (float(np.sum(match_ms)) * 1e-3
                                                         if match_ms is not None else 0.0))
                                                / timed * 1e6, 2),
+                   "wall_us_per_step": round(wall / timed * 1e6, 2),
                    "gather_gbps": round(moved / gsec / 1e9, 3) if gsec > 0 else 0.0,
+                   "frac_of_hipmemcpy_peak": round(moved / gsec / 1e9 / peak, 4) if gsec > 0 else 0.0,
+                   "frac_of_pcie_gen5_x16": (round(moved / gsec / 1e9 / PCIE_GEN5_X16_GBPS, 4)
+                                             if gsec > 0 else 0.0),
                    "lost_installs_per_step": round((d["lost_exhausted"] + d["lost_collision"]) / timed, 1)}
             results.append(row)
             print(json.dumps(row), flush=True)
+        us, threads = _oracle_us_per_step(spec, wl, ptrs, warm, timed)
+        row = {"workload": name, "strategy": "CPU oracle", "batch": spec.batch, "topk": spec.topk,
+               "slots": spec.slots, "n_q": spec.n_q, "wall_us_per_step": round(us, 1), "cores": threads}
+        results.append(row)
+        print(json.dumps(row), flush=True)
         for reg in regions:
             reg.free()
     with open(out_path, "w") as f:
