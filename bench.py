@@ -146,6 +146,7 @@ def main():
         op.step(X_dev[t], N_dev[t] if spec.speculative else None)
     torch.cuda.synchronize()
     before = op.stats()
+    before_r = [op.request_stats(r) for r in range(spec.batch)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for t in range(args.warmup, T):
@@ -155,6 +156,9 @@ def main():
     match_all, gather_all, tail_all = A.avsg_timing(op.h, T)
     A.avsg_set_timing(op.h, False)
     after = op.stats()
+    after_r = [op.request_stats(r) for r in range(spec.batch)]
+    # request-averaged hit rate over the timed steps (each request's own rate, then the mean)
+    per_req = [(a["hits"] - b["hits"]) / max(1, a["lookups"] - b["lookups"]) for a, b in zip(after_r, before_r)]
     match_ms, gather_ms = match_all[args.warmup:], gather_all[args.warmup:]
     tail_ms = tail_all[args.warmup:]
     wall_events = wall
@@ -243,6 +247,10 @@ def main():
             "steps_timed": f"{args.warmup}..{T - 1}",
         },
         "hit_rate": round(hits / max(1, lookups), 5),
+        "hit_rate_request_mean": round(float(np.mean(per_req)), 5),
+        "hit_rate_from_step0": round(after["hits"] / max(1, after["lookups"]), 5),
+        "lost_installs_per_step": round((after["lost_exhausted"] + after["lost_collision"]
+                                         - before["lost_exhausted"] - before["lost_collision"]) / K, 1),
         "misses_per_step": round(misses / K, 1),
         "host_rows_per_step": round(host_moved / row_total / K, 1) if row_total else 0.0,
         "delivered_gbps": round(moved / wall / 1e9, 3) if moved else 0.0,

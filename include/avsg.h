@@ -171,6 +171,12 @@ avsg_status avsg_step(avsg_handle *h, const int32_t *d_topk, const int64_t *d_ve
 
 /* Cumulative counters.  Synchronizes with the handle's last stream. */
 avsg_status avsg_stats(avsg_handle *h, avsg_stats_t *out);
+
+/* The same counters for request r alone (lookups = steps * N_q * K), for
+ * per-request hit rates such as the request-averaged rate the paper reports
+ * over real requests (Appendix A).  queue_timeouts is 0.  Synchronizes with the
+ * handle's last stream.  Errors: AVSG_E_INVAL (r outside [0, B)), AVSG_E_HIP. */
+avsg_status avsg_request_stats(avsg_handle *h, int32_t r, avsg_stats_t *out);
 avsg_status avsg_reset_stats(avsg_handle *h, void *stream);
 
 /* Return request r's table to the initial empty state (a new request takes

@@ -99,6 +99,8 @@ def load():
     lib.avsg_step.argtypes = [_P, _P, _P, _P, _P, _P]
     lib.avsg_stats.restype = i32
     lib.avsg_stats.argtypes = [_P, ctypes.POINTER(AvsgStats)]
+    lib.avsg_request_stats.restype = i32
+    lib.avsg_request_stats.argtypes = [_P, i32, ctypes.POINTER(AvsgStats)]
     lib.avsg_reset_stats.restype = i32
     lib.avsg_reset_stats.argtypes = [_P, _P]
     lib.avsg_reset_request.restype = i32
@@ -193,6 +195,12 @@ def avsg_step(h, d_topk: int, d_verified_len: Optional[int], d_slots: int, d_mis
 def avsg_stats(h) -> dict:
     s = AvsgStats()
     _check(load().avsg_stats(h, ctypes.byref(s)), "avsg_stats", h)
+    return s.as_dict()
+
+
+def avsg_request_stats(h, r: int) -> dict:
+    s = AvsgStats()
+    _check(load().avsg_request_stats(h, r, ctypes.byref(s)), "avsg_request_stats", h)
     return s.as_dict()
 
 
@@ -351,6 +359,9 @@ class Operator:
 
     def stats(self):
         return avsg_stats(self.h)
+
+    def request_stats(self, r: int):
+        return avsg_request_stats(self.h, r)
 
     def export_state(self, r: int):
         return avsg_export_state(self.h, r, self.cfg.slots)

@@ -539,17 +539,20 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
   return AVSG_OK;
 }
 
-avsg_status avsg_stats(avsg_handle* h, avsg_stats_t* out) {
-  if (!h || !out) return AVSG_E_INVAL;
+// Counters of requests [r0, r1) into *out (steps and lookups counted for
+// those requests only).
+static avsg_status collect_stats(avsg_handle* h, int r0, int r1, avsg_stats_t* out) {
   const avsg_config& c = h->cfg;
   HIP_TRY(h, hipStreamSynchronize(h->last_stream));
-  std::vector<unsigned long long> st(static_cast<size_t>(c.batch) * kNumStats);
-  HIP_TRY(h, hipMemcpy(st.data(), h->stats, st.size() * 8, hipMemcpyDeviceToHost));
+  const size_t n = static_cast<size_t>(r1 - r0) * kNumStats;
+  std::vector<unsigned long long> st(n);
+  HIP_TRY(h, hipMemcpy(st.data(), h->stats + static_cast<size_t>(r0) * kNumStats, n * 8,
+                       hipMemcpyDeviceToHost));
   std::memset(out, 0, sizeof(*out));
   out->steps = h->steps;
-  out->lookups = h->steps * static_cast<uint64_t>(c.batch) * c.n_q * c.topk;
+  out->lookups = h->steps * static_cast<uint64_t>(r1 - r0) * c.n_q * c.topk;
   uint64_t max_dec = 0;
-  for (int r = 0; r < c.batch; ++r) {
+  for (int r = 0; r < r1 - r0; ++r) {
     const unsigned long long* s = &st[static_cast<size_t>(r) * kNumStats];
     out->hits += s[kStatHits];
     out->misses += s[kStatMisses];
@@ -564,7 +567,20 @@ avsg_status avsg_stats(avsg_handle* h, avsg_stats_t* out) {
     max_dec = std::max<uint64_t>(max_dec, s[kStatMaxStepDecays]);
   }
   out->max_step_alloc_decays = static_cast<int32_t>(max_dec);
-  if (c.gather_mode == AVSG_GATHER_PIPELINED) {
+  uint64_t rb = 0;
+  for (int s = 0; s < c.n_streams; ++s) rb += static_cast<uint64_t>(c.row_bytes[s]);
+  out->bytes_moved = c.gather_mode == AVSG_GATHER_NONE ? 0 : out->misses * rb;
+  out->host_bytes = c.gather_mode == AVSG_GATHER_NONE
+                        ? 0
+                        : (out->misses - out->resident_rows - out->duplicate_rows) * rb;
+  return AVSG_OK;
+}
+
+avsg_status avsg_stats(avsg_handle* h, avsg_stats_t* out) {
+  if (!h || !out) return AVSG_E_INVAL;
+  avsg_status rc = collect_stats(h, 0, h->cfg.batch, out);
+  if (rc != AVSG_OK) return rc;
+  if (h->cfg.gather_mode == AVSG_GATHER_PIPELINED) {
     int ctl[5] = {0, 0, 0, 0, 0};
     HIP_TRY(h, hipMemcpy(ctl, h->pipe_ctl, sizeof(ctl), hipMemcpyDeviceToHost));
     out->queue_timeouts = ctl[4];
@@ -573,13 +589,12 @@ avsg_status avsg_stats(avsg_handle* h, avsg_stats_t* out) {
       return AVSG_E_INTERNAL;
     }
   }
-  uint64_t rb = 0;
-  for (int s = 0; s < c.n_streams; ++s) rb += static_cast<uint64_t>(c.row_bytes[s]);
-  out->bytes_moved = c.gather_mode == AVSG_GATHER_NONE ? 0 : out->misses * rb;
-  out->host_bytes = c.gather_mode == AVSG_GATHER_NONE
-                        ? 0
-                        : (out->misses - out->resident_rows - out->duplicate_rows) * rb;
   return AVSG_OK;
+}
+
+avsg_status avsg_request_stats(avsg_handle* h, int32_t r, avsg_stats_t* out) {
+  if (!h || !out || r < 0 || r >= h->cfg.batch) return AVSG_E_INVAL;
+  return collect_stats(h, r, r + 1, out);
 }
 
 avsg_status avsg_reset_stats(avsg_handle* h, void* stream) {

@@ -192,6 +192,11 @@ def run_parity(spec: W.Spec, steps: Optional[int] = None, table_every: int = 16,
         for k in ("hits", "misses", "lost_exhausted", "lost_collision", "alloc_decays", "revivals",
                   "invalidations", "max_step_alloc_decays"):
             assert ref[k] == got[k], f"counter {k}: oracle {ref[k]} gpu {got[k]}"
+        for r in sorted({0, spec.batch // 2, spec.batch - 1}):
+            rr, gr = orc.o.stats(r), gpu.op.request_stats(r)
+            for k in ("hits", "misses", "lost_exhausted", "lost_collision", "revivals", "invalidations"):
+                assert rr[k] == gr[k], f"request {r} counter {k}: oracle {rr[k]} gpu {gr[k]}"
+            assert gr["lookups"] == T * spec.n_q * spec.topk == gr["hits"] + gr["misses"]
         if resident:
             assert (got["resident_rows"], got["duplicate_rows"]) == (want_res, want_dup), \
                 f"plan counters: oracle ({want_res}, {want_dup}) gpu " \
