@@ -126,7 +126,7 @@ avsg_status avsg_check_config(const avsg_config *cfg);
  * (per-request tables of 8*S bytes, transfer lists of 8*N_q*K bytes, a hit
  * mask of N_q*K bytes, counters and pointer tables; with AVSG_GATHER_RESIDENT
  * three more lists of 8*N_q*K bytes, fan slots of 4*N_q*K bytes and bids of
- * 4*S bytes per request; with AVSG_GATHER_PIPELINED a
+ * 8*S bytes per request; with AVSG_GATHER_PIPELINED a
  * chunk queue of 16 bytes per 32 misses).  Returns 0 for an invalid cfg. */
 size_t avsg_workspace_bytes(const avsg_config *cfg);
 

@@ -30,7 +30,8 @@ struct avsg_handle {
   uint8_t* hit_mask = nullptr;
   int2* host_list = nullptr;    // resident-reuse plan (AVSG_GATHER_RESIDENT)
   int32_t* host_fan = nullptr;
-  int32_t* fan_slots = nullptr;
+  unsigned long long* fan_slots = nullptr;
+  uint32_t fan_stamp = 0;       // stamp of the last step's fan bids
   int2* res_list = nullptr;
   int2* rep_list = nullptr;
   int32_t* plan_counts = nullptr;  // [B][3]
@@ -101,7 +102,7 @@ Layout layout_of(const avsg_config& c) {
   L.plan = off;
   if (c.gather_mode == AVSG_GATHER_RESIDENT)   // host, resident, repeat lists; fan slots; bids; counts; claims
     off += 3 * up(B * static_cast<size_t>(c.n_q) * c.topk * 8) + up(B * static_cast<size_t>(c.n_q) * c.topk * 4) +
-           up(B * S * 4) + up(B * 12) + up(8);
+           up(B * S * 8) + up(B * 12) + up(8);
   L.pipe = off;
   L.pipe_bytes = up(kAlign + 16 * pipe_chunks_for(c));
   off += L.pipe_bytes;
@@ -272,9 +273,9 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
     h->res_list = reinterpret_cast<int2*>(ws + L.plan + list);
     h->rep_list = reinterpret_cast<int2*>(ws + L.plan + 2 * list);
     const size_t fan = up(static_cast<size_t>(B) * c.n_q * c.topk * 4);
-    const size_t bids = up(static_cast<size_t>(B) * c.slots * 4);
+    const size_t bids = up(static_cast<size_t>(B) * c.slots * 8);
     h->host_fan = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list);
-    h->fan_slots = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan);
+    h->fan_slots = reinterpret_cast<unsigned long long*>(ws + L.plan + 3 * list + fan);
     h->plan_counts = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan + bids);
     h->plan_claim =
         reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan + bids + up(static_cast<size_t>(B) * 12));
@@ -344,6 +345,10 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
     if ((e = launch_reset_dualptr(h->dp_state, B, c.topk, s)) != hipSuccess) return cleanup(AVSG_E_HIP);
   }
   if (launch_zero_u64(h->stats, static_cast<size_t>(B) * kNumStats, s) != hipSuccess)
+    return cleanup(AVSG_E_HIP);
+  // fan bids: stamp 0 is older than every step's
+  if (h->fan_slots &&
+      launch_zero_u64(h->fan_slots, static_cast<size_t>(B) * c.slots, s) != hipSuccess)
     return cleanup(AVSG_E_HIP);
   if (hipMemcpyAsync(h->host_ptrs, h->host_dev.data(), h->host_dev.size() * 8,
                      hipMemcpyHostToDevice, s) != hipSuccess ||
@@ -478,6 +483,12 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
       p.host_list = h->host_list;
       p.host_fan = h->host_fan;
       p.fan_slots = h->fan_slots;
+      if (++h->fan_stamp == 0) {
+        // after 2^32 - 1 steps the stamps start again from a cleared array
+        HIP_TRY(h, launch_zero_u64(h->fan_slots, static_cast<size_t>(c.batch) * c.slots, s));
+        h->fan_stamp = 1;
+      }
+      p.plan_stamp = h->fan_stamp;
       p.res_list = h->res_list;
       p.rep_list = h->rep_list;
       p.plan_counts = h->plan_counts;

@@ -165,8 +165,8 @@ __device__ __forceinline__ uint32_t plan_home(int32_t x, uint32_t P) {
 // A host entry also writes its row to the largest repeat destination of its
 // index (its fan slot), so with two tokens per step no repeat is left for a
 // later copy; repeats bid for the fan slot with a global atomicMax on a
-// per-slot word of the request (fan_slots, reset for this step's reservations
-// first).  The lists keep transfer-list order.  LDS map: P words, open
+// per-slot word of the request (fan_slots), stamped with the step so that a
+// word left by an earlier step always loses and needs no reset.  The lists keep transfer-list order.  LDS map: P words, open
 // addressing with linear probing keyed by the index a word names through c[];
 // a word is (resident bit | slot + 1), 0 = empty, and atomicMax makes every
 // choice deterministic.  The map holds at most N_q * K keys and
@@ -198,7 +198,8 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   const uint32_t P = static_cast<uint32_t>(p.plan_words);
   uint32_t* smp = sres + nb;                                        // [P] index map
   int* scnt = reinterpret_cast<int*>(smp + P);                      // [kPlanMiscWords]
-  int32_t* gfan = p.fan_slots + static_cast<size_t>(r) * S;         // [S] fan slot per reserved slot
+  unsigned long long* gfan = p.fan_slots + static_cast<size_t>(r) * S;   // [S] fan bid per slot
+  const unsigned long long stamp = static_cast<unsigned long long>(p.plan_stamp) << 32;
   const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
   const size_t lb = static_cast<size_t>(r) * p.n_q * p.K;
   const int2* ml = p.miss_list + lb;
@@ -215,7 +216,6 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
     const int2 v = e < MT ? v0 : ml[e];
     if (v.y < 0 || v.y >= S) continue;
     atomicOr(&sres[v.y >> 5], 1u << (v.y & 31));
-    if (p.n_q > 1) gfan[v.y] = -1;
     if (v.x < 0 || static_cast<int64_t>(v.x) >= rows_r) continue;
     const uint32_t val = static_cast<uint32_t>(v.y) + 1u;
     uint32_t h = plan_home(v.x, P);
@@ -303,15 +303,17 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
       int src = src_first, hw = hw_first;
       const int kind = e < MT ? kind_first : classify(e, &v, &src, &hw);
       if (kind == 2) {
-        atomicMax(&gfan[src], v.y);
+        atomicMax(&gfan[src], stamp | static_cast<unsigned long long>(v.y));
         atomicOr(&smp[hw], kPlanRepeat);
       }
     }
   }
   __syncthreads();
-  // fan words are read past the L1, where the bids were made
+  // fan words are read past the L1, where the bids were made; a word whose
+  // stamp is not this step's holds no bid of this step
   auto fan_of = [&](int slot) {
-    return __hip_atomic_load(&gfan[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned long long w = __hip_atomic_load(&gfan[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return (w & ~0xFFFFFFFFull) == stamp ? static_cast<int>(w & 0xFFFFFFFFull) : -1;
   };
 
   // (4) compact the three lists in transfer-list order; host entries carry

@@ -100,7 +100,7 @@ def test_workspace_size_and_validation(lib):
     assert ws(gather_mode=7) == 0
     # the resident-reuse plan adds three transfer lists, fan slots, bids, counts and claims
     B, nq, K = 64, 2, 2048
-    assert ws(gather_mode=A.AVSG_GATHER_RESIDENT) >= ws() + (3 * 8 + 4) * B * nq * K + 4 * B * 8192 + 12 * B
+    assert ws(gather_mode=A.AVSG_GATHER_RESIDENT) >= ws() + (3 * 8 + 4) * B * nq * K + 8 * B * 8192 + 12 * B
     assert ws(gather_mode=A.AVSG_GATHER_POSITION) > ws() - 1
     assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=1, slots=2048, gather_mode=A.AVSG_GATHER_POSITION) == 0
     assert ws(n_q=1, slots=2, topk=1, batch=1, row_bytes=(4,)) > 0

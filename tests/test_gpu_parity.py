@@ -93,6 +93,7 @@ EDGE_CASES = [
     ("spec_window", dict(batch=2, topk=256, slots=2048, n_q=3, steps=20, ctx=4096, mode="zipf_window",
                          window=64, retention=0.8)),
     ("batch_200", dict(batch=200, topk=128, slots=256, n_q=2, steps=6, ctx=2000)),
+    ("batch_1024_max", dict(batch=1024, topk=16, slots=64, n_q=2, steps=6, ctx=400)),
 ]
 
 
@@ -244,6 +245,7 @@ RESIDENT_CASES = [
     ("k_one", dict(batch=5, topk=1, slots=2, n_q=1, steps=40, ctx=6), 0),
     ("s_16384_max", dict(batch=2, topk=1024, slots=16384, n_q=3, steps=8, ctx=300000), 3),
     ("batch_200", dict(batch=200, topk=128, slots=256, n_q=2, steps=6, ctx=2000), 0),
+    ("batch_1024_max", dict(batch=1024, topk=16, slots=64, n_q=2, steps=6, ctx=400), 0),
 ]
 
 
