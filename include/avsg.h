@@ -125,8 +125,8 @@ avsg_status avsg_check_config(const avsg_config *cfg);
 /* Size in bytes of the device workspace that avsg_create needs for cfg
  * (per-request tables of 8*S bytes, transfer lists of 8*N_q*K bytes, a hit
  * mask of N_q*K bytes, counters and pointer tables; with AVSG_GATHER_RESIDENT
- * three more lists of 8*N_q*K bytes, fan slots of 4*N_q*K bytes and bids of
- * 8*S bytes per request; with AVSG_GATHER_PIPELINED a
+ * three more lists of 8*N_q*K bytes, fan slots of 4*N_q*K bytes, bids of
+ * 8*S bytes and a step stamp of 8 bytes per request; with AVSG_GATHER_PIPELINED a
  * chunk queue of 16 bytes per 32 misses).  Returns 0 for an invalid cfg. */
 size_t avsg_workspace_bytes(const avsg_config *cfg);
 
@@ -164,12 +164,20 @@ avsg_status avsg_create(const avsg_config *cfg, const void *const *host_rows,
  * When the step's kernels finish, every slot named in d_slots holds the row of
  * its index in every stream.  Indices outside [0, rows) are counted in
  * bad_indices and not copied.  The current HIP device must be the one that
- * was current at avsg_create.  Errors: AVSG_E_INVAL (null pointer, other
- * device), AVSG_E_HIP. */
+ * was current at avsg_create.  With timing off, a step of the balanced,
+ * request-level, position-level or resident-reuse transfer can be captured
+ * into a HIP graph (stream capture): it enqueues kernels only, keeps every
+ * piece of step state in the workspace, and each replay is the next decode
+ * step on whatever d_topk then holds.  The copy-engine transfer waits on the
+ * host and the pipelined step stamps its queue on the host, so neither can be
+ * captured.  Errors: AVSG_E_INVAL (null pointer, other device), AVSG_E_HIP. */
 avsg_status avsg_step(avsg_handle *h, const int32_t *d_topk, const int64_t *d_verified_len,
                       int32_t *d_slots, int32_t *d_miss_counts, void *stream);
 
-/* Cumulative counters.  Synchronizes with the handle's last stream. */
+/* Cumulative counters.  Synchronizes with the handle's last stream.  steps
+ * and lookups count avsg_step calls on the host, so replays of a captured
+ * step are not in them; every other counter is kept on the device and
+ * includes them. */
 avsg_status avsg_stats(avsg_handle *h, avsg_stats_t *out);
 
 /* The same counters for request r alone (lookups = steps * N_q * K), for

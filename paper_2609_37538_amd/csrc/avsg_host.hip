@@ -31,7 +31,7 @@ struct avsg_handle {
   int2* host_list = nullptr;    // resident-reuse plan (AVSG_GATHER_RESIDENT)
   int32_t* host_fan = nullptr;
   unsigned long long* fan_slots = nullptr;
-  uint32_t fan_stamp = 0;       // stamp of the last step's fan bids
+  unsigned long long* plan_stamps = nullptr;   // [B] per-request stamp of the fan bids
   int2* res_list = nullptr;
   int2* rep_list = nullptr;
   int32_t* plan_counts = nullptr;  // [B][3]
@@ -102,7 +102,7 @@ Layout layout_of(const avsg_config& c) {
   L.plan = off;
   if (c.gather_mode == AVSG_GATHER_RESIDENT)   // host, resident, repeat lists; fan slots; bids; counts; claims
     off += 3 * up(B * static_cast<size_t>(c.n_q) * c.topk * 8) + up(B * static_cast<size_t>(c.n_q) * c.topk * 4) +
-           up(B * S * 8) + up(B * 12) + up(8);
+           up(B * S * 8) + up(B * 12) + up(8) + up(B * 8);
   L.pipe = off;
   L.pipe_bytes = up(kAlign + 16 * pipe_chunks_for(c));
   off += L.pipe_bytes;
@@ -279,6 +279,8 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
     h->plan_counts = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan + bids);
     h->plan_claim =
         reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan + bids + up(static_cast<size_t>(B) * 12));
+    h->plan_stamps = reinterpret_cast<unsigned long long*>(ws + L.plan + 3 * list + fan + bids +
+                                                           up(static_cast<size_t>(B) * 12) + up(8));
     h->plan_words = plan_map_words(c.slots, c.topk, c.n_q);
   }
   h->pipe_ctl = reinterpret_cast<int*>(ws + L.pipe);
@@ -346,9 +348,10 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
   }
   if (launch_zero_u64(h->stats, static_cast<size_t>(B) * kNumStats, s) != hipSuccess)
     return cleanup(AVSG_E_HIP);
-  // fan bids: stamp 0 is older than every step's
+  // fan bids and their per-request stamps: stamp 0 is older than every step's
   if (h->fan_slots &&
-      launch_zero_u64(h->fan_slots, static_cast<size_t>(B) * c.slots, s) != hipSuccess)
+      (launch_zero_u64(h->fan_slots, static_cast<size_t>(B) * c.slots, s) != hipSuccess ||
+       launch_zero_u64(h->plan_stamps, static_cast<size_t>(B), s) != hipSuccess))
     return cleanup(AVSG_E_HIP);
   if (hipMemcpyAsync(h->host_ptrs, h->host_dev.data(), h->host_dev.size() * 8,
                      hipMemcpyHostToDevice, s) != hipSuccess ||
@@ -483,12 +486,7 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
       p.host_list = h->host_list;
       p.host_fan = h->host_fan;
       p.fan_slots = h->fan_slots;
-      if (++h->fan_stamp == 0) {
-        // after 2^32 - 1 steps the stamps start again from a cleared array
-        HIP_TRY(h, launch_zero_u64(h->fan_slots, static_cast<size_t>(c.batch) * c.slots, s));
-        h->fan_stamp = 1;
-      }
-      p.plan_stamp = h->fan_stamp;
+      p.plan_stamps = h->plan_stamps;
       p.res_list = h->res_list;
       p.rep_list = h->rep_list;
       p.plan_counts = h->plan_counts;

@@ -50,8 +50,8 @@ struct MatchParams {
   int32_t plan_words;           // words of the end-of-step index map in LDS
   int2* host_list;              // [B][n_q*K] (index, slot) copied from the host
   int32_t* host_fan;            // [B][n_q*K] second slot a host entry is also copied to, or -1
-  unsigned long long* fan_slots;  // [B][S] fan bids per slot: step stamp << 32 | slot (plan scratch)
-  uint32_t plan_stamp;          // this step's stamp of fan bids (>= 1, grows by one per step)
+  unsigned long long* fan_slots;  // [B][S] fan bids per slot: step stamp << 24 | slot (plan scratch)
+  unsigned long long* plan_stamps;  // [B] stamp of each request's last planned step (0 = none)
   int2* res_list;               // [B][n_q*K] (source slot, slot): row already resident
   int2* rep_list;               // [B][n_q*K] (source slot, slot): repeat of a host entry
   int32_t* plan_counts;         // [B][3] host, resident, repeat entries

@@ -147,6 +147,8 @@ constexpr int kPlanMiscWords = 6 * MW + 4;
 constexpr uint32_t kPlanResident = 0x80000000u;   // map word names a slot outside this step's reservations
 constexpr uint32_t kPlanRepeat = 0x40000000u;     // the word's index has a repeat this step
 constexpr uint32_t kPlanSlot = 0x00FFFFFFu;       // slot + 1
+constexpr unsigned long long kFanSlot = 0xFFFFFFull;       // fan word: stamp << 24 | slot
+constexpr unsigned long long kFanStampMax = (1ull << 40) - 1;
 
 // Home word of index x in the plan's map of P words (multiplicative hash).
 __device__ __forceinline__ uint32_t plan_home(int32_t x, uint32_t P) {
@@ -165,8 +167,10 @@ __device__ __forceinline__ uint32_t plan_home(int32_t x, uint32_t P) {
 // A host entry also writes its row to the largest repeat destination of its
 // index (its fan slot), so with two tokens per step no repeat is left for a
 // later copy; repeats bid for the fan slot with a global atomicMax on a
-// per-slot word of the request (fan_slots), stamped with the step so that a
-// word left by an earlier step always loses and needs no reset.  The lists keep transfer-list order.  LDS map: P words, open
+// per-slot word of the request (fan_slots), stamped with the request's step
+// count so that a word left by an earlier step always loses and needs no
+// reset.  The count lives in device memory and only this workgroup advances
+// it, so a captured and replayed step stamps every replay anew.  The lists keep transfer-list order.  LDS map: P words, open
 // addressing with linear probing keyed by the index a word names through c[];
 // a word is (resident bit | slot + 1), 0 = empty, and atomicMax makes every
 // choice deterministic.  The map holds at most N_q * K keys and
@@ -199,7 +203,13 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   uint32_t* smp = sres + nb;                                        // [P] index map
   int* scnt = reinterpret_cast<int*>(smp + P);                      // [kPlanMiscWords]
   unsigned long long* gfan = p.fan_slots + static_cast<size_t>(r) * S;   // [S] fan bid per slot
-  const unsigned long long stamp = static_cast<unsigned long long>(p.plan_stamp) << 32;
+  unsigned long long next = p.plan_stamps[r] + 1;
+  if (next > kFanStampMax) {
+    // after 2^40 - 1 steps of this request the stamps restart from a cleared array
+    for (int j = threadIdx.x; j < S; j += MT) gfan[j] = 0ull;
+    next = 1;
+  }
+  const unsigned long long stamp = next << 24;
   const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
   const size_t lb = static_cast<size_t>(r) * p.n_q * p.K;
   const int2* ml = p.miss_list + lb;
@@ -313,7 +323,7 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   // stamp is not this step's holds no bid of this step
   auto fan_of = [&](int slot) {
     const unsigned long long w = __hip_atomic_load(&gfan[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return (w & ~0xFFFFFFFFull) == stamp ? static_cast<int>(w & 0xFFFFFFFFull) : -1;
+    return (w & ~kFanSlot) == stamp ? static_cast<int>(w & kFanSlot) : -1;
   };
 
   // (4) compact the three lists in transfer-list order; host entries carry
@@ -363,6 +373,7 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   if (lane == 0 && n_rep) atomicAdd(&scnt[6 * MW], n_rep);
   __syncthreads();
   if (tid == 0) {
+    p.plan_stamps[r] = next;   // every thread read the old count before the first barrier
     int32_t* pc = p.plan_counts + 3 * static_cast<size_t>(r);
     pc[0] = n_list[0];
     pc[1] = n_list[1];

@@ -453,3 +453,101 @@ def test_resident_reuse_when_verified_length_shrinks():
     finally:
         gpu.close()
         host.free()
+
+
+def test_two_handles_on_two_streams():
+    """Two handles (balanced and resident-reuse Stage Two, each with its own
+    workspace and buffers) step the same selections on two streams with no
+    synchronization between them; slots, counts, tables and buffers of both
+    equal the oracle's after every step."""
+    from paper_2609_37538_amd import avsg as A
+    import torch
+    spec = W.custom_spec(name="two_streams", batch=6, topk=512, slots=2048, n_q=2, steps=10,
+                         ctx=30000, row_bytes=(1152, 132), retention=0.8)
+    wl = W.Workload(spec)
+    host = HostRows(wl)
+    orc = OracleSide(wl, host, retry=1)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    ops = []
+    try:
+        for gm, st in zip((A.AVSG_GATHER_BALANCED, A.AVSG_GATHER_RESIDENT), streams):
+            cfg = A.make_config(spec.batch, spec.topk, spec.n_q, spec.slots, retry=1,
+                                row_bytes=spec.row_bytes, gather_mode=gm)
+            ops.append(A.Operator(cfg, host.ptrs, wl.ctx, stream=st))
+        for t in range(spec.steps):
+            X = wl.topk(t)
+            log(f"[two streams] step {t}")
+            Xd = torch.from_numpy(np.ascontiguousarray(X, dtype=np.int32)).cuda()
+            torch.cuda.synchronize()
+            for op, st in zip(ops, streams):
+                with torch.cuda.stream(st):
+                    op.step(Xd)
+            O_ref, n_ref = orc.step(X, None)
+            torch.cuda.synchronize()
+            for op in ops:
+                compare_step(t, O_ref, n_ref, op.slots.cpu().numpy(), op.miss_counts.cpu().numpy())
+                bufs = [b.cpu().numpy() for b in op.buffers]
+                for s in range(len(spec.row_bytes)):
+                    assert np.array_equal(bufs[s], orc.images[s]), f"step {t} stream {s}: buffers differ"
+        for r in range(spec.batch):
+            c_ref, q_ref = orc.o.export(r)
+            for op in ops:
+                c_gpu, q_gpu = op.export_state(r)
+                assert np.array_equal(c_ref, c_gpu) and np.array_equal(q_ref, q_gpu)
+    finally:
+        for op in ops:
+            op.close()
+        host.free()
+
+
+@pytest.mark.parametrize("mode,n_q", [(0, 2), (1, 1), (4, 2), (6, 2), (6, 3)],
+                         ids=["balanced", "request_level", "position_level", "resident", "resident_3_tokens"])
+def test_graph_capture_replays_steps(mode, n_q):
+    """One avsg_step captured into a HIP graph and replayed once per decode
+    step (new selections copied into the captured input between replays, with
+    host synchronizations): after every replay the slots, counts and buffers
+    equal an operator stepped eagerly on the same selections, and at the end
+    so do the tables and counters."""
+    from paper_2609_37538_amd import avsg as A
+    import torch
+    spec = W.custom_spec(name=f"graph_{mode}_{n_q}", batch=4, topk=256, slots=1024, n_q=n_q, steps=12,
+                         ctx=6000, row_bytes=(1152, 132), retention=0.8)
+    wl = W.Workload(spec)
+    host = HostRows(wl)
+    cfg = A.make_config(spec.batch, spec.topk, spec.n_q, spec.slots, retry=0, max_life=8,
+                        row_bytes=spec.row_bytes, gather_mode=mode)
+    eager = A.Operator(cfg, host.ptrs, wl.ctx, stream=torch.cuda.Stream())
+    graphed = A.Operator(cfg, host.ptrs, wl.ctx, stream=torch.cuda.Stream())
+    X_in = torch.zeros((spec.batch, spec.n_q, spec.topk), dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    try:
+        with torch.cuda.graph(g, stream=graphed.stream):
+            graphed.step(X_in)
+        torch.cuda.synchronize()
+        assert graphed.stats()["steps"] == 1 and graphed.stats()["lookups"] > 0
+        for t in range(spec.steps):
+            log(f"[graph] mode {mode} n_q {n_q} replay {t}")
+            X = torch.from_numpy(np.ascontiguousarray(wl.topk(t), dtype=np.int32)).cuda()
+            X_in.copy_(X)
+            torch.cuda.synchronize()
+            g.replay()
+            eager.step(X)
+            torch.cuda.synchronize()
+            assert torch.equal(graphed.slots, eager.slots), f"replay {t}: slots differ"
+            assert torch.equal(graphed.miss_counts, eager.miss_counts), f"replay {t}: counts differ"
+            for b1, b2 in zip(graphed.buffers, eager.buffers):
+                assert torch.equal(b1, b2), f"replay {t}: buffers differ"
+        for r in range(spec.batch):
+            c1, q1 = graphed.export_state(r)
+            c2, q2 = eager.export_state(r)
+            assert np.array_equal(c1, c2) and np.array_equal(q1, q2)
+        s1, s2 = graphed.stats(), eager.stats()
+        for k in ("hits", "misses", "lost_exhausted", "lost_collision", "resident_rows", "duplicate_rows"):
+            assert s1[k] == s2[k], k
+        assert s2["misses"] > 0
+    finally:
+        del g
+        eager.close()
+        graphed.close()
+        host.free()
