@@ -588,7 +588,6 @@ def measured_traffic(args):
     counter summary (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0, copy-calibrated), or
     None when this run is not the profiled configuration or the gather source
     has changed since the counters were taken."""
-    import hashlib
     import re
     if (args.config, args.warmup, args.steps, args.workers, args.gather, args.match) != \
             ("batch64_mtp2", 16, 240, 0, "resident", "hash"):
@@ -600,12 +599,24 @@ def measured_traffic(args):
     if not m:
         return None
     block = json.loads(m.group(1))
-    h = hashlib.sha256()
-    for p in GATHER_SOURCES:
-        h.update(open(os.path.join(ROOT, p), "rb").read())
-    if h.hexdigest()[:16] != block.get("source_sha256_16"):
+    if gather_code_hash() != block.get("source_sha256_16"):
         return None
     return block
+
+
+def gather_code_hash(root=None):
+    """First 16 hex digits of the SHA-256 of the code of GATHER_SOURCES with
+    comments and whitespace removed (a comment edit keeps the counters valid;
+    any code change invalidates them)."""
+    import hashlib
+    import re
+    h = hashlib.sha256()
+    for p in GATHER_SOURCES:
+        text = open(os.path.join(root or ROOT, p), encoding="utf-8").read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
+    return h.hexdigest()[:16]
 
 
 def cpu_baseline(spec, wl, X_host, N_host, host_ptrs, args, gather_mode):

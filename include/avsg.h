@@ -229,7 +229,8 @@ avsg_status avsg_export_plan(avsg_handle *h, int32_t r, int32_t *n_host, int32_t
  * avsg_timing copies up to `cap` recorded steps (synchronizing):
  * match_ms[i] is the duration of step i's matching kernel, gather_ms[i] that
  * of its main Stage Two kernel (or copies), and tail_ms[i] (may be NULL) the
- * rest of Stage Two: the repeat copies of AVSG_GATHER_RESIDENT, ~0 otherwise. */
+ * rest of Stage Two: the repeat copies of AVSG_GATHER_RESIDENT with three or
+ * more tokens per step, 0 otherwise. */
 avsg_status avsg_set_timing(avsg_handle *h, int32_t enable);
 avsg_status avsg_timing(avsg_handle *h, float *match_ms, float *gather_ms, float *tail_ms,
                         int32_t cap, int32_t *n_out);

@@ -100,7 +100,7 @@ Layout layout_of(const avsg_config& c) {
   L.miss_list = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk * 8);
   L.hit_mask = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk);
   L.plan = off;
-  if (c.gather_mode == AVSG_GATHER_RESIDENT)   // host, resident, repeat lists; fan slots; bids; counts; claims
+  if (c.gather_mode == AVSG_GATHER_RESIDENT)   // host, resident, repeat lists; fan slots; bids; counts; claims; stamps
     off += 3 * up(B * static_cast<size_t>(c.n_q) * c.topk * 8) + up(B * static_cast<size_t>(c.n_q) * c.topk * 4) +
            up(B * S * 8) + up(B * 12) + up(8) + up(B * 8);
   L.pipe = off;
@@ -514,8 +514,8 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
     case AVSG_GATHER_REQUEST: HIP_TRY(h, launch_gather_request(g, s)); break;
     case AVSG_GATHER_POSITION: HIP_TRY(h, launch_gather_position(g, h->workers, s)); break;
     case AVSG_GATHER_RESIDENT: {
-      // host list (balanced) and resident copies in one kernel, then the
-      // repeats of this step's host rows
+      // host list (each row also to its fan slot) and resident copies in one
+      // kernel, then the repeats left over
       GatherParams gh = g, gr = g;
       gh.miss_counts = h->plan_counts; gh.counts_per_req = 1; gh.count_stride = 3;
       gh.miss_list = h->host_list; gh.fan = h->host_fan;

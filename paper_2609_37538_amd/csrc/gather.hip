@@ -12,9 +12,9 @@
 // position kernel (S2, Eq. 14) splits the flattened N_g*K selected positions
 // into C near-equal contiguous ranges; hit positions issue no copy but still
 // occupy their worker's share.  With the resident-reuse plan of the matching
-// kernel, the resident kernel copies the host list and the rows already in the
-// device buffer, and the device-copy kernel then fills repeats of this step's
-// host rows.
+// kernel, the resident kernel copies the host list (each row also to its fan
+// slot) and the rows already in the device buffer; with three or more tokens
+// per step the device-copy kernel then fills the repeats left over.
 #include "gather_body.h"
 
 namespace avsg {
