@@ -86,6 +86,14 @@ def load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
                           "(the operator has no other implementation)")
+    # PyTorch ships its own HIP runtime under the same soname as the system's;
+    # whichever loads first serves the whole process, and torch cannot start
+    # on a different one, so torch (when installed) goes first and the library
+    # shares its runtime
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(LIB_PATH)
     i32, i64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     lib.avsg_check_config.restype = i32

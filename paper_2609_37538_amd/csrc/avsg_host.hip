@@ -319,7 +319,9 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
   if (c.match_mode == AVSG_MATCH_HASH) {
     h->lds = match_lds_bytes(c.slots, c.topk);
     int max_lds = 0;
-    hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device);
+    if ((e = hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device)) !=
+        hipSuccess)
+      return cleanup(AVSG_E_HIP);
     if (max_lds > 0 && h->lds > static_cast<size_t>(max_lds)) {
       std::fprintf(stderr, "avsg_create: table of %d slots needs %zu B of LDS, limit %d\n",
                    c.slots, h->lds, max_lds);

@@ -18,7 +18,7 @@ __device__ __forceinline__ int lane_index() {
 }
 
 // Exclusive prefix of the per-request miss totals into pre[0..B] (pre[B] = N).
-__device__ void request_prefix(const GatherParams& p, long long* pre, long long* wtot) {
+__device__ inline void request_prefix(const GatherParams& p, long long* pre, long long* wtot) {
   const int tid = threadIdx.x, lane = lane_index(), wave = tid >> 6;
   const int per = (p.B + GT - 1) / GT;
   const int r0 = tid * per;
@@ -103,7 +103,7 @@ __device__ __forceinline__ void copy_rows(const uint64_t* src, const uint64_t* d
   }
 }
 
-__device__ void copy_tile_rows(const GatherParams& p, int tn, uint64_t* src0, uint64_t* dst0,
+__device__ inline void copy_tile_rows(const GatherParams& p, int tn, uint64_t* src0, uint64_t* dst0,
                                uint64_t* src1, uint64_t* dst1) {
   __syncthreads();
   if ((p.row_bytes0 & 15) == 0)

@@ -8,11 +8,12 @@ namespace avsg {
 namespace {
 
 
-constexpr int MT = kMatchThreads;
-constexpr int MW = MT / 64;
-constexpr int kMaxIPT = 4;                 // up to K = 4096 indices per token
-constexpr int kMaxSPT = 16;                // up to S = 16384 slots
-constexpr int kScratchInts = 2 * kMaxIPT * MW + MW + 4 + 8;
+// A workgroup has NT threads (1024, or 256 for small tables); the LDS
+// bookkeeping below is sized for the largest workgroup.
+constexpr int kMaxWaves = kMatchThreads / 64;
+constexpr int kMaxIPT = 4;                 // up to 4 NT indices per token
+constexpr int kMaxSPT = 16;                // up to 16 NT slots
+constexpr int kScratchInts = 2 * kMaxIPT * kMaxWaves + kMaxWaves + 4 + 8;
 constexpr uint32_t kBid = 0x80000000u;     // marks a bucket written by an install bid
 
 // 16-byte vectors as clang vector types (kept in registers)
@@ -143,7 +144,7 @@ struct Own {
 // Words of LDS bookkeeping of the end-of-step plan besides the reservation
 // bitmap and the two maps: per-wave counts of the three lists for two
 // compaction rounds, plus totals.
-constexpr int kPlanMiscWords = 6 * MW + 4;
+constexpr int kPlanMiscWords = 6 * kMaxWaves + 4;
 constexpr uint32_t kPlanResident = 0x80000000u;   // map word names a slot outside this step's reservations
 constexpr uint32_t kPlanRepeat = 0x40000000u;     // the word's index has a repeat this step
 constexpr uint32_t kPlanSlot = 0x00FFFFFFu;       // slot + 1
@@ -192,9 +193,11 @@ __device__ __forceinline__ int plan_lookup(const uint32_t* smp, const int32_t* s
   return -1;
 }
 
+template <int NT>
 __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, unsigned char* lds,
                                              const int listed, const int64_t rows_r,
                                              const int64_t n_verified, const int2 v0) {
+  constexpr int MT = NT, MW = NT / 64;
   const int S = p.S;
   const int32_t* sc = reinterpret_cast<const int32_t*>(lds);
   uint32_t* sres = reinterpret_cast<uint32_t*>(lds + 4 * static_cast<size_t>(S));  // reserved-slot bitmap
@@ -388,9 +391,11 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
 // After each token with misses, publish(r, first, count) is called by every
 // thread once the token's transfer-list entries are written (a no-op for the
 // plain matching kernel).
-template <int IPT, typename Publish>
+template <int IPT, int NT, typename Publish>
 __device__ __forceinline__ void match_request(const MatchParams& p, const int r, unsigned char* lds,
                               Publish& publish) {
+  constexpr int MT = NT, MW = NT / 64;
+  static_assert(NT % 64 == 0 && NT <= kMatchThreads, "whole waves, at most the largest workgroup");
   const int S = p.S, K = p.K, R = p.R;
   const uint32_t smask = static_cast<uint32_t>(S - 1);
   const Word W{static_cast<uint32_t>(p.m), smask, p.f_mask};
@@ -787,7 +792,7 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   }
   if (p.plan_words > 0) {
     __syncthreads();   // the counter reduction above is read before its LDS is reused
-    plan_request(p, r, lds, listed, rows_r, n_verified, v0);
+    plan_request<NT>(p, r, lds, listed, rows_r, n_verified, v0);
   }
 }
 

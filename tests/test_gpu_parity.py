@@ -94,6 +94,9 @@ EDGE_CASES = [
                          window=64, retention=0.8)),
     ("batch_200", dict(batch=200, topk=128, slots=256, n_q=2, steps=6, ctx=2000)),
     ("batch_1024_max", dict(batch=1024, topk=16, slots=64, n_q=2, steps=6, ctx=400)),
+    # four-wave workgroups (S <= 1024, K <= 512): two indices per thread, a ragged K
+    ("four_waves_two_per_thread", dict(batch=3, topk=512, slots=1024, n_q=2, steps=12, ctx=8000)),
+    ("four_waves_ragged", dict(batch=2, topk=300, slots=512, n_q=1, steps=12, ctx=3000)),
 ]
 
 
@@ -246,6 +249,7 @@ RESIDENT_CASES = [
     ("s_16384_max", dict(batch=2, topk=1024, slots=16384, n_q=3, steps=8, ctx=300000), 3),
     ("batch_200", dict(batch=200, topk=128, slots=256, n_q=2, steps=6, ctx=2000), 0),
     ("batch_1024_max", dict(batch=1024, topk=16, slots=64, n_q=2, steps=6, ctx=400), 0),
+    ("four_waves", dict(batch=3, topk=384, slots=1024, n_q=2, steps=12, ctx=6000, retention=0.8), 0),
 ]
 
 
