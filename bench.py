@@ -59,6 +59,9 @@ def parse():
     ap.add_argument("--config-table", default="",
                     help="run every workload under every Stage Two strategy (and the dual-pointer "
                          "ablation where it applies); write JSON rows here")
+    ap.add_argument("--copy-engine-bench", default="",
+                    help="copy-engine transfer of every workload in a process without torch, so the HIP "
+                         "runtime's batched copy call is available; write JSON rows here")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one device-to-device copy of this many MiB first (counter calibration)")
     return ap.parse_args()
@@ -71,6 +74,9 @@ def main():
               "(requests shard across GPUs with no communication, see the design notes)",
               file=sys.stderr)
         sys.exit(2)
+    if args.copy_engine_bench:
+        copy_engine_bench(args.copy_engine_bench)
+        return
     import torch
     import workload as W
     from paper_2609_37538_amd import avsg as A
@@ -483,6 +489,132 @@ def lifetime_sweep(out_path):
         results.append(row)
         print(json.dumps(row), flush=True)
     host.free()
+    with open(out_path, "w") as f:
+        json.dump(results, f, indent=1)
+
+
+class _Hip:
+    """The few HIP runtime calls a process without torch needs to own device
+    memory (the library already loaded the runtime; same soname)."""
+
+    def __init__(self):
+        import ctypes
+        self.ct = ctypes
+        self.lib = ctypes.CDLL("libamdhip64.so.7")
+        P, sz = ctypes.c_void_p, ctypes.c_size_t
+        self.lib.hipMalloc.argtypes = [ctypes.POINTER(P), sz]
+        self.lib.hipFree.argtypes = [P]
+        self.lib.hipMemcpy.argtypes = [P, P, sz, ctypes.c_int]
+        self.lib.hipSetDevice.argtypes = [ctypes.c_int]
+        self.lib.hipStreamCreate.argtypes = [ctypes.POINTER(P)]
+        self.lib.hipStreamSynchronize.argtypes = [P]
+        self._check(self.lib.hipSetDevice(0), "hipSetDevice")
+        self.blocks = []
+
+    def stream(self):
+        s = self.ct.c_void_p()
+        self._check(self.lib.hipStreamCreate(self.ct.byref(s)), "hipStreamCreate")
+        return s.value
+
+    def _check(self, rc, what):
+        if rc != 0:
+            raise RuntimeError(f"{what} failed ({rc})")
+
+    def alloc(self, nbytes):
+        p = self.ct.c_void_p()
+        self._check(self.lib.hipMalloc(self.ct.byref(p), max(256, int(nbytes))), "hipMalloc")
+        self.blocks.append(p.value)
+        return p.value
+
+    def upload(self, dst, arr):
+        self._check(self.lib.hipMemcpy(dst, arr.ctypes.data, arr.nbytes, 1), "hipMemcpy")
+
+    def download(self, arr, src):
+        self._check(self.lib.hipMemcpy(arr.ctypes.data, src, arr.nbytes, 2), "hipMemcpy")
+
+    def sync(self):
+        self._check(self.lib.hipDeviceSynchronize(), "hipDeviceSynchronize")
+
+    def free_all(self):
+        for p in self.blocks:
+            self.lib.hipFree(p)
+        self.blocks = []
+
+
+def copy_engine_bench(out_path, names=("tiny", "batch16", "batch64_mtp2", "imbalance", "stress"),
+                      warm=4, timed=16):
+    """The copy-engine transfer (miss list read back, copies issued by the host)
+    in a process that never loads torch: the system HIP runtime then serves
+    the process and its batched copy call (one call per step for every missed
+    row) is available, which the runtime PyTorch ships lacks.  Device memory
+    comes from hipMalloc.  Per workload: runtime copy calls per step, Stage
+    Two time (HIP events) and wall time per step, host GB/s."""
+    import workload as W
+    from paper_2609_37538_amd import avsg as A
+    assert "torch" not in sys.modules
+    A.load(share_torch_runtime=False)
+    hip = _Hip()
+    results = []
+    for name in names:
+        spec = W.get_spec(name)
+        wl = W.Workload(spec)
+        T = warm + timed
+        B, K, nq, S = spec.batch, spec.topk, spec.n_q, spec.slots
+        regions, host_ptrs = [], []
+        offs = wl.request_row_offsets()
+        for st, rb in enumerate(spec.row_bytes):
+            reg = A.HostRegion(wl.host_rows_total() * rb)
+            W.fill_host(wl, st, reg.ptr)
+            regions.append(reg)
+            host_ptrs += [reg.ptr + int(offs[r]) * rb for r in range(B)]
+        cfg = A.make_config(B, K, nq, S, row_bytes=spec.row_bytes, gather_mode=A.AVSG_GATHER_SDMA)
+        ws_bytes = A.avsg_workspace_bytes(cfg)
+        ws = hip.alloc(ws_bytes)
+        bufs = []
+        for rb in spec.row_bytes:
+            base = hip.alloc(B * S * rb)
+            bufs += [base + r * S * rb for r in range(B)]
+        X = np.ascontiguousarray(wl.all_steps(T), dtype=np.int32)
+        Xd = hip.alloc(X.nbytes)
+        hip.upload(Xd, X)
+        Nd = None
+        if spec.speculative:
+            N = np.ascontiguousarray(np.stack([wl.verified_len(t) for t in range(T)]), dtype=np.int64)
+            Nd = hip.alloc(N.nbytes)
+            hip.upload(Nd, N)
+        slots = hip.alloc(B * nq * K * 4)
+        counts = hip.alloc(B * nq * 4)
+        stream = hip.stream()       # the batched call refuses the legacy default stream
+        h = A.avsg_create(cfg, host_ptrs, wl.ctx, ws, ws_bytes, bufs, stream)
+        per_step = B * nq * K * 4
+        try:
+            for t in range(warm):
+                A.avsg_step(h, Xd + t * per_step, Nd + t * B * 8 if Nd else None, slots, counts, stream)
+            hip.sync()
+            before = A.avsg_stats(h)
+            A.avsg_set_timing(h, True)
+            t0 = time.perf_counter()
+            for t in range(warm, T):
+                A.avsg_step(h, Xd + t * per_step, Nd + t * B * 8 if Nd else None, slots, counts, stream)
+            hip.sync()
+            wall = time.perf_counter() - t0
+            _, gather_ms, _ = A.avsg_timing(h, timed)
+            after = A.avsg_stats(h)
+        finally:
+            A.avsg_destroy(h)
+        moved = after["host_bytes"] - before["host_bytes"]
+        gsec = float(np.sum(gather_ms)) * 1e-3
+        row = {"workload": name, "batch": B, "n_q": nq, "steps_timed": timed,
+               "copy_calls_per_step": round((after["copy_calls"] - before["copy_calls"]) / timed, 1),
+               "rows_per_step": round((after["misses"] - before["misses"]) * len(spec.row_bytes) / timed, 1),
+               "gather_us_median": round(float(np.median(gather_ms)) * 1e3, 2),
+               "wall_us_per_step": round(wall / timed * 1e6, 2),
+               "host_gbps": round(moved / gsec / 1e9, 3) if gsec > 0 else 0.0}
+        results.append(row)
+        print(json.dumps(row), flush=True)
+        hip.free_all()
+        for reg in regions:
+            reg.free()
     with open(out_path, "w") as f:
         json.dump(results, f, indent=1)
 

@@ -113,6 +113,8 @@ typedef struct avsg_stats_t {
     uint64_t host_bytes;      /* payload bytes read over the host link, all streams */
     int32_t max_step_alloc_decays; /* largest allocation-decay count of one request-step */
     int32_t queue_timeouts;   /* pipelined step: consumers that gave up waiting (0 in correct operation) */
+    uint64_t copy_calls;      /* AVSG_GATHER_SDMA: runtime copy calls issued (one per step when the HIP
+                                 runtime in the process has the batched copy call, else one per row) */
 } avsg_stats_t;
 
 typedef struct avsg_handle avsg_handle;

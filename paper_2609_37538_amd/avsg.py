@@ -59,7 +59,8 @@ class AvsgStats(ctypes.Structure):
         "steps", "lookups", "hits", "misses", "bytes_moved", "lost_exhausted", "lost_collision",
         "alloc_decays", "revivals", "invalidations", "bad_indices", "resident_rows",
         "duplicate_rows", "host_bytes")] + [
-        ("max_step_alloc_decays", ctypes.c_int32), ("queue_timeouts", ctypes.c_int32)]
+        ("max_step_alloc_decays", ctypes.c_int32), ("queue_timeouts", ctypes.c_int32),
+        ("copy_calls", ctypes.c_uint64)]
 
     def as_dict(self):
         return {f: int(getattr(self, f)) for f, _ in self._fields_}
@@ -78,8 +79,11 @@ _lib = None
 _P = ctypes.c_void_p
 
 
-def load():
-    """Load libavsg.so; raises if it has not been built."""
+def load(share_torch_runtime: bool = True):
+    """Load libavsg.so; raises if it has not been built.  With
+    share_torch_runtime (the default) torch is imported first when installed,
+    so the library runs on torch's HIP runtime; a process that never uses
+    torch passes False and gets the system runtime."""
     global _lib
     if _lib is not None:
         return _lib
@@ -90,10 +94,11 @@ def load():
     # whichever loads first serves the whole process, and torch cannot start
     # on a different one, so torch (when installed) goes first and the library
     # shares its runtime
-    try:
-        import torch  # noqa: F401
-    except ImportError:
-        pass
+    if share_torch_runtime:
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
     lib = ctypes.CDLL(LIB_PATH)
     i32, i64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     lib.avsg_check_config.restype = i32

@@ -5,6 +5,8 @@
 // Stage One / Stage Two kernels of each decode step on the caller's stream.
 #include "avsg.h"
 
+#include <dlfcn.h>
+
 #include <algorithm>
 #include <array>
 #include <cstdio>
@@ -58,7 +60,11 @@ struct avsg_handle {
                                                    // main Stage Two kernel, after Stage Two
   std::vector<bool> has_tail;                      // step recorded the fourth event
   size_t n_timed = 0;
-  // SDMA comparator staging (pinned host)
+  // SDMA comparator staging (pinned host); the batched copy call when the HIP
+  // runtime loaded in the process exports it
+  hipError_t (*batch_copy)(void**, void**, size_t*, size_t, hipMemcpyAttributes*, size_t*, size_t,
+                           size_t*, hipStream_t) = nullptr;
+  uint64_t copy_calls = 0;
   int32_t* h_counts = nullptr;
   int2* h_list = nullptr;
   std::vector<void*> dsts, srcs;
@@ -369,6 +375,9 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
       return cleanup(AVSG_E_HIP);
     h->dsts.reserve(nl * c.n_streams);
     h->srcs.reserve(nl * c.n_streams);
+    // looked up at run time: the library must also load into processes whose
+    // runtime predates the call (PyTorch ships such a runtime)
+    h->batch_copy = reinterpret_cast<decltype(h->batch_copy)>(dlsym(RTLD_DEFAULT, "hipMemcpyBatchAsync"));
     h->sizes.reserve(nl * c.n_streams);
   }
   if (hipStreamSynchronize(s) != hipSuccess) return cleanup(AVSG_E_HIP);
@@ -423,9 +432,27 @@ static avsg_status sdma_gather(avsg_handle* h, const int32_t* d_counts, hipStrea
       }
     }
   }
+  if (h->sizes.empty()) return AVSG_OK;
+  if (h->batch_copy) {
+    // every row and stream in one batched call (the runtime takes no copy
+    // attributes; the copies are ordered on the stream like any other)
+    size_t failed = 0;
+    const hipError_t e = h->batch_copy(h->dsts.data(), h->srcs.data(), h->sizes.data(), h->sizes.size(),
+                                       nullptr, nullptr, 0, &failed, s);
+    if (e == hipSuccess) {
+      h->copy_calls += 1;
+      return AVSG_OK;
+    }
+    if (e != hipErrorNotSupported) return hip_fail(h, e, "hipMemcpyBatchAsync");
+    // refused before any copy was queued (the legacy default stream, for
+    // one): this handle issues one call per row from now on
+    (void)hipGetLastError();
+    h->batch_copy = nullptr;
+  }
   // one copy-engine command per missed row and stream
   for (size_t i = 0; i < h->sizes.size(); ++i)
     HIP_TRY(h, hipMemcpyAsync(h->dsts[i], h->srcs[i], h->sizes[i], hipMemcpyHostToDevice, s));
+  h->copy_calls += h->sizes.size();
   return AVSG_OK;
 }
 
@@ -591,6 +618,7 @@ avsg_status avsg_stats(avsg_handle* h, avsg_stats_t* out) {
   if (!h || !out) return AVSG_E_INVAL;
   avsg_status rc = collect_stats(h, 0, h->cfg.batch, out);
   if (rc != AVSG_OK) return rc;
+  out->copy_calls = h->copy_calls;
   if (h->cfg.gather_mode == AVSG_GATHER_PIPELINED) {
     int ctl[5] = {0, 0, 0, 0, 0};
     HIP_TRY(h, hipMemcpy(ctl, h->pipe_ctl, sizeof(ctl), hipMemcpyDeviceToHost));
@@ -613,6 +641,7 @@ avsg_status avsg_reset_stats(avsg_handle* h, void* stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   HIP_TRY(h, launch_zero_u64(h->stats, static_cast<size_t>(h->cfg.batch) * kNumStats, s));
   h->steps = 0;
+  h->copy_calls = 0;
   h->last_stream = s;
   return AVSG_OK;
 }

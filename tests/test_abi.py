@@ -38,10 +38,30 @@ def test_binding_has_same_names(lib):
         assert hasattr(A, n), f"binding lacks {n}"
 
 
-def test_struct_sizes_match_header(lib):
-    # avsg_config: 10 int32 + 2 int64 + 2 int32 = 64 bytes; stats: 14 u64 + 2 i32
-    assert ctypes.sizeof(A.AvsgConfig) == 64
-    assert ctypes.sizeof(A.AvsgStats) == 120
+def test_struct_layouts_match_header(lib, tmp_path):
+    """Every field offset and the size of the binding's structs equal what a C
+    compiler makes of include/avsg.h."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    lines = ['#include <stddef.h>', '#include <stdio.h>', '#include "avsg.h"', "int main(void) {"]
+    for cname, py in (("avsg_config", A.AvsgConfig), ("avsg_stats_t", A.AvsgStats)):
+        lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
+        for fname, _ in py._fields_:
+            lines.append(f'printf("{cname} {fname} %zu\\n", offsetof({cname}, {fname}));')
+    lines += ["return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
+    got = {tuple(l.split()[:2]): int(l.split()[2]) for l in out if l}
+    for cname, py in (("avsg_config", A.AvsgConfig), ("avsg_stats_t", A.AvsgStats)):
+        assert got[(cname, "size")] == ctypes.sizeof(py), cname
+        for fname, _ in py._fields_:
+            assert got[(cname, fname)] == getattr(py, fname).offset, f"{cname}.{fname}"
 
 
 def test_strerror(lib):

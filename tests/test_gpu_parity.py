@@ -555,3 +555,16 @@ def test_graph_capture_replays_steps(mode, n_q):
         eager.close()
         graphed.close()
         host.free()
+
+
+def test_copy_engine_batched_call_without_torch():
+    """In a process that never loads torch, the copy-engine transfer issues one
+    batched runtime copy call per step and matches the oracle step by step
+    (tests/copy_engine_batched_check.py, run as a child process)."""
+    import subprocess
+    import sys
+    here = os.path.dirname(os.path.abspath(__file__))
+    r = subprocess.run([sys.executable, "-u", os.path.join(here, "copy_engine_batched_check.py")],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, (r.stdout[-3000:], r.stderr[-3000:])
+    assert r.stdout.strip().splitlines()[-1].startswith("ok copy_calls=")
