@@ -184,7 +184,8 @@ avsg_status avsg_stats(avsg_handle *h, avsg_stats_t *out);
 
 /* The same counters for request r alone (lookups = steps * N_q * K), for
  * per-request hit rates such as the request-averaged rate the paper reports
- * over real requests (Appendix A).  queue_timeouts is 0.  Synchronizes with the
+ * over real requests (Appendix A).  queue_timeouts and copy_calls (counted for
+ * the whole handle) are 0.  Synchronizes with the
  * handle's last stream.  Errors: AVSG_E_INVAL (r outside [0, B)), AVSG_E_HIP. */
 avsg_status avsg_request_stats(avsg_handle *h, int32_t r, avsg_stats_t *out);
 avsg_status avsg_reset_stats(avsg_handle *h, void *stream);
