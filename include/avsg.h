@@ -166,13 +166,12 @@ avsg_status avsg_create(const avsg_config *cfg, const void *const *host_rows,
  * When the step's kernels finish, every slot named in d_slots holds the row of
  * its index in every stream.  Indices outside [0, rows) are counted in
  * bad_indices and not copied.  The current HIP device must be the one that
- * was current at avsg_create.  With timing off, a step of the balanced,
- * request-level, position-level or resident-reuse transfer can be captured
- * into a HIP graph (stream capture): it enqueues kernels only, keeps every
- * piece of step state in the workspace, and each replay is the next decode
- * step on whatever d_topk then holds.  The copy-engine transfer waits on the
- * host and the pipelined step stamps its queue on the host, so neither can be
- * captured.  Errors: AVSG_E_INVAL (null pointer, other device), AVSG_E_HIP. */
+ * was current at avsg_create.  With timing off, a step of any transfer but
+ * the copy-engine one (which waits on the host) can be captured into a HIP
+ * graph (stream capture): it enqueues kernels only, keeps every piece of step
+ * state in the workspace (step stamps advance on the device), and each replay
+ * is the next decode step on whatever d_topk then holds.
+ * Errors: AVSG_E_INVAL (null pointer, other device), AVSG_E_HIP. */
 avsg_status avsg_step(avsg_handle *h, const int32_t *d_topk, const int64_t *d_verified_len,
                       int32_t *d_slots, int32_t *d_miss_counts, void *stream);
 

@@ -39,10 +39,9 @@ struct avsg_handle {
   int32_t* plan_counts = nullptr;  // [B][3]
   int32_t* plan_claim = nullptr;
   int plan_words = 0;
-  int* pipe_ctl = nullptr;      // head, tail, done, exit_count, error
+  int* pipe_ctl = nullptr;      // head, tail, done, exit_count, error, last epoch
   int4* pipe_chunks = nullptr;
   int pipe_max_chunks = 0;
-  int pipe_epoch = 0;
   int cus = 0;
   unsigned long long* stats = nullptr;
   uint64_t* host_ptrs = nullptr;
@@ -488,10 +487,8 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
     g.row_bytes1 = c.n_streams > 1 ? c.row_bytes[1] : 0;
     PipeParams q{};
     q.head = h->pipe_ctl; q.tail = h->pipe_ctl + 1; q.done = h->pipe_ctl + 2;
-    q.exit_count = h->pipe_ctl + 3; q.error = h->pipe_ctl + 4;
+    q.exit_count = h->pipe_ctl + 3; q.error = h->pipe_ctl + 4; q.last_epoch = h->pipe_ctl + 5;
     q.chunks = h->pipe_chunks; q.max_chunks = h->pipe_max_chunks;
-    if (++h->pipe_epoch <= 0) h->pipe_epoch = 1;
-    q.epoch = h->pipe_epoch;
     const int wgs = std::max(c.batch, c.gather_workers > 0 ? c.gather_workers : h->cus);
     HIP_TRY(h, launch_step_pipelined(p, g, q, wgs, h->lds, s));
     if ((rc = record(h, 1, s)) != AVSG_OK) return rc;

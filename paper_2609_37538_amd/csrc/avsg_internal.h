@@ -83,9 +83,10 @@ struct PipeParams {
   int* done;          // requests whose Stage One has finished
   int* exit_count;    // workgroups that have left
   int* error;         // set when a consumer gave up waiting
+  int* last_epoch;    // stamp of the last finished step (advanced on the device)
   int4* chunks;       // [max_chunks] (request, first miss, count, epoch)
   int max_chunks;
-  int epoch;          // step stamp, never 0
+  int epoch;          // this step's stamp, never 0 (set by the kernel from last_epoch)
 };
 
 struct DualPtrParams {

@@ -5,7 +5,9 @@
 // workgroup runs per CU.  Workgroups 0..B-1 first run Stage One for their
 // request (the same code as the matching kernel); after each token they
 // publish that token's transfer-list entries as chunks of kChunk misses in a
-// device-wide queue, stamped with the step's epoch.  Every workgroup -- the
+// device-wide queue, stamped with the step's epoch (one more than the last
+// step's, kept in device memory, so a captured step replayed from a HIP graph
+// stamps every replay anew).  Every workgroup -- the
 // producers once their request is matched -- then claims chunks with an
 // atomic counter and copies them, so copying starts after the first token of
 // the first requests instead of after the whole batch is matched.  Work is
@@ -143,6 +145,10 @@ template <int IPT>
 __global__ __launch_bounds__(kMatchThreads) void step_pipelined_kernel(MatchParams mp, GatherParams gp,
                                                                        PipeParams q) {
   extern __shared__ __align__(16) unsigned char lds[];
+  // every workgroup reads the last stamp before any can leave, and only the
+  // last to leave advances it
+  q.epoch = load_agent(q.last_epoch) + 1;
+  if (q.epoch <= 0) q.epoch = 1;
   if (static_cast<int>(blockIdx.x) < mp.B) {
     QueuePublish pub{q};
     match_request<IPT, kMatchThreads>(mp, static_cast<int>(blockIdx.x), lds, pub);
@@ -160,6 +166,7 @@ __global__ __launch_bounds__(kMatchThreads) void step_pipelined_kernel(MatchPara
       *q.head = 0;
       *q.tail = 0;
       *q.done = 0;
+      *q.last_epoch = q.epoch;
       __threadfence();
       *q.exit_count = 0;
     }

@@ -504,8 +504,9 @@ def test_two_handles_on_two_streams():
         host.free()
 
 
-@pytest.mark.parametrize("mode,n_q", [(0, 2), (1, 1), (4, 2), (6, 2), (6, 3)],
-                         ids=["balanced", "request_level", "position_level", "resident", "resident_3_tokens"])
+@pytest.mark.parametrize("mode,n_q", [(0, 2), (1, 1), (4, 2), (5, 2), (6, 2), (6, 3)],
+                         ids=["balanced", "request_level", "position_level", "pipelined", "resident",
+                              "resident_3_tokens"])
 def test_graph_capture_replays_steps(mode, n_q):
     """One avsg_step captured into a HIP graph and replayed once per decode
     step (new selections copied into the captured input between replays, with
