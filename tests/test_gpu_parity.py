@@ -569,3 +569,37 @@ def test_copy_engine_batched_call_without_torch():
                        capture_output=True, text=True, timeout=300)
     assert r.returncode == 0, (r.stdout[-3000:], r.stderr[-3000:])
     assert r.stdout.strip().splitlines()[-1].startswith("ok copy_calls=")
+
+
+@pytest.fixture(scope="module")
+def c_abi_program(tmp_path_factory):
+    """tests/c_abi_parity.c built with gcc against include/avsg.h, the
+    library, the C oracle and the HIP runtime."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    exe = str(tmp_path_factory.mktemp("c_abi") / "c_abi_parity")
+    pkg, orc = os.path.join(root, "paper_2609_37538_amd"), os.path.join(root, "oracle")
+    subprocess.run([cc, "-std=c11", "-O2", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__",
+                    "-I", "/opt/rocm/include", "-I", os.path.join(root, "include"), "-I", orc,
+                    os.path.join(root, "tests", "c_abi_parity.c"), "-o", exe,
+                    "-L", pkg, "-lavsg", "-L", orc, "-loracle_avsg", "-L", "/opt/rocm/lib", "-lamdhip64",
+                    f"-Wl,-rpath,{pkg}", f"-Wl,-rpath,{orc}", "-Wl,-rpath,/opt/rocm/lib"], check=True)
+    return exe
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2, 4, 5, 6],
+                         ids=["balanced", "request_level", "copy_engine", "position_level", "pipelined",
+                              "resident"])
+def test_c_caller_against_c_oracle(c_abi_program, mode):
+    """A C program drives the library through include/avsg.h (hipMalloc'd
+    device memory, its own stream) and the oracle through its C interface;
+    slots, counts and both streams' buffers agree after every step."""
+    import subprocess
+    log(f"[c abi] mode {mode}")
+    r = subprocess.run([c_abi_program, str(mode)], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, (r.stdout[-2000:], r.stderr[-2000:])
+    assert r.stdout.startswith(f"ok mode {mode} ")
