@@ -3,7 +3,9 @@
 The method's oracle is plain C (``avsg_oracle.c``), compiled with gcc into
 ``liboracle_avsg.so`` and driven through ctypes with NumPy arrays;
 ``transfer_plan`` (plain Python) defines which misses the resident-reuse
-transfer may fill from another slot.  Only the test suite, the smoke check and
+transfer may fill from another slot, and ``early_set`` / ``transfer_plan_early``
+which rows the early-fetch transfer may read from the host before Stage One
+and what is left to plan after it.  Only the test suite, the smoke check and
 the benchmark's CPU-baseline leg use this package; the product path never
 imports it.
 """
@@ -333,6 +335,49 @@ def transfer_plan(miss_x, miss_o, c_after, rows_r: int):
             lists[1].append(o)
             lists[2].append(fan.get(x, -1) if valid else -1)
     return tuple(np.asarray(v, dtype=np.int32) for v in lists)
+
+
+EARLY_MAX_POSITIONS = 4
+
+
+def early_set(X_r, c_before, rows_r: int, max_positions: int = EARLY_MAX_POSITIONS):
+    """Indices of one request-step whose rows can cross the host link before
+    Stage One has run.  Like transfer_plan, a property of the transfer, not of
+    the paper's method.
+
+    Plain definition: the distinct indices x of the step's selections X_r
+    (every token) such that
+      - 0 <= x < rows_r,
+      - c_before[j] != x for every slot j (no slot held x when the step began),
+      - x occurs at most max_positions times over the step's tokens.
+    Such an x misses where it first occurs (no slot can satisfy c[o] == x), and
+    no slot outside the step's reservations caches it afterwards, so the
+    paper's Stage Two reads its row from the host whatever the slots turn out
+    to be; every position of x ends with x's row in its slot.
+    Returns (keys ascending, positions): positions[k] lists the flat positions
+    g * K + i of keys[k] in increasing order."""
+    X_r = np.asarray(X_r).reshape(-1)
+    cached = {int(v) for v in np.asarray(c_before).tolist()}
+    where = {}
+    for pos, x in enumerate(X_r.tolist()):
+        if 0 <= x < rows_r:
+            where.setdefault(int(x), []).append(pos)
+    keys = sorted(x for x, p in where.items() if x not in cached and len(p) <= max_positions)
+    return np.asarray(keys, dtype=np.int32), [where[x] for x in keys]
+
+
+def transfer_plan_early(miss_x, miss_o, c_after, rows_r: int, early_keys):
+    """Resident-reuse plan of the misses left to Stage Two once the early
+    fetch (early_set) has written every position of its keys: transfer_plan
+    over the transfer list without the misses of early keys.  Dropping them
+    changes no other entry: an early key's slots cache that key (or nothing),
+    so they are never a resident source of another index.
+    Returns the seven lists of transfer_plan."""
+    early = {int(v) for v in np.asarray(early_keys).tolist()}
+    keep = [k for k, x in enumerate(np.asarray(miss_x).tolist()) if int(x) not in early]
+    mx = np.asarray(miss_x, dtype=np.int32)[keep]
+    mo = np.asarray(miss_o, dtype=np.int32)[keep]
+    return transfer_plan(mx, mo, c_after, rows_r)
 
 
 def partition_balanced(n_miss: int, C: int) -> np.ndarray:

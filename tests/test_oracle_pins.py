@@ -572,3 +572,113 @@ def test_transfer_plan_three_tokens_repeat(oracle_lib):
     hx, ho, hf, rs, rd, ps, pd = O.transfer_plan(mx, mo, c, 10)
     assert hx.tolist() == [7] and ho.tolist() == [4] and hf.tolist() == [3]
     assert ps.tolist() == [4] and pd.tolist() == [1] and len(rs) == 0
+
+
+# ---------------------------------------------------------------------------
+# early-fetch transfer: rows of indices no slot held when the step began are
+# read from the host before Stage One; the rest is planned as above
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("K,n_q,S,R,L,U,T,bad,share", [
+    (16, 2, 32, 0, 4, 60, 40, False, 0.0),
+    (8, 3, 32, 1, 2, 40, 40, False, 0.5),
+    (16, 4, 64, 0, 16, 120, 30, False, 0.7),
+    (16, 2, 32, 0, 4, 60, 30, True, 0.5),
+    (6, 5, 32, 0, 3, 30, 30, False, 0.9),    # ids listed by all five tokens exceed four positions
+])
+def test_early_fetch_replays_stage_two(oracle_lib, K, n_q, S, R, L, U, T, bad, share):
+    """Writing every early key's row into the slot of each of its positions and
+    then replaying the plan of the remaining misses gives, step after step,
+    the buffer of the paper's Stage Two.  Early keys are host entries of the
+    full plan, and their positions' slots are slots the step reserved for
+    them."""
+    rng = np.random.default_rng(K * 1000 + n_q * 10 + int(bad))
+    B = 2
+    rows = U
+    orc = O.Oracle(B, K, n_q, S, retry=R, max_life=L, nthreads=1)
+    paper = [np.full(S, -1, dtype=np.int64) for _ in range(B)]
+    early_buf = [np.full(S, -1, dtype=np.int64) for _ in range(B)]
+    n_early = n_left = n_capped = 0
+    for t in range(T):
+        X = np.empty((B, n_q, K), dtype=np.int32)
+        for r in range(B):
+            X[r, 0] = rng.choice(U, size=K, replace=False)
+            for g in range(1, n_q):
+                x = rng.choice(U, size=K, replace=False)
+                keep = rng.random(K) < share
+                x[keep] = X[r, 0][keep]             # later tokens repeat some of token 0's ids
+                _, first = np.unique(x, return_index=True)
+                if len(first) < K:                  # keep the token's ids distinct
+                    pool = np.setdiff1d(np.arange(U), x)
+                    dup = np.setdiff1d(np.arange(K), first)
+                    x[dup] = rng.choice(pool, size=len(dup), replace=False)
+                X[r, g] = x
+        if bad:
+            X[0, 0, 0] = U + 5
+        before = [orc.export(r)[0] for r in range(B)]
+        O_t, n = orc.step(X)
+        for r in range(B):
+            mx, mo = orc.misses(r, n[r])
+            for x, o in zip(mx.tolist(), mo.tolist()):
+                if 0 <= x < rows:
+                    paper[r][o] = x
+            keys, where = O.early_set(X[r], before[r], rows)
+            counts = {}
+            for x in X[r].ravel().tolist():
+                counts[x] = counts.get(x, 0) + 1
+            n_capped += sum(1 for x, c in counts.items()
+                            if 0 <= x < rows and c > O.EARLY_MAX_POSITIONS and x not in before[r])
+            c_after, _ = orc.export(r)
+            full = O.transfer_plan(mx, mo, c_after, rows)
+            host_keys = {int(x) for x in full[0].tolist() if 0 <= x < rows}
+            assert set(keys.tolist()) <= host_keys
+            flat = O_t[r].ravel()
+            for x, ps in zip(keys.tolist(), where):
+                reserved = {int(o) for xx, o in zip(mx.tolist(), mo.tolist()) if xx == x}
+                assert {int(flat[p]) for p in ps} == reserved
+                for p in ps:
+                    early_buf[r][flat[p]] = x
+            rest = O.transfer_plan_early(mx, mo, c_after, rows, keys)
+            _replay_plan(early_buf[r], rest, rows)
+            assert np.array_equal(early_buf[r], paper[r]), f"step {t} request {r}"
+            n_early += len(keys)
+            n_left += len([x for x in rest[0].tolist() if 0 <= x < rows])
+    assert n_early > 0
+    if n_q == 5:
+        assert n_capped > 0
+
+
+def test_early_set_excludes_cached_indices(oracle_lib):
+    """Hand case: id 42 sits in dead slot 0 with no bucket mapping it, id 43 is
+    nowhere.  Both miss; 42 takes slot 0 (the first dead slot), which already
+    holds its row, and 43 takes slot 1.  Only 43 is an early key; 42, cached
+    when the step began, stays with the planned transfer as a host entry (its
+    only copy is in a slot this step reserved)."""
+    S, m = 8, 3
+    orc = O.Oracle(1, 2, 1, S, retry=S - 1, max_life=4, nthreads=1)
+    c = np.full(S, -1, dtype=np.int32)
+    c[0] = 42
+    q = np.full(S, O.pack(m, -1, 1, 0, 3), dtype=np.uint32)   # every bucket names empty slot 3
+    orc.import_table(0, c, q)
+    before = orc.export(0)[0]
+    X = np.array([[[42, 43]]], dtype=np.int32)
+    O_t, n = orc.step(X, rows=np.array([100], dtype=np.int64))
+    assert n[0, 0] == 2 and O_t[0, 0].tolist() == [0, 1]
+    keys, where = O.early_set(X[0], before, 100)
+    assert keys.tolist() == [43] and where == [[1]]
+    mx, mo = orc.misses(0, n[0])
+    c_after, _ = orc.export(0)
+    hx, ho, hf, rs, rd, ps, pd = O.transfer_plan_early(mx, mo, c_after, 100, keys)
+    assert hx.tolist() == [42] and ho.tolist() == [0] and len(rs) == 0 and len(ps) == 0
+    full = O.transfer_plan(mx, mo, c_after, 100)
+    assert full[0].tolist() == [42, 43]
+
+
+def test_early_set_positions_and_limits(oracle_lib):
+    """Hand case: positions are flat g * K + i; an id at five positions (beyond
+    four), an out-of-range id and a cached id are not early keys."""
+    X = np.array([[5, 9, 2], [9, 5, 3], [9, 4, 7], [9, 8, 6], [9, 1, 0]], dtype=np.int32)
+    c = np.array([-1, 3, -1, -1], dtype=np.int32)
+    keys, where = O.early_set(X, c, rows_r=9)
+    assert keys.tolist() == [0, 1, 2, 4, 5, 6, 7, 8]
+    assert where[keys.tolist().index(5)] == [0, 4]
+    assert 9 not in keys.tolist() and 3 not in keys.tolist()
