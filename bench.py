@@ -40,7 +40,8 @@ def parse():
     ap.add_argument("--config", default="batch64_mtp2",
                     choices=["tiny", "batch16", "batch64_mtp2", "imbalance", "stress"])
     ap.add_argument("--gather", default="resident",
-                    choices=["balanced", "request", "position", "sdma", "none", "pipelined", "resident"])
+                    choices=["balanced", "request", "position", "sdma", "none", "pipelined", "resident",
+                             "early"])
     ap.add_argument("--match", default="hash", choices=["hash", "dualptr"])
     ap.add_argument("--workers", type=int, default=0, help="gather workgroups (0 = one per CU)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -97,7 +98,8 @@ def main():
                    "sdma": A.AVSG_GATHER_SDMA, "none": A.AVSG_GATHER_NONE,
                    "position": A.AVSG_GATHER_POSITION,
                    "pipelined": A.AVSG_GATHER_PIPELINED,
-                   "resident": A.AVSG_GATHER_RESIDENT}[args.gather]
+                   "resident": A.AVSG_GATHER_RESIDENT,
+                   "early": A.AVSG_GATHER_EARLY}[args.gather]
     match_mode = {"hash": A.AVSG_MATCH_HASH, "dualptr": A.AVSG_MATCH_DUALPTR}[args.match]
     spec = W.get_spec(args.config)
     if match_mode == A.AVSG_MATCH_DUALPTR:
@@ -191,7 +193,7 @@ def main():
     # ---- reference: the paper's Stage Two (S3, every miss copied from the
     # host) on the same steps, same host rows, same stream ----
     reference = None
-    if gather_mode == A.AVSG_GATHER_RESIDENT and not args.no_reference:
+    if gather_mode in (A.AVSG_GATHER_RESIDENT, A.AVSG_GATHER_EARLY) and not args.no_reference:
         cfg_ref = A.make_config(spec.batch, spec.topk, spec.n_q, spec.slots, row_bytes=spec.row_bytes,
                                 gather_workers=args.workers, match_mode=match_mode,
                                 gather_mode=A.AVSG_GATHER_BALANCED)
@@ -218,6 +220,22 @@ def main():
     moved = misses * row_total if gather_mode != A.AVSG_GATHER_NONE else 0
     host_moved = after["host_bytes"] - before["host_bytes"]
     pipelined = gather_mode == A.AVSG_GATHER_PIPELINED
+    early = gather_mode == A.AVSG_GATHER_EARLY
+    early_info = None
+    if early:
+        # three launches: the early list (timed in the matching slot), Stage
+        # One beside the early copies (the main Stage Two slot) and the
+        # finishing kernel (the tail slot); matching runs inside the second
+        early_info = {
+            "early_list_us_median": round(float(np.median(match_ms)) * 1e3, 2) if len(match_ms) else None,
+            "match_and_early_copy_us_median": round(float(np.median(gather_ms)) * 1e3, 2) if len(gather_ms) else None,
+            "finish_us_median": round(float(np.median(tail_ms)) * 1e3, 2) if len(tail_ms) else None,
+            "early_rows_per_step": round((after["early_rows"] - before["early_rows"]) / args.steps, 1),
+            "early_staged_rows_per_step": round((after["early_staged_rows"] - before["early_staged_rows"])
+                                                / args.steps, 1),
+            "early_deferred_rows_per_step": round((after["early_deferred_rows"]
+                                                   - before["early_deferred_rows"]) / args.steps, 1),
+        }
     if pipelined:
         # one fused launch: its duration is recorded in the matching slot
         gather_ms, match_ms = match_ms, np.zeros_like(match_ms)
@@ -270,6 +288,7 @@ def main():
         "gather_us_median": round(float(np.median(gather_ms)) * 1e3, 2) if len(gather_ms) else None,
         "repeat_copy_us_median": (round(float(np.median(tail_ms)) * 1e3, 2)
                                   if gather_mode == A.AVSG_GATHER_RESIDENT and len(tail_ms) else None),
+        "early_fetch": early_info,
         "match_us_p99": (round(float(np.percentile(match_ms, 99)) * 1e3, 2)
                          if len(match_ms) and not pipelined else None),
         "gather_us_p99": round(float(np.percentile(gather_ms, 99)) * 1e3, 2) if len(gather_ms) else None,
@@ -281,7 +300,8 @@ def main():
         "roofline": {
             "bound": "pcie",
             "kernel": {"balanced": "gather_balanced_kernel", "resident": "gather_resident_kernel",
-                       "pipelined": "step_pipelined_kernel"}.get(args.gather, args.gather),
+                       "pipelined": "step_pipelined_kernel",
+                       "early": "step_early_kernel"}.get(args.gather, args.gather),
             "achieved": round(gather_gbps, 3),
             "peak": PCIE_GEN5_X16_GBPS,
             "unit": "GB/s",

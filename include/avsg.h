@@ -77,6 +77,17 @@ typedef int32_t avsg_status;
                                    contents are identical to AVSG_GATHER_BALANCED.  Relies on the same
                                    property as a hit: a cached row below the verified length does not change
                                    on the host. */
+#define AVSG_GATHER_EARLY 7     /* resident reuse whose host reads start before Stage One (hash matching
+                                   only).  An index that no slot of its request holds when the step begins
+                                   misses where it first occurs (Eq. 10 needs c[o] == x) and is in no slot
+                                   outside the step's reservations afterwards, so Stage Two reads its row from
+                                   the host whatever slots Stage One picks.  A first kernel lists those indices
+                                   (at most four positions each); in the next launch workgroups beside the
+                                   matching ones copy their rows while Stage One runs, straight into the slots
+                                   of their positions once a request's O is written, else into HBM staging
+                                   that a third kernel moves to the slots.  The matching workgroup plans and
+                                   copies the rest as AVSG_GATHER_RESIDENT does.  Slots, counts, tables and
+                                   buffer contents are identical to AVSG_GATHER_BALANCED. */
 
 #define AVSG_MAX_STREAMS 2
 
@@ -93,6 +104,12 @@ typedef struct avsg_config {
     int64_t row_bytes[AVSG_MAX_STREAMS]; /* bytes per row of each stream, multiple of 4 */
     int32_t match_mode;  /* AVSG_MATCH_* */
     int32_t gather_mode; /* AVSG_GATHER_* */
+    /* AVSG_GATHER_EARLY only (0 = default for both): */
+    int32_t early_staging_rows; /* rows of HBM staging for rows fetched before their slots are known:
+                                   0 = min(B*N_q*K, 16384), -1 = none (such rows are read from the host
+                                   again after Stage One), else the count */
+    int32_t early_direct;       /* 0 = a fetched row goes straight into its slots once they are known;
+                                   -1 = every early row goes through staging (measurement and tests) */
 } avsg_config;
 
 /* Cumulative counters since create (or the last avsg_reset_stats). */
@@ -115,6 +132,9 @@ typedef struct avsg_stats_t {
     int32_t queue_timeouts;   /* pipelined step: consumers that gave up waiting (0 in correct operation) */
     uint64_t copy_calls;      /* AVSG_GATHER_SDMA: runtime copy calls issued (one per step when the HIP
                                  runtime in the process has the batched copy call, else one per row) */
+    uint64_t early_rows;      /* AVSG_GATHER_EARLY: host rows fetched before Stage One (one per index) */
+    uint64_t early_staged_rows;   /* of those, rows parked in staging until their slots were known */
+    uint64_t early_deferred_rows; /* of those, rows read after Stage One because staging was full */
 } avsg_stats_t;
 
 typedef struct avsg_handle avsg_handle;
@@ -205,9 +225,10 @@ avsg_status avsg_export_state(avsg_handle *h, int32_t r, int32_t *c_out, uint32_
 avsg_status avsg_export_misses(avsg_handle *h, int32_t r, int32_t *n_out, int32_t *x_out,
                                int32_t *o_out);
 
-/* Stage Two plan of request r from the last step (AVSG_GATHER_RESIDENT only),
- * copied to host memory (synchronous); every list keeps transfer-list order
- * and has capacity N_q*K:
+/* Stage Two plan of request r from the last step (AVSG_GATHER_RESIDENT, or
+ * AVSG_GATHER_EARLY, whose plan leaves out the misses of early-fetched
+ * indices), copied to host memory (synchronous); every list keeps
+ * transfer-list order and has capacity N_q*K:
  *   n_host, host_x[k], host_o[k],  misses copied from host row host_x[k] into
  *   host_fan[k]                    slot host_o[k], and also into slot
  *                                  host_fan[k] when it is not -1 (the largest
@@ -226,13 +247,24 @@ avsg_status avsg_export_plan(avsg_handle *h, int32_t r, int32_t *n_host, int32_t
                              int32_t *host_o, int32_t *host_fan, int32_t *n_res, int32_t *res_src,
                              int32_t *res_dst, int32_t *n_rep, int32_t *rep_src, int32_t *rep_dst);
 
+/* Early list of request r from the last step (AVSG_GATHER_EARLY only), copied
+ * to host memory (synchronous): *n_out indices x_out[k] (capacity N_q*K) whose
+ * rows were fetched before Stage One, in the kernel's order (a hash order),
+ * and pos_out[4*k .. 4*k+3] the flat positions g*K + i of x_out[k] among the
+ * step's selections, in no particular order, -1 padded.
+ * Errors: AVSG_E_INVAL, AVSG_E_UNSUPPORTED (another gather mode), AVSG_E_HIP. */
+avsg_status avsg_export_early(avsg_handle *h, int32_t r, int32_t *n_out, int32_t *x_out,
+                              int32_t *pos_out);
+
 /* Per-step kernel timing with HIP events recorded on the step's stream.
  * avsg_set_timing(h, 1) starts recording (and clears the record);
  * avsg_timing copies up to `cap` recorded steps (synchronizing):
  * match_ms[i] is the duration of step i's matching kernel, gather_ms[i] that
  * of its main Stage Two kernel (or copies), and tail_ms[i] (may be NULL) the
  * rest of Stage Two: the repeat copies of AVSG_GATHER_RESIDENT with three or
- * more tokens per step, 0 otherwise. */
+ * more tokens per step, 0 otherwise.  AVSG_GATHER_EARLY: match_ms is the early
+ * list kernel, gather_ms the launch that matches and copies, tail_ms the
+ * finishing kernel. */
 avsg_status avsg_set_timing(avsg_handle *h, int32_t enable);
 avsg_status avsg_timing(avsg_handle *h, float *match_ms, float *gather_ms, float *tail_ms,
                         int32_t cap, int32_t *n_out);

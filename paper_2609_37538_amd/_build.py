@@ -12,7 +12,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB_PATH = os.path.join(PKG, "libavsg.so")
 
-SOURCES = ["avsg_host.hip", "match_hash.hip", "match_dualptr.hip", "gather.hip", "step_pipelined.hip"]
+SOURCES = ["avsg_host.hip", "match_hash.hip", "match_dualptr.hip", "gather.hip", "step_pipelined.hip",
+           "step_early.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

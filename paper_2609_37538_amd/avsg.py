@@ -37,6 +37,7 @@ AVSG_GATHER_NONE = 3
 AVSG_GATHER_POSITION = 4
 AVSG_GATHER_PIPELINED = 5
 AVSG_GATHER_RESIDENT = 6
+AVSG_GATHER_EARLY = 7
 AVSG_MAX_STREAMS = 2
 
 A1_DEFAULT = 2654435761
@@ -51,6 +52,7 @@ class AvsgConfig(ctypes.Structure):
         ("n_streams", ctypes.c_int32), ("gather_workers", ctypes.c_int32),
         ("row_bytes", ctypes.c_int64 * AVSG_MAX_STREAMS),
         ("match_mode", ctypes.c_int32), ("gather_mode", ctypes.c_int32),
+        ("early_staging_rows", ctypes.c_int32), ("early_direct", ctypes.c_int32),
     ]
 
 
@@ -60,7 +62,8 @@ class AvsgStats(ctypes.Structure):
         "alloc_decays", "revivals", "invalidations", "bad_indices", "resident_rows",
         "duplicate_rows", "host_bytes")] + [
         ("max_step_alloc_decays", ctypes.c_int32), ("queue_timeouts", ctypes.c_int32),
-        ("copy_calls", ctypes.c_uint64)]
+        ("copy_calls", ctypes.c_uint64), ("early_rows", ctypes.c_uint64),
+        ("early_staged_rows", ctypes.c_uint64), ("early_deferred_rows", ctypes.c_uint64)]
 
     def as_dict(self):
         return {f: int(getattr(self, f)) for f, _ in self._fields_}
@@ -124,6 +127,8 @@ def load(share_torch_runtime: bool = True):
     lib.avsg_export_misses.argtypes = [_P, i32, _P, _P, _P]
     lib.avsg_export_plan.restype = i32
     lib.avsg_export_plan.argtypes = [_P, i32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+    lib.avsg_export_early.restype = i32
+    lib.avsg_export_early.argtypes = [_P, i32, _P, _P, _P]
     lib.avsg_set_timing.restype = i32
     lib.avsg_set_timing.argtypes = [_P, i32]
     lib.avsg_timing.restype = i32
@@ -171,10 +176,10 @@ def _ptr_array(ptrs: Sequence[int]):
 
 def make_config(batch, topk, n_q, slots, retry=3, max_life=16, a1=A1_DEFAULT, a2=A2_DEFAULT,
                 row_bytes=(1152,), gather_workers=0, match_mode=AVSG_MATCH_HASH,
-                gather_mode=AVSG_GATHER_BALANCED) -> AvsgConfig:
+                gather_mode=AVSG_GATHER_BALANCED, early_staging_rows=0, early_direct=0) -> AvsgConfig:
     rb = (ctypes.c_int64 * AVSG_MAX_STREAMS)(*(list(row_bytes) + [0] * (AVSG_MAX_STREAMS - len(row_bytes))))
     return AvsgConfig(batch, topk, n_q, slots, retry, max_life, a1, a2, len(row_bytes),
-                      gather_workers, rb, match_mode, gather_mode)
+                      gather_workers, rb, match_mode, gather_mode, early_staging_rows, early_direct)
 
 
 # ---------------------------------------------------------------------------
@@ -252,6 +257,16 @@ def avsg_export_misses(h, r: int, capacity: int):
     _check(load().avsg_export_misses(h, r, ctypes.byref(n), x.ctypes.data_as(_P),
                                      o.ctypes.data_as(_P)), "avsg_export_misses", h)
     return x[: n.value].copy(), o[: n.value].copy()
+
+
+def avsg_export_early(h, r: int, capacity: int):
+    """(keys, positions [n][4], -1 padded) of request r's last early list."""
+    n = ctypes.c_int32(0)
+    x = np.empty(capacity, dtype=np.int32)
+    pos = np.empty((capacity, 4), dtype=np.int32)
+    _check(load().avsg_export_early(h, r, ctypes.byref(n), x.ctypes.data_as(_P), pos.ctypes.data_as(_P)),
+           "avsg_export_early", h)
+    return x[: n.value].copy(), pos[: n.value].copy()
 
 
 def avsg_set_timing(h, enable: bool) -> None:
@@ -384,6 +399,9 @@ class Operator:
 
     def export_plan(self, r: int):
         return avsg_export_plan(self.h, r, self.cfg.n_q * self.cfg.topk)
+
+    def export_early(self, r: int):
+        return avsg_export_early(self.h, r, self.cfg.n_q * self.cfg.topk)
 
     def close(self):
         if getattr(self, "h", None):

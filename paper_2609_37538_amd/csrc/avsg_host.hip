@@ -39,6 +39,17 @@ struct avsg_handle {
   int32_t* plan_counts = nullptr;  // [B][3]
   int32_t* plan_claim = nullptr;
   int plan_words = 0;
+  // early-fetch transfer (AVSG_GATHER_EARLY)
+  int32_t* early_x = nullptr;
+  int4* early_pos = nullptr;
+  int32_t* early_n = nullptr;
+  uint32_t* early_done = nullptr;
+  int* early_ctl = nullptr;
+  int4* early_fin = nullptr;
+  uint64_t stage0 = 0, stage1 = 0;
+  int stage_rows = 0;
+  int early_workers = 0;
+  size_t early_list_lds = 0;
   int* pipe_ctl = nullptr;      // head, tail, done, exit_count, error, last epoch
   int4* pipe_chunks = nullptr;
   int pipe_max_chunks = 0;
@@ -78,6 +89,8 @@ constexpr int kMaxBatch = 1024;
 constexpr size_t kMaxTimedSteps = 16384;
 constexpr size_t kLdsPerWorkgroup = 160 * 1024;   // gfx950
 constexpr int kRepeatWorkersPerCu = 4;
+constexpr int kEarlyStagingRows = 16384;   // default staging capacity of the early-fetch transfer
+constexpr int kEarlyWorkers = 32;          // default copy workgroups beside the matching ones
 
 size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
@@ -92,9 +105,39 @@ bool is_prime_u32(uint32_t v) {
 size_t pipe_chunks_for(const avsg_config& c);
 
 struct Layout {
-  size_t table_c, table_q, miss_list, hit_mask, plan, pipe, pipe_bytes, stats, host_ptrs, buf_ptrs, rows,
-      total;
+  size_t table_c, table_q, miss_list, hit_mask, plan, early, pipe, pipe_bytes, stats, host_ptrs, buf_ptrs,
+      rows, total;
 };
+
+bool has_plan(const avsg_config& c) {
+  return c.gather_mode == AVSG_GATHER_RESIDENT || c.gather_mode == AVSG_GATHER_EARLY;
+}
+
+// Staging rows of the early-fetch transfer.
+int early_stage_rows(const avsg_config& c) {
+  const long long nk = static_cast<long long>(c.batch) * c.n_q * c.topk;
+  if (c.early_staging_rows < 0) return 0;
+  const long long want = c.early_staging_rows == 0 ? kEarlyStagingRows : c.early_staging_rows;
+  return static_cast<int>(want < nk ? want : nk);
+}
+
+// Early-fetch sections, in order: keys, positions, counts, flags, control
+// words, finish entries, staging of stream 0, staging of stream 1.
+std::array<size_t, 9> early_sections(const avsg_config& c) {
+  const size_t nk = static_cast<size_t>(c.batch) * c.n_q * c.topk;
+  const size_t rows = static_cast<size_t>(early_stage_rows(c));
+  std::array<size_t, 9> off{};
+  size_t o = 0;
+  const size_t sz[8] = {nk * 4, nk * 16, static_cast<size_t>(c.batch) * 4, static_cast<size_t>(c.batch) * 4,
+                        64, nk * 16, rows * static_cast<size_t>(c.row_bytes[0]),
+                        c.n_streams > 1 ? rows * static_cast<size_t>(c.row_bytes[1]) : 0};
+  for (int i = 0; i < 8; ++i) {
+    off[i] = o;
+    o += up(sz[i]);
+  }
+  off[8] = o;
+  return off;
+}
 
 Layout layout_of(const avsg_config& c) {
   Layout L{};
@@ -105,9 +148,11 @@ Layout layout_of(const avsg_config& c) {
   L.miss_list = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk * 8);
   L.hit_mask = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk);
   L.plan = off;
-  if (c.gather_mode == AVSG_GATHER_RESIDENT)   // host, resident, repeat lists; fan slots; bids; counts; claims; stamps
+  if (has_plan(c))   // host, resident, repeat lists; fan slots; bids; counts; claims; stamps
     off += 3 * up(B * static_cast<size_t>(c.n_q) * c.topk * 8) + up(B * static_cast<size_t>(c.n_q) * c.topk * 4) +
            up(B * S * 8) + up(B * 12) + up(8) + up(B * 8);
+  L.early = off;
+  if (c.gather_mode == AVSG_GATHER_EARLY) off += early_sections(c)[8];
   L.pipe = off;
   L.pipe_bytes = up(kAlign + 16 * pipe_chunks_for(c));
   off += L.pipe_bytes;
@@ -155,23 +200,28 @@ avsg_status check_config(const avsg_config* c, std::string* why) {
   if (c->gather_workers < 0) return fail(AVSG_E_INVAL, "gather_workers must be >= 0");
   if (c->match_mode != AVSG_MATCH_HASH && c->match_mode != AVSG_MATCH_DUALPTR)
     return fail(AVSG_E_INVAL, "unknown match_mode");
-  if (c->gather_mode < AVSG_GATHER_BALANCED || c->gather_mode > AVSG_GATHER_RESIDENT)
+  if (c->gather_mode < AVSG_GATHER_BALANCED || c->gather_mode > AVSG_GATHER_EARLY)
     return fail(AVSG_E_INVAL, "unknown gather_mode");
+  if (c->early_staging_rows < -1) return fail(AVSG_E_INVAL, "early_staging_rows must be >= -1");
+  if (c->early_direct != 0 && c->early_direct != -1) return fail(AVSG_E_INVAL, "early_direct must be 0 or -1");
   if (c->match_mode == AVSG_MATCH_DUALPTR) {
     if (c->n_q != 1) return fail(AVSG_E_UNSUPPORTED, "dual-pointer matching handles one token per step");
     if (c->slots != c->topk) return fail(AVSG_E_UNSUPPORTED, "dual-pointer matching needs slots == topk");
     if (c->topk > 4096) return fail(AVSG_E_CAPACITY, "dual-pointer matching supports topk <= 4096");
     if (c->gather_mode == AVSG_GATHER_POSITION || c->gather_mode == AVSG_GATHER_PIPELINED ||
-        c->gather_mode == AVSG_GATHER_RESIDENT)
-      return fail(AVSG_E_UNSUPPORTED, "position-level, pipelined and resident-reuse transfer need hash matching");
+        has_plan(*c))
+      return fail(AVSG_E_UNSUPPORTED,
+                  "position-level, pipelined, resident-reuse and early-fetch transfer need hash matching");
   } else {
-    const size_t lds = c->gather_mode == AVSG_GATHER_PIPELINED
-                           ? pipelined_lds_bytes(c->slots, c->topk)
-                           : match_lds_bytes(c->slots, c->topk);
+    const size_t lds = c->gather_mode == AVSG_GATHER_PIPELINED ? pipelined_lds_bytes(c->slots, c->topk)
+                       : c->gather_mode == AVSG_GATHER_EARLY  ? early_step_lds_bytes(c->slots, c->topk)
+                                                              : match_lds_bytes(c->slots, c->topk);
     if (match_lds_bytes(c->slots, c->topk) == 0 || lds > kLdsPerWorkgroup)
       return fail(AVSG_E_CAPACITY, "table and selection exceed one workgroup's LDS (9*S + 12*K bytes)");
-    if (c->gather_mode == AVSG_GATHER_RESIDENT && plan_map_words(c->slots, c->topk, c->n_q) == 0)
+    if (has_plan(*c) && plan_map_words(c->slots, c->topk, c->n_q) == 0)
       return fail(AVSG_E_CAPACITY, "resident-reuse plan: the index map of 1.5*n_q*topk words does not fit in LDS");
+    if (c->gather_mode == AVSG_GATHER_EARLY && early_map_words(c->topk, c->n_q) == 0)
+      return fail(AVSG_E_CAPACITY, "early fetch: the list map of 1.25*n_q*topk index words does not fit in LDS");
   }
   return AVSG_OK;
 }
@@ -272,7 +322,7 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
   h->dp_state = reinterpret_cast<int2*>(ws + L.table_c);  // S == K: the two table arrays hold [B][K] pairs
   h->miss_list = reinterpret_cast<int2*>(ws + L.miss_list);
   h->hit_mask = ws + L.hit_mask;
-  if (c.gather_mode == AVSG_GATHER_RESIDENT) {
+  if (has_plan(c)) {
     const size_t list = up(static_cast<size_t>(B) * c.n_q * c.topk * 8);
     h->host_list = reinterpret_cast<int2*>(ws + L.plan);
     h->res_list = reinterpret_cast<int2*>(ws + L.plan + list);
@@ -287,6 +337,19 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
     h->plan_stamps = reinterpret_cast<unsigned long long*>(ws + L.plan + 3 * list + fan + bids +
                                                            up(static_cast<size_t>(B) * 12) + up(8));
     h->plan_words = plan_map_words(c.slots, c.topk, c.n_q);
+  }
+  if (c.gather_mode == AVSG_GATHER_EARLY) {
+    const std::array<size_t, 9> o = early_sections(c);
+    unsigned char* eb = ws + L.early;
+    h->early_x = reinterpret_cast<int32_t*>(eb + o[0]);
+    h->early_pos = reinterpret_cast<int4*>(eb + o[1]);
+    h->early_n = reinterpret_cast<int32_t*>(eb + o[2]);
+    h->early_done = reinterpret_cast<uint32_t*>(eb + o[3]);
+    h->early_ctl = reinterpret_cast<int*>(eb + o[4]);
+    h->early_fin = reinterpret_cast<int4*>(eb + o[5]);
+    h->stage0 = reinterpret_cast<uint64_t>(eb + o[6]);
+    h->stage1 = c.n_streams > 1 ? reinterpret_cast<uint64_t>(eb + o[7]) : 0;
+    h->stage_rows = early_stage_rows(c);
   }
   h->pipe_ctl = reinterpret_cast<int*>(ws + L.pipe);
   h->pipe_chunks = reinterpret_cast<int4*>(ws + L.pipe + kAlign);
@@ -343,6 +406,18 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
       if ((e = prepare_step_pipelined(h->lds)) != hipSuccess) return cleanup(AVSG_E_HIP);
       if (launch_zero_u64(reinterpret_cast<unsigned long long*>(h->pipe_ctl), L.pipe_bytes / 8, s) !=
           hipSuccess)
+        return cleanup(AVSG_E_HIP);
+    }
+    if (c.gather_mode == AVSG_GATHER_EARLY) {
+      h->lds = early_step_lds_bytes(c.slots, c.topk);
+      h->early_list_lds = early_list_lds_bytes(c.topk, c.n_q);
+      if (max_lds > 0 && (h->lds > static_cast<size_t>(max_lds) || h->early_list_lds > static_cast<size_t>(max_lds)))
+        return cleanup(AVSG_E_CAPACITY);
+      if ((e = prepare_step_early(h->early_list_lds, h->lds)) != hipSuccess) return cleanup(AVSG_E_HIP);
+      h->early_workers = c.gather_workers > 0 ? c.gather_workers : kEarlyWorkers;
+      // a step that never ran has no early list
+      if (launch_zero_u64(reinterpret_cast<unsigned long long*>(ws + L.early),
+                          early_sections(c)[6] / 8, s) != hipSuccess)
         return cleanup(AVSG_E_HIP);
     }
     if ((e = launch_reset_tables(h->table_c, h->table_q,
@@ -497,6 +572,44 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
     h->steps++;
     return AVSG_OK;
   }
+  if (c.gather_mode == AVSG_GATHER_EARLY) {
+    // early list, then Stage One beside the early copies, then the rows that
+    // arrived before their slots were known
+    MatchParams p{};
+    p.B = c.batch; p.K = c.topk; p.n_q = c.n_q; p.S = c.slots; p.m = h->m;
+    p.R = c.retry; p.L = c.max_life; p.a1 = c.a1; p.a2 = c.a2;
+    p.f_mask = static_cast<uint32_t>((1u << (23 - h->m)) - 1u);
+    p.topk = d_topk; p.verified = d_verified_len; p.rows = h->rows_dev;
+    p.table_c = h->table_c; p.table_q = h->table_q;
+    p.slots_out = d_slots; p.miss_counts = d_miss_counts; p.miss_list = h->miss_list;
+    p.stats = h->stats; p.hit_mask = nullptr;
+    p.plan_words = h->plan_words;
+    p.host_list = h->host_list; p.host_fan = h->host_fan; p.fan_slots = h->fan_slots;
+    p.plan_stamps = h->plan_stamps; p.res_list = h->res_list; p.rep_list = h->rep_list;
+    p.plan_counts = h->plan_counts; p.plan_claim = h->plan_claim;
+    p.early_x = h->early_x; p.early_n = h->early_n; p.early_done = h->early_done;
+    EarlyParams e{};
+    e.B = c.batch; e.K = c.topk; e.n_q = c.n_q; e.S = c.slots;
+    e.map_words = early_map_words(c.topk, c.n_q);
+    e.topk = d_topk; e.rows = h->rows_dev; e.table_c = h->table_c; e.slots = d_slots;
+    e.early_x = h->early_x; e.early_pos = h->early_pos; e.early_n = h->early_n; e.done = h->early_done;
+    e.ctl = h->early_ctl; e.fin = h->early_fin; e.stage_rows = h->stage_rows;
+    e.direct = c.early_direct == 0 ? 1 : 0;
+    e.stage0 = h->stage0; e.stage1 = h->stage1; e.stats = h->stats;
+    e.n_streams = c.n_streams; e.host_ptrs = h->host_ptrs; e.buf_ptrs = h->buf_ptrs;
+    e.row_bytes0 = c.row_bytes[0];
+    e.row_bytes1 = c.n_streams > 1 ? c.row_bytes[1] : 0;
+    e.host_list = h->host_list; e.host_fan = h->host_fan; e.res_list = h->res_list; e.rep_list = h->rep_list;
+    HIP_TRY(h, launch_early_list(e, h->early_list_lds, s));
+    if ((rc = record(h, 1, s)) != AVSG_OK) return rc;
+    HIP_TRY(h, launch_step_early(p, e, h->early_workers, h->lds, s));
+    if ((rc = record(h, 2, s)) != AVSG_OK) return rc;
+    HIP_TRY(h, launch_finish_early(e, std::max(1, h->cus), s));
+    if ((rc = record(h, 3, s)) != AVSG_OK) return rc;
+    if (h->timing && h->n_timed < kMaxTimedSteps) h->has_tail[h->n_timed++] = true;
+    h->steps++;
+    return AVSG_OK;
+  }
   if (c.match_mode == AVSG_MATCH_HASH) {
     MatchParams p{};
     p.B = c.batch; p.K = c.topk; p.n_q = c.n_q; p.S = c.slots; p.m = h->m;
@@ -599,6 +712,9 @@ static avsg_status collect_stats(avsg_handle* h, int r0, int r1, avsg_stats_t* o
     out->bad_indices += s[kStatBadIndices];
     out->resident_rows += s[kStatResident];
     out->duplicate_rows += s[kStatDuplicate];
+    out->early_rows += s[kStatEarly];
+    out->early_staged_rows += s[kStatEarlyStaged];
+    out->early_deferred_rows += s[kStatEarlyDeferred];
     max_dec = std::max<uint64_t>(max_dec, s[kStatMaxStepDecays]);
   }
   out->max_step_alloc_decays = static_cast<int32_t>(max_dec);
@@ -701,7 +817,7 @@ avsg_status avsg_export_plan(avsg_handle* h, int32_t r, int32_t* n_host, int32_t
       !rep_src || !rep_dst || r < 0 || r >= h->cfg.batch)
     return AVSG_E_INVAL;
   const avsg_config& c = h->cfg;
-  if (c.gather_mode != AVSG_GATHER_RESIDENT) return AVSG_E_UNSUPPORTED;
+  if (!has_plan(c)) return AVSG_E_UNSUPPORTED;
   *n_host = *n_res = *n_rep = 0;
   if (!h->last_counts) return AVSG_OK;
   HIP_TRY(h, hipStreamSynchronize(h->last_stream));
@@ -732,6 +848,25 @@ avsg_status avsg_export_plan(avsg_handle* h, int32_t r, int32_t* n_host, int32_t
   *n_host = cnt[0];
   *n_res = cnt[1];
   *n_rep = cnt[2];
+  return AVSG_OK;
+}
+
+avsg_status avsg_export_early(avsg_handle* h, int32_t r, int32_t* n_out, int32_t* x_out,
+                              int32_t* pos_out) {
+  if (!h || !n_out || !x_out || !pos_out || r < 0 || r >= h->cfg.batch) return AVSG_E_INVAL;
+  const avsg_config& c = h->cfg;
+  if (c.gather_mode != AVSG_GATHER_EARLY) return AVSG_E_UNSUPPORTED;
+  HIP_TRY(h, hipStreamSynchronize(h->last_stream));
+  int32_t n = 0;
+  HIP_TRY(h, hipMemcpy(&n, h->early_n + r, 4, hipMemcpyDeviceToHost));
+  const int64_t cap = static_cast<int64_t>(c.n_q) * c.topk;
+  if (n < 0 || n > cap) return AVSG_E_INTERNAL;
+  const size_t base = static_cast<size_t>(r) * c.n_q * c.topk;
+  if (n > 0) {
+    HIP_TRY(h, hipMemcpy(x_out, h->early_x + base, static_cast<size_t>(n) * 4, hipMemcpyDeviceToHost));
+    HIP_TRY(h, hipMemcpy(pos_out, h->early_pos + base, static_cast<size_t>(n) * 16, hipMemcpyDeviceToHost));
+  }
+  *n_out = n;
   return AVSG_OK;
 }
 

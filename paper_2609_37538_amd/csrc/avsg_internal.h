@@ -26,6 +26,9 @@ enum StatIndex : int {
   kStatMaxStepDecays,
   kStatResident,
   kStatDuplicate,
+  kStatEarly,          // rows fetched before Stage One (early-fetch transfer)
+  kStatEarlyStaged,    // of those, rows parked in HBM staging until their slots were known
+  kStatEarlyDeferred,  // of those, rows read from the host only after Stage One (staging full)
   kNumStats
 };
 
@@ -56,6 +59,11 @@ struct MatchParams {
   int2* rep_list;               // [B][n_q*K] (source slot, slot): repeat of a host entry
   int32_t* plan_counts;         // [B][3] host, resident, repeat entries
   int32_t* plan_claim;          // [2] resident and host rows claimed by the gather (reset here)
+  // early-fetch transfer (nullptr otherwise): the keys fetched before Stage
+  // One leave the plan, and each request flags when its O is final
+  const int32_t* early_x;       // [B][n_q*K] early keys of each request
+  const int32_t* early_n;       // [B] number of early keys
+  uint32_t* early_done;         // [B] 1 once the request's slots are written
 };
 
 struct GatherParams {
@@ -89,6 +97,36 @@ struct PipeParams {
   int epoch;          // this step's stamp, never 0 (set by the kernel from last_epoch)
 };
 
+// Early-fetch transfer: the rows of indices that no slot held when the step
+// began are read from the host while Stage One runs (workspace resident).
+struct EarlyParams {
+  int32_t B, K, n_q, S;
+  uint32_t map_words;           // LDS map of the list kernel
+  const int32_t* topk;          // [B][n_q][K]
+  const int64_t* rows;          // [B]
+  const int32_t* table_c;       // [B][S] cached indices as the step begins
+  const int32_t* slots;         // [B][n_q][K] O of this step
+  int32_t* early_x;             // [B][n_q*K] early keys
+  int4* early_pos;              // [B][n_q*K] flat positions g*K+i of each key, -1 padded
+  int32_t* early_n;             // [B]
+  uint32_t* done;               // [B] O final (set by the matching workgroups)
+  int* ctl;                     // [0] rows claimed, [1] staging rows claimed, [2] finish entries
+  int4* fin;                    // [B*n_q*K] (request, key, staging row or -1, 0) left to finish
+  int32_t stage_rows;           // staging capacity in rows (0: none)
+  int32_t direct;               // write rows straight into known slots
+  uint64_t stage0, stage1;      // staging bases per stream
+  unsigned long long* stats;    // [B][kNumStats]
+  int32_t n_streams;
+  const uint64_t* host_ptrs;    // [n_streams][B]
+  const uint64_t* buf_ptrs;     // [n_streams][B]
+  int64_t row_bytes0, row_bytes1;
+  // the matching workgroup's own lists (resident-reuse plan of the rest)
+  const int2* host_list;
+  const int32_t* host_fan;
+  const int2* res_list;
+  const int2* rep_list;
+};
+
 struct DualPtrParams {
   int32_t B, K;
   const int32_t* topk;          // [B][K]
@@ -103,6 +141,8 @@ struct DualPtrParams {
 // LDS bytes of the matching kernel for (S, K); 0 if K exceeds the supported
 // indices per thread.
 size_t match_lds_bytes(int S, int K);
+// threads of the matching workgroup for (S, K)
+int match_threads(int S, int K);
 size_t dualptr_lds_bytes(int K);
 
 hipError_t launch_match_hash(const MatchParams& p, size_t lds, hipStream_t s);
@@ -126,6 +166,17 @@ size_t pipelined_lds_bytes(int S, int K);
 hipError_t prepare_step_pipelined(size_t lds);
 hipError_t launch_step_pipelined(const MatchParams& mp, const GatherParams& gp, const PipeParams& q,
                                  int workgroups, size_t lds, hipStream_t s);
+// early-fetch step: list kernel (one workgroup per request), matching +
+// early copies in one launch (B matching workgroups + `workers` copiers), then
+// the finishing kernel for rows fetched before their slots were known
+uint32_t early_map_words(int K, int n_q);
+size_t early_list_lds_bytes(int K, int n_q);
+size_t early_step_lds_bytes(int S, int K);
+hipError_t prepare_step_early(size_t list_lds, size_t step_lds);
+hipError_t launch_early_list(const EarlyParams& e, size_t lds, hipStream_t s);
+hipError_t launch_step_early(const MatchParams& mp, const EarlyParams& e, int workers, size_t lds,
+                             hipStream_t s);
+hipError_t launch_finish_early(const EarlyParams& e, int workers, hipStream_t s);
 hipError_t launch_match_dualptr(const DualPtrParams& p, size_t lds, hipStream_t s);
 hipError_t prepare_match_dualptr(size_t lds);
 hipError_t launch_reset_dualptr(int2* state, int B, int K, hipStream_t s);

@@ -147,6 +147,7 @@ struct Own {
 constexpr int kPlanMiscWords = 6 * kMaxWaves + 4;
 constexpr uint32_t kPlanResident = 0x80000000u;   // map word names a slot outside this step's reservations
 constexpr uint32_t kPlanRepeat = 0x40000000u;     // the word's index has a repeat this step
+constexpr uint32_t kPlanEarly = 0x20000000u;      // the word's index was fetched before Stage One
 constexpr uint32_t kPlanSlot = 0x00FFFFFFu;       // slot + 1
 constexpr unsigned long long kFanSlot = 0xFFFFFFull;       // fan word: stamp << 24 | slot
 constexpr unsigned long long kFanStampMax = (1ull << 40) - 1;
@@ -196,7 +197,8 @@ __device__ __forceinline__ int plan_lookup(const uint32_t* smp, const int32_t* s
 template <int NT>
 __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, unsigned char* lds,
                                              const int listed, const int64_t rows_r,
-                                             const int64_t n_verified, const int2 v0) {
+                                             const int64_t n_verified, const int2 v0,
+                                             int* counts_out) {
   constexpr int MT = NT, MW = NT / 64;
   const int S = p.S;
   const int32_t* sc = reinterpret_cast<const int32_t*>(lds);
@@ -281,8 +283,23 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   }
   __syncthreads();
 
+  // (2b) early-fetch transfer: the indices whose rows were requested from the
+  // host before Stage One (no slot held them when the step began) leave the
+  // plan; every position of such an index is written by that fetch
+  if (p.early_x) {
+    const int ne = p.early_n[r];
+    const int32_t* ex = p.early_x + lb;
+    for (int k = tid; k < ne; k += MT) {
+      uint32_t w = 0u;
+      const int hw = plan_lookup(smp, sc, P, ex[k], &w);
+      if (hw >= 0) atomicOr(&smp[hw], kPlanEarly);
+    }
+    __syncthreads();
+  }
+
   // classify one entry: 0 host, 1 resident, 2 repeat (src = source slot,
-  // *hw = its map position), -1 past the list
+  // *hw = its map position), 4 / 5 first / further miss of an early-fetched
+  // index, -1 past the list
   auto classify = [&](int e, int2* v, int* src, int* hw) {
     *src = 0;
     *hw = -1;
@@ -293,6 +310,7 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
     *hw = plan_lookup(smp, sc, P, v->x, &w);
     if (*hw < 0) return 0;
     const int o = static_cast<int>(w & kPlanSlot) - 1;
+    if (w & kPlanEarly) return o != v->y ? 5 : 4;   // fetched early; 5 = a further miss of it
     if (w & kPlanResident) {
       *src = o;
       return 1;
@@ -343,6 +361,7 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
       ++n_rep;
       if (fan_of(src) == v.y) kind = 3;   // written by the host copy
     }
+    if (kind == 5) ++n_rep;               // filled by the early fetch's copy of its index
     uint64_t mk[3];
     int* wc = scnt + (it & 1) * 3 * MW;
 #pragma unroll
@@ -375,6 +394,11 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   n_rep = wave_sum(n_rep);
   if (lane == 0 && n_rep) atomicAdd(&scnt[6 * MW], n_rep);
   __syncthreads();
+  if (counts_out) {
+    counts_out[0] = n_list[0];
+    counts_out[1] = n_list[1];
+    counts_out[2] = n_list[2];
+  }
   if (tid == 0) {
     p.plan_stamps[r] = next;   // every thread read the old count before the first barrier
     int32_t* pc = p.plan_counts + 3 * static_cast<size_t>(r);
@@ -393,7 +417,7 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
 // plain matching kernel).
 template <int IPT, int NT, typename Publish>
 __device__ __forceinline__ void match_request(const MatchParams& p, const int r, unsigned char* lds,
-                              Publish& publish) {
+                              Publish& publish, int* plan_counts = nullptr) {
   constexpr int MT = NT, MW = NT / 64;
   static_assert(NT % 64 == 0 && NT <= kMatchThreads, "whole waves, at most the largest workgroup");
   const int S = p.S, K = p.K, R = p.R;
@@ -727,6 +751,15 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   for (int u = 0; u < IPT; ++u)
     if (bid_v[u] && smap[bid_h[u]] != bid_v[u]) st_col++;
 
+  // every slot of the request's O is written: an early-fetch worker may now
+  // copy rows straight into them (each wave's stores are made visible at
+  // device scope before the flag)
+  if (p.early_done) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __syncthreads();
+    if (tid == 0) __hip_atomic_store(p.early_done + r, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  }
+
   // the first transfer-list entry of this thread, for the Stage Two plan
   int2 v0 = make_int2(-1, -1);
   if (p.plan_words > 0 && tid < listed) v0 = p.miss_list[static_cast<size_t>(r) * p.n_q * K + tid];
@@ -792,7 +825,7 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   }
   if (p.plan_words > 0) {
     __syncthreads();   // the counter reduction above is read before its LDS is reused
-    plan_request<NT>(p, r, lds, listed, rows_r, n_verified, v0);
+    plan_request<NT>(p, r, lds, listed, rows_r, n_verified, v0, plan_counts);
   }
 }
 

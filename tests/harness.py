@@ -78,7 +78,7 @@ class OracleSide:
 
 class GpuSide:
     def __init__(self, wl: W.Workload, host: HostRows, retry=3, max_life=16, gather_mode=0,
-                 match_mode=0, gather_workers=0, device="cuda"):
+                 match_mode=0, gather_workers=0, device="cuda", early_staging_rows=0, early_direct=0):
         import torch
         from paper_2609_37538_amd import avsg as A
         spec = wl.spec
@@ -86,7 +86,8 @@ class GpuSide:
         self.cfg = A.make_config(spec.batch, spec.topk, spec.n_q, spec.slots, retry=retry,
                                  max_life=max_life, row_bytes=spec.row_bytes,
                                  gather_workers=gather_workers, match_mode=match_mode,
-                                 gather_mode=gather_mode)
+                                 gather_mode=gather_mode, early_staging_rows=early_staging_rows,
+                                 early_direct=early_direct)
         self.op = A.Operator(self.cfg, host.ptrs, wl.ctx, device=device)
         self.device = device
 
@@ -130,7 +131,8 @@ def content_check(host: HostRows, wl: W.Workload, bufs, X, O):
 
 def run_parity(spec: W.Spec, steps: Optional[int] = None, table_every: int = 16,
                buffers_every: int = 64, miss_list_requests: int = 2, gather_mode: int = 0,
-               retry=3, max_life=16, coherent=False, gather_workers=0):
+               retry=3, max_life=16, coherent=False, gather_workers=0, early_staging_rows=0,
+               early_direct=0):
     """Drive `steps` decode steps through both sides; raise on any mismatch.
     Returns (oracle totals, gpu stats)."""
     wl = W.Workload(spec)
@@ -140,16 +142,19 @@ def run_parity(spec: W.Spec, steps: Optional[int] = None, table_every: int = 16,
     host = HostRows(wl, coherent=coherent)
     orc = OracleSide(wl, host, retry=retry, max_life=max_life)
     gpu = GpuSide(wl, host, retry=retry, max_life=max_life, gather_mode=gather_mode,
-                  gather_workers=gather_workers)
+                  gather_workers=gather_workers, early_staging_rows=early_staging_rows,
+                  early_direct=early_direct)
     from paper_2609_37538_amd import avsg as A
-    resident = gather_mode == A.AVSG_GATHER_RESIDENT
-    want_res = want_dup = 0
+    early = gather_mode == A.AVSG_GATHER_EARLY
+    resident = gather_mode in (A.AVSG_GATHER_RESIDENT, A.AVSG_GATHER_EARLY)
+    want_res = want_dup = want_early = 0
     t0 = time.time()
     try:
         for t in range(T):
             X = wl.topk(t)
             N = wl.verified_len(t)
             W.refresh_speculative(wl, t, host.stream_ptrs())
+            before = [orc.o.export(r)[0] for r in range(spec.batch)] if early else None
             O_ref, n_ref = orc.step(X, N)
             O_gpu, n_gpu = gpu.step(X, N)
             compare_step(t, O_ref, n_ref, O_gpu, n_gpu)
@@ -166,6 +171,17 @@ def run_parity(spec: W.Spec, steps: Optional[int] = None, table_every: int = 16,
                     plan = ORC.transfer_plan(mx, mo, c_ref, int(wl.ctx[r]))
                     want_res += len(plan[3])
                     want_dup += len(plan[5]) + int(np.sum(plan[2] >= 0))
+                    if early:
+                        keys, where = ORC.early_set(X[r], before[r], int(wl.ctx[r]))
+                        want_early += len(keys)
+                        if r in sampled:
+                            gk, gpos = gpu.op.export_early(r)
+                            order = np.argsort(gk, kind="stable")
+                            assert np.array_equal(gk[order], keys), f"step {t} request {r}: early keys differ"
+                            for k, ps in enumerate(where):
+                                got_ps = sorted(int(v) for v in gpos[order[k]] if v >= 0)
+                                assert got_ps == ps, f"step {t} request {r}: positions of {keys[k]} differ"
+                            plan = ORC.transfer_plan_early(mx, mo, c_ref, int(wl.ctx[r]), keys)
                     if r in sampled:
                         got = gpu.op.export_plan(r)
                         for k, name in enumerate(("host index", "host slot", "host fan slot",
@@ -203,6 +219,10 @@ def run_parity(spec: W.Spec, steps: Optional[int] = None, table_every: int = 16,
                 f"({got['resident_rows']}, {got['duplicate_rows']})"
             log(f"[parity] {spec.name}: {want_res} resident + {want_dup} repeated of "
                 f"{got['misses']} misses filled on the device")
+        if early:
+            assert got["early_rows"] == want_early, f"early rows: oracle {want_early} gpu {got['early_rows']}"
+            log(f"[parity] {spec.name}: {want_early} rows fetched before Stage One "
+                f"({got['early_staged_rows']} staged, {got['early_deferred_rows']} deferred)")
         log(f"[parity] {spec.name} done in {time.time() - t0:.1f}s: hit rate "
             f"{got['hits'] / max(1, got['lookups']):.4f}")
         return ref, got

@@ -98,7 +98,15 @@ def test_check_config_statuses(lib):
     assert chk(batch=1, topk=128, n_q=110, slots=16384, gather_mode=A.AVSG_GATHER_RESIDENT) == \
         A.AVSG_E_CAPACITY
     assert chk(batch=1, topk=128, n_q=110, slots=16384) == A.AVSG_OK
-    assert chk(gather_mode=7) == A.AVSG_E_INVAL
+    assert chk(gather_mode=8) == A.AVSG_E_INVAL
+    # early fetch: hash matching only; knobs 0 / -1
+    assert chk(gather_mode=A.AVSG_GATHER_EARLY) == A.AVSG_OK
+    assert chk(gather_mode=A.AVSG_GATHER_EARLY, early_staging_rows=-1, early_direct=-1) == A.AVSG_OK
+    assert chk(gather_mode=A.AVSG_GATHER_EARLY, early_staging_rows=-2) == A.AVSG_E_INVAL
+    assert chk(gather_mode=A.AVSG_GATHER_EARLY, early_direct=1) == A.AVSG_E_INVAL
+    assert chk(n_q=1, slots=2048, match_mode=A.AVSG_MATCH_DUALPTR,
+               gather_mode=A.AVSG_GATHER_EARLY) == A.AVSG_E_UNSUPPORTED
+    assert chk(batch=1, topk=128, n_q=100, slots=16384, gather_mode=A.AVSG_GATHER_EARLY) == A.AVSG_OK
 
 
 def test_workspace_size_and_validation(lib):
@@ -117,11 +125,15 @@ def test_workspace_size_and_validation(lib):
     assert ws(topk=8192, n_q=1, slots=8192) == 0   # beyond 4096 indices per token
     assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=1, slots=2048) > 0
     assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=2) == 0
-    assert ws(gather_mode=7) == 0
+    assert ws(gather_mode=8) == 0
     # the resident-reuse plan adds three transfer lists, fan slots, bids, counts and claims
     B, nq, K = 64, 2, 2048
     assert ws(gather_mode=A.AVSG_GATHER_RESIDENT) >= ws() + (3 * 8 + 4) * B * nq * K + 8 * B * 8192 + 12 * B
     assert ws(gather_mode=A.AVSG_GATHER_POSITION) > ws() - 1
+    # early fetch adds keys, positions, finish entries and 16384 staging rows of both streams
+    early = ws(gather_mode=A.AVSG_GATHER_EARLY)
+    assert early >= ws(gather_mode=A.AVSG_GATHER_RESIDENT) + 36 * B * nq * K + 16384 * (1152 + 132)
+    assert ws(gather_mode=A.AVSG_GATHER_EARLY, early_staging_rows=-1) == early - 16384 * (1152 + 132)
     assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=1, slots=2048, gather_mode=A.AVSG_GATHER_POSITION) == 0
     assert ws(n_q=1, slots=2, topk=1, batch=1, row_bytes=(4,)) > 0
     assert ws(n_q=127, topk=64, slots=8192, row_bytes=(4,)) > 0

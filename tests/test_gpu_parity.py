@@ -384,6 +384,13 @@ def test_parity_batch64_mtp2_full_resident():
 
 
 @pytest.mark.timeout(900)
+def test_parity_batch64_mtp2_full_early():
+    from paper_2609_37538_amd import avsg as A
+    ref, got = run_parity(W.get_spec("batch64_mtp2"), gather_mode=A.AVSG_GATHER_EARLY)
+    assert got["early_rows"] > 0.95 * (got["host_bytes"] // sum(W.get_spec("batch64_mtp2").row_bytes))
+
+
+@pytest.mark.timeout(900)
 def test_parity_imbalance_full():
     ref, got = run_parity(W.get_spec("imbalance"))
 
@@ -395,12 +402,81 @@ def test_parity_stress_full():
 
 
 @pytest.mark.timeout(1200)
+def test_parity_stress_full_early():
+    """Speculative rows are rewritten every step: an index cached at or above
+    the verified length is never an early key (some slot holds it), and an
+    early row is read from the host during the step it is listed in."""
+    from paper_2609_37538_amd import avsg as A
+    ref, got = run_parity(W.get_spec("stress"), buffers_every=64, gather_mode=A.AVSG_GATHER_EARLY)
+    assert got["invalidations"] > 0 and got["early_rows"] > 0
+
+
+@pytest.mark.timeout(1200)
 def test_parity_stress_full_resident():
     """Speculative rows are rewritten every step: the plan must never reuse a
     slot whose cached index was invalidated."""
     from paper_2609_37538_amd import avsg as A
     ref, got = run_parity(W.get_spec("stress"), buffers_every=64, gather_mode=A.AVSG_GATHER_RESIDENT)
     assert got["invalidations"] > 0 and got["resident_rows"] > 0
+
+
+EARLY_CASES = [
+    # name, kwargs of workload.custom_spec, retry R, staging rows, direct writes (0 on, -1 off)
+    ("lost_installs", dict(batch=4, topk=256, slots=512, n_q=2, steps=24, ctx=3000, retention=0.8), 0, 0, 0),
+    ("mtp4_exact_capacity", dict(batch=2, topk=512, slots=2048, n_q=4, steps=16, ctx=20000), 3, 0, 0),
+    ("mtp5_capped_keys", dict(batch=2, topk=64, slots=512, n_q=5, steps=16, ctx=400, overlap=0.9), 0, 0, 0),
+    ("two_streams_odd", dict(batch=3, topk=200, slots=512, n_q=2, steps=12, ctx=9000,
+                             row_bytes=(1152, 132)), 1, 0, 0),
+    ("spec_window", dict(batch=2, topk=256, slots=2048, n_q=3, steps=20, ctx=4096, mode="zipf_window",
+                         window=64, retention=0.8), 3, 0, 0),
+    ("k_one", dict(batch=5, topk=1, slots=2, n_q=1, steps=40, ctx=6), 0, 0, 0),
+    ("s_16384_max", dict(batch=2, topk=1024, slots=16384, n_q=3, steps=8, ctx=300000), 3, 0, 0),
+    ("batch_200", dict(batch=200, topk=128, slots=256, n_q=2, steps=6, ctx=2000), 0, 0, 0),
+    ("batch_1024_max", dict(batch=1024, topk=16, slots=64, n_q=2, steps=6, ctx=400), 0, 0, 0),
+    ("four_waves", dict(batch=3, topk=384, slots=1024, n_q=2, steps=12, ctx=6000, retention=0.8), 0, 0, 0),
+    ("all_staged", dict(batch=4, topk=256, slots=512, n_q=2, steps=12, ctx=3000, retention=0.8,
+                        row_bytes=(1152, 132)), 0, 0, -1),
+    ("all_deferred", dict(batch=4, topk=256, slots=512, n_q=2, steps=12, ctx=3000, retention=0.8,
+                          row_bytes=(1152, 132)), 0, -1, -1),
+    ("five_staging_rows", dict(batch=4, topk=256, slots=1024, n_q=3, steps=12, ctx=3000, retention=0.8,
+                               row_bytes=(1152, 132)), 0, 5, -1),
+]
+
+
+@pytest.mark.parametrize("name,kw,retry,staging,direct", EARLY_CASES, ids=[c[0] for c in EARLY_CASES])
+def test_early_fetch_parity(name, kw, retry, staging, direct):
+    """Early-fetch transfer: the early list equals the oracle's early_set (keys
+    and positions), the plan of the remaining misses equals
+    transfer_plan_early, and slots, tables, counters and every buffer byte
+    equal the oracle's paper-order Stage Two, with rows written straight into
+    their slots, parked in staging, or re-read from the host after Stage One."""
+    from paper_2609_37538_amd import avsg as A
+    spec = W.custom_spec(name=f"early_{name}", **kw)
+    ref, got = run_parity(spec, table_every=4, buffers_every=1, miss_list_requests=3,
+                          gather_mode=A.AVSG_GATHER_EARLY, retry=retry, early_staging_rows=staging,
+                          early_direct=direct)
+    moved_on_device = (got["resident_rows"] + got["duplicate_rows"]) * sum(spec.row_bytes)
+    assert got["host_bytes"] + moved_on_device == got["bytes_moved"]
+    assert got["early_rows"] > 0
+    if direct == -1:
+        assert got["early_staged_rows"] + got["early_deferred_rows"] == got["early_rows"]
+        if staging == -1:
+            assert got["early_deferred_rows"] == got["early_rows"]
+        if staging == 5:
+            assert got["early_staged_rows"] > 0 and got["early_deferred_rows"] > 0
+
+
+@pytest.mark.parametrize("workers", [1, 3, 1000])
+def test_early_fetch_worker_counts(workers):
+    """Early-fetch transfer with one, a few and more copy workgroups than
+    early rows: every early row is copied exactly once into every slot of its
+    positions."""
+    from paper_2609_37538_amd import avsg as A
+    spec = W.custom_spec(name=f"early_workers_{workers}", batch=3, topk=256, slots=512, n_q=2, steps=12,
+                         ctx=3000, retention=0.8, row_bytes=(1152, 132))
+    ref, got = run_parity(spec, table_every=4, buffers_every=1, miss_list_requests=3,
+                          gather_mode=A.AVSG_GATHER_EARLY, retry=0, gather_workers=workers)
+    assert got["early_rows"] > 0 and got["duplicate_rows"] > 0
 
 
 def test_resident_reuse_when_verified_length_shrinks():
@@ -504,9 +580,9 @@ def test_two_handles_on_two_streams():
         host.free()
 
 
-@pytest.mark.parametrize("mode,n_q", [(0, 2), (1, 1), (4, 2), (5, 2), (6, 2), (6, 3)],
+@pytest.mark.parametrize("mode,n_q", [(0, 2), (1, 1), (4, 2), (5, 2), (6, 2), (6, 3), (7, 2), (7, 3)],
                          ids=["balanced", "request_level", "position_level", "pipelined", "resident",
-                              "resident_3_tokens"])
+                              "resident_3_tokens", "early", "early_3_tokens"])
 def test_graph_capture_replays_steps(mode, n_q):
     """One avsg_step captured into a HIP graph and replayed once per decode
     step (new selections copied into the captured input between replays, with
@@ -548,7 +624,8 @@ def test_graph_capture_replays_steps(mode, n_q):
             c2, q2 = eager.export_state(r)
             assert np.array_equal(c1, c2) and np.array_equal(q1, q2)
         s1, s2 = graphed.stats(), eager.stats()
-        for k in ("hits", "misses", "lost_exhausted", "lost_collision", "resident_rows", "duplicate_rows"):
+        for k in ("hits", "misses", "lost_exhausted", "lost_collision", "resident_rows", "duplicate_rows",
+                  "early_rows"):
             assert s1[k] == s2[k], k
         assert s2["misses"] > 0
     finally:
@@ -591,9 +668,9 @@ def c_abi_program(tmp_path_factory):
     return exe
 
 
-@pytest.mark.parametrize("mode", [0, 1, 2, 4, 5, 6],
+@pytest.mark.parametrize("mode", [0, 1, 2, 4, 5, 6, 7],
                          ids=["balanced", "request_level", "copy_engine", "position_level", "pipelined",
-                              "resident"])
+                              "resident", "early"])
 def test_c_caller_against_c_oracle(c_abi_program, mode):
     """A C program drives the library through include/avsg.h (hipMalloc'd
     device memory, its own stream) and the oracle through its C interface;
