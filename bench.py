@@ -60,6 +60,10 @@ def parse():
     ap.add_argument("--config-table", default="",
                     help="run every workload under every Stage Two strategy (and the dual-pointer "
                          "ablation where it applies); write JSON rows here")
+    ap.add_argument("--layer-batching", default="",
+                    help="write the multi-layer batching comparison (one launch over every layer's tables "
+                         "against one step per layer) to this JSON file and exit")
+    ap.add_argument("--layers", type=int, default=8, help="layers of --layer-batching")
     ap.add_argument("--copy-engine-bench", default="",
                     help="copy-engine transfer of every workload in a process without torch, so the HIP "
                          "runtime's batched copy call is available; write JSON rows here")
@@ -92,6 +96,9 @@ def main():
         return
     if args.config_table:
         config_table(args.config_table)
+        return
+    if args.layer_batching:
+        layer_batching(args.layer_batching, args.layers)
         return
 
     gather_mode = {"balanced": A.AVSG_GATHER_BALANCED, "request": A.AVSG_GATHER_REQUEST,
@@ -414,6 +421,83 @@ def _timed_run(spec, cfg_kw, warm, timed, host_ptrs, dev, verified=False):
         op.close()
     delta = {k: after[k] - before[k] for k in after if k != "max_step_alloc_decays"}
     return match_ms, gather_ms, delta, wall
+
+
+def layer_batching(out_path, layers, warm=16, timed=64):
+    """Multi-layer batching: the 64 tables of batch64_mtp2 read as `layers`
+    layers of 64 / layers requests (every (layer, request) pair has its own
+    table, buffer and host rows).  A decode step is either one launch over
+    every pair (possible when all layers' selections are known together) or
+    one step per layer in sequence (in a model, a layer's selection waits for
+    the previous layer's attention).  Same selections, host rows and stream;
+    slots, counts and buffers must agree byte for byte."""
+    import torch
+    import workload as W
+    from paper_2609_37538_amd import avsg as A
+    spec = W.get_spec("batch64_mtp2")
+    B = spec.batch
+    if layers < 1 or B % layers:
+        raise SystemExit(f"--layers must divide {B}")
+    per = B // layers
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = W.Workload(spec)
+    X = torch.from_numpy(wl.all_steps(warm + timed)).to(dev)
+    offs = wl.request_row_offsets()
+    regions, ptrs = [], []
+    for s, rb in enumerate(spec.row_bytes):
+        reg = A.HostRegion(wl.host_rows_total() * rb)
+        W.fill_host(wl, s, reg.ptr)
+        regions.append(reg)
+        ptrs += [reg.ptr + int(offs[r]) * rb for r in range(B)]
+    ns = len(spec.row_bytes)
+    results = []
+    for name, gm in (("resident reuse", A.AVSG_GATHER_RESIDENT), ("early fetch", A.AVSG_GATHER_EARLY),
+                     ("S3 balanced", A.AVSG_GATHER_BALANCED)):
+        kw = dict(row_bytes=spec.row_bytes, gather_mode=gm)
+        one = A.Operator(A.make_config(B, spec.topk, spec.n_q, spec.slots, **kw), ptrs, wl.ctx, device=dev)
+        each = [A.Operator(A.make_config(per, spec.topk, spec.n_q, spec.slots, **kw),
+                           [ptrs[s * B + l * per + i] for s in range(ns) for i in range(per)],
+                           wl.ctx[l * per:(l + 1) * per], device=dev)
+                for l in range(layers)]
+        walls = {}
+        for how in ("one launch", "per layer"):
+            for t in range(warm + timed):
+                if t == warm:
+                    torch.cuda.synchronize()
+                    if how == "one launch":
+                        st0 = one.stats()
+                    t0 = time.perf_counter()
+                if how == "one launch":
+                    one.step(X[t])
+                else:
+                    for l, op in enumerate(each):
+                        op.step(X[t][l * per:(l + 1) * per])
+            torch.cuda.synchronize()
+            walls[how] = (time.perf_counter() - t0) / timed * 1e6
+        for l, op in enumerate(each):
+            sl = slice(l * per, (l + 1) * per)
+            assert torch.equal(one.slots[sl], op.slots) and torch.equal(one.miss_counts[sl], op.miss_counts)
+            for s in range(ns):
+                assert torch.equal(one.buffers[s][sl], op.buffers[s]), f"layer {l} stream {s}: buffers differ"
+        st = one.stats()
+        host_rows = (st["host_bytes"] - st0["host_bytes"]) / sum(spec.row_bytes) / timed
+        row = {"strategy": name, "layers": layers, "requests_per_layer": per, "topk": spec.topk,
+               "slots": spec.slots, "n_q": spec.n_q,
+               "one_launch_us_per_step": round(walls["one launch"], 1),
+               "per_layer_us_per_step": round(walls["per layer"], 1),
+               "per_layer_over_one_launch": round(walls["per layer"] / walls["one launch"], 3),
+               "host_rows_per_step": round(host_rows, 1),
+               "identical": True}
+        results.append(row)
+        print(json.dumps(row), flush=True)
+        one.close()
+        for op in each:
+            op.close()
+    for reg in regions:
+        reg.free()
+    with open(out_path, "w") as f:
+        json.dump(results, f, indent=1)
 
 
 def _oracle_us_per_step(spec, wl, host_ptrs, warm, timed):

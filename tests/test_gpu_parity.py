@@ -479,6 +479,50 @@ def test_early_fetch_worker_counts(workers):
     assert got["early_rows"] > 0 and got["duplicate_rows"] > 0
 
 
+@pytest.mark.parametrize("mode", [0, 6], ids=["balanced", "resident"])
+def test_layer_batching_matches_per_layer_steps(mode):
+    """Multi-layer batching: every (layer, request) pair owns its table,
+    buffer and host rows, so one launch over three layers of two requests
+    gives the slots, counts and buffer bytes of one step per layer, and both
+    equal the oracle."""
+    from paper_2609_37538_amd import avsg as A
+    import torch
+    layers, per = 3, 2
+    spec = W.custom_spec(name=f"layers_{mode}", batch=layers * per, topk=256, slots=1024, n_q=2, steps=10,
+                         ctx=5000, retention=0.8, row_bytes=(1152, 132))
+    wl = W.Workload(spec)
+    host = HostRows(wl)
+    orc = OracleSide(wl, host, retry=1)
+    B, ns = spec.batch, len(spec.row_bytes)
+    kw = dict(retry=1, row_bytes=spec.row_bytes, gather_mode=mode)
+    one = A.Operator(A.make_config(B, spec.topk, spec.n_q, spec.slots, **kw), host.ptrs, wl.ctx)
+    each = [A.Operator(A.make_config(per, spec.topk, spec.n_q, spec.slots, **kw),
+                       [host.ptrs[s * B + l * per + i] for s in range(ns) for i in range(per)],
+                       wl.ctx[l * per:(l + 1) * per]) for l in range(layers)]
+    try:
+        for t in range(spec.steps):
+            X = wl.topk(t)
+            O_ref, n_ref = orc.step(X, None)
+            Xd = torch.from_numpy(np.ascontiguousarray(X, dtype=np.int32)).cuda()
+            one.step(Xd)
+            for l, op in enumerate(each):
+                op.step(Xd[l * per:(l + 1) * per])
+            torch.cuda.synchronize()
+            compare_step(t, O_ref, n_ref, one.slots.cpu().numpy(), one.miss_counts.cpu().numpy())
+            for l, op in enumerate(each):
+                sl = slice(l * per, (l + 1) * per)
+                assert torch.equal(one.slots[sl], op.slots) and torch.equal(one.miss_counts[sl], op.miss_counts)
+                for s in range(ns):
+                    assert torch.equal(one.buffers[s][sl], op.buffers[s]), f"step {t} layer {l} stream {s}"
+            for s in range(ns):
+                assert np.array_equal(one.buffers[s].cpu().numpy(), orc.images[s]), f"step {t} stream {s}"
+    finally:
+        one.close()
+        for op in each:
+            op.close()
+        host.free()
+
+
 def test_resident_reuse_when_verified_length_shrinks():
     """A verified length that moves back: slots caching an index at or above
     the current verified length are never plan sources (the oracle sees them
