@@ -91,6 +91,12 @@ struct Own {
   static __device__ __forceinline__ uint32_t unbias(uint32_t b) {
     return ((b | 0x80808080u) - 0x01010101u) ^ ((b ^ 0xFEFEFEFEu) & 0x80808080u);
   }
+  // one decay, never below -1, of four two's-complement lifetime bytes:
+  // (v + 127) has bit 7 set exactly when the biased byte v is at least 1
+  static __device__ __forceinline__ uint32_t decay1(uint32_t raw) {
+    const uint32_t v = bias(raw);
+    return unbias(v - (((v + 0x7F7F7F7Fu) & 0x80808080u) >> 7));
+  }
   __device__ __forceinline__ void load(const int8_t* slife, int j0, int spt) {
 #pragma unroll
     for (int k = 0; k < kMaxSPT / 4; ++k) w[k] = 0xFFFFFFFFu;
@@ -459,7 +465,8 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   int32_t* gc = p.table_c + static_cast<size_t>(r) * S;
   uint32_t* gq = p.table_q + static_cast<size_t>(r) * S;
   // stage-in: 16-byte loads of 4 entries, the loads of two blocks issued
-  // before their LDS stores
+  // before their LDS stores.  The first token's decay of every lifetime
+  // (Pass 1 of Algorithm 1 at g = 0) is applied as the lifetimes come in.
   if ((S & (4 * MT - 1)) == 0) {
     for (int b = tid; b < S / 4; b += 2 * MT) {
       const i32x4 c0 = reinterpret_cast<const i32x4*>(gc)[b];
@@ -474,12 +481,12 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
       reinterpret_cast<i32x4*>(sc)[b] = c0;
       reinterpret_cast<u32x4*>(smap)[b] = q0 & 0xFFFFFFu;
       reinterpret_cast<uint32_t*>(slife)[b] =
-          (q0.x >> 24) | ((q0.y >> 24) << 8) | ((q0.z >> 24) << 16) | (q0.w & 0xFF000000u);
+          Own::decay1((q0.x >> 24) | ((q0.y >> 24) << 8) | ((q0.z >> 24) << 16) | (q0.w & 0xFF000000u));
       if (two) {
         reinterpret_cast<i32x4*>(sc)[b + MT] = c1;
         reinterpret_cast<u32x4*>(smap)[b + MT] = q1 & 0xFFFFFFu;
         reinterpret_cast<uint32_t*>(slife)[b + MT] =
-            (q1.x >> 24) | ((q1.y >> 24) << 8) | ((q1.z >> 24) << 16) | (q1.w & 0xFF000000u);
+            Own::decay1((q1.x >> 24) | ((q1.y >> 24) << 8) | ((q1.z >> 24) << 16) | (q1.w & 0xFF000000u));
       }
     }
   } else {
@@ -487,7 +494,8 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
       const uint32_t q = gq[j];
       sc[j] = gc[j];
       smap[j] = q & 0xFFFFFFu;
-      slife[j] = static_cast<int8_t>(q >> 24);
+      const int life = static_cast<int8_t>(q >> 24);
+      slife[j] = static_cast<int8_t>(life > -1 ? life - 1 : -1);
     }
   }
   if (tid < 4) sred[tid] = 0;
@@ -518,17 +526,9 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
 
   __syncthreads();
 
+  // Pass 1 (refresh) of the first token, the decay of every lifetime by one,
+  // was applied by the stage-in
   for (int g = 0; g < p.n_q; ++g) {
-    // Pass 1 (refresh): the first token decays every lifetime by one.
-    if (g == 0) {
-      Own o;
-      if (owns) {
-        o.load(slife, j0, spt);
-        o.decay(1, spt);
-        o.store(slife, j0, spt);
-      }
-      __syncthreads();
-    }
     const size_t row = static_cast<size_t>(r) * p.n_q + g;
     int32_t* og = p.slots_out + row * K;
     int32_t* wc = swc + (g & 1) * kMaxIPT * MW;
@@ -766,10 +766,6 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
     if (tid == 0) __hip_atomic_store(p.early_done + r, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
   }
 
-  // the first transfer-list entry of this thread, for the Stage Two plan
-  int2 v0 = make_int2(-1, -1);
-  if (p.plan_words > 0 && tid < listed) v0 = p.miss_list[static_cast<size_t>(r) * p.n_q * K + tid];
-
   // End of step: speculative invalidation fused into the write back.
   int st_inv = 0;
   if ((S & (4 * MT - 1)) == 0) {
@@ -803,6 +799,12 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
       gq[j] = (static_cast<uint32_t>(static_cast<uint8_t>(slife[j])) << 24) | W.canonical(smap[j]);
     }
   }
+
+  // the first transfer-list entry of this thread, for the Stage Two plan
+  // (requested after the write-back's stores; its latency overlaps the
+  // counter reduction)
+  int2 v0 = make_int2(-1, -1);
+  if (p.plan_words > 0 && tid < listed) v0 = p.miss_list[static_cast<size_t>(r) * p.n_q * K + tid];
 
   int vals[7] = {st_hits, st_miss, st_exh, st_col, st_rev, st_inv, st_bad};
 #pragma unroll

@@ -8,8 +8,9 @@
 // of q (invalid | fingerprint | slot) and the lifetime byte -- so lifetime
 // updates and mapping installs never share an LDS word.
 //
-// Per query token (Algorithm 1; tokens run in order on the shared table,
-// Algorithm 4):
+// The first token's decay of every lifetime (Pass 1 of Algorithm 1) is
+// applied to the lifetime bytes as they are staged in.  Per query token
+// (Algorithm 1; tokens run in order on the shared table, Algorithm 4):
 //   A  every index is probed by its own lane (Probe, Eq. 8-11; a lane's
 //      chains advance together); hits refresh their slot's lifetime to L and
 //      write their slot; misses are ranked in index order by wave ballots;
