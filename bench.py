@@ -726,7 +726,7 @@ def copy_engine_bench(out_path, names=("tiny", "batch16", "batch64_mtp2", "imbal
 def config_table(out_path):
     """Every workload (tiny, batch16, batch64_mtp2, imbalance, stress) under the
     balanced (S3), request-level (S1), position-level (S2), copy-engine,
-    pipelined and resident-reuse Stage Two, plus the dual-pointer matching
+    pipelined, resident-reuse and early-fetch Stage Two, plus the dual-pointer matching
     ablation (S = K) on the single-token workloads: 16 warm-up steps from a
     cold start, then 64 timed steps; medians and sums from HIP events on the
     step stream, wall time between two synchronizations around the timed
@@ -755,6 +755,7 @@ def config_table(out_path):
                   ("copy engines", A.AVSG_MATCH_HASH, A.AVSG_GATHER_SDMA),
                   ("pipelined", A.AVSG_MATCH_HASH, A.AVSG_GATHER_PIPELINED),
                   ("resident reuse", A.AVSG_MATCH_HASH, A.AVSG_GATHER_RESIDENT),
+                  ("early fetch", A.AVSG_MATCH_HASH, A.AVSG_GATHER_EARLY),
                   ("dual-pointer + S3", A.AVSG_MATCH_DUALPTR, A.AVSG_GATHER_BALANCED)]
     results = []
     for name in ("tiny", "batch16", "batch64_mtp2", "imbalance", "stress"):
@@ -780,6 +781,10 @@ def config_table(out_path):
                 warm, timed, ptrs, dev, verified=spec.speculative)
             if gm == A.AVSG_GATHER_PIPELINED:
                 gather_ms, match_ms = match_ms, None
+            if gm == A.AVSG_GATHER_EARLY:
+                # the list kernel, then matching beside the early copies, then
+                # the finishing kernel: all of it is Stage Two's launches
+                gather_ms, match_ms = gather_ms + match_ms, None
             moved = d["host_bytes"]
             gsec = float(np.sum(gather_ms)) * 1e-3
             row = {"workload": name, "strategy": label, "batch": spec.batch, "topk": spec.topk,
