@@ -112,88 +112,34 @@ __global__ __launch_bounds__(NT) void early_list_kernel(EarlyParams e) {
   }
   __syncthreads();
 
-  // one word per distinct valid index, counting its positions; a thread's
-  // chains advance together so their LDS latencies overlap
-  {
-    uint32_t h[kListPX];
-    bool pend[kListPX];
-#pragma unroll
-    for (int u = 0; u < kListPX; ++u) {
-      pend[u] = valid(xs[u]);
-      h[u] = early_home(xs[u], P);
-    }
-    for (uint32_t t = 0; t < P; ++t) {
-      int32_t old[kListPX];
-      bool any = false;
-#pragma unroll
-      for (int u = 0; u < kListPX; ++u)
-        if (pend[u]) old[u] = atomicCAS(&skey[h[u]], -1, xs[u]);
-#pragma unroll
-      for (int u = 0; u < kListPX; ++u)
-        if (pend[u]) {
-          if (old[u] == -1 || old[u] == xs[u]) {
-            atomicAdd(&smeta[h[u]], 1u);
-            pend[u] = false;
-          } else {
-            h[u] = (h[u] + 1u == P) ? 0u : h[u] + 1u;
-            any = true;
-          }
-        }
-      if (!any) break;
-    }
-  }
-  for (int pos = kListPX * NT + tid; pos < nk; pos += NT) {
-    const int32_t x = xr[pos];
-    if (!valid(x)) continue;
+  // one word per distinct valid index, counting its positions
+  auto insert = [&](int32_t x) {
     uint32_t h = early_home(x, P);
     for (uint32_t t = 0; t < P; ++t) {
       const int32_t old = atomicCAS(&skey[h], -1, x);
       if (old == -1 || old == x) {
         atomicAdd(&smeta[h], 1u);
-        break;
+        return;
       }
       h = (h + 1u == P) ? 0u : h + 1u;
     }
-  }
+  };
+#pragma unroll
+  for (int u = 0; u < kListPX; ++u)
+    if (valid(xs[u])) insert(xs[u]);
+  for (int pos = kListPX * NT + tid; pos < nk; pos += NT)
+    if (valid(xr[pos])) insert(xr[pos]);
   __syncthreads();
 
-  // indices that some slot holds as the step begins (chains in lockstep)
-  {
-    uint32_t h[kListPC];
-    bool pend[kListPC];
-#pragma unroll
-    for (int u = 0; u < kListPC; ++u) {
-      pend[u] = valid(cs[u]);
-      h[u] = early_home(cs[u], P);
-    }
-    for (uint32_t t = 0; t < P; ++t) {
-      int32_t k[kListPC];
-      bool any = false;
-#pragma unroll
-      for (int u = 0; u < kListPC; ++u)
-        if (pend[u]) k[u] = skey[h[u]];
-#pragma unroll
-      for (int u = 0; u < kListPC; ++u)
-        if (pend[u]) {
-          if (k[u] == cs[u]) {
-            atomicOr(&smeta[h[u]], kEarlyCached);
-            pend[u] = false;
-          } else if (k[u] == -1) {
-            pend[u] = false;
-          } else {
-            h[u] = (h[u] + 1u == P) ? 0u : h[u] + 1u;
-            any = true;
-          }
-        }
-      if (!any) break;
-    }
-  }
-  for (int j = kListPC * NT + tid; j < S; j += NT) {
-    const int32_t c = cr[j];
-    if (!valid(c)) continue;
+  // indices that some slot holds as the step begins
+  auto mark = [&](int32_t c) {
+    if (!valid(c)) return;
     const int h = early_find(skey, P, c);
     if (h >= 0) atomicOr(&smeta[h], kEarlyCached);
-  }
+  };
+#pragma unroll
+  for (int u = 0; u < kListPC; ++u) mark(cs[u]);
+  for (int j = kListPC * NT + tid; j < S; j += NT) mark(cr[j]);
   __syncthreads();
 
   // compact the keys nobody holds (listed at most four times): each thread
@@ -226,48 +172,18 @@ __global__ __launch_bounds__(NT) void early_list_kernel(EarlyParams e) {
   __syncthreads();
 
   // the positions of each key (their order inside a key does not matter)
-  auto place = [&](int h, int pos) {
+  auto place = [&](int32_t x, int pos) {
+    if (!valid(x)) return;
+    const int h = early_find(skey, P, x);
+    if (h < 0) return;
     const uint32_t m = smeta[h];
     if (!(m & kEarlyKey)) return;
     const int k = static_cast<int>(atomicAdd(&smeta[h], 1u) & 0xFFu);
     if (k < kEarlyMaxPos) reinterpret_cast<int*>(e.early_pos + lb + ((m >> 8) & 0x3FFFFFu))[k] = pos;
   };
-  {
-    uint32_t h[kListPX];
-    bool pend[kListPX];
 #pragma unroll
-    for (int u = 0; u < kListPX; ++u) {
-      pend[u] = valid(xs[u]);   // every valid index has its word
-      h[u] = early_home(xs[u], P);
-    }
-    for (uint32_t t = 0; t < P; ++t) {
-      int32_t k[kListPX];
-      bool any = false;
-#pragma unroll
-      for (int u = 0; u < kListPX; ++u)
-        if (pend[u]) k[u] = skey[h[u]];
-#pragma unroll
-      for (int u = 0; u < kListPX; ++u)
-        if (pend[u]) {
-          if (k[u] == xs[u]) {
-            place(static_cast<int>(h[u]), u * NT + tid);
-            pend[u] = false;
-          } else if (k[u] == -1) {
-            pend[u] = false;
-          } else {
-            h[u] = (h[u] + 1u == P) ? 0u : h[u] + 1u;
-            any = true;
-          }
-        }
-      if (!any) break;
-    }
-  }
-  for (int pos = kListPX * NT + tid; pos < nk; pos += NT) {
-    const int32_t x = xr[pos];
-    if (!valid(x)) continue;
-    const int h = early_find(skey, P, x);
-    if (h >= 0) place(h, pos);
-  }
+  for (int u = 0; u < kListPX; ++u) place(xs[u], u * NT + tid);
+  for (int pos = kListPX * NT + tid; pos < nk; pos += NT) place(xr[pos], pos);
   if (tid == 0) {
     e.early_n[r] = total;
     if (total) atomicAdd(&e.stats[static_cast<size_t>(r) * kNumStats + kStatEarly],

@@ -391,6 +391,16 @@ def test_parity_batch64_mtp2_full_early():
 
 
 @pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["batch16", "imbalance"])
+def test_parity_full_early(name):
+    """Early fetch at full size on the single-token workloads: the early list,
+    the remaining plan, slots, tables and buffers equal the oracle's."""
+    from paper_2609_37538_amd import avsg as A
+    ref, got = run_parity(W.get_spec(name), gather_mode=A.AVSG_GATHER_EARLY)
+    assert got["early_rows"] > 0
+
+
+@pytest.mark.timeout(900)
 def test_parity_imbalance_full():
     ref, got = run_parity(W.get_spec("imbalance"))
 
