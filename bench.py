@@ -315,6 +315,14 @@ def main():
             "frac": round(gather_gbps / PCIE_GEN5_X16_GBPS, 4),
             "traffic": traffic["traffic_bytes_per_launch"] if traffic else None,
             "traffic_source": TRAFFIC_SUMMARY if traffic else None,
+            # same basis as `traffic`: host-link reads + HBM reads (resident
+            # sources) + HBM writes (host, fan and resident rows)
+            "algorithmic_traffic_bytes_per_launch": (traffic.get("algorithmic_traffic_bytes_per_launch")
+                                                     if traffic else None),
+            "traffic_over_algorithmic": (round(traffic["traffic_bytes_per_launch"]
+                                               / traffic["algorithmic_traffic_bytes_per_launch"], 3)
+                                         if traffic and traffic.get("algorithmic_traffic_bytes_per_launch")
+                                         else None),
             "algorithmic_bytes_per_launch": round(host_moved / K) if host_moved else 0,
             "measured_hipmemcpy_peak": round(memcpy_peak, 3),
         },
