@@ -147,9 +147,13 @@ avsg_status avsg_check_config(const avsg_config *cfg);
 /* Size in bytes of the device workspace that avsg_create needs for cfg
  * (per-request tables of 8*S bytes, transfer lists of 8*N_q*K bytes, a hit
  * mask of N_q*K bytes, counters and pointer tables; with AVSG_GATHER_RESIDENT
- * three more lists of 8*N_q*K bytes, fan slots of 4*N_q*K bytes, bids of
- * 8*S bytes and a step stamp of 8 bytes per request; with AVSG_GATHER_PIPELINED a
- * chunk queue of 16 bytes per 32 misses).  Returns 0 for an invalid cfg. */
+ * or AVSG_GATHER_EARLY three more lists of 8*N_q*K bytes, fan slots of
+ * 4*N_q*K bytes, bids of 8*S bytes and a step stamp of 8 bytes per request;
+ * with AVSG_GATHER_EARLY also early keys, positions and finish entries of
+ * 36*N_q*K bytes per request and the staging rows (early_staging_rows, by
+ * default min(B*N_q*K, 16384), times the row bytes of every stream); with
+ * AVSG_GATHER_PIPELINED a chunk queue of 16 bytes per 32 misses).  Returns 0
+ * for an invalid cfg. */
 size_t avsg_workspace_bytes(const avsg_config *cfg);
 
 /* Create a handle and reset every table to empty (c_j = -1, lifetime -1, every
