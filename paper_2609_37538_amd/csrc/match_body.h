@@ -235,7 +235,13 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
     p.plan_claim[1] = 0;
   }
 
-  for (int j = tid; j < nb + static_cast<int>(P) + kPlanMiscWords; j += MT) sres[j] = 0u;
+  {
+    // 16-byte stores where sres (4 S bytes into the LDS) is 16-byte aligned
+    const int words = nb + static_cast<int>(P) + kPlanMiscWords;
+    const int vec = (S & 3) == 0 ? words / 4 : 0;
+    for (int j = tid; j < vec; j += MT) reinterpret_cast<u32x4*>(sres)[j] = 0u;
+    for (int j = 4 * vec + tid; j < words; j += MT) sres[j] = 0u;
+  }
   __syncthreads();
 
   // (1) mark this step's reservations; one map word per distinct valid index
