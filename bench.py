@@ -461,7 +461,7 @@ def layer_batching(out_path, layers, warm=16, timed=64):
     ns = len(spec.row_bytes)
     results = []
     for name, gm in (("resident reuse", A.AVSG_GATHER_RESIDENT), ("early fetch", A.AVSG_GATHER_EARLY),
-                     ("S3 balanced", A.AVSG_GATHER_BALANCED)):
+                     ("S3 balanced", A.AVSG_GATHER_BALANCED), ("pipelined", A.AVSG_GATHER_PIPELINED)):
         kw = dict(row_bytes=spec.row_bytes, gather_mode=gm)
         one = A.Operator(A.make_config(B, spec.topk, spec.n_q, spec.slots, **kw), ptrs, wl.ctx, device=dev)
         each = [A.Operator(A.make_config(per, spec.topk, spec.n_q, spec.slots, **kw),
