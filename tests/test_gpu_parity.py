@@ -533,18 +533,24 @@ def test_layer_batching_matches_per_layer_steps(mode):
         host.free()
 
 
-def test_resident_reuse_when_verified_length_shrinks():
+@pytest.mark.parametrize("early", [False, True], ids=["resident", "early"])
+def test_resident_reuse_when_verified_length_shrinks(early):
     """A verified length that moves back: slots caching an index at or above
     the current verified length are never plan sources (the oracle sees them
     invalidated), while the speculative rows beyond the largest length so far
     are rewritten every step; plans, slots and buffers equal the oracle's, and
-    the case is exercised (such an index misses while a slot still caches it)."""
+    the case is exercised (such an index misses while a slot still caches it).
+    With the early fetch, indices no slot caches at the start of a step
+    (speculative ones among them) are read from the rows as rewritten for that
+    step, and the early sets equal the oracle's."""
     from paper_2609_37538_amd import avsg as A
     spec = W.custom_spec(name="shrink_n", batch=2, topk=64, slots=512, n_q=2, steps=16, ctx=4096)
     wl = W.Workload(spec)
     host = HostRows(wl)
     orc = OracleSide(wl, host, retry=0, max_life=8)
-    gpu = GpuSide(wl, host, retry=0, max_life=8, gather_mode=A.AVSG_GATHER_RESIDENT)
+    mode = A.AVSG_GATHER_EARLY if early else A.AVSG_GATHER_RESIDENT
+    gpu = GpuSide(wl, host, retry=0, max_life=8, gather_mode=mode)
+    early_spec = 0
     rng = np.random.default_rng(11)
     n_max = 0
     exercised = 0
@@ -573,7 +579,18 @@ def test_resident_reuse_when_verified_length_shrinks():
             for r in range(spec.batch):
                 mx, mo = orc.o.misses(r, n_ref[r])
                 c_ref, _ = orc.o.export(r)
-                want = ORC.transfer_plan(mx, mo, c_ref, int(wl.ctx[r]))
+                if early:
+                    keys, where = ORC.early_set(X[r], cached[r], int(wl.ctx[r]))
+                    gk, gpos = gpu.op.export_early(r)
+                    order = np.argsort(gk, kind="stable")
+                    assert np.array_equal(gk[order], keys), f"step {t} request {r}: early keys differ"
+                    for k, ps in enumerate(where):
+                        got_ps = sorted(int(v) for v in gpos[order[k]] if v >= 0)
+                        assert got_ps == ps, f"step {t} request {r}: positions of {keys[k]} differ"
+                    early_spec += int(np.sum(keys >= n_t))
+                    want = ORC.transfer_plan_early(mx, mo, c_ref, int(wl.ctx[r]), keys)
+                else:
+                    want = ORC.transfer_plan(mx, mo, c_ref, int(wl.ctx[r]))
                 got = gpu.op.export_plan(r)
                 for k in range(7):
                     assert np.array_equal(want[k], got[k]), f"step {t} request {r}: plan list {k}"
@@ -584,16 +601,18 @@ def test_resident_reuse_when_verified_length_shrinks():
         st = gpu.op.stats()
         assert exercised > 0 and st["invalidations"] > 0
         assert st["resident_rows"] + st["duplicate_rows"] > 0
+        if early:
+            assert early_spec > 0 and st["early_rows"] > 0
     finally:
         gpu.close()
         host.free()
 
 
 def test_two_handles_on_two_streams():
-    """Two handles (balanced and resident-reuse Stage Two, each with its own
-    workspace and buffers) step the same selections on two streams with no
-    synchronization between them; slots, counts, tables and buffers of both
-    equal the oracle's after every step."""
+    """Three handles (balanced, resident-reuse and early-fetch Stage Two, each
+    with its own workspace and buffers) step the same selections on two
+    streams with no synchronization between them; slots, counts, tables and
+    buffers of all three equal the oracle's after every step."""
     from paper_2609_37538_amd import avsg as A
     import torch
     spec = W.custom_spec(name="two_streams", batch=6, topk=512, slots=2048, n_q=2, steps=10,
@@ -602,9 +621,10 @@ def test_two_handles_on_two_streams():
     host = HostRows(wl)
     orc = OracleSide(wl, host, retry=1)
     streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    streams.append(streams[0])
     ops = []
     try:
-        for gm, st in zip((A.AVSG_GATHER_BALANCED, A.AVSG_GATHER_RESIDENT), streams):
+        for gm, st in zip((A.AVSG_GATHER_BALANCED, A.AVSG_GATHER_RESIDENT, A.AVSG_GATHER_EARLY), streams):
             cfg = A.make_config(spec.batch, spec.topk, spec.n_q, spec.slots, retry=1,
                                 row_bytes=spec.row_bytes, gather_mode=gm)
             ops.append(A.Operator(cfg, host.ptrs, wl.ctx, stream=st))
