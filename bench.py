@@ -38,7 +38,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=240)
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--config", default="batch64_mtp2",
-                    choices=["tiny", "batch16", "batch64_mtp2", "imbalance", "stress"])
+                    choices=["tiny", "batch16", "batch64_mtp2", "imbalance", "stress",
+                             "stress_mtp3"])
     ap.add_argument("--gather", default="resident",
                     choices=["balanced", "request", "position", "sdma", "none", "pipelined", "resident",
                              "early"])

@@ -422,6 +422,19 @@ def test_parity_stress_full_early():
 
 
 @pytest.mark.timeout(1200)
+@pytest.mark.parametrize("mode", [0, 6], ids=["balanced", "resident"])
+def test_parity_stress_four_tokens(mode):
+    """The stress mix with four query tokens per step (three draft tokens):
+    the four tokens' reservations fill the whole table (N_q K = S, Eq. 7), so
+    every slot the step did not refresh may be reclaimed; 192 steps at full
+    size (32 requests, K = 2048, S = 8192, 1M-token contexts)."""
+    ref, got = run_parity(W.get_spec("stress_mtp3"), steps=192, buffers_every=64, gather_mode=mode)
+    assert got["invalidations"] > 0
+    if mode == 6:
+        assert got["resident_rows"] > 0
+
+
+@pytest.mark.timeout(1200)
 def test_parity_stress_full_resident():
     """Speculative rows are rewritten every step: the plan must never reuse a
     slot whose cached index was invalidated."""

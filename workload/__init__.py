@@ -74,6 +74,10 @@ SPECS = {
                       ctx_log_uniform=(4096, 1 << 20), retention_range=(0.5, 0.99)),
     "stress": Spec("stress", 4, batch=32, topk=2048, slots=8192, n_q=3, steps=512,
                    ctx=1 << 20, retention=0.8, mode="zipf_window", zipf_s=1.1, window=512),
+    # the stress mix with three draft tokens (four query tokens per step): the
+    # table holds exactly N_q * K = S reservations, the tightest case of Eq. 7
+    "stress_mtp3": Spec("stress_mtp3", 5, batch=32, topk=2048, slots=8192, n_q=4, steps=512,
+                        ctx=1 << 20, retention=0.8, mode="zipf_window", zipf_s=1.1, window=512),
 }
 
 
