@@ -722,6 +722,62 @@ def test_graph_capture_replays_steps(mode, n_q):
         host.free()
 
 
+@pytest.mark.parametrize("mode", [0, 5, 6, 7], ids=["balanced", "pipelined", "resident", "early"])
+def test_graph_of_several_steps(mode):
+    """Eight consecutive steps (each one's selections and verified lengths
+    copied into the captured inputs, then avsg_step) captured as one HIP graph
+    and replayed once after an eager warmup: slots, counts, buffers, tables and
+    counters equal an operator stepped eagerly through the same steps."""
+    from paper_2609_37538_amd import avsg as A
+    import torch
+    spec = W.custom_spec(name=f"graph_seq_{mode}", batch=3, topk=256, slots=1024, n_q=2, steps=12,
+                         ctx=6000, row_bytes=(1152, 132), retention=0.8)
+    wl = W.Workload(spec)
+    host = HostRows(wl)
+    cfg = A.make_config(spec.batch, spec.topk, spec.n_q, spec.slots, retry=1, max_life=8,
+                        row_bytes=spec.row_bytes, gather_mode=mode)
+    eager = A.Operator(cfg, host.ptrs, wl.ctx, stream=torch.cuda.Stream())
+    graphed = A.Operator(cfg, host.ptrs, wl.ctx, stream=torch.cuda.Stream())
+    Xs = torch.from_numpy(np.ascontiguousarray(wl.all_steps(spec.steps), dtype=np.int32)).cuda()
+    Ns = torch.from_numpy(np.stack([np.asarray(wl.ctx, dtype=np.int64) - (spec.steps - t)
+                                    for t in range(spec.steps)])).cuda()
+    X_in, N_in = torch.empty_like(Xs[0]), torch.empty_like(Ns[0])
+    g = torch.cuda.CUDAGraph()
+    try:
+        for t in range(4):
+            eager.step(Xs[t], Ns[t])
+            graphed.step(Xs[t], Ns[t])
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=graphed.stream):
+            for t in range(4, spec.steps):
+                X_in.copy_(Xs[t])
+                N_in.copy_(Ns[t])
+                graphed.step(X_in, N_in)
+        torch.cuda.synchronize()
+        log(f"[graph] mode {mode}: eight captured steps")
+        g.replay()
+        for t in range(4, spec.steps):
+            eager.step(Xs[t], Ns[t])
+        torch.cuda.synchronize()
+        assert torch.equal(graphed.slots, eager.slots) and torch.equal(graphed.miss_counts, eager.miss_counts)
+        for b1, b2 in zip(graphed.buffers, eager.buffers):
+            assert torch.equal(b1, b2)
+        for r in range(spec.batch):
+            c1, q1 = graphed.export_state(r)
+            c2, q2 = eager.export_state(r)
+            assert np.array_equal(c1, c2) and np.array_equal(q1, q2)
+        s1, s2 = graphed.stats(), eager.stats()
+        for k in ("hits", "misses", "lost_exhausted", "lost_collision", "invalidations", "resident_rows",
+                  "duplicate_rows", "early_rows", "host_bytes"):
+            assert s1[k] == s2[k], k
+        assert s2["misses"] > 0 and s2["invalidations"] > 0
+    finally:
+        del g
+        eager.close()
+        graphed.close()
+        host.free()
+
+
 def test_copy_engine_batched_call_without_torch():
     """In a process that never loads torch, the copy-engine transfer issues one
     batched runtime copy call per step and matches the oracle step by step
