@@ -286,6 +286,11 @@ def main():
         # one fused launch: its duration is recorded in the matching slot
         gather_ms, match_ms = match_ms, np.zeros_like(match_ms)
         gather_all, match_all = match_all, np.zeros_like(match_all)
+    n_step = min(len(match_ms), len(gather_ms))
+    step_ms = (np.nan_to_num(np.asarray(match_ms[:n_step], dtype=np.float64))
+               + np.nan_to_num(np.asarray(gather_ms[:n_step], dtype=np.float64)))
+    if len(tail_ms) >= n_step:
+        step_ms = step_ms + np.nan_to_num(np.asarray(tail_ms[:n_step], dtype=np.float64))
     gather_s = float(np.sum(gather_ms)) * 1e-3
     match_s = float(np.sum(match_ms)) * 1e-3
     gather_gbps = host_moved / gather_s / 1e9 if gather_s > 0 and host_moved else 0.0
@@ -338,6 +343,9 @@ def main():
         "match_us_p99": (round(float(np.percentile(match_ms, 99)) * 1e3, 2)
                          if len(match_ms) and not pipelined else None),
         "gather_us_p99": round(float(np.percentile(gather_ms, 99)) * 1e3, 2) if len(gather_ms) else None,
+        # every kernel of a step (matching, Stage Two, repeat or finishing kernel) summed per step
+        "step_kernels_us_median": (round(float(np.median(step_ms)) * 1e3, 2) if len(step_ms) else None),
+        "step_kernels_us_p99": (round(float(np.percentile(step_ms, 99)) * 1e3, 2) if len(step_ms) else None),
         "cold_start_step0_us": ({"match": None if pipelined else round(float(match_all[0]) * 1e3, 2),
                                  "gather": round(float(gather_all[0]) * 1e3, 2)}
                                 if len(gather_all) == T else None),
