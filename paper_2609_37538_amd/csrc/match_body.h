@@ -438,6 +438,9 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
                               Publish& publish, int* plan_counts = nullptr) {
   constexpr int MT = NT, MW = NT / 64;
   static_assert(NT % 64 == 0 && NT <= kMatchThreads, "whole waves, at most the largest workgroup");
+  // probe rounds whose LDS reads are issued together (fewer with more indices
+  // per thread, whose registers would otherwise spill)
+  constexpr int kChainBatch = IPT <= 1 ? 4 : (IPT == 2 ? 2 : 1);
   const int S = p.S, K = p.K, R = p.R;
   const uint32_t smask = static_cast<uint32_t>(S - 1);
   const Word W{static_cast<uint32_t>(p.m), smask, p.f_mask};
@@ -553,29 +556,38 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
       oo[u] = 0;
       if (act[u] && (xv[u] < 0 || static_cast<int64_t>(xv[u]) >= rows_r)) st_bad++;
     }
-    for (int rd = 0; rd <= R; ++rd) {
+    // the buckets of kChainBatch consecutive rounds depend only on the index,
+    // so their words and then their slots' ids are read together: two LDS
+    // round trips per batch instead of two per round; the first round whose
+    // slot holds the index decides, as in the round-by-round probe
+    for (int rd0 = 0; rd0 <= R; rd0 += kChainBatch) {
+      uint32_t qw[IPT][kChainBatch];
+      int32_t cv[IPT][kChainBatch];
+#pragma unroll
+      for (int u = 0; u < IPT; ++u)
+#pragma unroll
+        for (int b = 0; b < kChainBatch; ++b)
+          if (act[u] && !found[u] && rd0 + b <= R) qw[u][b] = smap[(hh[u] + b * dd[u]) & smask];
+#pragma unroll
+      for (int u = 0; u < IPT; ++u)
+#pragma unroll
+        for (int b = 0; b < kChainBatch; ++b)
+          if (act[u] && !found[u] && rd0 + b <= R) cv[u][b] = sc[W.slot(qw[u][b])];   // Eq. 10
       bool pending = false;
-      uint32_t qw[IPT];
 #pragma unroll
-      for (int u = 0; u < IPT; ++u)
-        if (act[u] && !found[u]) qw[u] = smap[hh[u]];
+      for (int u = 0; u < IPT; ++u) {
+        if (!act[u] || found[u]) continue;
 #pragma unroll
-      for (int u = 0; u < IPT; ++u)
-        if (act[u] && !found[u]) oo[u] = static_cast<int>(W.slot(qw[u]));   // Eq. 10
-      int32_t cv[IPT];
-#pragma unroll
-      for (int u = 0; u < IPT; ++u)
-        if (act[u] && !found[u]) cv[u] = sc[oo[u]];
-#pragma unroll
-      for (int u = 0; u < IPT; ++u)
-        if (act[u] && !found[u]) {
-          if (cv[u] == xv[u]) {
+        for (int b = 0; b < kChainBatch; ++b)
+          if (!found[u] && rd0 + b <= R && cv[u][b] == xv[u]) {
             found[u] = true;
-          } else {
-            hh[u] = (hh[u] + dd[u]) & smask;  // unresolved probes advance (Eq. 11)
-            pending = true;
+            oo[u] = static_cast<int>(W.slot(qw[u][b]));
           }
+        if (!found[u]) {
+          hh[u] = (hh[u] + kChainBatch * dd[u]) & smask;   // unresolved probes advance (Eq. 11)
+          pending = pending || rd0 + kChainBatch <= R;
         }
+      }
       if (!__ballot(pending)) break;
     }
     int rank[IPT];
@@ -700,33 +712,46 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
         mh[u] = (a1 * ux) & smask;
         md[u] = ((a2 * ux) & smask) | 1u;
       }
-      for (int rd = 0; rd <= R; ++rd) {
-        bool pending = false;
-        uint32_t qw[IPT];
+      // a batch of rounds at a time, as in the probe: every word of the batch,
+      // then the lifetime and id of each word's slot, then the first
+      // reusable bucket in round order
+      for (int rd0 = 0; rd0 <= R; rd0 += kChainBatch) {
+        uint32_t qw[IPT][kChainBatch];
+        int lf[IPT][kChainBatch];
+        int32_t cv[IPT][kChainBatch];
 #pragma unroll
         for (int u = 0; u < IPT; ++u)
-          if (mact[u] && !mv[u]) qw[u] = smap[mh[u]];
-        int lf[IPT];
-        int32_t cv[IPT];
+#pragma unroll
+          for (int b = 0; b < kChainBatch; ++b)
+            if (mact[u] && !mv[u] && rd0 + b <= R) qw[u][b] = smap[(mh[u] + b * md[u]) & smask];
 #pragma unroll
         for (int u = 0; u < IPT; ++u)
-          if (mact[u] && !mv[u]) {
-            const uint32_t o2 = W.slot(qw[u]);
-            lf[u] = slife[o2];
-            cv[u] = sc[o2];
-          }
 #pragma unroll
-        for (int u = 0; u < IPT; ++u)
-          if (mact[u] && !mv[u]) {
-            // reusable (Eq. 4): invalid, pointed slot inactive, or stale fingerprint
-            if (W.invalid(qw[u]) || lf[u] < 0 ||
-                W.fp(qw[u]) != (static_cast<uint32_t>(cv[u]) & fmask)) {
-              mv[u] = true;
-            } else if (rd < R) {
-              mh[u] = (mh[u] + md[u]) & smask;
-              pending = true;
+          for (int b = 0; b < kChainBatch; ++b)
+            if (mact[u] && !mv[u] && rd0 + b <= R) {
+              const uint32_t o2 = W.slot(qw[u][b]);
+              lf[u][b] = slife[o2];
+              cv[u][b] = sc[o2];
             }
+        bool pending = false;
+#pragma unroll
+        for (int u = 0; u < IPT; ++u) {
+          if (!mact[u] || mv[u]) continue;
+          int first = -1;
+#pragma unroll
+          for (int b = kChainBatch - 1; b >= 0; --b)
+            // reusable (Eq. 4): invalid, pointed slot inactive, or stale fingerprint
+            if (rd0 + b <= R && (W.invalid(qw[u][b]) || lf[u][b] < 0 ||
+                                 W.fp(qw[u][b]) != (static_cast<uint32_t>(cv[u][b]) & fmask)))
+              first = b;
+          if (first >= 0) {
+            mv[u] = true;
+            mh[u] = (mh[u] + static_cast<uint32_t>(first) * md[u]) & smask;
+          } else {
+            mh[u] = (mh[u] + kChainBatch * md[u]) & smask;
+            pending = pending || rd0 + kChainBatch <= R;
           }
+        }
         if (!__ballot(pending)) break;
       }
       __syncthreads();
