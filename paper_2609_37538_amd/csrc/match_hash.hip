@@ -12,7 +12,8 @@
 // applied to the lifetime bytes as they are staged in.  Per query token
 // (Algorithm 1; tokens run in order on the shared table, Algorithm 4):
 //   A  every index is probed by its own lane (Probe, Eq. 8-11; a lane's
-//      chains advance together); hits refresh their slot's lifetime to L and
+//      chains advance together, the reads of two rounds issued at once);
+//      hits refresh their slot's lifetime to L and
 //      write their slot; misses are ranked in index order by wave ballots;
 //   B  misses are compacted into dense LDS arrays (index, position); each
 //      thread loads the lifetimes it owns (a contiguous run) as whole words
