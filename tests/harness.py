@@ -135,97 +135,137 @@ def run_parity(spec: W.Spec, steps: Optional[int] = None, table_every: int = 16,
                early_direct=0):
     """Drive `steps` decode steps through both sides; raise on any mismatch.
     Returns (oracle totals, gpu stats)."""
+    ref, got = run_parity_modes(spec, (gather_mode,), steps=steps, table_every=table_every,
+                                buffers_every=buffers_every, miss_list_requests=miss_list_requests,
+                                retry=retry, max_life=max_life, coherent=coherent,
+                                gather_workers=gather_workers, early_staging_rows=early_staging_rows,
+                                early_direct=early_direct)
+    return ref, got[gather_mode]
+
+
+def _check_plan(t, r, mode, orc, gpu, X, before, wl, sampled, tally):
+    """Resident-reuse (and early-fetch) plan of request r at step t against the
+    oracle's definition; adds the oracle's counts to tally."""
+    import oracle as ORC
+    from paper_2609_37538_amd import avsg as A
+    early = mode == A.AVSG_GATHER_EARLY
+    mx, mo = orc.o.misses(r, orc.last_n[r])
+    c_ref, _ = orc.o.export(r)
+    if r not in orc.plans:       # the same step's plan serves every plan mode
+        orc.plans[r] = ORC.transfer_plan(mx, mo, c_ref, int(wl.ctx[r]))
+    plan = orc.plans[r]
+    tally["res"] += len(plan[3])
+    tally["dup"] += len(plan[5]) + int(np.sum(plan[2] >= 0))
+    if early:
+        keys, where = ORC.early_set(X[r], before[r], int(wl.ctx[r]))
+        tally["early"] += len(keys)
+        if r in sampled:
+            gk, gpos = gpu.op.export_early(r)
+            order = np.argsort(gk, kind="stable")
+            assert np.array_equal(gk[order], keys), f"step {t} request {r}: early keys differ"
+            for k, ps in enumerate(where):
+                got_ps = sorted(int(v) for v in gpos[order[k]] if v >= 0)
+                assert got_ps == ps, f"step {t} request {r}: positions of {keys[k]} differ"
+            plan = ORC.transfer_plan_early(mx, mo, c_ref, int(wl.ctx[r]), keys)
+    if r in sampled:
+        got = gpu.op.export_plan(r)
+        for k, name in enumerate(("host index", "host slot", "host fan slot", "resident source",
+                                  "resident slot", "repeat source", "repeat slot")):
+            assert np.array_equal(plan[k], got[k]), \
+                f"step {t} request {r} (mode {mode}): plan {name} list differs"
+
+
+def run_parity_modes(spec: W.Spec, modes, steps: Optional[int] = None, table_every: int = 16,
+                     buffers_every: int = 64, miss_list_requests: int = 2, retry=3, max_life=16,
+                     coherent=False, gather_workers=0, early_staging_rows=0, early_direct=0):
+    """One oracle and one set of pinned host rows, one GPU operator per Stage
+    Two mode in `modes`, all stepped on the same inputs; every operator is
+    compared with the oracle element by element (slots, counts, transfer
+    lists, plans, tables, counters, buffer bytes).  Returns
+    (oracle totals, {mode: gpu stats})."""
+    from paper_2609_37538_amd import avsg as A
     wl = W.Workload(spec)
     T = spec.steps if steps is None else steps
+    modes = tuple(modes)
     log(f"[parity] {spec.name}: B={spec.batch} K={spec.topk} n_q={spec.n_q} S={spec.slots} T={T} "
-        f"gather_mode={gather_mode}")
+        f"gather_modes={list(modes)}")
     host = HostRows(wl, coherent=coherent)
     orc = OracleSide(wl, host, retry=retry, max_life=max_life)
-    gpu = GpuSide(wl, host, retry=retry, max_life=max_life, gather_mode=gather_mode,
-                  gather_workers=gather_workers, early_staging_rows=early_staging_rows,
-                  early_direct=early_direct)
-    from paper_2609_37538_amd import avsg as A
-    early = gather_mode == A.AVSG_GATHER_EARLY
-    resident = gather_mode in (A.AVSG_GATHER_RESIDENT, A.AVSG_GATHER_EARLY)
-    want_res = want_dup = want_early = 0
-    t0 = time.time()
+    gpus = {}
     try:
+        for mode in modes:
+            gpus[mode] = GpuSide(wl, host, retry=retry, max_life=max_life, gather_mode=mode,
+                                 gather_workers=gather_workers, early_staging_rows=early_staging_rows,
+                                 early_direct=early_direct)
+        plan_modes = [m for m in modes if m in (A.AVSG_GATHER_RESIDENT, A.AVSG_GATHER_EARLY)]
+        any_early = A.AVSG_GATHER_EARLY in modes
+        tally = {m: {"res": 0, "dup": 0, "early": 0} for m in modes}
+        t0 = time.time()
         for t in range(T):
             X = wl.topk(t)
             N = wl.verified_len(t)
             W.refresh_speculative(wl, t, host.stream_ptrs())
-            before = [orc.o.export(r)[0] for r in range(spec.batch)] if early else None
+            before = [orc.o.export(r)[0] for r in range(spec.batch)] if any_early else None
             O_ref, n_ref = orc.step(X, N)
-            O_gpu, n_gpu = gpu.step(X, N)
-            compare_step(t, O_ref, n_ref, O_gpu, n_gpu)
-            for r in range(min(miss_list_requests, spec.batch)):
-                rr = (r * 7 + t) % spec.batch
-                mx, mo = orc.o.misses(rr, n_ref[rr])
-                gx, go = gpu.op.export_misses(rr)
-                assert np.array_equal(mx, gx) and np.array_equal(mo, go), f"step {t} request {rr} miss list"
-            if resident:
-                sampled = {(r * 7 + t) % spec.batch for r in range(min(miss_list_requests, spec.batch))}
-                for r in range(spec.batch):
-                    mx, mo = orc.o.misses(r, n_ref[r])
-                    c_ref, _ = orc.o.export(r)
-                    plan = ORC.transfer_plan(mx, mo, c_ref, int(wl.ctx[r]))
-                    want_res += len(plan[3])
-                    want_dup += len(plan[5]) + int(np.sum(plan[2] >= 0))
-                    if early:
-                        keys, where = ORC.early_set(X[r], before[r], int(wl.ctx[r]))
-                        want_early += len(keys)
-                        if r in sampled:
-                            gk, gpos = gpu.op.export_early(r)
-                            order = np.argsort(gk, kind="stable")
-                            assert np.array_equal(gk[order], keys), f"step {t} request {r}: early keys differ"
-                            for k, ps in enumerate(where):
-                                got_ps = sorted(int(v) for v in gpos[order[k]] if v >= 0)
-                                assert got_ps == ps, f"step {t} request {r}: positions of {keys[k]} differ"
-                            plan = ORC.transfer_plan_early(mx, mo, c_ref, int(wl.ctx[r]), keys)
-                    if r in sampled:
-                        got = gpu.op.export_plan(r)
-                        for k, name in enumerate(("host index", "host slot", "host fan slot",
-                                                  "resident source", "resident slot", "repeat source",
-                                                  "repeat slot")):
-                            assert np.array_equal(plan[k], got[k]), \
-                                f"step {t} request {r}: plan {name} list differs"
+            orc.last_n = n_ref
+            orc.plans = {}
+            sampled = {(r * 7 + t) % spec.batch for r in range(min(miss_list_requests, spec.batch))}
             last = t == T - 1
-            if last or (table_every and t % table_every == 0):
-                for r in range(spec.batch):
-                    c_ref, q_ref = orc.o.export(r)
-                    c_gpu, q_gpu = gpu.op.export_state(r)
-                    assert np.array_equal(c_ref, c_gpu), f"step {t} request {r}: cached ids differ"
-                    assert np.array_equal(q_ref, q_gpu), f"step {t} request {r}: metadata words differ"
-            if gather_mode != 3 and (last or (buffers_every and t % buffers_every == 0)):
-                bufs = gpu.buffers()
-                for s in range(len(spec.row_bytes)):
-                    assert np.array_equal(bufs[s], orc.images[s]), f"step {t} stream {s}: buffers differ"
-                content_check(host, wl, bufs, X, O_gpu)
+            for mode, gpu in gpus.items():
+                O_gpu, n_gpu = gpu.step(X, N)
+                compare_step(t, O_ref, n_ref, O_gpu, n_gpu)
+                for rr in sorted(sampled):
+                    mx, mo = orc.o.misses(rr, n_ref[rr])
+                    gx, go = gpu.op.export_misses(rr)
+                    assert np.array_equal(mx, gx) and np.array_equal(mo, go), \
+                        f"step {t} request {rr} (mode {mode}) miss list"
+                if mode in plan_modes:
+                    for r in range(spec.batch):
+                        _check_plan(t, r, mode, orc, gpu, X, before, wl, sampled, tally[mode])
+                if last or (table_every and t % table_every == 0):
+                    for r in range(spec.batch):
+                        c_ref, q_ref = orc.o.export(r)
+                        c_gpu, q_gpu = gpu.op.export_state(r)
+                        assert np.array_equal(c_ref, c_gpu), f"step {t} request {r}: cached ids differ"
+                        assert np.array_equal(q_ref, q_gpu), f"step {t} request {r}: metadata words differ"
+                if mode != A.AVSG_GATHER_NONE and (last or (buffers_every and t % buffers_every == 0)):
+                    bufs = gpu.buffers()
+                    for s in range(len(spec.row_bytes)):
+                        assert np.array_equal(bufs[s], orc.images[s]), \
+                            f"step {t} stream {s} (mode {mode}): buffers differ"
+                    content_check(host, wl, bufs, X, O_gpu)
+                    del bufs
             if t % 32 == 0:
                 log(f"[parity] {spec.name} step {t} ok ({time.time() - t0:.1f}s)")
         ref = orc.o.total_stats()
-        got = gpu.op.stats()
-        for k in ("hits", "misses", "lost_exhausted", "lost_collision", "alloc_decays", "revivals",
-                  "invalidations", "max_step_alloc_decays"):
-            assert ref[k] == got[k], f"counter {k}: oracle {ref[k]} gpu {got[k]}"
-        for r in sorted({0, spec.batch // 2, spec.batch - 1}):
-            rr, gr = orc.o.stats(r), gpu.op.request_stats(r)
-            for k in ("hits", "misses", "lost_exhausted", "lost_collision", "revivals", "invalidations"):
-                assert rr[k] == gr[k], f"request {r} counter {k}: oracle {rr[k]} gpu {gr[k]}"
-            assert gr["lookups"] == T * spec.n_q * spec.topk == gr["hits"] + gr["misses"]
-        if resident:
-            assert (got["resident_rows"], got["duplicate_rows"]) == (want_res, want_dup), \
-                f"plan counters: oracle ({want_res}, {want_dup}) gpu " \
-                f"({got['resident_rows']}, {got['duplicate_rows']})"
-            log(f"[parity] {spec.name}: {want_res} resident + {want_dup} repeated of "
-                f"{got['misses']} misses filled on the device")
-        if early:
-            assert got["early_rows"] == want_early, f"early rows: oracle {want_early} gpu {got['early_rows']}"
-            log(f"[parity] {spec.name}: {want_early} rows fetched before Stage One "
-                f"({got['early_staged_rows']} staged, {got['early_deferred_rows']} deferred)")
+        out = {}
+        for mode, gpu in gpus.items():
+            got = gpu.op.stats()
+            for k in ("hits", "misses", "lost_exhausted", "lost_collision", "alloc_decays", "revivals",
+                      "invalidations", "max_step_alloc_decays"):
+                assert ref[k] == got[k], f"mode {mode} counter {k}: oracle {ref[k]} gpu {got[k]}"
+            for r in sorted({0, spec.batch // 2, spec.batch - 1}):
+                rr, gr = orc.o.stats(r), gpu.op.request_stats(r)
+                for k in ("hits", "misses", "lost_exhausted", "lost_collision", "revivals", "invalidations"):
+                    assert rr[k] == gr[k], f"mode {mode} request {r} counter {k}: oracle {rr[k]} gpu {gr[k]}"
+                assert gr["lookups"] == T * spec.n_q * spec.topk == gr["hits"] + gr["misses"]
+            if mode in plan_modes:
+                want = tally[mode]
+                assert (got["resident_rows"], got["duplicate_rows"]) == (want["res"], want["dup"]), \
+                    f"mode {mode} plan counters: oracle ({want['res']}, {want['dup']}) gpu " \
+                    f"({got['resident_rows']}, {got['duplicate_rows']})"
+                log(f"[parity] {spec.name} mode {mode}: {want['res']} resident + {want['dup']} repeated "
+                    f"of {got['misses']} misses filled on the device")
+            if mode == A.AVSG_GATHER_EARLY:
+                want = tally[mode]["early"]
+                assert got["early_rows"] == want, f"early rows: oracle {want} gpu {got['early_rows']}"
+                log(f"[parity] {spec.name}: {want} rows fetched before Stage One "
+                    f"({got['early_staged_rows']} staged, {got['early_deferred_rows']} deferred)")
+            out[mode] = got
         log(f"[parity] {spec.name} done in {time.time() - t0:.1f}s: hit rate "
-            f"{got['hits'] / max(1, got['lookups']):.4f}")
-        return ref, got
+            f"{ref['hits'] / max(1, T * spec.batch * spec.n_q * spec.topk):.4f}")
+        return ref, out
     finally:
-        gpu.close()
+        for gpu in gpus.values():
+            gpu.close()
         host.free()

@@ -10,7 +10,8 @@ import pytest
 
 import oracle as ORC
 import workload as W
-from harness import GpuSide, HostRows, OracleSide, compare_step, content_check, log, run_parity
+from harness import (GpuSide, HostRows, OracleSide, compare_step, content_check, log, run_parity,
+                     run_parity_modes)
 
 pytestmark = pytest.mark.gpu
 
@@ -72,8 +73,11 @@ def test_hand_trace_on_gpu():
 
 
 def test_parity_tiny():
-    """1 request, context 8192, K = 256, S = 1024: every step, every table."""
-    run_parity(W.get_spec("tiny"), table_every=1, buffers_every=8, miss_list_requests=1)
+    """1 request, context 8192, K = 256, S = 1024: every step, every table,
+    with the balanced (S3, Eq. 6), request-level (S1, Eq. 13), position-level
+    (S2, Eq. 14) and resident-reuse transfers side by side."""
+    run_parity_modes(W.get_spec("tiny"), (0, 1, 4, 6), table_every=1, buffers_every=8,
+                     miss_list_requests=1)
 
 
 EDGE_CASES = [
@@ -156,30 +160,48 @@ def test_match_only_leaves_buffers():
         host.free()
 
 
-def test_dual_pointer_parity():
-    """Scalar dual-pointer baseline (S = K) against its oracle."""
+DUALPTR_CASES = [
+    # name, batch, K = S, steps, context, retention
+    ("k512", 4, 512, 20, 4000, 0.8),
+    # the operating points of the matching comparison (Appendix C, Fig. 3a):
+    # two and four indices per thread in the freed-slot compaction
+    ("k1024_b16", 16, 1024, 48, 65536, 0.9),
+    ("k2048_b16", 16, 2048, 48, 65536, 0.9),
+]
+
+
+@pytest.mark.parametrize("name,batch,k,steps,ctx,retention", DUALPTR_CASES, ids=[c[0] for c in DUALPTR_CASES])
+def test_dual_pointer_parity(name, batch, k, steps, ctx, retention):
+    """Scalar dual-pointer baseline (S = K) against its oracle: slots, miss
+    counts and transfer lists every step, buffers every 16 steps."""
     from paper_2609_37538_amd import avsg as A
-    spec = W.custom_spec(name="dualptr", batch=4, topk=512, slots=512, n_q=1, steps=20, ctx=4000,
-                         retention=0.8)
+    spec = W.custom_spec(name=f"dualptr_{name}", batch=batch, topk=k, slots=k, n_q=1, steps=steps,
+                         ctx=ctx, retention=retention)
     wl = W.Workload(spec)
     host = HostRows(wl)
     dp = ORC.DualPointerOracle(spec.batch, spec.topk)
     images = [np.zeros((spec.batch, spec.slots, spec.row_bytes[0]), dtype=np.uint8)]
     bptr = [images[0][r].ctypes.data for r in range(spec.batch)]
     gpu = GpuSide(wl, host, match_mode=A.AVSG_MATCH_DUALPTR)
+    log(f"[gpu] dual-pointer B={batch} K=S={k} T={steps}")
     try:
+        hits = 0
         for t in range(spec.steps):
             X = wl.topk(t)
             O_ref, n_ref = dp.step(X, host=host.ptrs, buf=bptr, row_bytes=list(spec.row_bytes))
             O_gpu, n_gpu = gpu.step(X, None)
             compare_step(t, O_ref, n_ref, O_gpu, n_gpu)
+            hits += int(spec.batch * k - n_ref.sum())
             for r in range(spec.batch):
                 gx, go = gpu.op.export_misses(r)
-                assert np.array_equal(gx, dp.miss_x[r, :n_ref[r, 0]])
-                assert np.array_equal(go, dp.miss_o[r, :n_ref[r, 0]])
-        bufs = gpu.buffers()
-        assert np.array_equal(bufs[0], images[0])
-        content_check(host, wl, bufs, X, O_gpu)
+                assert np.array_equal(gx, dp.miss_x[r, :n_ref[r, 0]]), f"step {t} request {r} miss ids"
+                assert np.array_equal(go, dp.miss_o[r, :n_ref[r, 0]]), f"step {t} request {r} miss slots"
+            if t % 16 == 0 or t == spec.steps - 1:
+                bufs = gpu.buffers()
+                assert np.array_equal(bufs[0], images[0]), f"step {t}: buffers differ"
+                content_check(host, wl, bufs, X, O_gpu)
+        st = gpu.op.stats()
+        assert st["hits"] == hits and st["misses"] == spec.steps * spec.batch * k - hits
     finally:
         gpu.close()
         host.free()
@@ -362,7 +384,10 @@ def test_pipelined_batch_limit():
 # ---- the five benchmark workloads at full size ----------------------------
 @pytest.mark.timeout(900)
 def test_parity_batch16_full():
-    run_parity(W.get_spec("batch16"))
+    """Batch 16 at full size with the paper's Stage Two (S3), resident reuse and
+    the early fetch stepped side by side on the same inputs."""
+    ref, got = run_parity_modes(W.get_spec("batch16"), (0, 6, 7))
+    assert got[6]["resident_rows"] > 0 and got[7]["early_rows"] > 0
 
 
 @pytest.mark.timeout(900)
@@ -391,18 +416,14 @@ def test_parity_batch64_mtp2_full_early():
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("name", ["batch16", "imbalance"])
-def test_parity_full_early(name):
-    """Early fetch at full size on the single-token workloads: the early list,
-    the remaining plan, slots, tables and buffers equal the oracle's."""
-    from paper_2609_37538_amd import avsg as A
-    ref, got = run_parity(W.get_spec(name), gather_mode=A.AVSG_GATHER_EARLY)
-    assert got["early_rows"] > 0
-
-
-@pytest.mark.timeout(900)
 def test_parity_imbalance_full():
-    ref, got = run_parity(W.get_spec("imbalance"))
+    """The load-imbalance workload at full size (32 requests whose miss counts
+    differ by more than 10x): CU-balanced (S3, Eq. 6) against request-level
+    (S1, Eq. 13) and position-level (S2, Eq. 14) transfer, plus resident reuse
+    and the early fetch, all stepped on the same inputs and each compared with
+    the oracle element by element."""
+    ref, got = run_parity_modes(W.get_spec("imbalance"), (0, 1, 4, 6, 7))
+    assert got[6]["resident_rows"] > 0 and got[7]["early_rows"] > 0
 
 
 @pytest.mark.timeout(1200)
