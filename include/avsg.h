@@ -48,7 +48,8 @@ typedef int32_t avsg_status;
 #define AVSG_E_CAPACITY (-3)    /* S < N_q * K (Eq. 7), or 9*S + 12*K bytes beyond one workgroup's LDS
                                    (or, resident reuse, no room beside the table for a map of 1.5*N_q*K words) */
 #define AVSG_E_RANGE (-4)       /* R < 0, L outside [1, 127], a1/a2 not distinct primes, row size */
-#define AVSG_E_BADINDEX (-5)    /* a selected index outside [0, rows of its request) */
+#define AVSG_E_BADINDEX (-5)    /* validate mode: a selected index outside [0, rows of its request), or an
+                                   index repeated within one token's top-K list */
 #define AVSG_E_HIP (-6)         /* a HIP runtime call failed */
 #define AVSG_E_INTERNAL (-7)    /* broken internal invariant */
 #define AVSG_E_UNSUPPORTED (-8) /* valid but unsupported combination (e.g. dual-pointer with N_q > 1) */
@@ -110,6 +111,13 @@ typedef struct avsg_config {
                                    again after Stage One), else the count */
     int32_t early_direct;       /* 0 = a fetched row goes straight into its slots once they are known;
                                    -1 = every early row goes through staging (measurement and tests) */
+    int32_t validate;   /* 1 = check the selections of every step before any table write: an index
+                           outside [0, rows of its request) or repeated within one token's top-K list
+                           (Section 3.2 "Problem formulation": a token's K selected indices) makes
+                           avsg_step return AVSG_E_BADINDEX with the tables untouched; costs one
+                           check kernel and one read-back (and a host synchronization) per step.
+                           0 = no check: out-of-range indices are counted and skipped (bad_indices),
+                           repeated indices are the caller's error. */
 } avsg_config;
 
 /* Cumulative counters since create (or the last avsg_reset_stats). */
@@ -141,10 +149,15 @@ typedef struct avsg_handle avsg_handle;
 
 /* Validate a configuration without touching the device: AVSG_OK or the status
  * avsg_create would return for it (AVSG_E_INVAL, AVSG_E_NOTPOW2,
- * AVSG_E_CAPACITY, AVSG_E_RANGE, AVSG_E_UNSUPPORTED). */
+ * AVSG_E_CAPACITY, AVSG_E_RANGE, AVSG_E_UNSUPPORTED).  The rules are the
+ * parameters of Section 3.2 (S = 2^m with m slot bits, Eq. 2; a1 and a2 two
+ * distinct primes; the retry budget R; the lifetime L of an 8-bit field,
+ * Section 3.5) and the capacity rule S >= N_q * K of Eq. 7. */
 avsg_status avsg_check_config(const avsg_config *cfg);
 
-/* Size in bytes of the device workspace that avsg_create needs for cfg
+/* A call of this library's own with no counterpart in the paper (which keeps
+ * the table in each core's on-chip buffer): size in bytes of the device
+ * workspace that avsg_create needs for cfg
  * (per-request tables of 8*S bytes, transfer lists of 8*N_q*K bytes, a hit
  * mask of N_q*K bytes, counters and pointer tables; with AVSG_GATHER_RESIDENT
  * or AVSG_GATHER_EARLY three more lists of 8*N_q*K bytes, fan slots of
@@ -157,7 +170,9 @@ avsg_status avsg_check_config(const avsg_config *cfg);
 size_t avsg_workspace_bytes(const avsg_config *cfg);
 
 /* Create a handle and reset every table to empty (c_j = -1, lifetime -1, every
- * bucket invalid) on `stream`.
+ * bucket invalid) on `stream`: one Hash-State table of S entries E_j = (c_j,
+ * q_j) per request, shared by the request's N_q tokens (Section 3.2 "Problem
+ * formulation" and "Hash-State table", Eq. 2), with S >= N_q * K (Eq. 7).
  *   host_rows        [n_streams*B] host row arrays, entry s*B + r is row 0 of
  *                    request r in stream s; each row is row_bytes[s] long.  The
  *                    memory must be pinned and mapped for the device
@@ -195,14 +210,23 @@ avsg_status avsg_create(const avsg_config *cfg, const void *const *host_rows,
  * graph (stream capture): it enqueues kernels only, keeps every piece of step
  * state in the workspace (step stamps advance on the device), and each replay
  * is the next decode step on whatever d_topk then holds.
- * Errors: AVSG_E_INVAL (null pointer, other device), AVSG_E_HIP. */
+ * With cfg.validate = 1 the step first checks every token's K indices (in
+ * [0, rows) and distinct within the token, the input of Section 3.2 "Problem
+ * formulation"), reads the verdict back (a host synchronization; such a step
+ * cannot be captured) and returns AVSG_E_BADINDEX, naming the first bad
+ * request and token in avsg_last_error, before any table is written.
+ * Errors: AVSG_E_INVAL (null pointer, other device), AVSG_E_BADINDEX
+ * (validate mode), AVSG_E_HIP. */
 avsg_status avsg_step(avsg_handle *h, const int32_t *d_topk, const int64_t *d_verified_len,
                       int32_t *d_slots, int32_t *d_miss_counts, void *stream);
 
 /* Cumulative counters.  Synchronizes with the handle's last stream.  steps
  * and lookups count avsg_step calls on the host, so replays of a captured
  * step are not in them; every other counter is kept on the device and
- * includes them. */
+ * includes them.  hits and misses count the hit indicator m_i of Eq. 1 over
+ * every selected index (hit rate = hits / lookups; a later token's hit on a
+ * slot an earlier token of the same step reserved counts as a hit,
+ * Section 3.6); misses also equal the transfers N_miss of Section 3.4. */
 avsg_status avsg_stats(avsg_handle *h, avsg_stats_t *out);
 
 /* The same counters for request r alone (lookups = steps * N_q * K), for
@@ -214,13 +238,27 @@ avsg_status avsg_request_stats(avsg_handle *h, int32_t r, avsg_stats_t *out);
 avsg_status avsg_reset_stats(avsg_handle *h, void *stream);
 
 /* Return request r's table to the initial empty state (a new request takes
- * over the batch position), enqueued on `stream`.  The buffers are untouched. */
+ * over the batch position), enqueued on `stream`: the cold start of Section
+ * 3.6, after which the request's first token misses every index and later
+ * tokens of the same step reuse its reservations.  The buffers are untouched. */
 avsg_status avsg_reset_request(avsg_handle *h, int32_t r, void *stream);
 
 /* Canonical table view of request r, copied to host memory (synchronous):
  * c_out[S] cached indices, q_out[S] metadata words in the layout of Eq. 2
  * (lifetime byte | invalid bit | fingerprint | slot).  Hash mode only. */
 avsg_status avsg_export_state(avsg_handle *h, int32_t r, int32_t *c_out, uint32_t *q_out);
+
+/* Replace request r's table with c_in[S] / q_in[S] in the layout of Eq. 2 (as
+ * avsg_export_state returns them; Section 3.2 "Hash-State table"), copied
+ * from host memory and synchronized on `stream` before returning: restores a
+ * checkpointed table, or hands a request's table to another handle of the
+ * same configuration.  Every lifetime byte must lie in [-1, L] (a lifetime the
+ * method can reach; Section 3.5); other fields are taken as they are.  The
+ * buffers are untouched: they must hold the rows the imported table names.
+ * Errors: AVSG_E_INVAL, AVSG_E_RANGE (a lifetime outside [-1, L]),
+ * AVSG_E_UNSUPPORTED (dual-pointer matching), AVSG_E_HIP. */
+avsg_status avsg_import_state(avsg_handle *h, int32_t r, const int32_t *c_in, const uint32_t *q_in,
+                              void *stream);
 
 /* Transfer list of request r from the last step, copied to host memory
  * (synchronous): n_out receives the request's miss total, x_out/o_out
@@ -274,6 +312,7 @@ avsg_status avsg_timing(avsg_handle *h, float *match_ms, float *gather_ms, float
                         int32_t cap, int32_t *n_out);
 
 avsg_status avsg_destroy(avsg_handle *h);
+
 
 const char *avsg_strerror(avsg_status s);
 const char *avsg_last_error(const avsg_handle *h);

@@ -94,6 +94,7 @@ def _load():
         lib.avsg_ref_partition_request.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                                    ctypes.c_int32, _P]
         lib.avsg_ref_partition_position.argtypes = [ctypes.c_int64, ctypes.c_int32, _P]
+        lib.avsg_ref_validate.argtypes = [_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P, _P]
         _lib = lib
     return _lib
 
@@ -378,6 +379,18 @@ def transfer_plan_early(miss_x, miss_o, c_after, rows_r: int, early_keys):
     mx = np.asarray(miss_x, dtype=np.int32)[keep]
     mo = np.asarray(miss_o, dtype=np.int32)[keep]
     return transfer_plan(mx, mo, c_after, rows_r)
+
+
+def validate(X: np.ndarray, rows) -> np.ndarray:
+    """Per token row of X [B][n_q][K]: 1 if an index lies outside
+    [0, rows[r]), plus 2 if an in-range index repeats in the row, else 0
+    (the C oracle's avsg_ref_validate)."""
+    X = np.ascontiguousarray(X, dtype=np.int32)
+    B, n_q, K = X.shape
+    rws = np.ascontiguousarray(rows, dtype=np.int64)
+    out = np.empty(B * n_q, dtype=np.int32)
+    _load().avsg_ref_validate(_ptr(X), B, n_q, K, _ptr(rws), _ptr(out))
+    return out.reshape(B, n_q)
 
 
 def partition_balanced(n_miss: int, C: int) -> np.ndarray:

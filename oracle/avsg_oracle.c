@@ -354,6 +354,31 @@ int32_t avsg_ref_step(avsg_ref_state *st, const int32_t *X, const int64_t *verif
     return 0;
 }
 
+static int cmp_i32(const void *a, const void *b) {
+    const int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+    return (x > y) - (x < y);
+}
+
+void avsg_ref_validate(const int32_t *X, int32_t B, int32_t n_q, int32_t K, const int64_t *rows,
+                       int32_t *verdict) {
+    int32_t *in_range = (int32_t *)malloc(sizeof(int32_t) * (size_t)K);
+    for (int64_t row = 0; row < (int64_t)B * n_q; ++row) {
+        const int32_t *x = X + (size_t)row * K;
+        const int64_t n_rows = rows[row / n_q];
+        int32_t v = 0, n = 0;
+        for (int32_t i = 0; i < K; ++i) {
+            if (x[i] < 0 || (int64_t)x[i] >= n_rows) v |= 1;
+            else in_range[n++] = x[i];
+        }
+        /* a repeated index sits next to its copy once the row is sorted */
+        qsort(in_range, (size_t)n, sizeof(int32_t), cmp_i32);
+        for (int32_t i = 1; i < n; ++i)
+            if (in_range[i] == in_range[i - 1]) v |= 2;
+        verdict[row] = v;
+    }
+    free(in_range);
+}
+
 void avsg_ref_export(const avsg_ref_state *st, int32_t r, int32_t *c, uint32_t *q) {
     memcpy(c, st->c + (size_t)r * st->S, sizeof(int32_t) * (size_t)st->S);
     memcpy(q, st->q + (size_t)r * st->S, sizeof(uint32_t) * (size_t)st->S);

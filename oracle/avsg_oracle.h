@@ -66,6 +66,14 @@ int32_t avsg_ref_step(avsg_ref_state *st, const int32_t *X, const int64_t *verif
                       int32_t n_streams, const void *const *host, void *const *buf,
                       const int64_t *row_bytes, const int64_t *rows, int32_t nthreads);
 
+/* Selection check (Section 3.2 "Problem formulation": every token contributes
+ * a top-K list of K selected positions of its request's context).  For each
+ * token row X[r][g] (row index r * n_q + g): verdict = 1 if some index lies
+ * outside [0, rows[r]), plus 2 if some index inside [0, rows[r]) occurs more
+ * than once in the row, else 0. */
+void avsg_ref_validate(const int32_t *X, int32_t B, int32_t n_q, int32_t K, const int64_t *rows,
+                       int32_t *verdict);
+
 /* Canonical table view of request r: c_j and the packed metadata word q_j. */
 void avsg_ref_export(const avsg_ref_state *st, int32_t r, int32_t *c, uint32_t *q);
 /* Replace request r's table (used to set up hand-made states in tests). */

@@ -53,6 +53,7 @@ class AvsgConfig(ctypes.Structure):
         ("row_bytes", ctypes.c_int64 * AVSG_MAX_STREAMS),
         ("match_mode", ctypes.c_int32), ("gather_mode", ctypes.c_int32),
         ("early_staging_rows", ctypes.c_int32), ("early_direct", ctypes.c_int32),
+        ("validate", ctypes.c_int32),
     ]
 
 
@@ -123,6 +124,8 @@ def load(share_torch_runtime: bool = True):
     lib.avsg_reset_request.argtypes = [_P, i32, _P]
     lib.avsg_export_state.restype = i32
     lib.avsg_export_state.argtypes = [_P, i32, _P, _P]
+    lib.avsg_import_state.restype = i32
+    lib.avsg_import_state.argtypes = [_P, i32, _P, _P, _P]
     lib.avsg_export_misses.restype = i32
     lib.avsg_export_misses.argtypes = [_P, i32, _P, _P, _P]
     lib.avsg_export_plan.restype = i32
@@ -176,10 +179,12 @@ def _ptr_array(ptrs: Sequence[int]):
 
 def make_config(batch, topk, n_q, slots, retry=3, max_life=16, a1=A1_DEFAULT, a2=A2_DEFAULT,
                 row_bytes=(1152,), gather_workers=0, match_mode=AVSG_MATCH_HASH,
-                gather_mode=AVSG_GATHER_BALANCED, early_staging_rows=0, early_direct=0) -> AvsgConfig:
+                gather_mode=AVSG_GATHER_BALANCED, early_staging_rows=0, early_direct=0,
+                validate=0) -> AvsgConfig:
     rb = (ctypes.c_int64 * AVSG_MAX_STREAMS)(*(list(row_bytes) + [0] * (AVSG_MAX_STREAMS - len(row_bytes))))
     return AvsgConfig(batch, topk, n_q, slots, retry, max_life, a1, a2, len(row_bytes),
-                      gather_workers, rb, match_mode, gather_mode, early_staging_rows, early_direct)
+                      gather_workers, rb, match_mode, gather_mode, early_staging_rows, early_direct,
+                      validate)
 
 
 # ---------------------------------------------------------------------------
@@ -236,6 +241,13 @@ def avsg_export_state(h, r: int, slots: int):
     _check(load().avsg_export_state(h, r, c.ctypes.data_as(_P), q.ctypes.data_as(_P)),
            "avsg_export_state", h)
     return c, q
+
+
+def avsg_import_state(h, r: int, c, q, stream: int = 0) -> None:
+    c = np.ascontiguousarray(c, dtype=np.int32)
+    q = np.ascontiguousarray(q, dtype=np.uint32)
+    _check(load().avsg_import_state(h, r, c.ctypes.data_as(_P), q.ctypes.data_as(_P), _vp(stream)),
+           "avsg_import_state", h)
 
 
 def avsg_export_plan(h, r: int, capacity: int):
@@ -318,6 +330,7 @@ def avsg_device_cus() -> int:
     return int(load().avsg_device_cus())
 
 
+
 # ---------------------------------------------------------------------------
 # convenience wrappers (torch supplies device memory and streams)
 # ---------------------------------------------------------------------------
@@ -396,6 +409,9 @@ class Operator:
 
     def export_misses(self, r: int):
         return avsg_export_misses(self.h, r, self.cfg.n_q * self.cfg.topk)
+
+    def import_state(self, r: int, c, q):
+        avsg_import_state(self.h, r, c, q, self.stream.cuda_stream)
 
     def export_plan(self, r: int):
         return avsg_export_plan(self.h, r, self.cfg.n_q * self.cfg.topk)

@@ -9,6 +9,7 @@
 
 #include <algorithm>
 #include <array>
+#include <cstdarg>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -79,7 +80,10 @@ struct avsg_handle {
   int2* h_list = nullptr;
   std::vector<void*> dsts, srcs;
   std::vector<size_t> sizes;
-  std::string err;
+  // validate mode: per-row verdicts of the last check, read back to the host
+  int32_t* val_rows = nullptr;
+  std::vector<int32_t> h_val;
+  char err[256] = {0};
 };
 
 namespace {
@@ -106,7 +110,7 @@ size_t pipe_chunks_for(const avsg_config& c);
 
 struct Layout {
   size_t table_c, table_q, miss_list, hit_mask, plan, early, pipe, pipe_bytes, stats, host_ptrs, buf_ptrs,
-      rows, total;
+      rows, val, total;
 };
 
 bool has_plan(const avsg_config& c) {
@@ -160,6 +164,8 @@ Layout layout_of(const avsg_config& c) {
   L.host_ptrs = off; off += up(static_cast<size_t>(c.n_streams) * B * 8);
   L.buf_ptrs = off; off += up(static_cast<size_t>(c.n_streams) * B * 8);
   L.rows = off; off += up(B * 8);
+  L.val = off;
+  if (c.validate) off += up(B * static_cast<size_t>(c.n_q) * 4);
   L.total = off;
   return L;
 }
@@ -204,6 +210,7 @@ avsg_status check_config(const avsg_config* c, std::string* why) {
     return fail(AVSG_E_INVAL, "unknown gather_mode");
   if (c->early_staging_rows < -1) return fail(AVSG_E_INVAL, "early_staging_rows must be >= -1");
   if (c->early_direct != 0 && c->early_direct != -1) return fail(AVSG_E_INVAL, "early_direct must be 0 or -1");
+  if (c->validate != 0 && c->validate != 1) return fail(AVSG_E_INVAL, "validate must be 0 or 1");
   if (c->match_mode == AVSG_MATCH_DUALPTR) {
     if (c->n_q != 1) return fail(AVSG_E_UNSUPPORTED, "dual-pointer matching handles one token per step");
     if (c->slots != c->topk) return fail(AVSG_E_UNSUPPORTED, "dual-pointer matching needs slots == topk");
@@ -226,10 +233,16 @@ avsg_status check_config(const avsg_config* c, std::string* why) {
   return AVSG_OK;
 }
 
+void set_err(avsg_handle* h, const char* fmt, ...) {
+  if (!h) return;
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(h->err, sizeof(h->err), fmt, ap);
+  va_end(ap);
+}
+
 avsg_status hip_fail(avsg_handle* h, hipError_t e, const char* what) {
-  if (h) {
-    h->err = std::string(what) + ": " + hipGetErrorString(e);
-  }
+  set_err(h, "%s: %s", what, hipGetErrorString(e));
   return AVSG_E_HIP;
 }
 
@@ -239,84 +252,10 @@ avsg_status hip_fail(avsg_handle* h, hipError_t e, const char* what) {
     if (e_ != hipSuccess) return hip_fail((h), e_, #call); \
   } while (0)
 
-int device_cus() {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  return cus;
-}
-
-}  // namespace
-
-extern "C" {
-
-avsg_status avsg_check_config(const avsg_config* cfg) { return check_config(cfg, nullptr); }
-
-size_t avsg_workspace_bytes(const avsg_config* cfg) {
-  if (check_config(cfg, nullptr) != AVSG_OK) return 0;
-  return layout_of(*cfg).total;
-}
-
-const char* avsg_strerror(avsg_status s) {
-  switch (s) {
-    case AVSG_OK: return "ok";
-    case AVSG_E_INVAL: return "invalid argument";
-    case AVSG_E_NOTPOW2: return "slots is not a power of two in [2, 2^23]";
-    case AVSG_E_CAPACITY: return "capacity: slots < n_q*topk, or beyond the on-chip limit";
-    case AVSG_E_RANGE: return "parameter out of range";
-    case AVSG_E_BADINDEX: return "selected index out of range";
-    case AVSG_E_HIP: return "HIP runtime error";
-    case AVSG_E_INTERNAL: return "internal error";
-    case AVSG_E_UNSUPPORTED: return "unsupported combination";
-    default: return "unknown status";
-  }
-}
-
-const char* avsg_last_error(const avsg_handle* h) { return h ? h->err.c_str() : ""; }
-
-int32_t avsg_device_cus(void) { return device_cus(); }
-
-avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
-                        const int64_t* rows_per_request, void* d_workspace, size_t workspace_bytes,
-                        void* const* d_buffers, void* stream, avsg_handle** out) {
-  if (!out) return AVSG_E_INVAL;
-  *out = nullptr;
-  std::string why;
-  avsg_status st = check_config(cfg, &why);
-  if (st != AVSG_OK) {
-    std::fprintf(stderr, "avsg_create: %s\n", why.c_str());
-    return st;
-  }
-  const avsg_config c = *cfg;
-  if (!host_rows || !rows_per_request || !d_workspace || !d_buffers) return AVSG_E_INVAL;
-  const Layout L = layout_of(c);
-  if (workspace_bytes < L.total) return AVSG_E_INVAL;
-  if ((reinterpret_cast<uintptr_t>(d_workspace) & (kAlign - 1)) != 0) return AVSG_E_INVAL;
+// Section pointers of a workspace laid out by layout_of(h->cfg) at ws.
+void bind_workspace(avsg_handle* h, unsigned char* ws, const Layout& L) {
+  const avsg_config& c = h->cfg;
   const int B = c.batch;
-  for (int r = 0; r < B; ++r)
-    if (rows_per_request[r] < 1) return AVSG_E_INVAL;
-  for (int i = 0; i < c.n_streams * B; ++i) {
-    if (!host_rows[i] || !d_buffers[i]) return AVSG_E_INVAL;
-    const int s = i / B;
-    if ((c.row_bytes[s] & 15) == 0 &&
-        ((reinterpret_cast<uintptr_t>(host_rows[i]) & 15) != 0 ||
-         (reinterpret_cast<uintptr_t>(d_buffers[i]) & 15) != 0))
-      return AVSG_E_INVAL;
-    if ((reinterpret_cast<uintptr_t>(host_rows[i]) & 3) != 0 ||
-        (reinterpret_cast<uintptr_t>(d_buffers[i]) & 3) != 0)
-      return AVSG_E_INVAL;
-  }
-
-  auto* h = new avsg_handle();
-  h->cfg = c;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  h->last_stream = s;
-  if (hipGetDevice(&h->device) != hipSuccess) {
-    delete h;
-    return AVSG_E_HIP;
-  }
-  h->m = log2_exact(c.slots);
-  unsigned char* ws = static_cast<unsigned char*>(d_workspace);
   h->table_c = reinterpret_cast<int32_t*>(ws + L.table_c);
   h->table_q = reinterpret_cast<uint32_t*>(ws + L.table_q);
   h->dp_state = reinterpret_cast<int2*>(ws + L.table_c);  // S == K: the two table arrays hold [B][K] pairs
@@ -358,6 +297,96 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
   h->host_ptrs = reinterpret_cast<uint64_t*>(ws + L.host_ptrs);
   h->buf_ptrs = reinterpret_cast<uint64_t*>(ws + L.buf_ptrs);
   h->rows_dev = reinterpret_cast<int64_t*>(ws + L.rows);
+  h->val_rows = c.validate ? reinterpret_cast<int32_t*>(ws + L.val) : nullptr;
+}
+
+// Request sizes, and host-row and buffer addresses aligned for the copies.
+bool rows_ok(const avsg_config& c, const void* const* host_rows, const int64_t* rows_per_request,
+             void* const* d_buffers) {
+  const int B = c.batch;
+  for (int r = 0; r < B; ++r)
+    if (rows_per_request[r] < 1) return false;
+  for (int i = 0; i < c.n_streams * B; ++i) {
+    if (!host_rows[i] || !d_buffers[i]) return false;
+    const int s = i / B;
+    if ((c.row_bytes[s] & 15) == 0 &&
+        ((reinterpret_cast<uintptr_t>(host_rows[i]) & 15) != 0 ||
+         (reinterpret_cast<uintptr_t>(d_buffers[i]) & 15) != 0))
+      return false;
+    if ((reinterpret_cast<uintptr_t>(host_rows[i]) & 3) != 0 ||
+        (reinterpret_cast<uintptr_t>(d_buffers[i]) & 3) != 0)
+      return false;
+  }
+  return true;
+}
+
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  return cus;
+}
+
+}  // namespace
+
+extern "C" {
+
+avsg_status avsg_check_config(const avsg_config* cfg) { return check_config(cfg, nullptr); }
+
+size_t avsg_workspace_bytes(const avsg_config* cfg) {
+  if (check_config(cfg, nullptr) != AVSG_OK) return 0;
+  return layout_of(*cfg).total;
+}
+
+const char* avsg_strerror(avsg_status s) {
+  switch (s) {
+    case AVSG_OK: return "ok";
+    case AVSG_E_INVAL: return "invalid argument";
+    case AVSG_E_NOTPOW2: return "slots is not a power of two in [2, 2^23]";
+    case AVSG_E_CAPACITY: return "capacity: slots < n_q*topk, or beyond the on-chip limit";
+    case AVSG_E_RANGE: return "parameter out of range";
+    case AVSG_E_BADINDEX: return "selected index out of range";
+    case AVSG_E_HIP: return "HIP runtime error";
+    case AVSG_E_INTERNAL: return "internal error";
+    case AVSG_E_UNSUPPORTED: return "unsupported combination";
+    default: return "unknown status";
+  }
+}
+
+const char* avsg_last_error(const avsg_handle* h) { return h ? h->err : ""; }
+
+int32_t avsg_device_cus(void) { return device_cus(); }
+
+avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
+                        const int64_t* rows_per_request, void* d_workspace, size_t workspace_bytes,
+                        void* const* d_buffers, void* stream, avsg_handle** out) {
+  if (!out) return AVSG_E_INVAL;
+  *out = nullptr;
+  std::string why;
+  avsg_status st = check_config(cfg, &why);
+  if (st != AVSG_OK) {
+    std::fprintf(stderr, "avsg_create: %s\n", why.c_str());
+    return st;
+  }
+  const avsg_config c = *cfg;
+  if (!host_rows || !rows_per_request || !d_workspace || !d_buffers) return AVSG_E_INVAL;
+  const Layout L = layout_of(c);
+  if (workspace_bytes < L.total) return AVSG_E_INVAL;
+  if ((reinterpret_cast<uintptr_t>(d_workspace) & (kAlign - 1)) != 0) return AVSG_E_INVAL;
+  const int B = c.batch;
+  if (!rows_ok(c, host_rows, rows_per_request, d_buffers)) return AVSG_E_INVAL;
+
+  auto* h = new avsg_handle();
+  h->cfg = c;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  h->last_stream = s;
+  if (hipGetDevice(&h->device) != hipSuccess) {
+    delete h;
+    return AVSG_E_HIP;
+  }
+  h->m = log2_exact(c.slots);
+  bind_workspace(h, static_cast<unsigned char*>(d_workspace), L);
+  if (c.validate) h->h_val.resize(static_cast<size_t>(B) * c.n_q);
   h->rows.assign(rows_per_request, rows_per_request + B);
   h->host_dev.resize(static_cast<size_t>(c.n_streams) * B);
   h->bufs.resize(static_cast<size_t>(c.n_streams) * B);
@@ -365,8 +394,8 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
     void* dptr = nullptr;
     hipError_t e = hipHostGetDevicePointer(&dptr, const_cast<void*>(host_rows[i]), 0);
     if (e != hipSuccess || !dptr) {
-      h->err = "host rows must be pinned, device-mapped memory (avsg_host_alloc / hipHostMalloc)";
-      std::fprintf(stderr, "avsg_create: %s (%s)\n", h->err.c_str(), hipGetErrorString(e));
+      set_err(h, "host rows must be pinned, device-mapped memory (avsg_host_alloc / hipHostMalloc)");
+      std::fprintf(stderr, "avsg_create: %s (%s)\n", h->err, hipGetErrorString(e));
       delete h;
       return AVSG_E_INVAL;
     }
@@ -416,7 +445,7 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
       if ((e = prepare_step_early(h->early_list_lds, h->lds)) != hipSuccess) return cleanup(AVSG_E_HIP);
       h->early_workers = c.gather_workers > 0 ? c.gather_workers : kEarlyWorkers;
       // a step that never ran has no early list
-      if (launch_zero_u64(reinterpret_cast<unsigned long long*>(ws + L.early),
+      if (launch_zero_u64(reinterpret_cast<unsigned long long*>(static_cast<unsigned char*>(d_workspace) + L.early),
                           early_sections(c)[6] / 8, s) != hipSuccess)
         return cleanup(AVSG_E_HIP);
     }
@@ -530,16 +559,10 @@ static avsg_status sdma_gather(avsg_handle* h, const int32_t* d_counts, hipStrea
   return AVSG_OK;
 }
 
-avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_verified_len,
-                      int32_t* d_slots, int32_t* d_miss_counts, void* stream) {
-  if (!h || !d_topk || !d_slots || !d_miss_counts) return AVSG_E_INVAL;
+// The kernels of one decode step for the handle's configuration, enqueued on s.
+static avsg_status enqueue_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_verified_len,
+                                int32_t* d_slots, int32_t* d_miss_counts, hipStream_t s) {
   const avsg_config& c = h->cfg;
-  int dev = -1;
-  if (hipGetDevice(&dev) != hipSuccess || dev != h->device) {
-    h->err = "avsg_step: the current device is not the one the handle was created on";
-    return AVSG_E_INVAL;
-  }
-  hipStream_t s = static_cast<hipStream_t>(stream);
   h->last_stream = s;
   h->last_counts = d_miss_counts;
   avsg_status rc;
@@ -687,6 +710,41 @@ avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_ve
   return AVSG_OK;
 }
 
+// Validate mode: every token row's verdict, read back before any table write.
+static avsg_status validate_step(avsg_handle* h, const int32_t* d_topk, hipStream_t s) {
+  const avsg_config& c = h->cfg;
+  const size_t n = static_cast<size_t>(c.batch) * c.n_q;
+  HIP_TRY(h, launch_validate_topk(d_topk, h->rows_dev, c.batch, c.n_q, c.topk, h->val_rows, s));
+  HIP_TRY(h, hipMemcpyAsync(h->h_val.data(), h->val_rows, n * 4, hipMemcpyDeviceToHost, s));
+  HIP_TRY(h, hipStreamSynchronize(s));
+  for (size_t i = 0; i < n; ++i)
+    if (h->h_val[i] != 0) {
+      const int r = static_cast<int>(i / c.n_q), g = static_cast<int>(i % c.n_q);
+      set_err(h, "avsg_step: request %d token %d: %s%s%s", r, g,
+              (h->h_val[i] & 1) ? "an index outside [0, rows)" : "",
+              (h->h_val[i] & 3) == 3 ? " and " : "", (h->h_val[i] & 2) ? "a repeated index" : "");
+      return AVSG_E_BADINDEX;
+    }
+  return AVSG_OK;
+}
+
+avsg_status avsg_step(avsg_handle* h, const int32_t* d_topk, const int64_t* d_verified_len,
+                      int32_t* d_slots, int32_t* d_miss_counts, void* stream) {
+  if (!h || !d_topk || !d_slots || !d_miss_counts) return AVSG_E_INVAL;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev != h->device) {
+    set_err(h, "avsg_step: the current device is not the one the handle was created on");
+    return AVSG_E_INVAL;
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (h->cfg.validate) {
+    h->last_stream = s;
+    const avsg_status rc = validate_step(h, d_topk, s);
+    if (rc != AVSG_OK) return rc;
+  }
+  return enqueue_step(h, d_topk, d_verified_len, d_slots, d_miss_counts, s);
+}
+
 // Counters of requests [r0, r1) into *out (steps and lookups counted for
 // those requests only).
 static avsg_status collect_stats(avsg_handle* h, int r0, int r1, avsg_stats_t* out) {
@@ -737,7 +795,7 @@ avsg_status avsg_stats(avsg_handle* h, avsg_stats_t* out) {
     HIP_TRY(h, hipMemcpy(ctl, h->pipe_ctl, sizeof(ctl), hipMemcpyDeviceToHost));
     out->queue_timeouts = ctl[4];
     if (ctl[4]) {
-      h->err = "pipelined step: a consumer timed out waiting for the chunk queue";
+      set_err(h, "pipelined step: a consumer timed out waiting for the chunk queue");
       return AVSG_E_INTERNAL;
     }
   }
@@ -780,6 +838,26 @@ avsg_status avsg_export_state(avsg_handle* h, int32_t r, int32_t* c_out, uint32_
   HIP_TRY(h, hipStreamSynchronize(h->last_stream));
   HIP_TRY(h, hipMemcpy(c_out, h->table_c + r * S, S * 4, hipMemcpyDeviceToHost));
   HIP_TRY(h, hipMemcpy(q_out, h->table_q + r * S, S * 4, hipMemcpyDeviceToHost));
+  return AVSG_OK;
+}
+
+avsg_status avsg_import_state(avsg_handle* h, int32_t r, const int32_t* c_in, const uint32_t* q_in,
+                              void* stream) {
+  if (!h || !c_in || !q_in || r < 0 || r >= h->cfg.batch) return AVSG_E_INVAL;
+  if (h->cfg.match_mode != AVSG_MATCH_HASH) return AVSG_E_UNSUPPORTED;
+  const size_t S = static_cast<size_t>(h->cfg.slots);
+  for (size_t j = 0; j < S; ++j) {
+    const int life = static_cast<int8_t>(q_in[j] >> 24);
+    if (life < -1 || life > h->cfg.max_life) {
+      set_err(h, "avsg_import_state: entry %zu has lifetime %d outside [-1, %d]", j, life, h->cfg.max_life);
+      return AVSG_E_RANGE;
+    }
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  HIP_TRY(h, hipMemcpyAsync(h->table_c + r * S, c_in, S * 4, hipMemcpyHostToDevice, s));
+  HIP_TRY(h, hipMemcpyAsync(h->table_q + r * S, q_in, S * 4, hipMemcpyHostToDevice, s));
+  HIP_TRY(h, hipStreamSynchronize(s));
+  h->last_stream = s;
   return AVSG_OK;
 }
 

@@ -149,6 +149,10 @@ hipError_t launch_match_hash(const MatchParams& p, size_t lds, hipStream_t s);
 hipError_t prepare_match_hash(size_t lds);
 hipError_t launch_reset_tables(int32_t* c, uint32_t* q, size_t n, hipStream_t s);
 hipError_t launch_zero_u64(unsigned long long* p, size_t n, hipStream_t s);
+// validate mode: verdict[B * n_q] per token row (1 index out of range, 2 index
+// repeated, 3 both, 0 valid); K <= 8192
+hipError_t launch_validate_topk(const int32_t* topk, const int64_t* rows, int B, int n_q, int K,
+                                int32_t* verdict, hipStream_t s);
 hipError_t launch_gather_balanced(const GatherParams& p, int workers, hipStream_t s);
 hipError_t launch_gather_request(const GatherParams& p, hipStream_t s);
 hipError_t launch_gather_position(const GatherParams& p, int workers, hipStream_t s);

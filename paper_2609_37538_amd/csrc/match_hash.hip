@@ -65,8 +65,67 @@ __global__ void zero_u64_kernel(unsigned long long* p, size_t n) {
 }
 
 constexpr int kSmallThreads = 256;
+constexpr int kValidateThreads = 256;
+
+// Selection check of the validate mode, one workgroup per token row (request
+// r = row / n_q): every index must lie in [0, rows_r) and appear once in the
+// row (a token's top-K list holds K distinct indices).  An LDS set of P >= 2K
+// words (index + 1, 0 = empty, linear probing) finds repeats.  verdict[row] =
+// 1 if an index is out of range, | 2 if an index repeats, 0 if the row is
+// valid.
+__global__ __launch_bounds__(kValidateThreads) void validate_topk_kernel(const int32_t* topk,
+                                                                         const int64_t* rows, int K,
+                                                                         int n_q, uint32_t P,
+                                                                         int32_t* verdict) {
+  extern __shared__ uint32_t seen[];   // [P]
+  __shared__ int flags;
+  const int row = static_cast<int>(blockIdx.x), tid = static_cast<int>(threadIdx.x);
+  const int64_t rows_r = rows[row / n_q];
+  for (uint32_t j = tid; j < P; j += kValidateThreads) seen[j] = 0u;
+  if (tid == 0) flags = 0;
+  __syncthreads();
+  const int32_t* x = topk + static_cast<size_t>(row) * K;
+  int f = 0;
+  for (int i = tid; i < K; i += kValidateThreads) {
+    const int32_t v = x[i];
+    if (v < 0 || static_cast<int64_t>(v) >= rows_r) {
+      f |= 1;
+      continue;
+    }
+    const uint32_t key = static_cast<uint32_t>(v) + 1u;
+    uint32_t h = (static_cast<uint32_t>(v) * 0x9E3779B1u) & (P - 1u);
+    for (uint32_t t = 0; t < P; ++t) {   // at most K keys in P >= 2K words: an empty word is reached
+      const uint32_t w = atomicCAS(&seen[h], 0u, key);
+      if (w == 0u) break;
+      if (w == key) {
+        f |= 2;
+        break;
+      }
+      h = (h + 1u) & (P - 1u);
+    }
+  }
+  if (f) atomicOr(&flags, f);
+  __syncthreads();
+  if (tid == 0) verdict[row] = flags;
+}
 
 }  // namespace
+
+uint32_t validate_set_words(int K) {
+  uint32_t P = 1;
+  while (P < 2u * static_cast<uint32_t>(K)) P <<= 1;
+  return P;
+}
+
+hipError_t launch_validate_topk(const int32_t* topk, const int64_t* rows, int B, int n_q, int K,
+                                int32_t* verdict, hipStream_t s) {
+  const uint32_t P = validate_set_words(K);
+  const size_t lds = 4 * static_cast<size_t>(P);
+  if (lds > 64 * 1024) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(validate_topk_kernel, dim3(static_cast<unsigned>(B) * static_cast<unsigned>(n_q)),
+                     dim3(kValidateThreads), lds, s, topk, rows, K, n_q, P, verdict);
+  return hipGetLastError();
+}
 
 // Threads of the matching workgroup for (S, K): a table of at most 1024 slots
 // with at most 512 indices per token runs on four waves (each thread owns at

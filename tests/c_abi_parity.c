@@ -179,6 +179,81 @@ int main(int argc, char **argv) {
       }
     }
   }
+  /* handover to a validating handle */
+  avsg_config cfg2 = cfg;
+  cfg2.validate = 1;
+  const size_t ws2_bytes = avsg_workspace_bytes(&cfg2);
+  void *ws2, *bufs2[NSTREAMS], *buf2_rows[NSTREAMS * B];
+  HIP_OK(hipMalloc(&ws2, ws2_bytes));
+  for (int s = 0; s < NSTREAMS; ++s) {
+    const size_t bytes = (size_t)B * S * kRowBytes[s];
+    HIP_OK(hipMalloc(&bufs2[s], bytes));
+    HIP_OK(hipMemcpy(bufs2[s], bufs[s], bytes, hipMemcpyDeviceToDevice));
+    for (int r = 0; r < B; ++r) buf2_rows[s * B + r] = (uint8_t *)bufs2[s] + (size_t)r * S * kRowBytes[s];
+  }
+  avsg_handle *h2 = NULL;
+  AVSG_OK_(avsg_create(&cfg2, host_rows, rows, ws2, ws2_bytes, buf2_rows, stream, &h2));
+  static int32_t tc[S], tc2[S];
+  static uint32_t q1[S], q2[S];
+  for (int r = 0; r < B && !failures; ++r) {
+    AVSG_OK_(avsg_export_state(h, r, tc, q1));
+    AVSG_OK_(avsg_import_state(h2, r, tc, q1, stream));
+    AVSG_OK_(avsg_export_state(h2, r, tc2, q2));
+    if (memcmp(tc, tc2, sizeof(tc)) != 0 || memcmp(q1, q2, sizeof(q1)) != 0) {
+      fprintf(stderr, "request %d: imported table differs from the exported one\n", r);
+      failures++;
+    }
+  }
+  for (int t = T; t < T + 2 && !failures; ++t) {
+    select_step(t, X, prev);
+    if (t == T) {
+      /* a repeated index inside token 1 of request 2: refused before any write */
+      static int32_t Xd[B * NQ * K];
+      memcpy(Xd, X, sizeof(X));
+      Xd[(2 * NQ + 1) * K + 7] = Xd[(2 * NQ + 1) * K + 3];
+      HIP_OK(hipMemcpy(d_x, Xd, sizeof(Xd), hipMemcpyHostToDevice));
+      const avsg_status bad = avsg_step(h2, d_x, NULL, d_slots, d_counts, stream);
+      if (bad != AVSG_E_BADINDEX || strstr(avsg_last_error(h2), "request 2 token 1") == NULL) {
+        fprintf(stderr, "validate: status %d (%s), expected AVSG_E_BADINDEX for request 2 token 1\n", bad,
+                avsg_last_error(h2));
+        failures++;
+      }
+      for (int r = 0; r < B; ++r) {
+        AVSG_OK_(avsg_export_state(h, r, tc, q1));
+        AVSG_OK_(avsg_export_state(h2, r, tc2, q2));
+        if (memcmp(tc, tc2, sizeof(tc)) != 0 || memcmp(q1, q2, sizeof(q1)) != 0) {
+          fprintf(stderr, "validate: request %d's table changed by a refused step\n", r);
+          failures++;
+        }
+      }
+    }
+    HIP_OK(hipMemcpy(d_x, X, sizeof(X), hipMemcpyHostToDevice));
+    AVSG_OK_(avsg_step(h2, d_x, NULL, d_slots, d_counts, stream));
+    if (avsg_ref_step(ref, X, NULL, O_ref, n_ref, mx, mo, NSTREAMS, host_rows, image_rows, kRowBytes, rows,
+                      1) != 0) {
+      fprintf(stderr, "oracle step %d failed\n", t);
+      return 2;
+    }
+    HIP_OK(hipStreamSynchronize(stream));
+    HIP_OK(hipMemcpy(O, d_slots, sizeof(O), hipMemcpyDeviceToHost));
+    HIP_OK(hipMemcpy(n, d_counts, sizeof(n), hipMemcpyDeviceToHost));
+    if (memcmp(O, O_ref, sizeof(O)) != 0 || memcmp(n, n_ref, sizeof(n)) != 0) {
+      fprintf(stderr, "step %d after the handover: slots or counts differ\n", t);
+      failures++;
+    }
+    for (int s = 0; s < NSTREAMS; ++s) {
+      const size_t bytes = (size_t)B * S * kRowBytes[s];
+      HIP_OK(hipMemcpy(got, bufs2[s], bytes, hipMemcpyDeviceToHost));
+      if (memcmp(got, images[s], bytes) != 0) {
+        fprintf(stderr, "step %d after the handover, stream %d: buffers differ\n", t, s);
+        failures++;
+      }
+    }
+  }
+  AVSG_OK_(avsg_destroy(h2));
+  for (int s = 0; s < NSTREAMS; ++s) HIP_OK(hipFree(bufs2[s]));
+  HIP_OK(hipFree(ws2));
+
   avsg_stats_t stats;
   AVSG_OK_(avsg_stats(h, &stats));
   AVSG_OK_(avsg_destroy(h));
@@ -195,7 +270,8 @@ int main(int argc, char **argv) {
   HIP_OK(hipFree(d_counts));
   HIP_OK(hipStreamDestroy(stream));
   if (failures) return 1;
-  printf("ok mode %d steps %d hits %llu misses %llu\n", mode, T, (unsigned long long)stats.hits,
+  printf("ok mode %d steps %d (+2 after a validated handover) hits %llu misses %llu\n", mode, T,
+         (unsigned long long)stats.hits,
          (unsigned long long)stats.misses);
   return 0;
 }

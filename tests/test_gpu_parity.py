@@ -259,6 +259,117 @@ def test_bad_indices_are_counted_not_copied():
         host.free()
 
 
+def test_validate_mode_rejects_bad_selections():
+    """Validate mode: a step whose selections hold an index outside [0, rows)
+    or an index repeated within one token fails with AVSG_E_BADINDEX before
+    any table write (every table unchanged), the error names the first bad
+    (request, token) of the oracle's selection check, and the clean steps
+    around it equal the oracle's, buffers included."""
+    from paper_2609_37538_amd import avsg as A
+    import torch
+    spec = W.custom_spec(name="validate", batch=4, topk=256, slots=1024, n_q=2, steps=14, ctx=3000,
+                         row_bytes=(1152, 132))
+    wl = W.Workload(spec)
+    host = HostRows(wl)
+    orc = OracleSide(wl, host)
+    cfg = A.make_config(spec.batch, spec.topk, spec.n_q, spec.slots, row_bytes=spec.row_bytes,
+                        gather_mode=A.AVSG_GATHER_RESIDENT, validate=1)
+    op = A.Operator(cfg, host.ptrs, wl.ctx)
+    rng = np.random.default_rng(11)
+    log("[gpu] validate mode")
+    refused = 0
+    try:
+        for t in range(spec.steps):
+            X = wl.topk(t)
+            if t % 3 == 1:
+                bad = X.copy()
+                for _ in range(1 + t % 2):
+                    r, g = int(rng.integers(spec.batch)), int(rng.integers(spec.n_q))
+                    i, j = rng.choice(spec.topk, size=2, replace=False)
+                    kind = (t // 3) % 3
+                    if kind == 0:
+                        bad[r, g, i] = bad[r, g, j]                  # repeated within the token
+                    elif kind == 1:
+                        bad[r, g, i] = int(wl.ctx[r])                # one past the last row
+                    else:
+                        bad[r, g, i] = -3
+                verdict = ORC.validate(bad, wl.ctx).ravel()
+                first = int(np.flatnonzero(verdict)[0])
+                before = [op.export_state(r) for r in range(spec.batch)]
+                with pytest.raises(A.AvsgError) as e:
+                    op.step(torch.from_numpy(bad).cuda())
+                assert e.value.status == A.AVSG_E_BADINDEX
+                msg = str(e.value)
+                assert f"request {first // spec.n_q} token {first % spec.n_q}:" in msg, msg
+                assert ("outside" in msg) == bool(verdict[first] & 1) and \
+                       ("repeated" in msg) == bool(verdict[first] & 2), msg
+                for r in range(spec.batch):
+                    c, q = op.export_state(r)
+                    assert np.array_equal(c, before[r][0]) and np.array_equal(q, before[r][1])
+                refused += 1
+            O_ref, n_ref = orc.step(X, None)
+            O_gpu, n_gpu = op.step(torch.from_numpy(X).cuda())
+            torch.cuda.synchronize()
+            compare_step(t, O_ref, n_ref, O_gpu.cpu().numpy(), n_gpu.cpu().numpy())
+        bufs = [b.cpu().numpy() for b in op.buffers]
+        for s_ in range(len(spec.row_bytes)):
+            assert np.array_equal(bufs[s_], orc.images[s_])
+        assert refused == 5 and op.stats()["steps"] == spec.steps
+    finally:
+        op.close()
+        host.free()
+
+
+def test_import_state_round_trip():
+    """A table exported from one handle and imported into another (with the
+    buffer bytes copied) continues exactly: both handles and the oracle step
+    the same inputs with equal slots, counts, tables and buffers; a lifetime
+    outside [-1, L] is refused."""
+    from paper_2609_37538_amd import avsg as A
+    import torch
+    spec = W.custom_spec(name="import", batch=3, topk=256, slots=1024, n_q=2, steps=16, ctx=4000,
+                         row_bytes=(1152, 132), retention=0.8)
+    wl = W.Workload(spec)
+    host = HostRows(wl)
+    orc = OracleSide(wl, host)
+    gpus = [GpuSide(wl, host, gather_mode=A.AVSG_GATHER_RESIDENT)]
+    log("[gpu] export -> import round trip")
+    try:
+        for t in range(spec.steps):
+            X = wl.topk(t)
+            if t == 8:
+                second = GpuSide(wl, host, gather_mode=A.AVSG_GATHER_RESIDENT)
+                for r in range(spec.batch):
+                    c, q = gpus[0].op.export_state(r)
+                    second.op.import_state(r, c, q)
+                for a, b in zip(gpus[0].op.buffers, second.op.buffers):
+                    b.copy_(a)
+                torch.cuda.synchronize()
+                gpus.append(second)
+                c, q = gpus[0].op.export_state(0)
+                q_bad = q.copy()
+                q_bad[5] = (q_bad[5] & 0x00FFFFFF) | (17 << 24)   # lifetime L + 1
+                with pytest.raises(A.AvsgError) as e:
+                    second.op.import_state(0, c, q_bad)
+                assert e.value.status == A.AVSG_E_RANGE
+            O_ref, n_ref = orc.step(X, None)
+            for gpu in gpus:
+                O_gpu, n_gpu = gpu.step(X, None)
+                compare_step(t, O_ref, n_ref, O_gpu, n_gpu)
+                for r in range(spec.batch):
+                    c_ref, q_ref = orc.o.export(r)
+                    c_gpu, q_gpu = gpu.op.export_state(r)
+                    assert np.array_equal(c_ref, c_gpu) and np.array_equal(q_ref, q_gpu), f"step {t}"
+        for gpu in gpus:
+            bufs = gpu.buffers()
+            for s_ in range(len(spec.row_bytes)):
+                assert np.array_equal(bufs[s_], orc.images[s_])
+    finally:
+        for gpu in gpus:
+            gpu.close()
+        host.free()
+
+
 RESIDENT_CASES = [
     # name, kwargs of workload.custom_spec, retry R (R = 0 loses many installs)
     ("lost_installs", dict(batch=4, topk=256, slots=512, n_q=2, steps=24, ctx=3000, retention=0.8), 0),

@@ -454,6 +454,29 @@ def test_config_errors(oracle_lib):
 
 
 # ---------------------------------------------------------------------------
+# selection check of the validate mode (the input of Section 3.2: each token's
+# top-K list holds K distinct positions of its request's context)
+# ---------------------------------------------------------------------------
+def test_validate_hand_cases(oracle_lib):
+    """Rows checked by eye: distinct in-range ids are valid; an id below 0 or
+    at or above the request's rows sets bit 0; an in-range id seen twice sets
+    bit 1; an out-of-range id seen twice is only out of range."""
+    X = np.array([[[0, 1, 2, 4]], [[3, 1, 3, 0]], [[-1, 1, 2, 0]], [[5, 1, 2, 0]],
+                  [[7, 7, 1, 1]], [[9, 9, 0, 1]], [[4, 3, 2, 1]]], dtype=np.int32)
+    rows = np.array([5, 5, 5, 5, 5, 5, 4])
+    assert O.validate(X, rows).ravel().tolist() == [0, 2, 1, 1, 3, 1, 1]
+
+
+def test_validate_two_tokens_share_ids(oracle_lib):
+    """Tokens of one step may share indices (that is the MTP reuse of Section
+    3.6); only a repeat inside one token's list is flagged, and each row is
+    checked against its own request's rows."""
+    X = np.array([[[0, 1, 2], [2, 1, 0]], [[6, 7, 8], [6, 6, 1]]], dtype=np.int32)
+    assert O.validate(X, [3, 9]).tolist() == [[0, 0], [0, 2]]
+    assert O.validate(X, [3, 8]).tolist() == [[0, 0], [1, 2]]
+
+
+# ---------------------------------------------------------------------------
 # resident-reuse transfer plan (a property of the transfer: every slot must end
 # up with the bytes the paper's Stage Two writes)
 # ---------------------------------------------------------------------------
