@@ -28,7 +28,8 @@
  *   - avsg_step is asynchronous on the given stream.  Calls on one handle are
  *     not thread-safe and must be ordered by the caller.
  *   - Nothing here allocates device memory except avsg_host_alloc (pinned host
- *     memory) and the HIP events/staging kept by a handle.
+ *     memory) and the HIP events/staging kept by a handle; avsg_step_static
+ *     allocates nothing at all.
  */
 #ifndef AVSG_H
 #define AVSG_H
@@ -91,6 +92,10 @@ typedef int32_t avsg_status;
                                    buffer contents are identical to AVSG_GATHER_BALANCED. */
 
 #define AVSG_MAX_STREAMS 2
+
+/* Bytes of the library's own static device array behind avsg_step_static (one
+ * array per GPU the library runs on, held until the process ends). */
+#define AVSG_STATIC_SCRATCH_BYTES ((size_t)32 << 20)
 
 typedef struct avsg_config {
     int32_t batch;      /* B >= 1 */
@@ -313,6 +318,34 @@ avsg_status avsg_timing(avsg_handle *h, float *match_ms, float *gather_ms, float
 
 avsg_status avsg_destroy(avsg_handle *h);
 
+/* For callers that cannot allocate memory -- code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc: one decode step like
+ * avsg_step, without a handle or a caller workspace.  The tables, transfer
+ * lists, plan lists, counters and pointer tables live in the library's own
+ * static device array of AVSG_STATIC_SCRATCH_BYTES on the current GPU; the
+ * call makes no hipMalloc, hipFree or other allocating call.
+ *   cfg, host_rows, rows_per_request, d_buffers   as for avsg_create (host_rows
+ *                    pinned and device-mapped; the host arrays are read during
+ *                    the call only);
+ *   d_topk, d_verified_len, d_slots, d_miss_counts, stream   as for avsg_step;
+ *   cold_start       nonzero: every table starts empty (and the counters at
+ *                    zero) before this step; 0: the step continues from the
+ *                    tables the previous call on this GPU left, which must have
+ *                    succeeded with the same configuration.
+ * Every call on a GPU shares that GPU's array, which keeps the last call's
+ * contents: calls on one GPU must be ordered on one stream, and calls that
+ * overlap (two streams, two host threads) race.
+ * Hash matching with AVSG_GATHER_BALANCED, _REQUEST, _POSITION, _RESIDENT or
+ * _NONE, and dual-pointer matching with _BALANCED, _REQUEST or _NONE.
+ * Errors: AVSG_E_INVAL (null pointer, misaligned rows, a continuing call after
+ * another configuration or a failed call), AVSG_E_NOTPOW2, AVSG_E_RANGE,
+ * AVSG_E_CAPACITY (avsg_workspace_bytes(cfg) above AVSG_STATIC_SCRATCH_BYTES,
+ * or the LDS limit), AVSG_E_UNSUPPORTED (validate mode or another transfer),
+ * AVSG_E_HIP; each error is described on stderr. */
+avsg_status avsg_step_static(const avsg_config *cfg, const void *const *host_rows,
+                             const int64_t *rows_per_request, void *const *d_buffers,
+                             const int32_t *d_topk, const int64_t *d_verified_len, int32_t *d_slots,
+                             int32_t *d_miss_counts, int32_t cold_start, void *stream);
 
 const char *avsg_strerror(avsg_status s);
 const char *avsg_last_error(const avsg_handle *h);

@@ -150,6 +150,8 @@ def load(share_torch_runtime: bool = True):
     lib.avsg_h2d_peak.argtypes = [_P, _P, sz, i32, _P, ctypes.POINTER(ctypes.c_double)]
     lib.avsg_device_cus.restype = i32
     lib.avsg_device_cus.argtypes = []
+    lib.avsg_step_static.restype = i32
+    lib.avsg_step_static.argtypes = [ctypes.POINTER(AvsgConfig), _P, _P, _P, _P, _P, _P, _P, i32, _P]
     _lib = lib
     return lib
 
@@ -329,6 +331,15 @@ def avsg_h2d_peak(host: int, device: int, nbytes: int, iters: int = 20, stream: 
 def avsg_device_cus() -> int:
     return int(load().avsg_device_cus())
 
+
+def avsg_step_static(cfg: AvsgConfig, host_rows: Sequence[int], rows_per_request, d_buffers: Sequence[int],
+                     d_topk: int, d_verified_len: Optional[int], d_slots: int, d_miss_counts: int,
+                     cold_start: bool, stream: int = 0) -> None:
+    rows = np.ascontiguousarray(rows_per_request, dtype=np.int64)
+    _check(load().avsg_step_static(ctypes.byref(cfg), _ptr_array(host_rows), rows.ctypes.data_as(_P),
+                                   _ptr_array(d_buffers), _vp(d_topk), _vp(d_verified_len), _vp(d_slots),
+                                   _vp(d_miss_counts), 1 if cold_start else 0, _vp(stream)),
+           "avsg_step_static")
 
 
 # ---------------------------------------------------------------------------

@@ -12,6 +12,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -85,6 +86,11 @@ struct avsg_handle {
   std::vector<int32_t> h_val;
   char err[256] = {0};
 };
+
+// Device memory of avsg_step_static: one array per GPU the library runs on,
+// held until the process ends.  In host code `scratch` names a host-side
+// stand-in; its device address on each GPU comes from hipGetSymbolAddress.
+static __device__ __align__(256) unsigned char scratch[AVSG_STATIC_SCRATCH_BYTES];
 
 namespace {
 
@@ -1036,3 +1042,158 @@ avsg_status avsg_h2d_peak(const void* host, void* device, size_t bytes, int32_t 
 }
 
 }  // extern "C"
+
+namespace {
+constexpr int kMaxStaticDevices = 64;
+// Per-GPU state of avsg_step_static (host memory, fixed size).
+struct StaticDevice {
+  unsigned char* ptr = nullptr;   // device address of `scratch` on this GPU
+  size_t match_lds = 0;           // dynamic LDS the matching kernels are prepared for
+  size_t dualptr_lds = 0;
+  bool has_last = false;          // a call completed since the last failure
+  avsg_config last{};             // its configuration
+};
+StaticDevice g_static[kMaxStaticDevices];
+std::mutex g_static_mu;
+
+bool same_config(const avsg_config& a, const avsg_config& b) {
+  return a.batch == b.batch && a.topk == b.topk && a.n_q == b.n_q && a.slots == b.slots &&
+         a.retry == b.retry && a.max_life == b.max_life && a.a1 == b.a1 && a.a2 == b.a2 &&
+         a.n_streams == b.n_streams && a.gather_workers == b.gather_workers &&
+         a.row_bytes[0] == b.row_bytes[0] && (a.n_streams < 2 || a.row_bytes[1] == b.row_bytes[1]) &&
+         a.match_mode == b.match_mode && a.gather_mode == b.gather_mode;
+}
+
+// n values produced by value(i), written to device memory through kernel
+// arguments (no host staging that must outlive the call)
+template <typename F>
+hipError_t put_values(unsigned long long* dst, size_t n, F value, hipStream_t s) {
+  unsigned long long chunk[120];
+  for (size_t i = 0; i < n; i += 120) {
+    const size_t m = std::min<size_t>(120, n - i);
+    for (size_t k = 0; k < m; ++k) chunk[k] = value(i + k);
+    const hipError_t e = launch_put_u64(dst + i, chunk, m, s);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+}  // namespace
+
+extern "C" avsg_status avsg_step_static(const avsg_config* cfg, const void* const* host_rows,
+                                        const int64_t* rows_per_request, void* const* d_buffers,
+                                        const int32_t* d_topk, const int64_t* d_verified_len,
+                                        int32_t* d_slots, int32_t* d_miss_counts, int32_t cold_start,
+                                        void* stream) {
+  avsg_status st = check_config(cfg, nullptr);
+  if (st != AVSG_OK) return st;
+  const avsg_config& c = *cfg;
+  if (c.validate || c.gather_mode == AVSG_GATHER_SDMA || c.gather_mode == AVSG_GATHER_PIPELINED ||
+      c.gather_mode == AVSG_GATHER_EARLY) {
+    std::fprintf(stderr, "avsg_step_static: validate mode and the copy-engine, pipelined and early-fetch "
+                         "transfers are not available without a handle\n");
+    return AVSG_E_UNSUPPORTED;
+  }
+  if (!host_rows || !rows_per_request || !d_buffers || !d_topk || !d_slots || !d_miss_counts)
+    return AVSG_E_INVAL;
+  if (!rows_ok(c, host_rows, rows_per_request, d_buffers)) return AVSG_E_INVAL;
+  const Layout L = layout_of(c);
+  if (L.total > AVSG_STATIC_SCRATCH_BYTES) {
+    std::fprintf(stderr, "avsg_step_static: this configuration needs %zu bytes of scratch; the library's "
+                         "array holds %zu (AVSG_STATIC_SCRATCH_BYTES)\n",
+                 L.total, static_cast<size_t>(AVSG_STATIC_SCRATCH_BYTES));
+    return AVSG_E_CAPACITY;
+  }
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return AVSG_E_HIP;
+  if (dev >= kMaxStaticDevices) return AVSG_E_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  StaticDevice& sd = g_static[dev];
+  if (!sd.ptr) {
+    // once per GPU, with that GPU current: the array's address on it
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      std::fprintf(stderr, "avsg_step_static: hipGetSymbolAddress: %s\n", hipGetErrorString(e));
+      return AVSG_E_HIP;
+    }
+    sd.ptr = static_cast<unsigned char*>(p);
+  }
+  if (!cold_start && !(sd.has_last && same_config(sd.last, c))) {
+    std::fprintf(stderr, "avsg_step_static: cold_start = 0 continues the tables of the previous call on "
+                         "this GPU, which must have succeeded with the same configuration\n");
+    return AVSG_E_INVAL;
+  }
+  sd.has_last = false;
+
+  avsg_handle h;   // section pointers into this GPU's array; allocates nothing
+  h.cfg = c;
+  h.device = dev;
+  h.m = log2_exact(c.slots);
+  bind_workspace(&h, sd.ptr, L);
+  h.cus = device_cus();
+  h.workers = c.gather_workers > 0 ? c.gather_workers : std::max(1, h.cus);
+  int max_lds = 0;
+  if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+    return AVSG_E_HIP;
+  if (c.match_mode == AVSG_MATCH_HASH) {
+    h.lds = match_lds_bytes(c.slots, c.topk);
+    if (max_lds > 0 && h.lds > static_cast<size_t>(max_lds)) return AVSG_E_CAPACITY;
+    if (sd.match_lds < h.lds) {
+      if (prepare_match_hash(h.lds) != hipSuccess) return AVSG_E_HIP;
+      sd.match_lds = h.lds;
+    }
+  } else {
+    h.lds = dualptr_lds_bytes(c.topk);
+    if (sd.dualptr_lds < h.lds) {
+      if (prepare_match_dualptr(h.lds) != hipSuccess) return AVSG_E_HIP;
+      sd.dualptr_lds = h.lds;
+    }
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const size_t B = static_cast<size_t>(c.batch), nsb = static_cast<size_t>(c.n_streams) * B;
+  for (size_t i = 0; i < nsb; ++i) {
+    void* dp = nullptr;
+    if (hipHostGetDevicePointer(&dp, const_cast<void*>(host_rows[i]), 0) != hipSuccess || !dp) {
+      std::fprintf(stderr, "avsg_step_static: host rows must be pinned, device-mapped memory\n");
+      return AVSG_E_INVAL;
+    }
+  }
+  hipError_t e = put_values(
+      reinterpret_cast<unsigned long long*>(h.host_ptrs), nsb,
+      [&](size_t i) {
+        void* dp = nullptr;
+        (void)hipHostGetDevicePointer(&dp, const_cast<void*>(host_rows[i]), 0);
+        return static_cast<unsigned long long>(reinterpret_cast<uintptr_t>(dp));
+      },
+      s);
+  if (e == hipSuccess)
+    e = put_values(reinterpret_cast<unsigned long long*>(h.buf_ptrs), nsb,
+                   [&](size_t i) { return static_cast<unsigned long long>(reinterpret_cast<uintptr_t>(d_buffers[i])); },
+                   s);
+  if (e == hipSuccess)
+    e = put_values(reinterpret_cast<unsigned long long*>(h.rows_dev), B,
+                   [&](size_t i) { return static_cast<unsigned long long>(rows_per_request[i]); }, s);
+  if (e == hipSuccess && cold_start) {
+    // every table empty, counters and the plan's fan bids and stamps at zero
+    // (fill kernels)
+    if (c.match_mode == AVSG_MATCH_HASH)
+      e = launch_reset_tables(h.table_c, h.table_q, B * static_cast<size_t>(c.slots), s);
+    else
+      e = launch_reset_dualptr(h.dp_state, c.batch, c.topk, s);
+    if (e == hipSuccess) e = launch_zero_u64(h.stats, B * kNumStats, s);
+    if (e == hipSuccess && h.fan_slots) e = launch_zero_u64(h.fan_slots, B * static_cast<size_t>(c.slots), s);
+    if (e == hipSuccess && h.plan_stamps) e = launch_zero_u64(h.plan_stamps, B, s);
+  }
+  if (e != hipSuccess) {
+    std::fprintf(stderr, "avsg_step_static: %s\n", hipGetErrorString(e));
+    return AVSG_E_HIP;
+  }
+  st = enqueue_step(&h, d_topk, d_verified_len, d_slots, d_miss_counts, s);
+  if (st != AVSG_OK) {
+    std::fprintf(stderr, "avsg_step_static: %s\n", h.err);
+    return st;
+  }
+  sd.last = c;
+  sd.has_last = true;
+  return AVSG_OK;
+}

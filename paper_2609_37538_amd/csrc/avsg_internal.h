@@ -153,6 +153,9 @@ hipError_t launch_zero_u64(unsigned long long* p, size_t n, hipStream_t s);
 // repeated, 3 both, 0 valid); K <= 8192
 hipError_t launch_validate_topk(const int32_t* topk, const int64_t* rows, int B, int n_q, int K,
                                 int32_t* verdict, hipStream_t s);
+// n 64-bit values from host memory to device memory through kernel arguments
+// (the host array may be reused as soon as the call returns)
+hipError_t launch_put_u64(unsigned long long* dst, const unsigned long long* v, size_t n, hipStream_t s);
 hipError_t launch_gather_balanced(const GatherParams& p, int workers, hipStream_t s);
 hipError_t launch_gather_request(const GatherParams& p, hipStream_t s);
 hipError_t launch_gather_position(const GatherParams& p, int workers, hipStream_t s);

@@ -109,6 +109,21 @@ __global__ __launch_bounds__(kValidateThreads) void validate_topk_kernel(const i
   if (tid == 0) verdict[row] = flags;
 }
 
+// Values written by one launch of put_u64_kernel; the chunk travels in the
+// kernel arguments, so a caller's host array needs to live only for the launch
+// call.
+constexpr int kPutWords = 120;
+struct PutChunk {
+  unsigned long long* dst;
+  int32_t n;
+  int32_t pad;
+  unsigned long long v[kPutWords];
+};
+
+__global__ void put_u64_kernel(PutChunk c) {
+  for (int i = static_cast<int>(threadIdx.x); i < c.n; i += static_cast<int>(blockDim.x)) c.dst[i] = c.v[i];
+}
+
 }  // namespace
 
 uint32_t validate_set_words(int K) {
@@ -125,6 +140,19 @@ hipError_t launch_validate_topk(const int32_t* topk, const int64_t* rows, int B,
   hipLaunchKernelGGL(validate_topk_kernel, dim3(static_cast<unsigned>(B) * static_cast<unsigned>(n_q)),
                      dim3(kValidateThreads), lds, s, topk, rows, K, n_q, P, verdict);
   return hipGetLastError();
+}
+
+hipError_t launch_put_u64(unsigned long long* dst, const unsigned long long* v, size_t n, hipStream_t s) {
+  for (size_t i = 0; i < n; i += kPutWords) {
+    PutChunk c{};
+    c.dst = dst + i;
+    c.n = static_cast<int32_t>(n - i < static_cast<size_t>(kPutWords) ? n - i : kPutWords);
+    for (int k = 0; k < c.n; ++k) c.v[k] = v[i + k];
+    hipLaunchKernelGGL(put_u64_kernel, dim3(1), dim3(128), 0, s, c);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 // Threads of the matching workgroup for (S, K): a table of at most 1024 slots
