@@ -27,13 +27,23 @@ A1_DEFAULT = 2654435761
 A2_DEFAULT = 2246822519
 
 
-def build(force: bool = True, sanitize: bool = False) -> str:
-    """Compile the oracle with gcc (-O2, OpenMP over requests)."""
-    out = LIB_PATH if not sanitize else os.path.join(_HERE, "liboracle_avsg_asan.so")
+ASAN_LIB_PATH = os.path.join(_HERE, "liboracle_avsg_asan.so")
+
+
+def build(force: bool = True, sanitize: bool = False, native: bool = False, out: Optional[str] = None) -> str:
+    """Compile the oracle with gcc (-O3, OpenMP over requests).  sanitize:
+    AddressSanitizer + UndefinedBehaviorSanitizer build (-O1) for the
+    sanitizer test; native: -march=native for the host it is built on (the
+    benchmark builds that on the machine it times)."""
+    if out is None:
+        out = ASAN_LIB_PATH if sanitize else LIB_PATH
     if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(_SRC):
-        flags = ["-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11", "-Wall", "-Wextra"]
+        flags = ["-O3", "-fopenmp", "-shared", "-fPIC", "-std=c11", "-Wall", "-Wextra"]
+        if native:
+            flags.append("-march=native")
         if sanitize:
-            flags += ["-fsanitize=address,undefined", "-fno-omit-frame-pointer", "-O1"]
+            flags += ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined",
+                      "-fno-omit-frame-pointer", "-O1"]
         tmp = out + ".tmp"
         subprocess.check_call(["gcc", *flags, "-o", tmp, _SRC])
         os.replace(tmp, out)
@@ -64,9 +74,12 @@ _P = ctypes.c_void_p
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
+        # AVSG_ORACLE_LIB names another build of the same source (the
+        # sanitizer test's, or the benchmark's -march=native build)
+        path = os.environ.get("AVSG_ORACLE_LIB") or LIB_PATH
+        if path == LIB_PATH and not os.path.exists(LIB_PATH):
             build(force=False)
-        lib = ctypes.CDLL(LIB_PATH)
+        lib = ctypes.CDLL(path)
         lib.avsg_ref_create.restype = _P
         lib.avsg_ref_create.argtypes = [ctypes.POINTER(_Cfg), ctypes.POINTER(ctypes.c_int32)]
         lib.avsg_ref_destroy.argtypes = [_P]
@@ -108,12 +121,26 @@ def _ptr_array(ptrs: Sequence[int]):
     return arr
 
 
-def default_threads() -> int:
+def affinity_cpus() -> int:
+    """CPUs this process may run on."""
     try:
-        n = len(os.sched_getaffinity(0))
+        return len(os.sched_getaffinity(0))
     except AttributeError:
-        n = os.cpu_count() or 1
-    return max(1, min(n, 16))
+        return os.cpu_count() or 1
+
+
+def thread_cap() -> int:
+    """Upper bound on oracle threads: OMP_NUM_THREADS when set (the GPU
+    machines set it to the CPU share of one GPU), else 16."""
+    try:
+        v = int(os.environ.get("OMP_NUM_THREADS", "0"))
+    except ValueError:
+        v = 0
+    return v if v > 0 else 16
+
+
+def default_threads() -> int:
+    return max(1, min(affinity_cpus(), thread_cap()))
 
 
 class OracleError(RuntimeError):
