@@ -20,6 +20,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import subprocess
 import sys
 import time
 
@@ -70,6 +71,12 @@ def parse():
     ap.add_argument("--copy-engine-bench", default="",
                     help="copy-engine transfer of every workload in a process without torch, so the HIP "
                          "runtime's batched copy call is available; write JSON rows here")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-workload block (tiny, batch16, imbalance, stress) and the "
+                         "multi-token cold-start reuse")
+    ap.add_argument("--access-shape-probe", default="",
+                    help="time the balanced gather on all-miss steps of three host layouts (1,152-byte KV "
+                         "rows only, 132-byte indexer rows only, both) and write JSON rows here")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one device-to-device copy of this many MiB first (counter calibration)")
     return ap.parse_args()
@@ -102,6 +109,9 @@ def main():
         return
     if args.layer_batching:
         layer_batching(args.layer_batching, args.layers)
+        return
+    if args.access_shape_probe:
+        access_shape_probe(args.access_shape_probe)
         return
 
     gather_mode = {"balanced": A.AVSG_GATHER_BALANCED, "request": A.AVSG_GATHER_REQUEST,
@@ -252,10 +262,35 @@ def main():
             op_ref.step(X_dev[t], N_dev[t] if spec.speculative else None)
         torch.cuda.synchronize()
         wall_ref = time.perf_counter() - t1
+        # the same steps once more from a cold start with HIP events around
+        # each kernel: the S3 gather kernel's own duration and bandwidth
         op_ref.close()
+        op_ref = A.Operator(cfg_ref, host_ptrs, wl.ctx, device=dev, stream=stream)
+        for t in range(args.warmup):
+            op_ref.step(X_dev[t], N_dev[t] if spec.speculative else None)
+        torch.cuda.synchronize()
+        ref_before = op_ref.stats()
+        A.avsg_set_timing(op_ref.h, True)
+        for t in range(args.warmup, T):
+            op_ref.step(X_dev[t], N_dev[t] if spec.speculative else None)
+        ref_match_ms, ref_gather_ms, _ = A.avsg_timing(op_ref.h, args.steps)
+        ref_after = op_ref.stats()
+        op_ref.close()
+        ref_host = ref_after["host_bytes"] - ref_before["host_bytes"]
+        ref_gsec = float(np.sum(ref_gather_ms)) * 1e-3
+        ref_gbps = ref_host / ref_gsec / 1e9 if ref_gsec > 0 else 0.0
         reference = {"gather": "balanced", "value": round(wall_ref / args.steps * 1e6, 2),
                      "unit": "us/step",
-                     "what": "the paper's Stage Two (S3, Eq. 6): every miss copied from the host"}
+                     "what": "the paper's Stage Two (S3, Eq. 6): every miss copied from the host",
+                     "match_us_median": round(float(np.median(ref_match_ms)) * 1e3, 2),
+                     "gather_us_median": round(float(np.median(ref_gather_ms)) * 1e3, 2),
+                     "roofline": {"bound": "pcie", "kernel": "gather_balanced_kernel",
+                                  "achieved": round(ref_gbps, 3), "peak": PCIE_GEN5_X16_GBPS, "unit": "GB/s",
+                                  "frac": round(ref_gbps / PCIE_GEN5_X16_GBPS, 4),
+                                  "frac_of_hipmemcpy_peak": round(ref_gbps / memcpy_peak, 4) if memcpy_peak else None,
+                                  "algorithmic_bytes_per_launch": round(ref_host / args.steps),
+                                  "what": "every miss's row bytes over the host link / the S3 kernel's "
+                                          "average duration (HIP events on the step stream)"}}
 
     K = args.steps
     us_per_step = wall / K * 1e6
@@ -302,6 +337,29 @@ def main():
         cpu = cpu_baseline(spec, wl, X_host, N_host, host_ptrs, args, gather_mode)
 
     traffic = measured_traffic(args)
+    configs = None
+    cold = None
+    if not args.no_configs and args.config == "batch64_mtp2" and args.gather == "resident" \
+            and args.match == "hash":
+        configs = {"batch64_mtp2": {
+            "us_per_step": round(us_per_step, 2),
+            "match_us_median": round(float(np.median(match_ms)) * 1e3, 2),
+            "stage_two_us_median": round(float(np.median(gather_ms)) * 1e3, 2),
+            "h2d_gbps_gather_kernel": round(gather_gbps, 3),
+            "frac_of_hipmemcpy_peak": round(gather_gbps / memcpy_peak, 4) if memcpy_peak else None,
+            "frac_of_pcie_gen5_x16": round(gather_gbps / PCIE_GEN5_X16_GBPS, 4),
+            "hit_rate": round(hits / max(1, lookups), 5),
+            "s3_us_per_step": reference["value"] if reference else None,
+            "s3_gbps_gather_kernel": reference["roofline"]["achieved"] if reference else None,
+            "s3_frac_of_hipmemcpy_peak": reference["roofline"]["frac_of_hipmemcpy_peak"] if reference else None,
+            "cpu_oracle_us_per_step": cpu["value"] if cpu else None,
+            "cpu_oracle_threads": cpu["cores"] if cpu else None,
+            "steps_timed": f"{args.warmup}..{T - 1}"}}
+        for reg in regions:
+            reg.free()
+        regions = []
+        configs.update(config_block(memcpy_peak, dev, with_cpu=not args.no_cpu_baseline))
+        cold = mtp_cold_start_reuse(dev)
     out = {
         "metric": METRIC,
         "value": round(us_per_step, 2),
@@ -376,6 +434,8 @@ def main():
         "cpu_baseline": cpu,
         "graph_replay": graph,
         "reference_all_misses_from_host": reference,
+        "configs": configs,
+        "mtp_cold_start_reuse": cold,
     }
     print(json.dumps(out), flush=True)
     if args.report:
@@ -389,6 +449,219 @@ def main():
     op.close()
     for reg in regions:
         reg.free()
+
+
+def _fill_regions(spec, wl):
+    """Pinned host regions of every stream, filled with the workload's rows;
+    returns (regions, row pointers ordered s*B + r)."""
+    import workload as W
+    from paper_2609_37538_amd import avsg as A
+    offs = wl.request_row_offsets()
+    regions, ptrs = [], []
+    for s, rb in enumerate(spec.row_bytes):
+        reg = A.HostRegion(wl.host_rows_total() * rb)
+        W.fill_host(wl, s, reg.ptr)
+        regions.append(reg)
+        ptrs += [reg.ptr + int(offs[r]) * rb for r in range(spec.batch)]
+    return regions, ptrs
+
+
+def _measure(spec, gather_mode, X, N, ptrs, ctx, warm, timed, dev):
+    """One Stage Two mode on prepared inputs: a pass without per-kernel events
+    (wall time per step, as a caller sees it) and a pass with HIP events
+    around each kernel, each on a fresh operator from the same cold start;
+    both must move the same rows."""
+    import torch
+    from paper_2609_37538_amd import avsg as A
+    cfg = A.make_config(spec.batch, spec.topk, spec.n_q, spec.slots, row_bytes=spec.row_bytes,
+                        gather_mode=gather_mode)
+    res = {}
+    for events in (False, True):
+        op = A.Operator(cfg, ptrs, ctx, device=dev)
+        try:
+            for t in range(warm):
+                op.step(X[t], N[t] if N is not None else None)
+            torch.cuda.synchronize()
+            before = op.stats()
+            if events:
+                A.avsg_set_timing(op.h, True)
+            t0 = time.perf_counter()
+            for t in range(warm, warm + timed):
+                op.step(X[t], N[t] if N is not None else None)
+            torch.cuda.synchronize()
+            wall = time.perf_counter() - t0
+            if events:
+                match_ms, gather_ms, tail_ms = A.avsg_timing(op.h, timed)
+            after = op.stats()
+        finally:
+            op.close()
+        d = {k: after[k] - before[k] for k in ("hits", "lookups", "misses", "host_bytes")}
+        if events:
+            if d != res["delta"]:
+                raise RuntimeError(f"{spec.name}: the timed pass with events differs from the plain pass")
+            stage_two = np.asarray(gather_ms, dtype=np.float64) + np.asarray(tail_ms, dtype=np.float64)
+            res["match_ms"], res["stage_two_ms"] = np.asarray(match_ms, dtype=np.float64), stage_two
+        else:
+            res["wall"], res["delta"] = wall, d
+    return res
+
+
+def config_block(memcpy_peak, dev, warm=8, timed=32, with_cpu=True):
+    """The other benchmark workloads (tiny, batch16, imbalance, stress) at full
+    size, each from a cold start: `warm` untimed steps, then `timed` steps under
+    the default resident-reuse Stage Two and under the paper's S3 (and, on the
+    imbalance mix, the request-level S1 it is compared with).  Per workload:
+    µs per step (wall time between two synchronizations, no per-kernel events),
+    matching and Stage Two kernel medians (HIP events), host-link payload GB/s
+    of the Stage Two kernels and its fractions of the measured hipMemcpy H2D
+    peak and of PCIe Gen5 x16, hit rate, and the CPU oracle on the same steps."""
+    import torch
+    import workload as W
+    from paper_2609_37538_amd import avsg as A
+    out = {}
+    for name in ("tiny", "batch16", "imbalance", "stress"):
+        t_start = time.time()
+        spec = W.get_spec(name)
+        wl = W.Workload(spec)
+        X_host = wl.all_steps(warm + timed)
+        N_host = np.stack([wl.verified_len(t) for t in range(warm + timed)])
+        X = torch.from_numpy(X_host).to(dev)
+        N = torch.from_numpy(N_host).to(dev) if spec.speculative else None
+        regions, ptrs = _fill_regions(spec, wl)
+        row_total = sum(spec.row_bytes)
+        entry = {"batch": spec.batch, "topk": spec.topk, "slots": spec.slots, "n_q": spec.n_q,
+                 "context": int(wl.ctx.max()), "row_bytes": list(spec.row_bytes),
+                 "steps_timed": f"{warm}..{warm + timed - 1}"}
+        modes = [("resident", A.AVSG_GATHER_RESIDENT), ("s3", A.AVSG_GATHER_BALANCED)]
+        if name == "imbalance":
+            modes.append(("s1", A.AVSG_GATHER_REQUEST))
+        try:
+            for label, gm in modes:
+                m = _measure(spec, gm, X, N, ptrs, wl.ctx, warm, timed, dev)
+                d = m["delta"]
+                gsec = float(np.sum(m["stage_two_ms"])) * 1e-3
+                gbps = d["host_bytes"] / gsec / 1e9 if gsec > 0 and d["host_bytes"] else 0.0
+                pre = "" if label == "resident" else label + "_"
+                entry[pre + "us_per_step"] = round(m["wall"] / timed * 1e6, 2)
+                entry[pre + "match_us_median"] = round(float(np.median(m["match_ms"])) * 1e3, 2)
+                entry[pre + "stage_two_us_median"] = round(float(np.median(m["stage_two_ms"])) * 1e3, 2)
+                entry[pre + "h2d_gbps_gather_kernel"] = round(gbps, 3)
+                entry[pre + "frac_of_hipmemcpy_peak"] = round(gbps / memcpy_peak, 4) if memcpy_peak else None
+                entry[pre + "frac_of_pcie_gen5_x16"] = round(gbps / PCIE_GEN5_X16_GBPS, 4)
+                if label == "resident":
+                    entry["hit_rate"] = round(d["hits"] / max(1, d["lookups"]), 5)
+                    entry["misses_per_step"] = round(d["misses"] / timed, 1)
+                    entry["host_rows_per_step"] = round(d["host_bytes"] / row_total / timed, 1)
+                    entry["match_frac_of_step"] = round(float(np.sum(m["match_ms"])) * 1e-3 / m["wall"], 4)
+            if with_cpu:
+                us, threads = _oracle_us_per_step(spec, X_host, N_host, ptrs, warm, timed)
+                entry["cpu_oracle_us_per_step"] = round(us, 1)
+                entry["cpu_oracle_threads"] = threads
+        finally:
+            for reg in regions:
+                reg.free()
+        entry["seconds"] = round(time.time() - t_start, 1)
+        out[name] = entry
+        print(json.dumps({"config": name, **entry}), file=sys.stderr, flush=True)
+    return out
+
+
+def mtp_cold_start_reuse(dev):
+    """Reuse at the cold start (step 0 of an empty table) with N_q = 1..4 query
+    tokens per request: one table shared by a request's tokens (later tokens
+    hit the slots earlier tokens reserved) against one independent table per
+    token (no index of a token can hit at step 0).  Matching only, on the
+    token mixes of batch64_mtp2 (token g >= 1 keeps 95% of token 0's indices)
+    and of stress (recency window shifted per token, 95% of the hot set kept).
+    reuse = hits / (B * N_q * K) at step 0."""
+    import dataclasses
+    import torch
+    import workload as W
+    from paper_2609_37538_amd import avsg as A
+    host = A.HostRegion(1 << 16)
+    out = {}
+    try:
+        for mix in ("batch64_mtp2", "stress"):
+            rows = {}
+            for n_q in (1, 2, 3, 4):
+                spec = dataclasses.replace(W.get_spec(mix), n_q=n_q)
+                wl = W.Workload(spec)
+                X = wl.topk(0)
+                B, K = spec.batch, spec.topk
+                res = {}
+                for label, (b, nq, Xs) in (("shared", (B, n_q, X)),
+                                            ("independent", (B * n_q, 1, X.reshape(B * n_q, 1, K)))):
+                    cfg = A.make_config(b, K, nq, spec.slots, row_bytes=(16,), gather_mode=A.AVSG_GATHER_NONE)
+                    ctx = np.repeat(wl.ctx, n_q) if label == "independent" else wl.ctx
+                    op = A.Operator(cfg, [host.ptr] * b, ctx, device=dev)
+                    try:
+                        op.step(torch.from_numpy(np.ascontiguousarray(Xs)).to(dev))
+                        st = op.stats()
+                    finally:
+                        op.close()
+                    res[label] = round(st["hits"] / max(1, st["lookups"]), 5)
+                    if label == "shared":
+                        res["lost_installs"] = int(st["lost_exhausted"] + st["lost_collision"])
+                rows[str(n_q)] = res
+            out[mix] = rows
+    finally:
+        host.free()
+    return out
+
+
+def access_shape_probe(out_path, warm=4, timed=16):
+    """The balanced gather (S3) on steps where nearly every selected index
+    misses (retention 0 over 1M-token contexts), for three host layouts: 1,152-
+    byte KV rows only (nine whole 128-byte lines per row), 132-byte indexer
+    rows only (two lines per row), and both regions (the batch64_mtp2 layout:
+    eleven lines per token).  Reports payload GB/s and line GB/s (bytes of the
+    128-byte lines the rows touch) of the gather kernel, from HIP events on
+    the step stream, beside the measured hipMemcpy H2D peak."""
+    import torch
+    import workload as W
+    from paper_2609_37538_amd import avsg as A
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    probe = A.HostRegion(512 << 20)
+    tmp = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    peak = A.avsg_h2d_peak(probe.ptr, tmp.data_ptr(), 512 << 20, 20, torch.cuda.current_stream(dev).cuda_stream)
+    del tmp
+    probe.free()
+    results = [{"hipmemcpy_h2d_peak_gbps": round(peak, 3)}]
+    print(json.dumps(results[0]), flush=True)
+
+    def lines(rb):
+        # rows of rb bytes at offsets x * rb from a 4 KiB-aligned base
+        if rb % 128 == 0:
+            return rb // 128
+        return 2 if rb == 132 else -1
+
+    for label, row_bytes in (("kv_1152", (W.KV_ROW_BYTES,)), ("indexer_132", (W.INDEXER_ROW_BYTES,)),
+                             ("kv_and_indexer", (W.KV_ROW_BYTES, W.INDEXER_ROW_BYTES))):
+        spec = W.custom_spec(name=f"shape_{label}", cfg_id=12, batch=16, topk=2048, slots=8192, n_q=1,
+                             steps=warm + timed, ctx=1 << 20, retention=0.0, row_bytes=row_bytes)
+        wl = W.Workload(spec)
+        X = torch.from_numpy(wl.all_steps(warm + timed)).to(dev)
+        regions, ptrs = _fill_regions(spec, wl)
+        try:
+            m = _measure(spec, A.AVSG_GATHER_BALANCED, X, None, ptrs, wl.ctx, warm, timed, dev)
+        finally:
+            for reg in regions:
+                reg.free()
+        d = m["delta"]
+        gsec = float(np.sum(m["stage_two_ms"])) * 1e-3
+        misses = d["misses"]
+        line_bytes = misses * 128 * sum(lines(rb) for rb in row_bytes)
+        row = {"layout": label, "row_bytes": list(row_bytes), "batch": 16, "topk": 2048,
+               "misses_per_step": round(misses / timed, 1),
+               "gather_us_median": round(float(np.median(m["stage_two_ms"])) * 1e3, 2),
+               "payload_gbps": round(d["host_bytes"] / gsec / 1e9, 3),
+               "line_gbps": round(line_bytes / gsec / 1e9, 3),
+               "line_frac_of_hipmemcpy_peak": round(line_bytes / gsec / 1e9 / peak, 4)}
+        results.append(row)
+        print(json.dumps(row), flush=True)
+    with open(out_path, "w") as f:
+        json.dump(results, f, indent=1)
 
 
 def appendix_d_sweep(out_path):
@@ -556,19 +829,19 @@ def layer_batching(out_path, layers, warm=16, timed=64):
         json.dump(results, f, indent=1)
 
 
-def _oracle_us_per_step(spec, wl, host_ptrs, warm, timed):
+def _oracle_us_per_step(spec, X, N_host, host_ptrs, warm, timed):
     """The CPU oracle (match + Stage Two copy into host images of the buffers)
     on the same warm + timed steps from a cold start: µs per timed step and
     the threads it used."""
     import oracle as ORC
+    _native_oracle()
     threads = ORC.default_threads()
     o = ORC.Oracle(spec.batch, spec.topk, spec.n_q, spec.slots, nthreads=threads)
     images = [np.zeros((spec.batch, spec.slots, rb), dtype=np.uint8) for rb in spec.row_bytes]
     bptr = [images[s][r].ctypes.data for s in range(len(spec.row_bytes)) for r in range(spec.batch)]
-    X = wl.all_steps(warm + timed)
     spent = 0.0
     for t in range(warm + timed):
-        N = wl.verified_len(t) if spec.speculative else None
+        N = N_host[t] if spec.speculative else None
         t0 = time.perf_counter()
         o.step(X[t], N, host=host_ptrs, buf=bptr, row_bytes=list(spec.row_bytes))
         if t >= warm:
@@ -862,7 +1135,10 @@ def config_table(out_path):
                    "lost_installs_per_step": round((d["lost_exhausted"] + d["lost_collision"]) / timed, 1)}
             results.append(row)
             print(json.dumps(row), flush=True)
-        us, threads = _oracle_us_per_step(spec, wl, ptrs, warm, timed)
+        wl_c = W.Workload(spec)
+        X_c = wl_c.all_steps(warm + timed)
+        N_c = np.stack([wl_c.verified_len(t) for t in range(warm + timed)])
+        us, threads = _oracle_us_per_step(spec, X_c, N_c, ptrs, warm, timed)
         row = {"workload": name, "strategy": "CPU oracle", "batch": spec.batch, "topk": spec.topk,
                "slots": spec.slots, "n_q": spec.n_q, "wall_us_per_step": round(us, 1), "cores": threads}
         results.append(row)
@@ -883,11 +1159,12 @@ TRAFFIC_SUMMARY = "profiles/gather_resident_traffic_batch64_mtp2.md"
 def measured_traffic(args):
     """HBM + host-link bytes per gather launch from the committed rocprofv3
     counter summary (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0, copy-calibrated), or
-    None when this run is not the profiled configuration or the gather source
-    has changed since the counters were taken."""
+    None when this run is not the profiled workload and transfer or the gather
+    source has changed since the counters were taken.  The counters were
+    taken over the steady-state launches of one run of the workload; a step's
+    traffic changes little from step to step (the summary names its sample)."""
     import re
-    if (args.config, args.warmup, args.steps, args.workers, args.gather, args.match) != \
-            ("batch64_mtp2", 16, 240, 0, "resident", "hash"):
+    if (args.config, args.workers, args.gather, args.match) != ("batch64_mtp2", 0, "resident", "hash"):
         return None
     path = os.path.join(ROOT, TRAFFIC_SUMMARY)
     if not os.path.exists(path):
@@ -921,6 +1198,7 @@ def cpu_baseline(spec, wl, X_host, N_host, host_ptrs, args, gather_mode):
     on the warmup+timed steps of the same workload, from the same cold start;
     report µs per timed step."""
     import oracle as ORC
+    build = _native_oracle()
     threads = ORC.default_threads()
     o = ORC.Oracle(spec.batch, spec.topk, spec.n_q, spec.slots, nthreads=threads)
     images = [np.zeros((spec.batch, spec.slots, rb), dtype=np.uint8) for rb in spec.row_bytes]
@@ -965,7 +1243,36 @@ def cpu_baseline(spec, wl, X_host, N_host, host_ptrs, args, gather_mode):
         "single_thread_us_per_step": round(t1 / max(1, n1 - first_timed) * 1e6, 1),
         "single_thread_sample": f"steps {first_timed}..{n1 - 1} of the same run",
         "cpu_model": _cpu_model(),
+        "affinity_cpus": ORC.affinity_cpus(),
+        "thread_cap": ORC.thread_cap(),
+        "build": build,
     }
+
+
+_NATIVE = None
+
+
+def _native_oracle():
+    """Build the oracle with -O3 -march=native on this host (into a temporary
+    directory) and make it the one the oracle package loads; returns the
+    build's description.  Falls back to the in-tree -O3 build when gcc is
+    unavailable.  Must run before the oracle is first used in the process."""
+    global _NATIVE
+    if _NATIVE is not None:
+        return _NATIVE
+    import tempfile
+    import oracle as ORC
+    if ORC._lib is not None:
+        _NATIVE = "gcc -O3 (in-tree build, already loaded)"
+        return _NATIVE
+    try:
+        out = os.path.join(tempfile.mkdtemp(prefix="avsg_oracle_"), "liboracle_avsg_native.so")
+        ORC.build(force=True, native=True, out=out)
+        os.environ["AVSG_ORACLE_LIB"] = out
+        _NATIVE = "gcc -O3 -march=native -fopenmp, built on this host"
+    except (OSError, subprocess.CalledProcessError):
+        _NATIVE = "gcc -O3 -fopenmp (in-tree build)"
+    return _NATIVE
 
 
 def _cpu_model():

@@ -14,9 +14,10 @@
 // balanced dynamically: any two workgroups' shares differ by at most a chunk.
 //
 // Progress does not depend on scheduling: producers never wait, consumers wait
-// only for producers, and producers have the lowest workgroup ids.  A consumer
-// that spins longer than a fixed bound sets an error flag and leaves rather
-// than hang.  The last workgroup to leave resets the queue for the next step.
+// only for producers, and producers have the lowest workgroup ids.  Every
+// poll of a consumer counts against a fixed bound: past it the consumer sets
+// an error flag and leaves rather than hang; a producer whose chunks do not
+// fit in the queue sets the same flag.  The last workgroup to leave resets the queue for the next step.
 #include "gather_body.h"
 #include "match_body.h"
 
@@ -55,6 +56,9 @@ struct QueuePublish {
     if (threadIdx.x == 0) {
       const int nch = (count + kChunk - 1) / kChunk;
       const int base = atomicAdd(q.tail, nch);
+      // a queue sized below a step's chunks is a broken invariant: report it
+      // (consumers waiting for the dropped chunks then time out and leave)
+      if (base + nch > q.max_chunks) atomicExch(q.error, 1);
       for (int c = 0; c < nch && base + c < q.max_chunks; ++c) {
         int4* e = q.chunks + base + c;
         store_agent(&e->x, r);
@@ -93,7 +97,8 @@ __device__ __forceinline__ void consume(const GatherParams& gp, const PipeParams
             stop = 1;
             break;
           }
-          continue;          // entry i is published but not yet visible here
+          // else entry i is published but not yet visible here: keep polling,
+          // under the same bound
         }
         if (spins > kSpinLimit) {
           atomicExch(q.error, 1);
