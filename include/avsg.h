@@ -47,7 +47,8 @@ typedef int32_t avsg_status;
 #define AVSG_E_INVAL (-1)       /* null pointer, non-positive size, bad mode */
 #define AVSG_E_NOTPOW2 (-2)     /* S is not a power of two in [2, 2^23] */
 #define AVSG_E_CAPACITY (-3)    /* S < N_q * K (Eq. 7), or 9*S + 12*K bytes beyond one workgroup's LDS
-                                   (or, resident reuse, no room beside the table for a map of 1.5*N_q*K words) */
+                                   (or, resident reuse, no room beside the table for a map of 1.5*N_q*K
+                                   positions of two words each) */
 #define AVSG_E_RANGE (-4)       /* R < 0, L outside [1, 127], a1/a2 not distinct primes, row size */
 #define AVSG_E_BADINDEX (-5)    /* validate mode: a selected index outside [0, rows of its request), or an
                                    index repeated within one token's top-K list */
@@ -165,8 +166,8 @@ avsg_status avsg_check_config(const avsg_config *cfg);
  * workspace that avsg_create needs for cfg
  * (per-request tables of 8*S bytes, transfer lists of 8*N_q*K bytes, a hit
  * mask of N_q*K bytes, counters and pointer tables; with AVSG_GATHER_RESIDENT
- * or AVSG_GATHER_EARLY three more lists of 8*N_q*K bytes, fan slots of
- * 4*N_q*K bytes, bids of 8*S bytes and a step stamp of 8 bytes per request;
+ * or AVSG_GATHER_EARLY three more lists of 8*N_q*K bytes and fan slots of
+ * 4*N_q*K bytes per request;
  * with AVSG_GATHER_EARLY also early keys, positions and finish entries of
  * 36*N_q*K bytes per request and the staging rows (early_staging_rows, by
  * default min(B*N_q*K, 16384), times the row bytes of every stream); with

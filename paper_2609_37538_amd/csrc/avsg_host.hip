@@ -34,8 +34,6 @@ struct avsg_handle {
   uint8_t* hit_mask = nullptr;
   int2* host_list = nullptr;    // resident-reuse plan (AVSG_GATHER_RESIDENT)
   int32_t* host_fan = nullptr;
-  unsigned long long* fan_slots = nullptr;
-  unsigned long long* plan_stamps = nullptr;   // [B] per-request stamp of the fan bids
   int2* res_list = nullptr;
   int2* rep_list = nullptr;
   int32_t* plan_counts = nullptr;  // [B][3]
@@ -158,9 +156,9 @@ Layout layout_of(const avsg_config& c) {
   L.miss_list = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk * 8);
   L.hit_mask = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk);
   L.plan = off;
-  if (has_plan(c))   // host, resident, repeat lists; fan slots; bids; counts; claims; stamps
+  if (has_plan(c))   // host, resident, repeat lists; fan slots; counts; claims
     off += 3 * up(B * static_cast<size_t>(c.n_q) * c.topk * 8) + up(B * static_cast<size_t>(c.n_q) * c.topk * 4) +
-           up(B * S * 8) + up(B * 12) + up(8) + up(B * 8);
+           up(B * 12) + up(8);
   L.early = off;
   if (c.gather_mode == AVSG_GATHER_EARLY) off += early_sections(c)[8];
   L.pipe = off;
@@ -227,8 +225,9 @@ avsg_status check_config(const avsg_config* c, std::string* why) {
                   "position-level, pipelined, resident-reuse and early-fetch transfer need hash matching");
   } else {
     const size_t lds = c->gather_mode == AVSG_GATHER_PIPELINED ? pipelined_lds_bytes(c->slots, c->topk)
-                       : c->gather_mode == AVSG_GATHER_EARLY  ? early_step_lds_bytes(c->slots, c->topk)
-                                                              : match_lds_bytes(c->slots, c->topk);
+                       : c->gather_mode == AVSG_GATHER_EARLY
+                           ? early_step_lds_bytes(c->slots, c->topk, c->n_q)
+                           : stage_one_lds_bytes(c->slots, c->topk, c->n_q, has_plan(*c));
     if (match_lds_bytes(c->slots, c->topk) == 0 || lds > kLdsPerWorkgroup)
       return fail(AVSG_E_CAPACITY, "table and selection exceed one workgroup's LDS (9*S + 12*K bytes)");
     if (has_plan(*c) && plan_map_words(c->slots, c->topk, c->n_q) == 0)
@@ -273,14 +272,9 @@ void bind_workspace(avsg_handle* h, unsigned char* ws, const Layout& L) {
     h->res_list = reinterpret_cast<int2*>(ws + L.plan + list);
     h->rep_list = reinterpret_cast<int2*>(ws + L.plan + 2 * list);
     const size_t fan = up(static_cast<size_t>(B) * c.n_q * c.topk * 4);
-    const size_t bids = up(static_cast<size_t>(B) * c.slots * 8);
     h->host_fan = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list);
-    h->fan_slots = reinterpret_cast<unsigned long long*>(ws + L.plan + 3 * list + fan);
-    h->plan_counts = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan + bids);
-    h->plan_claim =
-        reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan + bids + up(static_cast<size_t>(B) * 12));
-    h->plan_stamps = reinterpret_cast<unsigned long long*>(ws + L.plan + 3 * list + fan + bids +
-                                                           up(static_cast<size_t>(B) * 12) + up(8));
+    h->plan_counts = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan);
+    h->plan_claim = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan + up(static_cast<size_t>(B) * 12));
     h->plan_words = plan_map_words(c.slots, c.topk, c.n_q);
   }
   if (c.gather_mode == AVSG_GATHER_EARLY) {
@@ -420,7 +414,7 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
   };
   hipError_t e;
   if (c.match_mode == AVSG_MATCH_HASH) {
-    h->lds = match_lds_bytes(c.slots, c.topk);
+    h->lds = stage_one_lds_bytes(c.slots, c.topk, c.n_q, has_plan(c));
     int max_lds = 0;
     if ((e = hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device)) !=
         hipSuccess)
@@ -444,7 +438,7 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
         return cleanup(AVSG_E_HIP);
     }
     if (c.gather_mode == AVSG_GATHER_EARLY) {
-      h->lds = early_step_lds_bytes(c.slots, c.topk);
+      h->lds = early_step_lds_bytes(c.slots, c.topk, c.n_q);
       h->early_list_lds = early_list_lds_bytes(c.topk, c.n_q);
       if (max_lds > 0 && (h->lds > static_cast<size_t>(max_lds) || h->early_list_lds > static_cast<size_t>(max_lds)))
         return cleanup(AVSG_E_CAPACITY);
@@ -464,11 +458,6 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
     if ((e = launch_reset_dualptr(h->dp_state, B, c.topk, s)) != hipSuccess) return cleanup(AVSG_E_HIP);
   }
   if (launch_zero_u64(h->stats, static_cast<size_t>(B) * kNumStats, s) != hipSuccess)
-    return cleanup(AVSG_E_HIP);
-  // fan bids and their per-request stamps: stamp 0 is older than every step's
-  if (h->fan_slots &&
-      (launch_zero_u64(h->fan_slots, static_cast<size_t>(B) * c.slots, s) != hipSuccess ||
-       launch_zero_u64(h->plan_stamps, static_cast<size_t>(B), s) != hipSuccess))
     return cleanup(AVSG_E_HIP);
   if (hipMemcpyAsync(h->host_ptrs, h->host_dev.data(), h->host_dev.size() * 8,
                      hipMemcpyHostToDevice, s) != hipSuccess ||
@@ -613,8 +602,8 @@ static avsg_status enqueue_step(avsg_handle* h, const int32_t* d_topk, const int
     p.slots_out = d_slots; p.miss_counts = d_miss_counts; p.miss_list = h->miss_list;
     p.stats = h->stats; p.hit_mask = nullptr;
     p.plan_words = h->plan_words;
-    p.host_list = h->host_list; p.host_fan = h->host_fan; p.fan_slots = h->fan_slots;
-    p.plan_stamps = h->plan_stamps; p.res_list = h->res_list; p.rep_list = h->rep_list;
+    p.host_list = h->host_list; p.host_fan = h->host_fan;
+    p.res_list = h->res_list; p.rep_list = h->rep_list;
     p.plan_counts = h->plan_counts; p.plan_claim = h->plan_claim;
     p.early_x = h->early_x; p.early_n = h->early_n; p.early_done = h->early_done;
     EarlyParams e{};
@@ -653,8 +642,6 @@ static avsg_status enqueue_step(avsg_handle* h, const int32_t* d_topk, const int
       p.plan_words = h->plan_words;
       p.host_list = h->host_list;
       p.host_fan = h->host_fan;
-      p.fan_slots = h->fan_slots;
-      p.plan_stamps = h->plan_stamps;
       p.res_list = h->res_list;
       p.rep_list = h->rep_list;
       p.plan_counts = h->plan_counts;
@@ -1136,7 +1123,7 @@ extern "C" avsg_status avsg_step_static(const avsg_config* cfg, const void* cons
   if (hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
     return AVSG_E_HIP;
   if (c.match_mode == AVSG_MATCH_HASH) {
-    h.lds = match_lds_bytes(c.slots, c.topk);
+    h.lds = stage_one_lds_bytes(c.slots, c.topk, c.n_q, has_plan(c));
     if (max_lds > 0 && h.lds > static_cast<size_t>(max_lds)) return AVSG_E_CAPACITY;
     if (sd.match_lds < h.lds) {
       if (prepare_match_hash(h.lds) != hipSuccess) return AVSG_E_HIP;
@@ -1174,15 +1161,12 @@ extern "C" avsg_status avsg_step_static(const avsg_config* cfg, const void* cons
     e = put_values(reinterpret_cast<unsigned long long*>(h.rows_dev), B,
                    [&](size_t i) { return static_cast<unsigned long long>(rows_per_request[i]); }, s);
   if (e == hipSuccess && cold_start) {
-    // every table empty, counters and the plan's fan bids and stamps at zero
-    // (fill kernels)
+    // every table empty and the counters at zero (fill kernels)
     if (c.match_mode == AVSG_MATCH_HASH)
       e = launch_reset_tables(h.table_c, h.table_q, B * static_cast<size_t>(c.slots), s);
     else
       e = launch_reset_dualptr(h.dp_state, c.batch, c.topk, s);
     if (e == hipSuccess) e = launch_zero_u64(h.stats, B * kNumStats, s);
-    if (e == hipSuccess && h.fan_slots) e = launch_zero_u64(h.fan_slots, B * static_cast<size_t>(c.slots), s);
-    if (e == hipSuccess && h.plan_stamps) e = launch_zero_u64(h.plan_stamps, B, s);
   }
   if (e != hipSuccess) {
     std::fprintf(stderr, "avsg_step_static: %s\n", hipGetErrorString(e));

@@ -53,8 +53,6 @@ struct MatchParams {
   int32_t plan_words;           // words of the end-of-step index map in LDS
   int2* host_list;              // [B][n_q*K] (index, slot) copied from the host
   int32_t* host_fan;            // [B][n_q*K] second slot a host entry is also copied to, or -1
-  unsigned long long* fan_slots;  // [B][S] fan bids per slot: step stamp << 24 | slot (plan scratch)
-  unsigned long long* plan_stamps;  // [B] stamp of each request's last planned step (0 = none)
   int2* res_list;               // [B][n_q*K] (source slot, slot): row already resident
   int2* rep_list;               // [B][n_q*K] (source slot, slot): repeat of a host entry
   int32_t* plan_counts;         // [B][3] host, resident, repeat entries
@@ -168,6 +166,9 @@ hipError_t launch_gather_resident(const GatherParams& host, const GatherParams& 
 // words of the end-of-step index map the matching kernel can hold for (S, K, n_q);
 // 0 when the plan does not fit in the kernel's LDS
 int plan_map_words(int S, int K, int n_q);
+// dynamic LDS of the matching workgroup for (S, K, n_q), with room for the
+// end-of-step plan when `plan`; 0 when it does not fit
+size_t stage_one_lds_bytes(int S, int K, int n_q, bool plan);
 int pipelined_chunk_misses();
 size_t pipelined_lds_bytes(int S, int K);
 hipError_t prepare_step_pipelined(size_t lds);
@@ -178,7 +179,7 @@ hipError_t launch_step_pipelined(const MatchParams& mp, const GatherParams& gp, 
 // the finishing kernel for rows fetched before their slots were known
 uint32_t early_map_words(int K, int n_q);
 size_t early_list_lds_bytes(int K, int n_q);
-size_t early_step_lds_bytes(int S, int K);
+size_t early_step_lds_bytes(int S, int K, int n_q);
 hipError_t prepare_step_early(size_t list_lds, size_t step_lds);
 hipError_t launch_early_list(const EarlyParams& e, size_t lds, hipStream_t s);
 hipError_t launch_step_early(const MatchParams& mp, const EarlyParams& e, int workers, size_t lds,

@@ -154,19 +154,42 @@ struct Own {
 };
 
 // Words of LDS bookkeeping of the end-of-step plan besides the reservation
-// bitmap and the two maps: per-wave counts of the three lists for two
-// compaction rounds, plus totals.
+// bitmap, the index map and its fan words: per-wave counts of the three lists
+// for two compaction rounds, plus totals.
 constexpr int kPlanMiscWords = 6 * kMaxWaves + 4;
+// Words of the plan's reservation bitmap for S slots, padded to a multiple of
+// four so that the map behind it starts 16-byte aligned.
+__host__ __device__ constexpr int plan_bitmap_words(int S) { return (((S + 31) >> 5) + 3) & ~3; }
 constexpr uint32_t kPlanResident = 0x80000000u;   // map word names a slot outside this step's reservations
-constexpr uint32_t kPlanRepeat = 0x40000000u;     // the word's index has a repeat this step
-constexpr uint32_t kPlanEarly = 0x20000000u;      // the word's index was fetched before Stage One
+constexpr uint32_t kPlanEarly = 0x40000000u;      // the word's index was fetched before Stage One
+constexpr uint32_t kPlanTag = 0x3F000000u;        // six bits of a second hash of the word's index
 constexpr uint32_t kPlanSlot = 0x00FFFFFFu;       // slot + 1
-constexpr unsigned long long kFanSlot = 0xFFFFFFull;       // fan word: stamp << 24 | slot
-constexpr unsigned long long kFanStampMax = (1ull << 40) - 1;
 
 // Home word of index x in the plan's map of P words (multiplicative hash).
 __device__ __forceinline__ uint32_t plan_home(int32_t x, uint32_t P) {
   return static_cast<uint32_t>((static_cast<uint64_t>(static_cast<uint32_t>(x) * 0x9E3779B1u) * P) >> 32);
+}
+// Tag bits of index x kept in its map word: a word whose tag differs is
+// passed over without reading the slot it names.
+__device__ __forceinline__ uint32_t plan_tag(int32_t x) {
+  return ((static_cast<uint32_t>(x) * 0x85EBCA77u) >> 26) << 24;
+}
+
+// Position of index x's word in the map (its word in *word), or -1.
+__device__ __forceinline__ int plan_lookup(const uint32_t* smp, const int32_t* sc, uint32_t P,
+                                           int32_t x, uint32_t* word) {
+  uint32_t h = plan_home(x, P);
+  const uint32_t tag = plan_tag(x);
+  for (uint32_t t = 0; t < P; ++t) {
+    const uint32_t w = smp[h];
+    if (w == 0u) break;
+    if ((w & kPlanTag) == tag && sc[(w & kPlanSlot) - 1u] == x) {
+      *word = w;
+      return static_cast<int>(h);
+    }
+    h = (h + 1u == P) ? 0u : h + 1u;
+  }
+  return -1;
 }
 
 // Stage Two plan of the resident-reuse gather, after the step's table write
@@ -180,32 +203,15 @@ __device__ __forceinline__ uint32_t plan_home(int32_t x, uint32_t P) {
 //   a host copy.
 // A host entry also writes its row to the largest repeat destination of its
 // index (its fan slot), so with two tokens per step no repeat is left for a
-// later copy; repeats bid for the fan slot with a global atomicMax on a
-// per-slot word of the request (fan_slots), stamped with the request's step
-// count so that a word left by an earlier step always loses and needs no
-// reset.  The count lives in device memory and only this workgroup advances
-// it, so a captured and replayed step stamps every replay anew.  The lists keep transfer-list order.  LDS map: P words, open
-// addressing with linear probing keyed by the index a word names through c[];
-// a word is (resident bit | slot + 1), 0 = empty, and atomicMax makes every
-// choice deterministic.  The map holds at most N_q * K keys and
-// P >= 1.5 N_q K, so every probe sequence ends at an empty word.
+// later copy.  The lists keep transfer-list order.  LDS: a map of P words,
+// open addressing with linear probing keyed by the index a word names through
+// c[]; a word is (resident bit | early bit | tag | slot + 1), 0 = free, and
+// atomicMax makes every choice deterministic; beside it S fan words, one per
+// slot: the largest repeat destination + 1 of the index whose host copy goes
+// to that slot (0 = none).  The map holds at most N_q * K keys and
+// P >= 1.5 N_q K, so every probe sequence ends at a free word.
 // v0: this thread's entry tid of the transfer list (loaded by the caller
 // before the table write-back, so its latency overlaps the write-back).
-__device__ __forceinline__ int plan_lookup(const uint32_t* smp, const int32_t* sc, uint32_t P,
-                                           int32_t x, uint32_t* word) {
-  uint32_t h = plan_home(x, P);
-  for (uint32_t t = 0; t < P; ++t) {
-    const uint32_t w = smp[h];
-    if (w == 0u) break;
-    if (sc[(w & kPlanSlot) - 1u] == x) {
-      *word = w;
-      return static_cast<int>(h);
-    }
-    h = (h + 1u == P) ? 0u : h + 1u;
-  }
-  return -1;
-}
-
 template <int NT>
 __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, unsigned char* lds,
                                              const int listed, const int64_t rows_r,
@@ -214,19 +220,12 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   constexpr int MT = NT, MW = NT / 64;
   const int S = p.S;
   const int32_t* sc = reinterpret_cast<const int32_t*>(lds);
-  uint32_t* sres = reinterpret_cast<uint32_t*>(lds + 4 * static_cast<size_t>(S));  // reserved-slot bitmap
-  const int nb = (S + 31) >> 5;
-  const uint32_t P = static_cast<uint32_t>(p.plan_words);
+  uint32_t* sres = reinterpret_cast<uint32_t*>(lds + align16(4 * static_cast<size_t>(S)));  // reserved-slot bitmap
+  const int nb = plan_bitmap_words(S);
+  const uint32_t P = static_cast<uint32_t>(p.plan_words);   // a multiple of 4
   uint32_t* smp = sres + nb;                                        // [P] index map
-  int* scnt = reinterpret_cast<int*>(smp + P);                      // [kPlanMiscWords]
-  unsigned long long* gfan = p.fan_slots + static_cast<size_t>(r) * S;   // [S] fan bid per slot
-  unsigned long long next = p.plan_stamps[r] + 1;
-  if (next > kFanStampMax) {
-    // after 2^40 - 1 steps of this request the stamps restart from a cleared array
-    for (int j = threadIdx.x; j < S; j += MT) gfan[j] = 0ull;
-    next = 1;
-  }
-  const unsigned long long stamp = next << 24;
+  uint32_t* sfan = smp + P;                                         // [S] fan words per slot
+  int* scnt = reinterpret_cast<int*>(sfan + S);                     // [kPlanMiscWords]
   const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
   const size_t lb = static_cast<size_t>(r) * p.n_q * p.K;
   const int2* ml = p.miss_list + lb;
@@ -236,11 +235,13 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   }
 
   {
-    // 16-byte stores where sres (4 S bytes into the LDS) is 16-byte aligned
-    const int words = nb + static_cast<int>(P) + kPlanMiscWords;
-    const int vec = (S & 3) == 0 ? words / 4 : 0;
+    // the bitmap, map and fan words, four words per 16-byte store where they
+    // come in fours
+    const int words = nb + static_cast<int>(P) + S;
+    const int vec = words / 4;
     for (int j = tid; j < vec; j += MT) reinterpret_cast<u32x4*>(sres)[j] = 0u;
     for (int j = 4 * vec + tid; j < words; j += MT) sres[j] = 0u;
+    for (int j = tid; j < kPlanMiscWords; j += MT) scnt[j] = 0;
   }
   __syncthreads();
 
@@ -250,13 +251,14 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
     if (v.y < 0 || v.y >= S) continue;
     atomicOr(&sres[v.y >> 5], 1u << (v.y & 31));
     if (v.x < 0 || static_cast<int64_t>(v.x) >= rows_r) continue;
-    const uint32_t val = static_cast<uint32_t>(v.y) + 1u;
+    const uint32_t tag = plan_tag(v.x);
+    const uint32_t val = tag | (static_cast<uint32_t>(v.y) + 1u);
     uint32_t h = plan_home(v.x, P);
     for (uint32_t t = 0; t < P; ++t) {
       const uint32_t w = atomicCAS(&smp[h], 0u, val);
       if (w == 0u) break;
-      if (sc[(w & kPlanSlot) - 1u] == v.x) {
-        atomicMax(&smp[h], val);
+      if ((w & kPlanTag) == tag && sc[(w & kPlanSlot) - 1u] == v.x) {
+        atomicMax(&smp[h], val);   // the largest reserved slot of the index
         break;
       }
       h = (h + 1u == P) ? 0u : h + 1u;
@@ -289,9 +291,10 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
       // the reservation bitmap is read only for the few slots whose home word is taken
       if (ws[u] != 0u && ((sres[j >> 5] >> (j & 31)) & 1u)) ws[u] = 0u;
       uint32_t h = hs[u], w = ws[u];
+      const uint32_t tag = plan_tag(xs[u]);
       for (uint32_t t = 0; w != 0u && t < P; ++t) {
-        if (sc[(w & kPlanSlot) - 1u] == xs[u]) {
-          atomicMax(&smp[h], kPlanResident | (static_cast<uint32_t>(j0 + u * MT) + 1u));
+        if ((w & kPlanTag) == tag && sc[(w & kPlanSlot) - 1u] == xs[u]) {
+          atomicMax(&smp[h], kPlanResident | tag | (static_cast<uint32_t>(j) + 1u));
           break;
         }
         h = (h + 1u == P) ? 0u : h + 1u;
@@ -315,71 +318,61 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
     __syncthreads();
   }
 
-  // classify one entry: 0 host, 1 resident, 2 repeat (src = source slot,
-  // *hw = its map position), 4 / 5 first / further miss of an early-fetched
-  // index, -1 past the list
-  auto classify = [&](int e, int2* v, int* src, int* hw) {
-    *src = 0;
-    *hw = -1;
-    if (e >= listed) return -1;
-    *v = e < MT ? v0 : ml[e];
-    if (v->x < 0 || static_cast<int64_t>(v->x) >= rows_r) return 0;
+  // classify one entry: kind 0 host, 1 resident, 2 repeat (src = source
+  // slot, hw = its map position), 4 / 5 first / further miss of an
+  // early-fetched index, -1 past the list (returned by value: out-parameters
+  // would put these locals on the stack)
+  struct Entry {
+    int kind, src, hw;
+    int2 v;
+  };
+  auto classify = [&](int e) __attribute__((always_inline)) {
+    Entry c{-1, 0, -1, make_int2(0, 0)};
+    if (e >= listed) return c;
+    c.v = e < MT ? v0 : ml[e];
+    c.kind = 0;
+    if (c.v.x < 0 || static_cast<int64_t>(c.v.x) >= rows_r) return c;
     uint32_t w = 0u;
-    *hw = plan_lookup(smp, sc, P, v->x, &w);
-    if (*hw < 0) return 0;
+    c.hw = plan_lookup(smp, sc, P, c.v.x, &w);
+    if (c.hw < 0) return c;
     const int o = static_cast<int>(w & kPlanSlot) - 1;
-    if (w & kPlanEarly) return o != v->y ? 5 : 4;   // fetched early; 5 = a further miss of it
-    if (w & kPlanResident) {
-      *src = o;
-      return 1;
+    if (w & kPlanEarly) {
+      c.kind = o != c.v.y ? 5 : 4;   // fetched early; 5 = a further miss of it
+    } else if (w & kPlanResident) {
+      c.kind = 1;
+      c.src = o;
+    } else if (o != c.v.y) {
+      c.kind = 2;
+      c.src = o;
     }
-    if (o != v->y) {
-      *src = o;
-      return 2;
-    }
-    return 0;
+    return c;
   };
 
-  // (3) every repeat bids for its source's fan slot (the largest destination
-  // wins) and flags its index's map word; repeats need two tokens in the
-  // step.  The first round's classification is kept for (4).
-  int2 v_first = make_int2(0, 0);
-  int src_first = 0, hw_first = -1;
-  const int kind_first = classify(tid, &v_first, &src_first, &hw_first);
+  // (3) every repeat bids for the fan word of its source slot (the largest
+  // destination wins); repeats need two tokens in the step.  The first round's
+  // classification is kept for (4).
+  const Entry first = classify(tid);
   if (p.n_q > 1) {
     for (int e = tid; e < listed; e += MT) {
-      int2 v = v_first;
-      int src = src_first, hw = hw_first;
-      const int kind = e < MT ? kind_first : classify(e, &v, &src, &hw);
-      if (kind == 2) {
-        atomicMax(&gfan[src], stamp | static_cast<unsigned long long>(v.y));
-        atomicOr(&smp[hw], kPlanRepeat);
-      }
+      const Entry c = e < MT ? first : classify(e);
+      if (c.kind == 2) atomicMax(&sfan[c.src], static_cast<uint32_t>(c.v.y) + 1u);
     }
+    __syncthreads();
   }
-  __syncthreads();
-  // fan words are read past the L1, where the bids were made; a word whose
-  // stamp is not this step's holds no bid of this step
-  auto fan_of = [&](int slot) {
-    const unsigned long long w = __hip_atomic_load(&gfan[slot], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return (w & ~kFanSlot) == stamp ? static_cast<int>(w & kFanSlot) : -1;
-  };
 
   // (4) compact the three lists in transfer-list order; host entries carry
   // their fan slot, repeats that won the fan word leave the repeat list
   int n_list[3] = {0, 0, 0}, n_rep = 0;
   for (int e0 = 0, it = 0; e0 < listed; e0 += MT, ++it) {
-    int2 v = v_first;
-    int src = src_first, hw = hw_first;
-    int kind = it == 0 ? kind_first : classify(e0 + tid, &v, &src, &hw);
+    Entry c = it == 0 ? first : classify(e0 + tid);
     int fan = -1;
-    // only indices flagged by a repeat read their fan slot
-    if (kind == 0 && hw >= 0 && (smp[hw] & kPlanRepeat) && v.y >= 0 && v.y < S) fan = fan_of(v.y);
-    if (kind == 2) {
+    if (c.kind == 0 && c.hw >= 0 && c.v.y >= 0 && c.v.y < S) fan = static_cast<int>(sfan[c.v.y]) - 1;
+    if (c.kind == 2) {
       ++n_rep;
-      if (fan_of(src) == v.y) kind = 3;   // written by the host copy
+      if (static_cast<int>(sfan[c.src]) - 1 == c.v.y) c.kind = 3;   // written by the host copy
     }
-    if (kind == 5) ++n_rep;               // filled by the early fetch's copy of its index
+    if (c.kind == 5) ++n_rep;             // filled by the early fetch's copy of its index
+    const int kind = c.kind;
     uint64_t mk[3];
     int* wc = scnt + (it & 1) * 3 * MW;
 #pragma unroll
@@ -392,19 +385,19 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
     for (int w = 0; w < MW; ++w) {
 #pragma unroll
       for (int k = 0; k < 3; ++k) {
-        const int c = wc[k * MW + w];
-        total[k] += c;
-        before[k] += (w < wave) ? c : 0;
+        const int cnt = wc[k * MW + w];
+        total[k] += cnt;
+        before[k] += (w < wave) ? cnt : 0;
       }
     }
     if (kind == 0) {
       const size_t at = lb + n_list[0] + before[0] + bits_below(mk[0]);
-      p.host_list[at] = v;
+      p.host_list[at] = c.v;
       p.host_fan[at] = fan;
     } else if (kind == 1) {
-      p.res_list[lb + n_list[1] + before[1] + bits_below(mk[1])] = make_int2(src, v.y);
+      p.res_list[lb + n_list[1] + before[1] + bits_below(mk[1])] = make_int2(c.src, c.v.y);
     } else if (kind == 2) {
-      p.rep_list[lb + n_list[2] + before[2] + bits_below(mk[2])] = make_int2(src, v.y);
+      p.rep_list[lb + n_list[2] + before[2] + bits_below(mk[2])] = make_int2(c.src, c.v.y);
     }
 #pragma unroll
     for (int k = 0; k < 3; ++k) n_list[k] += total[k];
@@ -418,7 +411,6 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
     counts_out[2] = n_list[2];
   }
   if (tid == 0) {
-    p.plan_stamps[r] = next;   // every thread read the old count before the first barrier
     int32_t* pc = p.plan_counts + 3 * static_cast<size_t>(r);
     pc[0] = n_list[0];
     pc[1] = n_list[1];

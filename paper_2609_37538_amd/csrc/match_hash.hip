@@ -177,16 +177,35 @@ size_t match_lds_bytes(int S, int K) {
          4 * static_cast<size_t>(kScratchInts);
 }
 
+// LDS of one workgroup (gfx950), the bound of the end-of-step plan's map.
+constexpr size_t kWorkgroupLds = 160 * 1024;
+
 int plan_map_words(int S, int K, int n_q) {
-  const size_t lds = match_lds_bytes(S, K);
-  if (lds == 0 || n_q < 1) return 0;
-  // every array but c[] (4 S bytes) is free once the table is written back
-  const long long words = static_cast<long long>((lds - 4 * static_cast<size_t>(S)) / 4) -
-                          (S + 31) / 32 - kPlanMiscWords;
+  if (match_lds_bytes(S, K) == 0 || n_q < 1) return 0;
+  // the plan keeps c[] (4 S bytes, padded to 16) and takes the rest of the
+  // workgroup's LDS: the reservation bitmap, P map words, S fan words and its
+  // counters; P is a power of two where one fits, else a multiple of four
+  const long long words = static_cast<long long>((kWorkgroupLds - align16(4 * static_cast<size_t>(S))) / 4) -
+                          plan_bitmap_words(S) - S - kPlanMiscWords;
   const long long keys = static_cast<long long>(n_q) * K;
+  const long long need = (3 * keys + 1) / 2;   // keep the map at most two-thirds full
   long long P = words < 4 * keys ? words : 4 * keys;
-  if (P < (3 * keys + 1) / 2) return 0;   // keep the map at most two-thirds full
+  long long pow2 = 1;
+  while (2 * pow2 <= P) pow2 *= 2;
+  P = pow2 >= need ? pow2 : (P & ~3ll);
+  if (P < need) return 0;
   return static_cast<int>(P);
+}
+
+size_t stage_one_lds_bytes(int S, int K, int n_q, bool plan) {
+  const size_t m = match_lds_bytes(S, K);
+  if (m == 0 || !plan) return m;
+  const int P = plan_map_words(S, K, n_q);
+  if (P == 0) return 0;
+  const size_t need = align16(4 * static_cast<size_t>(S)) +
+                      4 * (static_cast<size_t>(plan_bitmap_words(S)) + static_cast<size_t>(P) +
+                           static_cast<size_t>(S) + kPlanMiscWords);
+  return m > need ? m : need;
 }
 
 hipError_t prepare_match_hash(size_t lds) {

@@ -506,8 +506,8 @@ size_t early_list_lds_bytes(int K, int n_q) {
   return P ? 8 * static_cast<size_t>(P) + 4 * (kMatchThreads / 64) : 0;
 }
 
-size_t early_step_lds_bytes(int S, int K) {
-  const size_t m = match_lds_bytes(S, K);
+size_t early_step_lds_bytes(int S, int K, int n_q) {
+  const size_t m = stage_one_lds_bytes(S, K, n_q, true);
   if (m == 0) return 0;
   const size_t copier = match_threads(S, K) == kSmallThreads ? early_copy_lds<kSmallThreads>()
                                                              : early_copy_lds<kMatchThreads>();

@@ -94,8 +94,8 @@ def test_check_config_statuses(lib):
     assert chk(gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_OK
     assert chk(n_q=1, slots=2048, match_mode=A.AVSG_MATCH_DUALPTR,
                gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_E_UNSUPPORTED
-    assert chk(batch=1, topk=128, n_q=100, slots=16384, gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_OK
-    assert chk(batch=1, topk=128, n_q=110, slots=16384, gather_mode=A.AVSG_GATHER_RESIDENT) == \
+    assert chk(batch=1, topk=128, n_q=39, slots=16384, gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_OK
+    assert chk(batch=1, topk=128, n_q=40, slots=16384, gather_mode=A.AVSG_GATHER_RESIDENT) == \
         A.AVSG_E_CAPACITY
     assert chk(batch=1, topk=128, n_q=110, slots=16384) == A.AVSG_OK
     assert chk(gather_mode=8) == A.AVSG_E_INVAL
@@ -106,7 +106,7 @@ def test_check_config_statuses(lib):
     assert chk(gather_mode=A.AVSG_GATHER_EARLY, early_direct=1) == A.AVSG_E_INVAL
     assert chk(n_q=1, slots=2048, match_mode=A.AVSG_MATCH_DUALPTR,
                gather_mode=A.AVSG_GATHER_EARLY) == A.AVSG_E_UNSUPPORTED
-    assert chk(batch=1, topk=128, n_q=100, slots=16384, gather_mode=A.AVSG_GATHER_EARLY) == A.AVSG_OK
+    assert chk(batch=1, topk=128, n_q=39, slots=16384, gather_mode=A.AVSG_GATHER_EARLY) == A.AVSG_OK
 
 
 def test_workspace_size_and_validation(lib):
@@ -128,7 +128,7 @@ def test_workspace_size_and_validation(lib):
     assert ws(gather_mode=8) == 0
     # the resident-reuse plan adds three transfer lists, fan slots, bids, counts and claims
     B, nq, K = 64, 2, 2048
-    assert ws(gather_mode=A.AVSG_GATHER_RESIDENT) >= ws() + (3 * 8 + 4) * B * nq * K + 8 * B * 8192 + 12 * B
+    assert ws(gather_mode=A.AVSG_GATHER_RESIDENT) >= ws() + (3 * 8 + 4) * B * nq * K + 12 * B
     assert ws(gather_mode=A.AVSG_GATHER_POSITION) > ws() - 1
     # early fetch adds keys, positions, finish entries and 16384 staging rows of both streams
     early = ws(gather_mode=A.AVSG_GATHER_EARLY)

@@ -370,6 +370,49 @@ def test_import_state_round_trip():
         host.free()
 
 
+@pytest.mark.parametrize("mix", ["batch64_mtp2", "stress"])
+def test_mtp_cold_start_reuse(mix):
+    """Cold start with N_q = 1..4 query tokens on the full-batch token mixes
+    of batch64_mtp2 and stress (Section 3.6): with one table per request, the
+    first token misses every index and the step's slots, counts and hits
+    equal the oracle's (later tokens reuse the first token's reservations);
+    with an independent table per token nothing hits at step 0."""
+    import dataclasses
+    import torch
+    from paper_2609_37538_amd import avsg as A
+    host = A.HostRegion(1 << 16)
+    try:
+        for n_q in (1, 2, 3, 4):
+            spec = dataclasses.replace(W.get_spec(mix), n_q=n_q)
+            wl = W.Workload(spec)
+            X, N = wl.topk(0), wl.verified_len(0)
+            B, K = spec.batch, spec.topk
+            log(f"[gpu] cold start {mix} n_q={n_q}")
+            for label, b, nq in (("shared", B, n_q), ("independent", B * n_q, 1)):
+                Xs = np.ascontiguousarray(X.reshape(b, nq, K))
+                ctx = wl.ctx if label == "shared" else np.repeat(wl.ctx, n_q)
+                Ns = N if label == "shared" else np.repeat(N, n_q)
+                orc = ORC.Oracle(b, K, nq, spec.slots)
+                O_ref, n_ref = orc.step(Xs, Ns, rows=ctx)
+                cfg = A.make_config(b, K, nq, spec.slots, row_bytes=(16,), gather_mode=A.AVSG_GATHER_NONE)
+                op = A.Operator(cfg, [host.ptr] * b, ctx)
+                try:
+                    O_gpu, n_gpu = op.step(torch.from_numpy(Xs).cuda(), torch.from_numpy(Ns).cuda())
+                    torch.cuda.synchronize()
+                    compare_step(0, O_ref, n_ref, O_gpu.cpu().numpy(), n_gpu.cpu().numpy())
+                    hits = op.stats()["hits"]
+                finally:
+                    op.close()
+                assert hits == orc.total_stats()["hits"]
+                assert np.all(n_ref[:, 0] == K)
+                if label == "independent" or n_q == 1:
+                    assert hits == 0
+                else:
+                    assert hits > 0.3 * B * (n_q - 1) * K
+    finally:
+        host.free()
+
+
 RESIDENT_CASES = [
     # name, kwargs of workload.custom_spec, retry R (R = 0 loses many installs)
     ("lost_installs", dict(batch=4, topk=256, slots=512, n_q=2, steps=24, ctx=3000, retention=0.8), 0),
@@ -449,9 +492,9 @@ def test_resident_reuse_refused_without_room():
     needs hash matching."""
     from paper_2609_37538_amd import avsg as A
     chk = lambda **kw: A.avsg_check_config(A.make_config(**kw))
-    assert chk(batch=1, topk=128, n_q=100, slots=16384, row_bytes=(16,),
+    assert chk(batch=1, topk=128, n_q=39, slots=16384, row_bytes=(16,),
                gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_OK
-    assert chk(batch=1, topk=128, n_q=110, slots=16384, row_bytes=(16,),
+    assert chk(batch=1, topk=128, n_q=40, slots=16384, row_bytes=(16,),
                gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_E_CAPACITY
     assert chk(batch=1, topk=128, n_q=110, slots=16384, row_bytes=(16,)) == A.AVSG_OK
     assert chk(batch=1, topk=64, n_q=1, slots=64, row_bytes=(16,), match_mode=A.AVSG_MATCH_DUALPTR,
