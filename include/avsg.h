@@ -48,7 +48,7 @@ typedef int32_t avsg_status;
 #define AVSG_E_NOTPOW2 (-2)     /* S is not a power of two in [2, 2^23] */
 #define AVSG_E_CAPACITY (-3)    /* S < N_q * K (Eq. 7), or 9*S + 12*K bytes beyond one workgroup's LDS
                                    (or, resident reuse, no room beside the table for a map of 1.5*N_q*K
-                                   positions of two words each) */
+                                   words and S fan words) */
 #define AVSG_E_RANGE (-4)       /* R < 0, L outside [1, 127], a1/a2 not distinct primes, row size */
 #define AVSG_E_BADINDEX (-5)    /* validate mode: a selected index outside [0, rows of its request), or an
                                    index repeated within one token's top-K list */

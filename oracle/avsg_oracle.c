@@ -4,13 +4,16 @@
  * benchmark's CPU-baseline leg are the only users.  Nothing here is shared with
  * the GPU library.
  *
- * The code follows the AVSG paper (arXiv 2609.37538) step by step, in its
- * order and notation, with scalar loops and no blocking or fusion:
+ * The code is written from the AVSG paper (arXiv 2609.37538), in its order
+ * and notation, with scalar loops and no blocking or fusion:
  *   - Section 3.2: Hash-State table, Eq. 1 (hit indicator), Eq. 2 (metadata
  *     word layout), Eq. 3 (packed mapping), Eq. 4 (reusable predicate);
- *   - Section 3.3 / Algorithm 1: the three passes per token;
- *   - Appendix B: Probe (Eq. 8-11), Algorithm 2 (UpdateState), CollectDead
- *     (Eq. 12), Algorithm 3 (life-cycle update), Algorithm 4 (MTP-aware step);
+ *   - Sections 3.3 and 3.5 (Algorithms 1-3): per token, each index is looked
+ *     up (Eq. 8-11) and a hit renews its slot; the misses get the smallest
+ *     reclaimable slots (Eq. 12) after as much ageing as needed, and each is
+ *     linked to the first reusable bucket of its chain;
+ *   - Section 3.6 (Algorithm 4): a request's tokens in order on one table,
+ *     then speculative invalidation;
  *   - Section 3.4 and Appendix D: Stage Two and the S1/S2/S3 assignments
  *     (Eq. 5, 6, 13, 14);
  *   - Appendix F: metadata decode chain (Eq. 16-18).
@@ -128,7 +131,7 @@ void avsg_ref_destroy(avsg_ref_state *st) {
 }
 
 /* ------------------------------------------------------------------ */
-/* primitives of Appendix B                                            */
+/* one request's table                                                 */
 /* ------------------------------------------------------------------ */
 typedef struct {
     const avsg_ref_state *st;
@@ -143,160 +146,177 @@ static int64_t stride_of(const avsg_ref_state *st, int32_t x) { /* Eq. 9, odd st
     return (int64_t)(((uint64_t)st->cfg.a2 * (uint64_t)(int64_t)x) % (uint64_t)st->S) | 1;
 }
 
-/* Probe (Eq. 8-11): hit indicator and the matching / last examined bucket. */
-static void probe(const table_view *t, int32_t x, int32_t *m_out, int64_t *h_out) {
+/* The lookup of one selected index (Eq. 8-11): walks x's chain of R+1
+ * buckets and stops at the first bucket whose slot field names a slot that
+ * caches x.  Returns the hit flag m; *h_out is the matching bucket on a hit,
+ * the last bucket examined on a miss.  Reads slot fields and ids only. */
+static int32_t find_index(const table_view *t, int32_t x, int64_t *h_out) {
     const avsg_ref_state *st = t->st;
+    const int64_t d = stride_of(st, x);
     int64_t h = initial_bucket(st, x);
-    int64_t d = stride_of(st, x);
-    int32_t m = 0;
+    int32_t hit = 0;
     for (int32_t r = 0; r <= st->cfg.retry; ++r) {
-        int64_t o = (int64_t)t->q[h] % st->S;     /* Eq. 10 */
-        m = (t->c[o] == x);
-        if (r < st->cfg.retry && !m) h = (h + d) % st->S; /* Eq. 11 */
+        if (r > 0) h = (h + d) % st->S;                 /* Eq. 11: only an unresolved probe moves on */
+        hit = (t->c[(int64_t)t->q[h] % st->S] == x);    /* Eq. 10 */
+        if (hit) break;
     }
-    *m_out = m;
     *h_out = h;
+    return hit;
 }
 
-/* All lifetimes decay by one (never below -1). */
-static void decay_all(table_view *t) {
+/* One unit of ageing for every slot, never below -1 (reading I4). */
+static void age_table(table_view *t) {
     for (int64_t j = 0; j < t->st->S; ++j) {
         int32_t l = field_life(t->q[j]);
-        if (l > -1) l -= 1;
-        t->q[j] = with_life(t->q[j], l);
+        t->q[j] = with_life(t->q[j], l > -1 ? l - 1 : -1);
     }
 }
 
-/* CollectDead (Eq. 12): slots with negative lifetime, increasing order. */
-static int64_t collect_dead(const table_view *t, int32_t *e) {
-    int64_t ne = 0;
+/* The reclaimable slots (Eq. 12): every slot whose lifetime is negative, in
+ * increasing slot order.  Returns how many there are. */
+static int64_t list_dead(const table_view *t, int32_t *dead) {
+    int64_t n = 0;
     for (int64_t j = 0; j < t->st->S; ++j)
-        if (field_life(t->q[j]) < 0) e[ne++] = (int32_t)j;
-    return ne;
+        if (field_life(t->q[j]) < 0) dead[n++] = (int32_t)j;
+    return n;
 }
 
-/* reusable(q_h) (Eq. 4): invalid mapping, inactive pointed slot, or a stored
- * fingerprint that no longer matches the slot's occupant. */
-static int reusable(const table_view *t, uint32_t qh) {
+/* Eq. 4: a bucket may take a new mapping when its own mapping is invalid,
+ * when the slot it names is inactive, or when its stored fingerprint is no
+ * longer that of the slot's occupant. */
+static int bucket_reusable(const table_view *t, uint32_t qh) {
     const avsg_ref_state *st = t->st;
-    int64_t o = field_slot(st, qh);
-    int valid = (field_invalid(qh) == 0);
-    int active = (field_life(t->q[o]) >= 0);
-    int fp_match = (field_phi(st, qh) == phi_of(st, t->c[o]));
-    return !valid || !active || !fp_match;
+    const int64_t o = field_slot(st, qh);
+    const int invalid = field_invalid(qh) != 0;
+    const int inactive = field_life(t->q[o]) < 0;
+    const int stale = field_phi(st, qh) != phi_of(st, t->c[o]);
+    return invalid || inactive || stale;
+}
+
+/* The install bucket of a missed index: the first reusable bucket among the
+ * R+1 of its chain (the chain of Eq. 9, 11), in *h_out.  Returns 0 when all
+ * R+1 buckets hold live mappings (the index is cached but not mapped). */
+static int find_install_bucket(const table_view *t, int32_t x, int64_t *h_out) {
+    const avsg_ref_state *st = t->st;
+    const int64_t d = stride_of(st, x);
+    int64_t h = initial_bucket(st, x);
+    for (int32_t r = 0; r <= st->cfg.retry; ++r) {
+        if (r > 0) h = (h + d) % st->S;
+        if (bucket_reusable(t, t->q[h])) {
+            *h_out = h;
+            return 1;
+        }
+    }
+    *h_out = h;
+    return 0;
 }
 
 typedef struct {
-    int32_t *m, *tt, *omiss, *e, *v;
-    int64_t *h, *hk;
-} scratch;
+    int32_t *pending;   /* [K] positions of the token's misses, increasing */
+    int32_t *dead;      /* [S] reclaimable slots */
+    int32_t *found;     /* [K] the miss found an install bucket */
+    int64_t *bucket;    /* [K] its install bucket */
+} token_scratch;
 
-/* UpdateState (Algorithm 2). */
-static void update_state(table_view *t, const int32_t *tt, const int32_t *omiss, int64_t n_g,
-                         scratch *w, avsg_ref_counters *stats) {
-    const avsg_ref_state *st = t->st;
-    const int32_t L = st->cfg.max_life;
-    /* reusable chains, evaluated on the table before this call's writes */
-    for (int64_t k = 0; k < n_g; ++k) {
-        int64_t h = initial_bucket(st, tt[k]);
-        int64_t d = stride_of(st, tt[k]);
-        int v = 0;
-        for (int32_t i = 0; i <= st->cfg.retry; ++i) {
-            v = reusable(t, t->q[h]);
-            if (i < st->cfg.retry && !v) h = (h + d) % st->S;
-        }
-        w->hk[k] = h;
-        w->v[k] = v;
-    }
-    /* every miss owns its allocated slot: id and lifetime L */
-    for (int64_t k = 0; k < n_g; ++k) {
-        t->c[omiss[k]] = tt[k];
-        t->q[omiss[k]] = with_life(t->q[omiss[k]], L);
-    }
-    /* mappings, in increasing miss rank: the last writer keeps the bucket */
-    for (int64_t k = 0; k < n_g; ++k) {
-        if (!w->v[k]) continue;
-        int64_t h = w->hk[k];
-        int32_t keep_life = field_life(t->q[h]);
-        t->q[h] = pack_word(st, keep_life, 0, phi_of(st, tt[k]), omiss[k]);
-    }
-    for (int64_t k = 0; k < n_g; ++k) {
-        if (!w->v[k]) stats->lost_exhausted++;
-        else if (field_slot(st, t->q[w->hk[k]]) != omiss[k]) stats->lost_collision++;
-    }
-}
-
-/* Algorithm 1 for token g of one request; appends its misses at list+listed. */
-static int64_t token_passes(table_view *t, int32_t g, const int32_t *x, int32_t *o,
-                            int32_t *miss_x, int32_t *miss_o, scratch *w, avsg_ref_counters *stats,
-                            int32_t *step_decays) {
+/* Token g of one request (Section 3.3 with the lifetime rules of Section 3.5;
+ * Algorithm 1, whose lifetime steps Algorithm 3 restates, and Algorithm 2 for
+ * the installs).  Writes the token's slots into o[K], its misses (index,
+ * slot), in increasing position, into miss_x / miss_o, and returns their
+ * number n_g. */
+static int64_t run_token(table_view *t, int32_t g, const int32_t *x, int32_t *o, int32_t *miss_x,
+                         int32_t *miss_o, token_scratch *w, avsg_ref_counters *stats,
+                         int32_t *step_decays) {
     const avsg_ref_state *st = t->st;
     const int32_t K = st->cfg.topk, L = st->cfg.max_life;
-    /* Pass 1 -- refresh */
-    if (g == 0) decay_all(t);
-    for (int32_t i = 0; i < K; ++i) probe(t, x[i], &w->m[i], &w->h[i]);
-    for (int32_t i = 0; i < K; ++i) {
-        if (!w->m[i]) continue;
-        int64_t om = (int64_t)t->q[w->h[i]] % st->S;   /* o^match = q_h.slot */
-        if (field_life(t->q[om]) < 0) stats->revivals++;
-        t->q[om] = with_life(t->q[om], L);
-        /* Pass 2 -- classify: o[m] = o^match */
-        o[i] = (int32_t)om;
-    }
+
+    /* the request's first token ages every slot once (global pre-decay) */
+    if (g == 0) age_table(t);
+
+    /* each index on its own: a hit renews its slot's lifetime to L.  The
+     * lookup reads slot fields and ids, the renewal writes a lifetime byte
+     * only (reading I5), so renewing before the next lookup changes nothing */
     int64_t n_g = 0;
-    for (int32_t i = 0; i < K; ++i) n_g += 1 - w->m[i];
+    for (int32_t i = 0; i < K; ++i) {
+        int64_t h;
+        if (find_index(t, x[i], &h)) {
+            const int64_t slot = field_slot(st, t->q[h]);
+            if (field_life(t->q[slot]) < 0) stats->revivals++;   /* reading I9 */
+            t->q[slot] = with_life(t->q[slot], L);
+            o[i] = (int32_t)slot;
+        } else {
+            w->pending[n_g++] = i;
+        }
+    }
     stats->hits += (uint64_t)(K - n_g);
     stats->misses += (uint64_t)n_g;
-    /* Pass 3 -- allocate */
-    int64_t ne = collect_dead(t, w->e);
-    while (ne < n_g) {
-        decay_all(t);
+    if (n_g == 0) return 0;   /* reading I11 */
+
+    /* enough reclaimable slots for the misses: further unit ageing of every
+     * slot until there are (Eq. 12) */
+    int64_t n_dead = list_dead(t, w->dead);
+    while (n_dead < n_g) {
+        age_table(t);
         (*step_decays)++;
         stats->alloc_decays++;
-        ne = collect_dead(t, w->e);
+        n_dead = list_dead(t, w->dead);
     }
-    int64_t k = 0;
-    for (int32_t i = 0; i < K; ++i)
-        if (!w->m[i]) w->tt[k++] = x[i];               /* t = x[not m] */
-    for (k = 0; k < n_g; ++k) w->omiss[k] = w->e[k];   /* o^miss = e[:n_g] */
-    update_state(t, w->tt, w->omiss, n_g, w, stats);
-    k = 0;
-    for (int32_t i = 0; i < K; ++i)
-        if (!w->m[i]) o[i] = w->omiss[k++];            /* o[not m] = o^miss */
-    for (k = 0; k < n_g; ++k) {
-        miss_x[k] = w->tt[k];
-        miss_o[k] = w->omiss[k];
+
+    /* every miss's install bucket is chosen on the table as it is before any
+     * of this token's writes (reading I6) */
+    for (int64_t k = 0; k < n_g; ++k)
+        w->found[k] = find_install_bucket(t, x[w->pending[k]], &w->bucket[k]);
+
+    /* the k-th miss (by position) takes the k-th smallest reclaimable slot
+     * (reading I10): the slot caches the index with lifetime L, and a found
+     * bucket is linked to it with the index's fingerprint (Eq. 3, keeping the
+     * bucket's own lifetime, reading I5).  A later miss linking the same bucket
+     * replaces an earlier one (reading I7). */
+    for (int64_t k = 0; k < n_g; ++k) {
+        const int32_t xk = x[w->pending[k]];
+        const int32_t slot = w->dead[k];
+        t->c[slot] = xk;
+        t->q[slot] = with_life(t->q[slot], L);
+        if (w->found[k]) {
+            const int64_t h = w->bucket[k];
+            t->q[h] = pack_word(st, field_life(t->q[h]), 0, phi_of(st, xk), slot);
+        }
+        o[w->pending[k]] = slot;
+        miss_x[k] = xk;
+        miss_o[k] = slot;
+    }
+    /* installs that did not stick: no reusable bucket, or a later miss took it */
+    for (int64_t k = 0; k < n_g; ++k) {
+        if (!w->found[k]) stats->lost_exhausted++;
+        else if (field_slot(st, t->q[w->bucket[k]]) != miss_o[k]) stats->lost_collision++;
     }
     return n_g;
 }
 
-/* Stage One for request r (the token loop of Algorithm 4). */
+/* Stage One for request r: its tokens in order on the shared table
+ * (Algorithm 4); the transfer list is the tokens' misses in order. */
 static void stage_one(avsg_ref_state *st, int32_t r, const int32_t *X, int32_t *O, int32_t *n,
                       int32_t *miss_x, int32_t *miss_o) {
     const int32_t K = st->cfg.topk, Nq = st->cfg.n_q;
     const int64_t S = st->S;
     table_view t = {st, st->c + (size_t)r * S, st->q + (size_t)r * S};
-    scratch w;
-    w.m = (int32_t *)malloc(sizeof(int32_t) * K);
-    w.tt = (int32_t *)malloc(sizeof(int32_t) * K);
-    w.omiss = (int32_t *)malloc(sizeof(int32_t) * K);
-    w.v = (int32_t *)malloc(sizeof(int32_t) * K);
-    w.e = (int32_t *)malloc(sizeof(int32_t) * S);
-    w.h = (int64_t *)malloc(sizeof(int64_t) * K);
-    w.hk = (int64_t *)malloc(sizeof(int64_t) * K);
+    token_scratch w;
+    w.pending = (int32_t *)malloc(sizeof(int32_t) * K);
+    w.dead = (int32_t *)malloc(sizeof(int32_t) * S);
+    w.found = (int32_t *)malloc(sizeof(int32_t) * K);
+    w.bucket = (int64_t *)malloc(sizeof(int64_t) * K);
     avsg_ref_counters *stats = &st->stats[r];
     int32_t step_decays = 0;
     int64_t listed = 0;
     const size_t lbase = (size_t)r * Nq * K;
     for (int32_t g = 0; g < Nq; ++g) {
         const size_t xo = ((size_t)r * Nq + g) * K;
-        int64_t n_g = token_passes(&t, g, X + xo, O + xo, miss_x + lbase + listed,
-                                   miss_o + lbase + listed, &w, stats, &step_decays);
+        const int64_t n_g = run_token(&t, g, X + xo, O + xo, miss_x + lbase + listed,
+                                      miss_o + lbase + listed, &w, stats, &step_decays);
         n[(size_t)r * Nq + g] = (int32_t)n_g;
         listed += n_g;
     }
     if (step_decays > stats->max_step_alloc_decays) stats->max_step_alloc_decays = step_decays;
-    free(w.m); free(w.tt); free(w.omiss); free(w.v); free(w.e); free(w.h); free(w.hk);
+    free(w.pending); free(w.dead); free(w.found); free(w.bucket);
 }
 
 /* Stage Two: copy every listed miss from its host row to its buffer slot. */
@@ -428,7 +448,7 @@ int64_t avsg_ref_phi(int32_t m, int64_t x) {
 void avsg_ref_probe(const avsg_ref_state *st, int32_t r, int32_t x, int32_t *hit, int32_t *h) {
     table_view t = {st, st->c + (size_t)r * st->S, st->q + (size_t)r * st->S};
     int64_t hh;
-    probe(&t, x, hit, &hh);
+    *hit = find_index(&t, x, &hh);
     *h = (int32_t)hh;
 }
 
