@@ -466,8 +466,8 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   int32_t* gc = p.table_c + static_cast<size_t>(r) * S;
   uint32_t* gq = p.table_q + static_cast<size_t>(r) * S;
   // stage-in: 16-byte loads of 4 entries, the loads of two blocks issued
-  // before their LDS stores.  The first token's decay of every lifetime
-  // (Pass 1 of Algorithm 1 at g = 0) is applied as the lifetimes come in.
+  // before their LDS stores.  The first token's decay of every lifetime (the
+  // global pre-decay of Algorithm 1) is applied as the lifetimes come in.
   if ((S & (4 * MT - 1)) == 0) {
     for (int b = tid; b < S / 4; b += 2 * MT) {
       const i32x4 c0 = reinterpret_cast<const i32x4*>(gc)[b];
@@ -527,8 +527,8 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
 
   __syncthreads();
 
-  // Pass 1 (refresh) of the first token, the decay of every lifetime by one,
-  // was applied by the stage-in
+  // the first token's global pre-decay (every lifetime down by one) was
+  // applied by the stage-in
   for (int g = 0; g < p.n_q; ++g) {
     const size_t row = static_cast<size_t>(r) * p.n_q + g;
     int32_t* og = p.slots_out + row * K;
@@ -589,7 +589,7 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
       if (found[u]) {
         if (slife[oo[u]] < 0) st_rev++;
         slife[oo[u]] = static_cast<int8_t>(L);   // refresh the hit slot
-        og[i] = oo[u];                           // Pass 2: o[m] = o^match
+        og[i] = oo[u];                           // a hit's output slot
         st_hits++;
       }
       if (p.hit_mask && act[u]) p.hit_mask[row * K + i] = found[u] ? 1 : 0;
@@ -756,7 +756,7 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
         const int k = u * MT + tid;
         sc[mo[u]] = mt[u];
         slife[mo[u]] = static_cast<int8_t>(L);
-        og[mp[u]] = mo[u];                                   // o[not m] = o^miss
+        og[mp[u]] = mo[u];                                   // a miss's output slot
         p.miss_list[lbase + k] = make_int2(mt[u], mo[u]);
         if (mv[u]) {
           const uint32_t bid = kBid | (static_cast<uint32_t>(g) << 24) |

@@ -8,7 +8,7 @@
 // of q (invalid | fingerprint | slot) and the lifetime byte -- so lifetime
 // updates and mapping installs never share an LDS word.
 //
-// The first token's decay of every lifetime (Pass 1 of Algorithm 1) is
+// The first token's decay of every lifetime (Algorithm 1's global pre-decay) is
 // applied to the lifetime bytes as they are staged in.  Per query token
 // (Algorithm 1; tokens run in order on the shared table, Algorithm 4):
 //   A  every index is probed by its own lane (Probe, Eq. 8-11; a lane's
