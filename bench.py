@@ -41,9 +41,10 @@ def parse():
     ap.add_argument("--config", default="batch64_mtp2",
                     choices=["tiny", "batch16", "batch64_mtp2", "imbalance", "stress",
                              "stress_mtp3"])
-    ap.add_argument("--gather", default="resident",
-                    choices=["balanced", "request", "position", "sdma", "none", "pipelined", "resident",
-                             "early"])
+    ap.add_argument("--gather", default="auto",
+                    choices=["auto", "balanced", "request", "position", "sdma", "none", "pipelined", "resident",
+                             "early"],
+                    help="Stage Two (auto: resident reuse from 8192 lookups per step, else the paper's S3)")
     ap.add_argument("--match", default="hash", choices=["hash", "dualptr"])
     ap.add_argument("--workers", type=int, default=0, help="gather workgroups (0 = one per CU)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -119,7 +120,7 @@ def main():
                    "position": A.AVSG_GATHER_POSITION,
                    "pipelined": A.AVSG_GATHER_PIPELINED,
                    "resident": A.AVSG_GATHER_RESIDENT,
-                   "early": A.AVSG_GATHER_EARLY}[args.gather]
+                   "early": A.AVSG_GATHER_EARLY, "auto": A.AVSG_GATHER_AUTO}[args.gather]
     match_mode = {"hash": A.AVSG_MATCH_HASH, "dualptr": A.AVSG_MATCH_DUALPTR}[args.match]
     spec = W.get_spec(args.config)
     if match_mode == A.AVSG_MATCH_DUALPTR:
@@ -151,6 +152,12 @@ def main():
 
     cfg = A.make_config(spec.batch, spec.topk, spec.n_q, spec.slots, row_bytes=spec.row_bytes,
                         gather_workers=args.workers, match_mode=match_mode, gather_mode=gather_mode)
+    # the transfer the library runs for this configuration (auto resolved)
+    gather_mode = A.avsg_resolve_config(cfg).gather_mode
+    gather_name = {A.AVSG_GATHER_BALANCED: "balanced", A.AVSG_GATHER_REQUEST: "request",
+                   A.AVSG_GATHER_SDMA: "sdma", A.AVSG_GATHER_NONE: "none", A.AVSG_GATHER_POSITION: "position",
+                   A.AVSG_GATHER_PIPELINED: "pipelined", A.AVSG_GATHER_RESIDENT: "resident",
+                   A.AVSG_GATHER_EARLY: "early"}[gather_mode]
     stream = torch.cuda.current_stream(dev)
     op = A.Operator(cfg, host_ptrs, wl.ctx, device=dev, stream=stream)
 
@@ -279,6 +286,8 @@ def main():
         ref_host = ref_after["host_bytes"] - ref_before["host_bytes"]
         ref_gsec = float(np.sum(ref_gather_ms)) * 1e-3
         ref_gbps = ref_host / ref_gsec / 1e9 if ref_gsec > 0 else 0.0
+        s3_block = (_traffic_block(TRAFFIC_SUMMARY_S3)
+                    if (args.config, args.workers, args.match) == ("batch64_mtp2", 0, "hash") else None)
         reference = {"gather": "balanced", "value": round(wall_ref / args.steps * 1e6, 2),
                      "unit": "us/step",
                      "what": "the paper's Stage Two (S3, Eq. 6): every miss copied from the host",
@@ -289,8 +298,14 @@ def main():
                                   "frac": round(ref_gbps / PCIE_GEN5_X16_GBPS, 4),
                                   "frac_of_hipmemcpy_peak": round(ref_gbps / memcpy_peak, 4) if memcpy_peak else None,
                                   "algorithmic_bytes_per_launch": round(ref_host / args.steps),
+                                  "traffic": None, "traffic_source": None,
                                   "what": "every miss's row bytes over the host link / the S3 kernel's "
                                           "average duration (HIP events on the step stream)"}}
+        if s3_block:
+            reference["roofline"]["traffic"] = s3_block["traffic_bytes_per_launch"]
+            reference["roofline"]["traffic_source"] = TRAFFIC_SUMMARY_S3
+            reference["roofline"]["traffic_over_algorithmic"] = round(
+                s3_block["traffic_bytes_per_launch"] / s3_block["algorithmic_traffic_bytes_per_launch"], 3)
 
     K = args.steps
     us_per_step = wall / K * 1e6
@@ -336,12 +351,13 @@ def main():
     if not args.no_cpu_baseline and match_mode == A.AVSG_MATCH_HASH:
         cpu = cpu_baseline(spec, wl, X_host, N_host, host_ptrs, args, gather_mode)
 
-    traffic = measured_traffic(args)
+    traffic = measured_traffic(args, gather_name)
     configs = None
     cold = None
-    if not args.no_configs and args.config == "batch64_mtp2" and args.gather == "resident" \
+    if not args.no_configs and args.config == "batch64_mtp2" and gather_name == "resident" \
             and args.match == "hash":
         configs = {"batch64_mtp2": {
+            "transfer": gather_name,
             "us_per_step": round(us_per_step, 2),
             "match_us_median": round(float(np.median(match_ms)) * 1e3, 2),
             "stage_two_us_median": round(float(np.median(gather_ms)) * 1e3, 2),
@@ -376,7 +392,8 @@ def main():
         "config": {
             "workload": spec.name, "batch": spec.batch, "topk": spec.topk, "slots": spec.slots,
             "n_q": spec.n_q, "context": int(wl.ctx.max()), "row_bytes": list(spec.row_bytes),
-            "retention": spec.retention, "match": args.match, "gather": args.gather,
+            "retention": spec.retention, "match": args.match,
+            "gather": gather_name if args.gather == gather_name else f"{args.gather} ({gather_name})",
             "steps_timed": f"{args.warmup}..{T - 1}",
         },
         "hit_rate": round(hits / max(1, lookups), 5),
@@ -413,7 +430,7 @@ def main():
             "bound": "pcie",
             "kernel": {"balanced": "gather_balanced_kernel", "resident": "gather_resident_kernel",
                        "pipelined": "step_pipelined_kernel",
-                       "early": "step_early_kernel"}.get(args.gather, args.gather),
+                       "early": "step_early_kernel"}.get(gather_name, gather_name),
             "achieved": round(gather_gbps, 3),
             "peak": PCIE_GEN5_X16_GBPS,
             "unit": "GB/s",
@@ -509,8 +526,10 @@ def _measure(spec, gather_mode, X, N, ptrs, ctx, warm, timed, dev):
 def config_block(memcpy_peak, dev, warm=8, timed=32, with_cpu=True):
     """The other benchmark workloads (tiny, batch16, imbalance, stress) at full
     size, each from a cold start: `warm` untimed steps, then `timed` steps under
-    the default resident-reuse Stage Two and under the paper's S3 (and, on the
-    imbalance mix, the request-level S1 it is compared with).  Per workload:
+    the default Stage Two (AVSG_GATHER_AUTO: resident reuse from 8192 lookups per
+    step, else S3; `transfer` names it), under the paper's S3, under resident
+    reuse where that is not the default, and on the imbalance mix under the
+    request-level S1 it is compared with.  Per workload:
     µs per step (wall time between two synchronizations, no per-kernel events),
     matching and Stage Two kernel medians (HIP events), host-link payload GB/s
     of the Stage Two kernels and its fractions of the measured hipMemcpy H2D
@@ -532,7 +551,13 @@ def config_block(memcpy_peak, dev, warm=8, timed=32, with_cpu=True):
         entry = {"batch": spec.batch, "topk": spec.topk, "slots": spec.slots, "n_q": spec.n_q,
                  "context": int(wl.ctx.max()), "row_bytes": list(spec.row_bytes),
                  "steps_timed": f"{warm}..{warm + timed - 1}"}
-        modes = [("resident", A.AVSG_GATHER_RESIDENT), ("s3", A.AVSG_GATHER_BALANCED)]
+        auto = A.avsg_resolve_config(A.make_config(spec.batch, spec.topk, spec.n_q, spec.slots,
+                                                   row_bytes=spec.row_bytes,
+                                                   gather_mode=A.AVSG_GATHER_AUTO)).gather_mode
+        entry["transfer"] = "resident" if auto == A.AVSG_GATHER_RESIDENT else "s3"
+        modes = [("default", A.AVSG_GATHER_AUTO), ("s3", A.AVSG_GATHER_BALANCED)]
+        if auto != A.AVSG_GATHER_RESIDENT:
+            modes.append(("resident", A.AVSG_GATHER_RESIDENT))
         if name == "imbalance":
             modes.append(("s1", A.AVSG_GATHER_REQUEST))
         try:
@@ -541,14 +566,14 @@ def config_block(memcpy_peak, dev, warm=8, timed=32, with_cpu=True):
                 d = m["delta"]
                 gsec = float(np.sum(m["stage_two_ms"])) * 1e-3
                 gbps = d["host_bytes"] / gsec / 1e9 if gsec > 0 and d["host_bytes"] else 0.0
-                pre = "" if label == "resident" else label + "_"
+                pre = "" if label == "default" else label + "_"
                 entry[pre + "us_per_step"] = round(m["wall"] / timed * 1e6, 2)
                 entry[pre + "match_us_median"] = round(float(np.median(m["match_ms"])) * 1e3, 2)
                 entry[pre + "stage_two_us_median"] = round(float(np.median(m["stage_two_ms"])) * 1e3, 2)
                 entry[pre + "h2d_gbps_gather_kernel"] = round(gbps, 3)
                 entry[pre + "frac_of_hipmemcpy_peak"] = round(gbps / memcpy_peak, 4) if memcpy_peak else None
                 entry[pre + "frac_of_pcie_gen5_x16"] = round(gbps / PCIE_GEN5_X16_GBPS, 4)
-                if label == "resident":
+                if label == "default":
                     entry["hit_rate"] = round(d["hits"] / max(1, d["lookups"]), 5)
                     entry["misses_per_step"] = round(d["misses"] / timed, 1)
                     entry["host_rows_per_step"] = round(d["host_bytes"] / row_total / timed, 1)
@@ -1154,19 +1179,26 @@ def config_table(out_path):
 GATHER_SOURCES = ("paper_2609_37538_amd/csrc/gather.hip", "paper_2609_37538_amd/csrc/gather_body.h",
                   "paper_2609_37538_amd/csrc/match_body.h", "paper_2609_37538_amd/csrc/avsg_internal.h")
 TRAFFIC_SUMMARY = "profiles/gather_resident_traffic_batch64_mtp2.md"
+TRAFFIC_SUMMARY_S3 = "profiles/gather_balanced_traffic_batch64_mtp2.md"
 
 
-def measured_traffic(args):
+def measured_traffic(args, gather_name):
     """HBM + host-link bytes per gather launch from the committed rocprofv3
     counter summary (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0, copy-calibrated), or
     None when this run is not the profiled workload and transfer or the gather
     source has changed since the counters were taken.  The counters were
     taken over the steady-state launches of one run of the workload; a step's
     traffic changes little from step to step (the summary names its sample)."""
-    import re
-    if (args.config, args.workers, args.gather, args.match) != ("batch64_mtp2", 0, "resident", "hash"):
+    if (args.config, args.workers, gather_name, args.match) != ("batch64_mtp2", 0, "resident", "hash"):
         return None
-    path = os.path.join(ROOT, TRAFFIC_SUMMARY)
+    return _traffic_block(TRAFFIC_SUMMARY)
+
+
+def _traffic_block(summary):
+    """The JSON block of a committed counter summary, or None when the gather
+    and matching code has changed since it was taken."""
+    import re
+    path = os.path.join(ROOT, summary)
     if not os.path.exists(path):
         return None
     m = re.search(r"```json\n(.*?)\n```", open(path).read(), re.S)

@@ -92,6 +92,13 @@ typedef int32_t avsg_status;
                                    copies the rest as AVSG_GATHER_RESIDENT does.  Slots, counts, tables and
                                    buffer contents are identical to AVSG_GATHER_BALANCED. */
 
+#define AVSG_GATHER_AUTO 8      /* AVSG_GATHER_RESIDENT when a step looks up at least 8192 indices
+                                   (B*N_q*K) with hash matching and the resident plan fits beside the
+                                   table, else AVSG_GATHER_BALANCED: below that size the plan costs more
+                                   than the host rows it saves (measured crossover between 4096 and 8192
+                                   lookups per step).  Resolved once, at create; avsg_resolve_config
+                                   tells which. */
+
 #define AVSG_MAX_STREAMS 2
 
 /* Bytes of the library's own static device array behind avsg_step_static (one
@@ -160,6 +167,11 @@ typedef struct avsg_handle avsg_handle;
  * distinct primes; the retry budget R; the lifetime L of an 8-bit field,
  * Section 3.5) and the capacity rule S >= N_q * K of Eq. 7. */
 avsg_status avsg_check_config(const avsg_config *cfg);
+
+/* The configuration a handle of cfg runs: cfg with AVSG_GATHER_AUTO replaced by
+ * the transfer it selects (a call of this library's own).  Returns the status
+ * avsg_check_config gives cfg; *out is written only on AVSG_OK. */
+avsg_status avsg_resolve_config(const avsg_config *cfg, avsg_config *out);
 
 /* A call of this library's own with no counterpart in the paper (which keeps
  * the table in each core's on-chip buffer): size in bytes of the device

@@ -38,6 +38,7 @@ AVSG_GATHER_POSITION = 4
 AVSG_GATHER_PIPELINED = 5
 AVSG_GATHER_RESIDENT = 6
 AVSG_GATHER_EARLY = 7
+AVSG_GATHER_AUTO = 8
 AVSG_MAX_STREAMS = 2
 
 A1_DEFAULT = 2654435761
@@ -107,6 +108,8 @@ def load(share_torch_runtime: bool = True):
     i32, i64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     lib.avsg_check_config.restype = i32
     lib.avsg_check_config.argtypes = [ctypes.POINTER(AvsgConfig)]
+    lib.avsg_resolve_config.restype = i32
+    lib.avsg_resolve_config.argtypes = [ctypes.POINTER(AvsgConfig), ctypes.POINTER(AvsgConfig)]
     lib.avsg_workspace_bytes.restype = sz
     lib.avsg_workspace_bytes.argtypes = [ctypes.POINTER(AvsgConfig)]
     lib.avsg_create.restype = i32
@@ -194,6 +197,12 @@ def make_config(batch, topk, n_q, slots, retry=3, max_life=16, a1=A1_DEFAULT, a2
 # ---------------------------------------------------------------------------
 def avsg_check_config(cfg: AvsgConfig) -> int:
     return int(load().avsg_check_config(ctypes.byref(cfg)))
+
+
+def avsg_resolve_config(cfg: AvsgConfig) -> AvsgConfig:
+    out = AvsgConfig()
+    _check(load().avsg_resolve_config(ctypes.byref(cfg), ctypes.byref(out)), "avsg_resolve_config")
+    return out
 
 
 def avsg_workspace_bytes(cfg: AvsgConfig) -> int:

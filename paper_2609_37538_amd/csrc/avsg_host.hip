@@ -185,7 +185,7 @@ int log2_exact(int32_t s) {
   return m;
 }
 
-avsg_status check_config(const avsg_config* c, std::string* why) {
+avsg_status check_resolved(const avsg_config* c, std::string* why) {
   auto fail = [&](avsg_status s, const char* msg) {
     if (why) *why = msg;
     return s;
@@ -236,6 +236,35 @@ avsg_status check_config(const avsg_config* c, std::string* why) {
       return fail(AVSG_E_CAPACITY, "early fetch: the list map of 1.25*n_q*topk index words does not fit in LDS");
   }
   return AVSG_OK;
+}
+
+// AVSG_GATHER_AUTO: resident reuse when a step looks up at least this many
+// indices (B * N_q * K) and its plan fits beside the table, else the paper's
+// S3.  Measured crossover (µs per step, S3 / resident): 4096 lookups 33.5 / 35.4
+// (B = 2, K = 2048) and 40.6 / 43.8 (B = 1, two tokens); 8192 lookups 48.6 /
+// 44.7 (B = 4) and 55.1 / 52.8 (B = 2, two tokens).
+constexpr long long kAutoResidentLookups = 8192;
+
+avsg_config resolved(const avsg_config& c) {
+  avsg_config r = c;
+  if (c.gather_mode != AVSG_GATHER_AUTO) return r;
+  r.gather_mode = AVSG_GATHER_BALANCED;
+  const long long lookups = static_cast<long long>(c.batch) * c.n_q * c.topk;
+  if (c.match_mode == AVSG_MATCH_HASH && lookups >= kAutoResidentLookups) {
+    avsg_config t = c;
+    t.gather_mode = AVSG_GATHER_RESIDENT;
+    if (check_resolved(&t, nullptr) == AVSG_OK) r.gather_mode = AVSG_GATHER_RESIDENT;
+  }
+  return r;
+}
+
+avsg_status check_config(const avsg_config* c, std::string* why) {
+  if (!c) {
+    if (why) *why = "null config";
+    return AVSG_E_INVAL;
+  }
+  const avsg_config r = resolved(*c);
+  return check_resolved(&r, why);
 }
 
 void set_err(avsg_handle* h, const char* fmt, ...) {
@@ -335,7 +364,15 @@ avsg_status avsg_check_config(const avsg_config* cfg) { return check_config(cfg,
 
 size_t avsg_workspace_bytes(const avsg_config* cfg) {
   if (check_config(cfg, nullptr) != AVSG_OK) return 0;
-  return layout_of(*cfg).total;
+  return layout_of(resolved(*cfg)).total;
+}
+
+avsg_status avsg_resolve_config(const avsg_config* cfg, avsg_config* out) {
+  if (!out) return AVSG_E_INVAL;
+  const avsg_status st = check_config(cfg, nullptr);
+  if (st != AVSG_OK) return st;
+  *out = resolved(*cfg);
+  return AVSG_OK;
 }
 
 const char* avsg_strerror(avsg_status s) {
@@ -368,7 +405,7 @@ avsg_status avsg_create(const avsg_config* cfg, const void* const* host_rows,
     std::fprintf(stderr, "avsg_create: %s\n", why.c_str());
     return st;
   }
-  const avsg_config c = *cfg;
+  const avsg_config c = resolved(*cfg);
   if (!host_rows || !rows_per_request || !d_workspace || !d_buffers) return AVSG_E_INVAL;
   const Layout L = layout_of(c);
   if (workspace_bytes < L.total) return AVSG_E_INVAL;
@@ -1073,7 +1110,7 @@ extern "C" avsg_status avsg_step_static(const avsg_config* cfg, const void* cons
                                         void* stream) {
   avsg_status st = check_config(cfg, nullptr);
   if (st != AVSG_OK) return st;
-  const avsg_config& c = *cfg;
+  const avsg_config c = resolved(*cfg);
   if (c.validate || c.gather_mode == AVSG_GATHER_SDMA || c.gather_mode == AVSG_GATHER_PIPELINED ||
       c.gather_mode == AVSG_GATHER_EARLY) {
     std::fprintf(stderr, "avsg_step_static: validate mode and the copy-engine, pipelined and early-fetch "

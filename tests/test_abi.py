@@ -98,7 +98,7 @@ def test_check_config_statuses(lib):
     assert chk(batch=1, topk=128, n_q=40, slots=16384, gather_mode=A.AVSG_GATHER_RESIDENT) == \
         A.AVSG_E_CAPACITY
     assert chk(batch=1, topk=128, n_q=110, slots=16384) == A.AVSG_OK
-    assert chk(gather_mode=8) == A.AVSG_E_INVAL
+    assert chk(gather_mode=9) == A.AVSG_E_INVAL
     # early fetch: hash matching only; knobs 0 / -1
     assert chk(gather_mode=A.AVSG_GATHER_EARLY) == A.AVSG_OK
     assert chk(gather_mode=A.AVSG_GATHER_EARLY, early_staging_rows=-1, early_direct=-1) == A.AVSG_OK
@@ -125,8 +125,9 @@ def test_workspace_size_and_validation(lib):
     assert ws(topk=8192, n_q=1, slots=8192) == 0   # beyond 4096 indices per token
     assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=1, slots=2048) > 0
     assert ws(match_mode=A.AVSG_MATCH_DUALPTR, n_q=2) == 0
-    assert ws(gather_mode=8) == 0
-    # the resident-reuse plan adds three transfer lists, fan slots, bids, counts and claims
+    assert ws(gather_mode=9) == 0
+    assert ws(gather_mode=A.AVSG_GATHER_AUTO) == ws(gather_mode=A.AVSG_GATHER_RESIDENT)
+    # the resident-reuse plan adds three transfer lists, fan slots, counts and claims
     B, nq, K = 64, 2, 2048
     assert ws(gather_mode=A.AVSG_GATHER_RESIDENT) >= ws() + (3 * 8 + 4) * B * nq * K + 12 * B
     assert ws(gather_mode=A.AVSG_GATHER_POSITION) > ws() - 1
@@ -138,3 +139,32 @@ def test_workspace_size_and_validation(lib):
     assert ws(n_q=1, slots=2, topk=1, batch=1, row_bytes=(4,)) > 0
     assert ws(n_q=127, topk=64, slots=8192, row_bytes=(4,)) > 0
     assert ws(n_q=128, topk=64, slots=8192, row_bytes=(4,)) == 0
+
+
+def test_auto_transfer_resolution(lib):
+    """AVSG_GATHER_AUTO: resident reuse from 8192 lookups per step (B * N_q * K)
+    with hash matching when its plan fits, else the paper's S3; the workspace
+    is the chosen transfer's."""
+    def res(**kw):
+        base = dict(row_bytes=(1152,), gather_mode=A.AVSG_GATHER_AUTO)
+        base.update(kw)
+        cfg = A.make_config(**base)
+        return A.avsg_resolve_config(cfg).gather_mode, A.avsg_workspace_bytes(cfg)
+    def ws_of(mode, **kw):
+        return A.avsg_workspace_bytes(A.make_config(row_bytes=(1152,), gather_mode=mode, **kw))
+    tiny = dict(batch=1, topk=256, n_q=1, slots=1024)
+    assert res(**tiny) == (A.AVSG_GATHER_BALANCED, ws_of(A.AVSG_GATHER_BALANCED, **tiny))
+    b16 = dict(batch=16, topk=2048, n_q=1, slots=8192)
+    assert res(**b16) == (A.AVSG_GATHER_RESIDENT, ws_of(A.AVSG_GATHER_RESIDENT, **b16))
+    assert res(batch=2, topk=2048, n_q=1, slots=8192)[0] == A.AVSG_GATHER_BALANCED    # 4096 lookups
+    assert res(batch=2, topk=2048, n_q=2, slots=8192)[0] == A.AVSG_GATHER_RESIDENT    # 8192 lookups
+    assert res(batch=4, topk=2048, n_q=1, slots=2048,
+               match_mode=A.AVSG_MATCH_DUALPTR)[0] == A.AVSG_GATHER_BALANCED
+    # the resident plan would not fit beside this table: S3
+    assert res(batch=1, topk=128, n_q=64, slots=16384)[0] == A.AVSG_GATHER_BALANCED
+    # errors are those of the configuration itself
+    assert A.avsg_check_config(A.make_config(batch=0, topk=64, n_q=1, slots=256,
+                                             gather_mode=A.AVSG_GATHER_AUTO)) == A.AVSG_E_INVAL
+    assert A.avsg_check_config(A.make_config(batch=1, topk=64, n_q=1, slots=96,
+                                             gather_mode=A.AVSG_GATHER_AUTO)) == A.AVSG_E_NOTPOW2
+    assert A.avsg_check_config(A.make_config(batch=1, topk=64, n_q=1, slots=256, gather_mode=9)) == A.AVSG_E_INVAL

@@ -129,6 +129,20 @@ def test_gather_modes_match_balanced(mode):
     run_parity(spec, table_every=0, buffers_every=4, gather_mode=mode)
 
 
+@pytest.mark.parametrize("batch,n_q", [(2, 1), (2, 2)], ids=["s3_side", "resident_side"])
+def test_auto_transfer_parity(batch, n_q):
+    """AVSG_GATHER_AUTO on both sides of its threshold (4096 and 8192 lookups
+    per step): slots, tables, counters and buffers equal the oracle's."""
+    from paper_2609_37538_amd import avsg as A
+    spec = W.custom_spec(name=f"auto_{batch}_{n_q}", batch=batch, topk=2048, slots=8192, n_q=n_q, steps=10,
+                         ctx=60000, row_bytes=(1152, 132))
+    cfg = A.make_config(batch, 2048, n_q, 8192, row_bytes=(1152, 132), gather_mode=A.AVSG_GATHER_AUTO)
+    want = A.AVSG_GATHER_RESIDENT if batch * n_q * 2048 >= 8192 else A.AVSG_GATHER_BALANCED
+    assert A.avsg_resolve_config(cfg).gather_mode == want
+    ref, got = run_parity(spec, table_every=2, buffers_every=2, gather_mode=A.AVSG_GATHER_AUTO)
+    assert (got["resident_rows"] + got["duplicate_rows"] > 0) == (want == A.AVSG_GATHER_RESIDENT)
+
+
 def test_lds_capacity_error():
     """A table larger than one workgroup's LDS is refused at create time."""
     from paper_2609_37538_amd import avsg as A

@@ -53,10 +53,15 @@ def test_traffic_summary_block_is_complete():
     assert b["kernel"] == "gather_resident_kernel" and b["workload"] == "batch64_mtp2"
 
 
-@pytest.mark.parametrize("change", [dict(config="batch16"), dict(steps=100), dict(warmup=4),
-                                    dict(workers=64), dict(gather="balanced"), dict(match="dualptr")])
+@pytest.mark.parametrize("change", [dict(config="batch16"), dict(workers=64), dict(gather="balanced"),
+                                    dict(match="dualptr")])
 def test_traffic_only_for_the_profiled_run(change):
-    assert _bench().measured_traffic(_default_args(**change)) is None
+    """Traffic is reported for the profiled workload and transfer only (the
+    step counts do not matter: a launch's traffic changes little from step to
+    step).  The current summary matches the current code."""
+    args = _default_args(**change)
+    assert _bench().measured_traffic(args, args.gather) is None
+    assert _bench().measured_traffic(_default_args(steps=20, warmup=5), "resident") is not None
 
 
 def test_traffic_follows_the_source_hash(tmp_path, monkeypatch):
@@ -71,7 +76,7 @@ def test_traffic_follows_the_source_hash(tmp_path, monkeypatch):
         dst.parent.mkdir(parents=True, exist_ok=True)
         dst.write_bytes(open(os.path.join(ROOT, p), "rb").read())
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
-    assert bench.measured_traffic(_default_args()) is None
+    assert bench.measured_traffic(_default_args(), "resident") is None
 
 
 def _imports(path):
