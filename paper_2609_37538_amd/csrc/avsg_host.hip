@@ -39,6 +39,7 @@ struct avsg_handle {
   int32_t* plan_counts = nullptr;  // [B][3]
   int32_t* plan_claim = nullptr;
   int plan_words = 0;
+  int plan_list_off = 0;   // LDS offset of the transfer list the plan reads
   // early-fetch transfer (AVSG_GATHER_EARLY)
   int32_t* early_x = nullptr;
   int4* early_pos = nullptr;
@@ -305,6 +306,7 @@ void bind_workspace(avsg_handle* h, unsigned char* ws, const Layout& L) {
     h->plan_counts = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan);
     h->plan_claim = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan + up(static_cast<size_t>(B) * 12));
     h->plan_words = plan_map_words(c.slots, c.topk, c.n_q);
+    h->plan_list_off = static_cast<int>(plan_list_offset(c.slots, c.topk, c.n_q));
   }
   if (c.gather_mode == AVSG_GATHER_EARLY) {
     const std::array<size_t, 9> o = early_sections(c);
@@ -639,6 +641,7 @@ static avsg_status enqueue_step(avsg_handle* h, const int32_t* d_topk, const int
     p.slots_out = d_slots; p.miss_counts = d_miss_counts; p.miss_list = h->miss_list;
     p.stats = h->stats; p.hit_mask = nullptr;
     p.plan_words = h->plan_words;
+    p.plan_list_off = h->plan_list_off;
     p.host_list = h->host_list; p.host_fan = h->host_fan;
     p.res_list = h->res_list; p.rep_list = h->rep_list;
     p.plan_counts = h->plan_counts; p.plan_claim = h->plan_claim;
@@ -677,6 +680,7 @@ static avsg_status enqueue_step(avsg_handle* h, const int32_t* d_topk, const int
     p.hit_mask = c.gather_mode == AVSG_GATHER_POSITION ? h->hit_mask : nullptr;
     if (c.gather_mode == AVSG_GATHER_RESIDENT) {
       p.plan_words = h->plan_words;
+      p.plan_list_off = h->plan_list_off;
       p.host_list = h->host_list;
       p.host_fan = h->host_fan;
       p.res_list = h->res_list;

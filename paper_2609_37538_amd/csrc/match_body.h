@@ -13,7 +13,7 @@ namespace {
 constexpr int kMaxWaves = kMatchThreads / 64;
 constexpr int kMaxIPT = 4;                 // up to 4 NT indices per token
 constexpr int kMaxSPT = 16;                // up to 16 NT slots
-constexpr int kScratchInts = 2 * kMaxIPT * kMaxWaves + kMaxWaves + 4 + 8;
+constexpr int kScratchInts = 2 * kMaxIPT * kMaxWaves + kMaxWaves + 4;
 constexpr uint32_t kBid = 0x80000000u;     // marks a bucket written by an install bid
 
 // 16-byte vectors as clang vector types (kept in registers)
@@ -46,6 +46,22 @@ __device__ __forceinline__ int wave_inclusive_scan(int v, int /*lane*/) {
 // Sum over the 64 lanes of a wave, in every lane (every lane active).
 __device__ __forceinline__ int wave_sum(int v) {
   return __builtin_amdgcn_readlane(wave_inclusive_scan(v, 0), 63);
+}
+// Index of this thread's wave, held in a scalar register.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6); }
+// Per-wave values cnt[0..nw) (nw <= 64) as seen by wave `wave`: the sum over
+// the waves before it and over all of them.  Lane w reads cnt[w] and a wave
+// scan adds them up, so the sums take one LDS read (every lane active).
+struct WavePrefix {
+  int before, total;
+};
+__device__ __forceinline__ WavePrefix wave_prefix(const int* cnt, int nw, int wave) {
+  const int lane = lane_id();
+  const int incl = wave_inclusive_scan(lane < nw ? cnt[lane] : 0, lane);
+  WavePrefix r;
+  r.total = __builtin_amdgcn_readlane(incl, 63);
+  r.before = wave > 0 ? __builtin_amdgcn_readlane(incl, wave - 1) : 0;
+  return r;
 }
 
 __host__ __device__ constexpr size_t align16(size_t v) { return (v + 15) & ~size_t(15); }
@@ -160,41 +176,62 @@ constexpr int kPlanMiscWords = 6 * kMaxWaves + 4;
 // Words of the plan's reservation bitmap for S slots, padded to a multiple of
 // four so that the map behind it starts 16-byte aligned.
 __host__ __device__ constexpr int plan_bitmap_words(int S) { return (((S + 31) >> 5) + 3) & ~3; }
-constexpr uint32_t kPlanResident = 0x80000000u;   // map word names a slot outside this step's reservations
+// All LDS words of the plan past c[]: the reservation bitmap, P map words, P
+// fan words and the counters.
+__host__ __device__ constexpr size_t plan_state_words(int S, int P) {
+  return static_cast<size_t>(plan_bitmap_words(S)) + 2 * static_cast<size_t>(P) + kPlanMiscWords;
+}
+// A map word, from the high bits down; atomicMax on words of one index
+// orders them by (resident, slot).
+constexpr uint32_t kPlanResident = 0x80000000u;   // names a slot outside this step's reservations
 constexpr uint32_t kPlanEarly = 0x40000000u;      // the word's index was fetched before Stage One
 constexpr uint32_t kPlanTag = 0x3F000000u;        // six bits of a second hash of the word's index
-constexpr uint32_t kPlanSlot = 0x00FFFFFFu;       // slot + 1
+constexpr uint32_t kPlanSlot = 0x00FFFFFEu;       // slot + 1, shifted up by one
+constexpr uint32_t kPlanDisp = 0x00000001u;       // another index whose home is this word sits further on
+__device__ __forceinline__ uint32_t plan_val(int slot) { return (static_cast<uint32_t>(slot) + 1u) << 1; }
+__device__ __forceinline__ int plan_slot(uint32_t w) { return static_cast<int>((w & kPlanSlot) >> 1) - 1; }
 
-// Home word of index x in the plan's map of P words (multiplicative hash).
-__device__ __forceinline__ uint32_t plan_home(int32_t x, uint32_t P) {
-  return static_cast<uint32_t>((static_cast<uint64_t>(static_cast<uint32_t>(x) * 0x9E3779B1u) * P) >> 32);
-}
-// Tag bits of index x kept in its map word: a word whose tag differs is
-// passed over without reading the slot it names.
-__device__ __forceinline__ uint32_t plan_tag(int32_t x) {
-  return ((static_cast<uint32_t>(x) * 0x85EBCA77u) >> 26) << 24;
-}
+// Home word and tag of index x in the plan's map of P words, from one
+// multiplicative hash h = x * 0x9E3779B1: with P = 2^p the home is the top p
+// bits of h and the tag the six bits below them; otherwise the home is
+// floor(h * P / 2^32) and the tag bits 8..13 of h.  The tag is kept in the
+// map word so that a probe passes over most foreign words without reading the
+// slot they name.
+struct PlanHash {
+  uint32_t P;
+  int shift;   // 32 - p when P = 2^p, else 0
+  __device__ __forceinline__ explicit PlanHash(uint32_t words) : P(words), shift(0) {
+    if ((words & (words - 1u)) == 0u) shift = 32 - (31 - __builtin_clz(words));
+  }
+  __device__ __forceinline__ uint32_t hash(int32_t x) const { return static_cast<uint32_t>(x) * 0x9E3779B1u; }
+  __device__ __forceinline__ uint32_t home(uint32_t h) const { return shift ? h >> shift : __umulhi(h, P); }
+  __device__ __forceinline__ uint32_t tag(uint32_t h) const {
+    return (shift ? (h >> (shift - 6)) & 0x3Fu : (h >> 8) & 0x3Fu) << 24;
+  }
+  __device__ __forceinline__ uint32_t next(uint32_t h) const { return h + 1u == P ? 0u : h + 1u; }
+};
 
 // Position of index x's word in the map (its word in *word), or -1.
-__device__ __forceinline__ int plan_lookup(const uint32_t* smp, const int32_t* sc, uint32_t P,
+__device__ __forceinline__ int plan_lookup(const uint32_t* smp, const int32_t* sc, const PlanHash& ph,
                                            int32_t x, uint32_t* word) {
-  uint32_t h = plan_home(x, P);
-  const uint32_t tag = plan_tag(x);
-  for (uint32_t t = 0; t < P; ++t) {
+  const uint32_t hx = ph.hash(x), tag = ph.tag(hx);
+  uint32_t h = ph.home(hx);
+  for (uint32_t t = 0; t < ph.P; ++t) {
     const uint32_t w = smp[h];
     if (w == 0u) break;
-    if ((w & kPlanTag) == tag && sc[(w & kPlanSlot) - 1u] == x) {
+    if ((w & kPlanTag) == tag && sc[plan_slot(w)] == x) {
       *word = w;
       return static_cast<int>(h);
     }
-    h = (h + 1u == P) ? 0u : h + 1u;
+    h = ph.next(h);
   }
   return -1;
 }
 
 // Stage Two plan of the resident-reuse gather, after the step's table write
-// back (every LDS array but c[] is free).  Each of the step's listed misses
-// (index x, slot o) becomes
+// back (every LDS array but c[] and the slot list is free, and the write back
+// has cleared the plan's words).  Each of the step's listed misses (index x,
+// slot o) becomes
 //   a resident copy from the largest slot outside this step's reservations
 //   that still caches x below the verified length (its row arrived in an
 //   earlier step and cannot have changed), or else
@@ -202,20 +239,26 @@ __device__ __forceinline__ int plan_lookup(const uint32_t* smp, const int32_t* s
 //   not o (a later token missed x again after its install was lost), or else
 //   a host copy.
 // A host entry also writes its row to the largest repeat destination of its
-// index (its fan slot), so with two tokens per step no repeat is left for a
-// later copy.  The lists keep transfer-list order.  LDS: a map of P words,
+// index (its fan slot: the second largest slot reserved for the index), so
+// with two tokens per step no repeat is left for a later copy.  The lists keep transfer-list order.  LDS: a map of P words,
 // open addressing with linear probing keyed by the index a word names through
 // c[]; a word is (resident bit | early bit | tag | slot + 1), 0 = free, and
-// atomicMax makes every choice deterministic; beside it S fan words, one per
-// slot: the largest repeat destination + 1 of the index whose host copy goes
-// to that slot (0 = none).  The map holds at most N_q * K keys and
-// P >= 1.5 N_q K, so every probe sequence ends at a free word.
-// v0: this thread's entry tid of the transfer list (loaded by the caller
-// before the table write-back, so its latency overlaps the write-back).
+// atomicMax makes every choice deterministic; beside it P fan words, one per
+// map word: the second largest slot + 1 reserved for the word's index (0 =
+// none), the largest destination among its repeats.  A word's lowest bit marks that an index whose home is that word
+// sits further on (it may also be set on a word whose own index took a
+// larger slot; that only costs the scan below a probe).  The map holds at
+// most N_q * K keys and P >= 1.5 N_q K, so every probe sequence ends at a
+// free word.  The transfer list is read from the
+// slot list the token loop kept in LDS where there was room (entry e is slot
+// o = slist[e], index c[o]: no reserved slot is reassigned within a step),
+// else from device memory.
+// rows_u / lim_u: an index x is valid when (uint32)x < rows_u, and a cached
+// index qualifies as a resident source when (uint32)x < lim_u (both bounds
+// clamped to 2^31, so negative indices fail).
 template <int NT>
 __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, unsigned char* lds,
-                                             const int listed, const int64_t rows_r,
-                                             const int64_t n_verified, const int2 v0,
+                                             const int listed, const uint32_t rows_u, const uint32_t lim_u,
                                              int* counts_out) {
   constexpr int MT = NT, MW = NT / 64;
   const int S = p.S;
@@ -223,82 +266,97 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   uint32_t* sres = reinterpret_cast<uint32_t*>(lds + align16(4 * static_cast<size_t>(S)));  // reserved-slot bitmap
   const int nb = plan_bitmap_words(S);
   const uint32_t P = static_cast<uint32_t>(p.plan_words);   // a multiple of 4
+  const PlanHash ph(P);
   uint32_t* smp = sres + nb;                                        // [P] index map
-  uint32_t* sfan = smp + P;                                         // [S] fan words per slot
-  int* scnt = reinterpret_cast<int*>(sfan + S);                     // [kPlanMiscWords]
-  const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
+  uint32_t* sfan = smp + P;                                         // [P] fan word of each map word
+  int* scnt = reinterpret_cast<int*>(sfan + P);                     // [kPlanMiscWords]
+  const uint16_t* slist = reinterpret_cast<const uint16_t*>(lds + p.plan_list_off);
+  const int tid = threadIdx.x, wave = wave_id(), lane = lane_id();
   const size_t lb = static_cast<size_t>(r) * p.n_q * p.K;
   const int2* ml = p.miss_list + lb;
+  // entry e of the transfer list: (index, slot)
+  auto entry = [&](int e) __attribute__((always_inline)) {
+    if (p.plan_list_off == 0) return ml[e];
+    const int o = slist[e];
+    return make_int2(sc[o], o);
+  };
   if (r == 0 && tid == 0) {
     p.plan_claim[0] = 0;
     p.plan_claim[1] = 0;
   }
 
-  {
-    // the bitmap, map and fan words, four words per 16-byte store where they
-    // come in fours
-    const int words = nb + static_cast<int>(P) + S;
-    const int vec = words / 4;
-    for (int j = tid; j < vec; j += MT) reinterpret_cast<u32x4*>(sres)[j] = 0u;
-    for (int j = 4 * vec + tid; j < words; j += MT) sres[j] = 0u;
-    for (int j = tid; j < kPlanMiscWords; j += MT) scnt[j] = 0;
-  }
-  __syncthreads();
-
   // (1) mark this step's reservations; one map word per distinct valid index
   for (int e = tid; e < listed; e += MT) {
-    const int2 v = e < MT ? v0 : ml[e];
-    if (v.y < 0 || v.y >= S) continue;
-    atomicOr(&sres[v.y >> 5], 1u << (v.y & 31));
-    if (v.x < 0 || static_cast<int64_t>(v.x) >= rows_r) continue;
-    const uint32_t tag = plan_tag(v.x);
-    const uint32_t val = tag | (static_cast<uint32_t>(v.y) + 1u);
-    uint32_t h = plan_home(v.x, P);
+    const int2 v = entry(e);
+    const int32_t x = v.x, o = v.y;
+    atomicOr(&sres[o >> 5], 1u << (o & 31));
+    if (static_cast<uint32_t>(x) >= rows_u) continue;
+    const uint32_t hx = ph.hash(x), tag = ph.tag(hx);
+    const uint32_t val = tag | plan_val(o);
+    uint32_t h = ph.home(hx);
     for (uint32_t t = 0; t < P; ++t) {
       const uint32_t w = atomicCAS(&smp[h], 0u, val);
       if (w == 0u) break;
-      if ((w & kPlanTag) == tag && sc[(w & kPlanSlot) - 1u] == v.x) {
-        atomicMax(&smp[h], val);   // the largest reserved slot of the index
+      if ((w & kPlanTag) == tag && sc[plan_slot(w)] == x) {
+        // the largest reserved slot of the index (the mark bit is set with it
+        // since a mark already on the word must not be lost); whichever of
+        // the old and the new slot is smaller bids for the fan word, so it
+        // ends as the second largest
+        const uint32_t old = atomicMax(&smp[h], val | kPlanDisp);
+        const int other = (old & kPlanSlot) < (val & kPlanSlot) ? plan_slot(old) : o;
+        atomicMax(&sfan[h], static_cast<uint32_t>(other) + 1u);
         break;
       }
-      h = (h + 1u == P) ? 0u : h + 1u;
+      if (t == 0) atomicOr(&smp[h], kPlanDisp);   // another index holds the home word
+      h = ph.next(h);
     }
   }
   __syncthreads();
 
-  // (2) slots outside the reservations that cache one of those indices; four
-  // slots per thread at a time so their LDS reads overlap (the map is sparse:
-  // most home words are empty and end the probe at once)
-  constexpr int kScanILP = 4;
-  for (int j0 = tid; j0 < S; j0 += kScanILP * MT) {
-    int32_t xs[kScanILP];
-    uint32_t hs[kScanILP], ws[kScanILP];
+  // (2) slots outside the reservations that cache one of those indices.  A
+  // first pass reads kScan slots per thread (their LDS reads in flight
+  // together) and keeps, as bits, the slots that may cache a key: qualified,
+  // not reserved, and the home word of their index holds a word with the
+  // index's tag or one marked as the home of an index placed further on.
+  // Every slot that caches a key passes (its key sits at its home word or
+  // further on from a marked home); only those walk a probe sequence, in a
+  // second pass.  A key is often cached in several slots outside the
+  // reservations (copies left by lost installs), so most candidates bid.
+  constexpr int kScan = 8;
+  for (int j0 = tid; j0 < S; j0 += kScan * MT) {
+    int32_t xs[kScan];
+    uint32_t cand = 0u;
 #pragma unroll
-    for (int u = 0; u < kScanILP; ++u) {
+    for (int u = 0; u < kScan; ++u) {
       const int j = j0 + u * MT;
-      xs[u] = j < S ? sc[j] : -1;
+      xs[u] = sc[j < S ? j : S - 1];
     }
 #pragma unroll
-    for (int u = 0; u < kScanILP; ++u) {
-      const bool ok = xs[u] >= 0 && static_cast<int64_t>(xs[u]) < rows_r &&
-                      static_cast<int64_t>(xs[u]) < n_verified;
-      hs[u] = plan_home(xs[u], P);
-      ws[u] = ok ? smp[hs[u]] : 0u;
+    for (int u = 0; u < kScan; ++u) {
+      const int j = j0 + u * MT < S ? j0 + u * MT : S - 1;
+      const uint32_t hx = ph.hash(xs[u]);
+      const uint32_t w = smp[ph.home(hx)];
+      const uint32_t rb = sres[j >> 5] >> (j & 31);
+      const bool ok = j0 + u * MT < S && static_cast<uint32_t>(xs[u]) < lim_u && !(rb & 1u) && w != 0u &&
+                      ((w & kPlanTag) == ph.tag(hx) || (w & kPlanDisp));
+      cand |= ok ? (1u << u) : 0u;
     }
-#pragma unroll
-    for (int u = 0; u < kScanILP; ++u) {
+    while (cand) {
+      const int u = __builtin_ctz(cand);
+      cand &= cand - 1u;
       const int j = j0 + u * MT;
-      // the reservation bitmap is read only for the few slots whose home word is taken
-      if (ws[u] != 0u && ((sres[j >> 5] >> (j & 31)) & 1u)) ws[u] = 0u;
-      uint32_t h = hs[u], w = ws[u];
-      const uint32_t tag = plan_tag(xs[u]);
-      for (uint32_t t = 0; w != 0u && t < P; ++t) {
-        if ((w & kPlanTag) == tag && sc[(w & kPlanSlot) - 1u] == xs[u]) {
-          atomicMax(&smp[h], kPlanResident | tag | (static_cast<uint32_t>(j) + 1u));
+      const int32_t x = sc[j];
+      const uint32_t hx = ph.hash(x), tag = ph.tag(hx);
+      uint32_t h = ph.home(hx);
+      for (uint32_t t = 0; t < P; ++t) {
+        const uint32_t w = smp[h];
+        if (w == 0u) break;
+        if ((w & kPlanTag) == tag && sc[plan_slot(w)] == x) {
+          // the marks are final by now: keep the word's own
+          atomicMax(&smp[h], kPlanResident | tag | plan_val(j) | (w & kPlanDisp));
           break;
         }
-        h = (h + 1u == P) ? 0u : h + 1u;
-        w = smp[h];
+        h = ph.next(h);
       }
     }
   }
@@ -312,16 +370,16 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
     const int32_t* ex = p.early_x + lb;
     for (int k = tid; k < ne; k += MT) {
       uint32_t w = 0u;
-      const int hw = plan_lookup(smp, sc, P, ex[k], &w);
+      const int hw = plan_lookup(smp, sc, ph, ex[k], &w);
       if (hw >= 0) atomicOr(&smp[hw], kPlanEarly);
     }
     __syncthreads();
   }
 
   // classify one entry: kind 0 host, 1 resident, 2 repeat (src = source
-  // slot, hw = its map position), 4 / 5 first / further miss of an
-  // early-fetched index, -1 past the list (returned by value: out-parameters
-  // would put these locals on the stack)
+  // slot), 4 / 5 first / further miss of an early-fetched index, -1 past the
+  // list; hw = the map position of the entry's index (returned by value:
+  // out-parameters would put these locals on the stack)
   struct Entry {
     int kind, src, hw;
     int2 v;
@@ -329,36 +387,28 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   auto classify = [&](int e) __attribute__((always_inline)) {
     Entry c{-1, 0, -1, make_int2(0, 0)};
     if (e >= listed) return c;
-    c.v = e < MT ? v0 : ml[e];
+    c.v = entry(e);
+    const int o = c.v.y;
     c.kind = 0;
-    if (c.v.x < 0 || static_cast<int64_t>(c.v.x) >= rows_r) return c;
+    if (static_cast<uint32_t>(c.v.x) >= rows_u) return c;
     uint32_t w = 0u;
-    c.hw = plan_lookup(smp, sc, P, c.v.x, &w);
+    c.hw = plan_lookup(smp, sc, ph, c.v.x, &w);
     if (c.hw < 0) return c;
-    const int o = static_cast<int>(w & kPlanSlot) - 1;
+    const int src = plan_slot(w);
     if (w & kPlanEarly) {
-      c.kind = o != c.v.y ? 5 : 4;   // fetched early; 5 = a further miss of it
+      c.kind = src != o ? 5 : 4;   // fetched early; 5 = a further miss of it
     } else if (w & kPlanResident) {
       c.kind = 1;
-      c.src = o;
-    } else if (o != c.v.y) {
+      c.src = src;
+    } else if (src != o) {
       c.kind = 2;
-      c.src = o;
+      c.src = src;
     }
     return c;
   };
 
-  // (3) every repeat bids for the fan word of its source slot (the largest
-  // destination wins); repeats need two tokens in the step.  The first round's
-  // classification is kept for (4).
+  // (3) classify the first round's entries (kept for the compaction)
   const Entry first = classify(tid);
-  if (p.n_q > 1) {
-    for (int e = tid; e < listed; e += MT) {
-      const Entry c = e < MT ? first : classify(e);
-      if (c.kind == 2) atomicMax(&sfan[c.src], static_cast<uint32_t>(c.v.y) + 1u);
-    }
-    __syncthreads();
-  }
 
   // (4) compact the three lists in transfer-list order; host entries carry
   // their fan slot, repeats that won the fan word leave the repeat list
@@ -366,30 +416,26 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   for (int e0 = 0, it = 0; e0 < listed; e0 += MT, ++it) {
     Entry c = it == 0 ? first : classify(e0 + tid);
     int fan = -1;
-    if (c.kind == 0 && c.hw >= 0 && c.v.y >= 0 && c.v.y < S) fan = static_cast<int>(sfan[c.v.y]) - 1;
+    if (c.kind == 0 && c.hw >= 0) fan = static_cast<int>(sfan[c.hw]) - 1;
     if (c.kind == 2) {
       ++n_rep;
-      if (static_cast<int>(sfan[c.src]) - 1 == c.v.y) c.kind = 3;   // written by the host copy
+      if (static_cast<int>(sfan[c.hw]) - 1 == c.v.y) c.kind = 3;   // written by the host copy
     }
     if (c.kind == 5) ++n_rep;             // filled by the early fetch's copy of its index
     const int kind = c.kind;
     uint64_t mk[3];
     int* wc = scnt + (it & 1) * 3 * MW;
 #pragma unroll
-    for (int k = 0; k < 3; ++k) {
-      mk[k] = __ballot(kind == k);
-      if (lane == 0) wc[k * MW + wave] = __popcll(mk[k]);
+    for (int k = 0; k < 3; ++k) mk[k] = __ballot(kind == k);
+    // host and resident counts share a word (16 bits each: at most MT entries)
+    if (lane == 0) {
+      wc[wave] = __popcll(mk[0]) | (__popcll(mk[1]) << 16);
+      wc[MW + wave] = __popcll(mk[2]);
     }
     __syncthreads();
-    int before[3] = {0, 0, 0}, total[3] = {0, 0, 0};
-    for (int w = 0; w < MW; ++w) {
-#pragma unroll
-      for (int k = 0; k < 3; ++k) {
-        const int cnt = wc[k * MW + w];
-        total[k] += cnt;
-        before[k] += (w < wave) ? cnt : 0;
-      }
-    }
+    const WavePrefix p01 = wave_prefix(wc, MW, wave), p2 = wave_prefix(wc + MW, MW, wave);
+    const int before[3] = {p01.before & 0xFFFF, p01.before >> 16, p2.before};
+    const int total[3] = {p01.total & 0xFFFF, p01.total >> 16, p2.total};
     if (kind == 0) {
       const size_t at = lb + n_list[0] + before[0] + bits_below(mk[0]);
       p.host_list[at] = c.v;
@@ -403,21 +449,19 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
     for (int k = 0; k < 3; ++k) n_list[k] += total[k];
   }
   n_rep = wave_sum(n_rep);
-  if (lane == 0 && n_rep) atomicAdd(&scnt[6 * MW], n_rep);
-  __syncthreads();
   if (counts_out) {
     counts_out[0] = n_list[0];
     counts_out[1] = n_list[1];
     counts_out[2] = n_list[2];
   }
+  unsigned long long* st = p.stats + static_cast<size_t>(r) * kNumStats;
+  if (lane == 0 && n_rep) atomicAdd(&st[kStatDuplicate], static_cast<unsigned long long>(n_rep));
   if (tid == 0) {
     int32_t* pc = p.plan_counts + 3 * static_cast<size_t>(r);
     pc[0] = n_list[0];
     pc[1] = n_list[1];
     pc[2] = n_list[2];
-    unsigned long long* st = p.stats + static_cast<size_t>(r) * kNumStats;
     if (n_list[1]) atomicAdd(&st[kStatResident], static_cast<unsigned long long>(n_list[1]));
-    if (scnt[6 * MW]) atomicAdd(&st[kStatDuplicate], static_cast<unsigned long long>(scnt[6 * MW]));
   }
 }
 
@@ -445,10 +489,11 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   int32_t* swc = smp + K;                    // [2][IPT][MW] miss counts per wave
   int32_t* sdead = swc + 2 * kMaxIPT * MW;   // [MW] dead counts per wave
   int32_t* sred = sdead + MW;                // [4] rotating reduction slots
-  int32_t* sstat = sred + 4;                 // [8] counter reduction
+  // the step's transfer list as slots, kept for the Stage Two plan
+  uint16_t* slist = reinterpret_cast<uint16_t*>(lds + p.plan_list_off);
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = wave_id();
   const int lane = lane_id();
 
   // the first token's indices are requested before the table, so the two
@@ -500,7 +545,6 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
     }
   }
   if (tid < 4) sred[tid] = 0;
-  if (tid < 8) sstat[tid] = 0;
 
   // lifetimes owned by this thread: [j0, j0 + spt) if it owns any (tid < S).
   // spt is uniform, so the Own loops branch on scalars; only tables smaller
@@ -510,6 +554,17 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   const int j0 = owns ? tid * spt : 0;
   const int64_t rows_r = p.rows[r];
   const int64_t n_verified = p.verified ? p.verified[r] : INT64_MAX;
+  // 32-bit forms of the bounds: x is a valid index when (uint32)x < rows_u
+  // (negative x fail), a cached index lies below the verified length when
+  // (uint32)x < ver_u, and c >= N (speculative invalidation) is decided on
+  // int32 c with the two out-of-range cases of N taken apart
+  auto clamp_u = [](int64_t v) { return static_cast<uint32_t>(v <= 0 ? 0 : (v > 0x80000000ll ? 0x80000000ll : v)); };
+  const uint32_t rows_u = clamp_u(rows_r);
+  const uint32_t lim_u = rows_u < clamp_u(n_verified) ? rows_u : clamp_u(n_verified);
+  const bool inv_all = n_verified <= static_cast<int64_t>(INT32_MIN);
+  const bool inv_none = n_verified > static_cast<int64_t>(INT32_MAX);
+  const int32_t ver32 = (inv_all || inv_none) ? 0 : static_cast<int32_t>(n_verified);
+  auto invalidated = [&](int32_t c) { return inv_all || (!inv_none && c >= ver32); };
   const uint32_t a1 = p.a1, a2 = p.a2, fmask = p.f_mask;
   const int m = p.m, L = p.L;
 
@@ -546,7 +601,7 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
       dd[u] = ((a2 * ux) & smask) | 1u;       // odd stride (Eq. 9)
       found[u] = false;
       oo[u] = 0;
-      if (act[u] && (xv[u] < 0 || static_cast<int64_t>(xv[u]) >= rows_r)) st_bad++;
+      if (act[u] && static_cast<uint32_t>(xv[u]) >= rows_u) st_bad++;
     }
     // the buckets of kChainBatch consecutive rounds depend only on the index,
     // so their words and then their slots' ids are read together: two LDS
@@ -583,6 +638,8 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
       if (!__ballot(pending)) break;
     }
     int rank[IPT];
+    // per-wave miss counts, two indices per word (16 bits each)
+    int packed[2] = {0, 0};
 #pragma unroll
     for (int u = 0; u < IPT; ++u) {
       const int i = u * MT + tid;
@@ -594,8 +651,12 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
       }
       if (p.hit_mask && act[u]) p.hit_mask[row * K + i] = found[u] ? 1 : 0;
       const uint64_t mm = __ballot(act[u] && !found[u]);
-      if (lane == 0) wc[u * MW + wave] = __popcll(mm);
+      packed[u >> 1] |= __popcll(mm) << (16 * (u & 1));
       rank[u] = bits_below(mm);
+    }
+    if (lane == 0) {
+      wc[wave] = packed[0];
+      if (IPT > 2) wc[MW + wave] = packed[1];
     }
     // installs of the previous token that lost their bucket
 #pragma unroll
@@ -608,16 +669,15 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
 
     // ---- B: classify, compact misses, count dead slots ---------------------
     int n_g = 0;
+    {
+      const WavePrefix pf[2] = {wave_prefix(wc, MW, wave),
+                                IPT > 2 ? wave_prefix(wc + MW, MW, wave) : WavePrefix{0, 0}};
 #pragma unroll
-    for (int u = 0; u < IPT; ++u) {
-      int tot = 0, before = 0;
-      for (int w = 0; w < MW; ++w) {
-        const int c = wc[u * MW + w];
-        tot += c;
-        before += (w < wave) ? c : 0;
+      for (int u = 0; u < IPT; ++u) {
+        const int sh = 16 * (u & 1);
+        rank[u] += n_g + ((pf[u >> 1].before >> sh) & 0xFFFF);
+        n_g += (pf[u >> 1].total >> sh) & 0xFFFF;
       }
-      rank[u] += n_g + before;
-      n_g += tot;
     }
     if (tid == 0) {
       p.miss_counts[row] = n_g;
@@ -647,12 +707,9 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
 
     if (n_g > 0) {
       // ---- C: enough dead slots (decay loop of Algorithm 1), CollectDead --
-      int dead = 0, wbase = 0;
-      for (int w = 0; w < MW; ++w) {
-        const int c = sdead[w];
-        dead += c;
-        wbase += (w < wave) ? c : 0;
-      }
+      const WavePrefix pd = wave_prefix(sdead, MW, wave);
+      const int dead = pd.total;
+      int wbase = pd.before;
       if (dead < n_g) {
         // smallest k with #{lifetime_j < k} >= n_g; k = L + 1 always suffices
         int kstar = 1;
@@ -677,8 +734,7 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
         incl = wave_inclusive_scan(dcnt, lane);
         if (lane == 63) sdead[wave] = incl;   // every wave read sdead before the loop's barrier
         __syncthreads();
-        wbase = 0;
-        for (int w = 0; w < wave; ++w) wbase += sdead[w];
+        wbase = wave_prefix(sdead, MW, wave).before;
       }
       int drank = wbase + incl - dcnt;
       if (drank < n_g) {
@@ -758,6 +814,7 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
         slife[mo[u]] = static_cast<int8_t>(L);
         og[mp[u]] = mo[u];                                   // a miss's output slot
         p.miss_list[lbase + k] = make_int2(mt[u], mo[u]);
+        if (p.plan_list_off > 0) slist[listed + k] = static_cast<uint16_t>(mo[u]);
         if (mv[u]) {
           const uint32_t bid = kBid | (static_cast<uint32_t>(g) << 24) |
                                (static_cast<uint32_t>(mo[u]) << (23 - m)) |
@@ -775,10 +832,15 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
     }
   }
 
-  // installs of the last token that lost their bucket
+  // installs of the last token that lost their bucket: of the bids it made,
+  // all but one per bucket it bid for (the write back counts the buckets
+  // whose word is a bid of the last token; the sum over the workgroup is what
+  // matters, not which thread counts)
 #pragma unroll
   for (int u = 0; u < IPT; ++u)
-    if (bid_v[u] && smap[bid_h[u]] != bid_v[u]) st_col++;
+    if (bid_v[u]) st_col++;
+  const uint32_t last_bid = kBid | (static_cast<uint32_t>(p.n_q - 1) << 24);
+  auto last_token_bid = [&](uint32_t w) { return (w & 0xFF000000u) == last_bid ? 1 : 0; };
 
   // every slot of the request's O is written: an early-fetch worker may now
   // copy rows straight into them (each wave's stores are made visible at
@@ -789,7 +851,11 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
     if (tid == 0) __hip_atomic_store(p.early_done + r, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
   }
 
-  // End of step: speculative invalidation fused into the write back.
+  // End of step: speculative invalidation fused into the write back.  With a
+  // Stage Two plan to follow, each thread also clears the plan's LDS words
+  // that it has just read (bucket words and lifetimes), and the threads share
+  // the rest of the plan's words, which the write back does not read.
+  const bool plan = p.plan_words > 0;
   int st_inv = 0;
   if ((S & (4 * MT - 1)) == 0) {
     // four entries per 16-byte store
@@ -797,12 +863,17 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
       i32x4 c = reinterpret_cast<const i32x4*>(sc)[b];
       const u32x4 m = reinterpret_cast<const u32x4*>(smap)[b];
       const uint32_t l = reinterpret_cast<const uint32_t*>(slife)[b];
+      if (plan) {
+        reinterpret_cast<u32x4*>(smap)[b] = 0u;
+        reinterpret_cast<uint32_t*>(slife)[b] = 0u;
+      }
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        if (static_cast<int64_t>(c[e]) >= n_verified) {
+        if (invalidated(c[e])) {
           c[e] = -1;
           st_inv++;
         }
+      st_col -= last_token_bid(m.x) + last_token_bid(m.y) + last_token_bid(m.z) + last_token_bid(m.w);
       u32x4 q;
       q.x = (l << 24) | W.canonical(m.x);
       q.y = ((l << 16) & 0xFF000000u) | W.canonical(m.y);
@@ -814,49 +885,51 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   } else {
     for (int j = tid; j < S; j += MT) {
       int32_t c = sc[j];
-      if (static_cast<int64_t>(c) >= n_verified) {
+      const uint32_t m = smap[j];
+      const uint8_t l = static_cast<uint8_t>(slife[j]);
+      if (plan) {
+        smap[j] = 0u;
+        slife[j] = 0;
+      }
+      if (invalidated(c)) {
         c = -1;
         st_inv++;
       }
+      st_col -= last_token_bid(m);
       gc[j] = c;
-      gq[j] = (static_cast<uint32_t>(static_cast<uint8_t>(slife[j])) << 24) | W.canonical(smap[j]);
+      gq[j] = (static_cast<uint32_t>(l) << 24) | W.canonical(m);
     }
   }
-
-  // the first transfer-list entry of this thread, for the Stage Two plan
-  // (requested after the write-back's stores; its latency overlaps the
-  // counter reduction)
-  int2 v0 = make_int2(-1, -1);
-  if (p.plan_words > 0 && tid < listed) v0 = p.miss_list[static_cast<size_t>(r) * p.n_q * K + tid];
-
-  int vals[7] = {st_hits, st_miss, st_exh, st_col, st_rev, st_inv, st_bad};
-#pragma unroll
-  for (int k = 0; k < 7; ++k) {
-    const int v = wave_sum(vals[k]);
-    if (lane == 0 && v) atomicAdd(&sstat[k], v);
+  if (plan) {
+    // plan words past the bucket words and lifetimes (16-byte aligned ends)
+    const size_t from = 8 * static_cast<size_t>(S) + align16(S);
+    const size_t to = align16(4 * static_cast<size_t>(S)) + 4 * plan_state_words(S, p.plan_words);
+    for (size_t o = from + 16 * static_cast<size_t>(tid); o < to; o += 16 * static_cast<size_t>(MT))
+      *reinterpret_cast<u32x4*>(lds + o) = 0u;
   }
-  __syncthreads();
-  if (tid == 0) {
-    // atomics without a return value: thread 0 does not wait for the counters
+
+  // counters: each wave adds its sums with atomics that return nothing
+  {
     unsigned long long* st = p.stats + static_cast<size_t>(r) * kNumStats;
-    auto add = [&](StatIndex i, int v) {
-      if (v) atomicAdd(&st[i], static_cast<unsigned long long>(v));
-    };
-    add(kStatHits, sstat[0]);
-    add(kStatMisses, sstat[1]);
-    add(kStatLostExhausted, sstat[2]);
-    add(kStatLostCollision, sstat[3]);
-    add(kStatRevivals, sstat[4]);
-    add(kStatInvalidations, sstat[5]);
-    add(kStatBadIndices, sstat[6]);
-    if (step_decays) {
-      atomicAdd(&st[kStatAllocDecays], static_cast<unsigned long long>(step_decays));
-      atomicMax(&st[kStatMaxStepDecays], static_cast<unsigned long long>(step_decays));
+    const int vals[6] = {st_hits, st_exh, st_col, st_rev, st_inv, st_bad};
+    const StatIndex idx[6] = {kStatHits, kStatLostExhausted, kStatLostCollision,
+                              kStatRevivals, kStatInvalidations, kStatBadIndices};
+#pragma unroll
+    for (int k = 0; k < 6; ++k) {
+      const int v = wave_sum(vals[k]);
+      if (lane == 0 && v) atomicAdd(&st[idx[k]], static_cast<unsigned long long>(v));
+    }
+    if (tid == 0) {
+      if (st_miss) atomicAdd(&st[kStatMisses], static_cast<unsigned long long>(st_miss));
+      if (step_decays) {
+        atomicAdd(&st[kStatAllocDecays], static_cast<unsigned long long>(step_decays));
+        atomicMax(&st[kStatMaxStepDecays], static_cast<unsigned long long>(step_decays));
+      }
     }
   }
-  if (p.plan_words > 0) {
-    __syncthreads();   // the counter reduction above is read before its LDS is reused
-    plan_request<NT>(p, r, lds, listed, rows_r, n_verified, v0, plan_counts);
+  if (plan) {
+    __syncthreads();   // the plan's words are clear
+    plan_request<NT>(p, r, lds, listed, rows_u, lim_u, plan_counts);
   }
 }
 

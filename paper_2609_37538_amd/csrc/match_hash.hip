@@ -180,32 +180,63 @@ size_t match_lds_bytes(int S, int K) {
 // LDS of one workgroup (gfx950), the bound of the end-of-step plan's map.
 constexpr size_t kWorkgroupLds = 160 * 1024;
 
-int plan_map_words(int S, int K, int n_q) {
-  if (match_lds_bytes(S, K) == 0 || n_q < 1) return 0;
-  // the plan keeps c[] (4 S bytes, padded to 16) and takes the rest of the
-  // workgroup's LDS: the reservation bitmap, P map words, S fan words and its
-  // counters; P is a power of two where one fits, else a multiple of four
-  const long long words = static_cast<long long>((kWorkgroupLds - align16(4 * static_cast<size_t>(S))) / 4) -
-                          plan_bitmap_words(S) - S - kPlanMiscWords;
-  const long long keys = static_cast<long long>(n_q) * K;
-  const long long need = (3 * keys + 1) / 2;   // keep the map at most two-thirds full
-  long long P = words < 4 * keys ? words : 4 * keys;
+// The plan's LDS: c[] (4 S bytes, padded to 16) stays, then the reservation
+// bitmap, P map words, P fan words and its counters.  Where there is room, the
+// step's transfer list (2 bytes per entry, n_q K entries at most) is kept at
+// the end, past both the token loop's arrays and the plan's words; otherwise
+// the plan reads the list back from device memory.
+static size_t plan_list_bytes(int K, int n_q) { return align16(2 * static_cast<size_t>(n_q) * K); }
+
+static size_t plan_words_end(int S, long long P) {
+  return align16(4 * static_cast<size_t>(S)) + 4 * plan_state_words(S, static_cast<int>(P));
+}
+
+// P for `words` free LDS words (map and fan words take P each): a power of
+// two where one fits, else a multiple of four; at most four words per key and
+// at least 1.5 (the map is at most two-thirds full); 0 if that does not fit
+static long long plan_words_for(long long words, long long keys) {
+  const long long need = (3 * keys + 1) / 2;
+  long long P = (4 * keys < words / 2 ? 4 * keys : words / 2) & ~3ll;
   long long pow2 = 1;
   while (2 * pow2 <= P) pow2 *= 2;
-  P = pow2 >= need ? pow2 : (P & ~3ll);
-  if (P < need) return 0;
-  return static_cast<int>(P);
+  P = pow2 >= need ? pow2 : P;
+  return P >= need ? P : 0;
 }
+
+struct PlanLayout {
+  int P;             // map words (0: no plan fits)
+  size_t list_off;   // LDS offset of the kept transfer list (0: none)
+  size_t total;      // LDS bytes of the matching workgroup
+};
+
+static PlanLayout plan_layout(int S, int K, int n_q) {
+  const size_t m = match_lds_bytes(S, K);
+  if (m == 0 || n_q < 1 || S > 65536) return {0, 0, 0};   // kept slots are 16-bit values
+  const size_t A = align16(4 * static_cast<size_t>(S));
+  const long long keys = static_cast<long long>(n_q) * K;
+  const long long fixed = plan_bitmap_words(S) + kPlanMiscWords;   // besides map and fan words
+  const size_t list = plan_list_bytes(K, n_q);
+  if (align16(m) + list <= kWorkgroupLds) {
+    const long long P = plan_words_for(static_cast<long long>((kWorkgroupLds - list - A) / 4) - fixed, keys);
+    if (P > 0) {
+      const size_t e = plan_words_end(S, P), off = align16(m > e ? m : e);
+      return {static_cast<int>(P), off, off + list};
+    }
+  }
+  const long long P = plan_words_for(static_cast<long long>((kWorkgroupLds - A) / 4) - fixed, keys);
+  if (P == 0) return {0, 0, 0};
+  const size_t e = plan_words_end(S, P);
+  return {static_cast<int>(P), 0, m > e ? m : e};
+}
+
+int plan_map_words(int S, int K, int n_q) { return plan_layout(S, K, n_q).P; }
+
+size_t plan_list_offset(int S, int K, int n_q) { return plan_layout(S, K, n_q).list_off; }
 
 size_t stage_one_lds_bytes(int S, int K, int n_q, bool plan) {
   const size_t m = match_lds_bytes(S, K);
   if (m == 0 || !plan) return m;
-  const int P = plan_map_words(S, K, n_q);
-  if (P == 0) return 0;
-  const size_t need = align16(4 * static_cast<size_t>(S)) +
-                      4 * (static_cast<size_t>(plan_bitmap_words(S)) + static_cast<size_t>(P) +
-                           static_cast<size_t>(S) + kPlanMiscWords);
-  return m > need ? m : need;
+  return plan_layout(S, K, n_q).total;
 }
 
 hipError_t prepare_match_hash(size_t lds) {

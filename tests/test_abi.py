@@ -94,8 +94,8 @@ def test_check_config_statuses(lib):
     assert chk(gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_OK
     assert chk(n_q=1, slots=2048, match_mode=A.AVSG_MATCH_DUALPTR,
                gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_E_UNSUPPORTED
-    assert chk(batch=1, topk=128, n_q=39, slots=16384, gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_OK
-    assert chk(batch=1, topk=128, n_q=40, slots=16384, gather_mode=A.AVSG_GATHER_RESIDENT) == \
+    assert chk(batch=1, topk=128, n_q=62, slots=16384, gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_OK
+    assert chk(batch=1, topk=128, n_q=63, slots=16384, gather_mode=A.AVSG_GATHER_RESIDENT) == \
         A.AVSG_E_CAPACITY
     assert chk(batch=1, topk=128, n_q=110, slots=16384) == A.AVSG_OK
     assert chk(gather_mode=9) == A.AVSG_E_INVAL
@@ -106,7 +106,7 @@ def test_check_config_statuses(lib):
     assert chk(gather_mode=A.AVSG_GATHER_EARLY, early_direct=1) == A.AVSG_E_INVAL
     assert chk(n_q=1, slots=2048, match_mode=A.AVSG_MATCH_DUALPTR,
                gather_mode=A.AVSG_GATHER_EARLY) == A.AVSG_E_UNSUPPORTED
-    assert chk(batch=1, topk=128, n_q=39, slots=16384, gather_mode=A.AVSG_GATHER_EARLY) == A.AVSG_OK
+    assert chk(batch=1, topk=128, n_q=62, slots=16384, gather_mode=A.AVSG_GATHER_EARLY) == A.AVSG_OK
 
 
 def test_workspace_size_and_validation(lib):

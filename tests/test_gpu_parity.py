@@ -440,6 +440,10 @@ RESIDENT_CASES = [
     ("batch_200", dict(batch=200, topk=128, slots=256, n_q=2, steps=6, ctx=2000), 0),
     ("batch_1024_max", dict(batch=1024, topk=16, slots=64, n_q=2, steps=6, ctx=400), 0),
     ("four_waves", dict(batch=3, topk=384, slots=1024, n_q=2, steps=12, ctx=6000, retention=0.8), 0),
+    # the largest plans that fit one workgroup's LDS: with the transfer list
+    # kept in LDS (53 tokens) and read back from device memory (62 tokens)
+    ("lds_edge_list", dict(batch=2, topk=128, slots=16384, n_q=53, steps=6, ctx=60000), 3),
+    ("lds_edge_no_list", dict(batch=2, topk=128, slots=16384, n_q=62, steps=6, ctx=60000), 3),
 ]
 
 
@@ -506,9 +510,9 @@ def test_resident_reuse_refused_without_room():
     needs hash matching."""
     from paper_2609_37538_amd import avsg as A
     chk = lambda **kw: A.avsg_check_config(A.make_config(**kw))
-    assert chk(batch=1, topk=128, n_q=39, slots=16384, row_bytes=(16,),
+    assert chk(batch=1, topk=128, n_q=62, slots=16384, row_bytes=(16,),
                gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_OK
-    assert chk(batch=1, topk=128, n_q=40, slots=16384, row_bytes=(16,),
+    assert chk(batch=1, topk=128, n_q=63, slots=16384, row_bytes=(16,),
                gather_mode=A.AVSG_GATHER_RESIDENT) == A.AVSG_E_CAPACITY
     assert chk(batch=1, topk=128, n_q=110, slots=16384, row_bytes=(16,)) == A.AVSG_OK
     assert chk(batch=1, topk=64, n_q=1, slots=64, row_bytes=(16,), match_mode=A.AVSG_MATCH_DUALPTR,
