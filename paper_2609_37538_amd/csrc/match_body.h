@@ -468,8 +468,10 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
 // Stage One for request r (Algorithm 4's token loop) in workgroup-owned LDS.
 // After each token with misses, publish(r, first, count) is called by every
 // thread once the token's transfer-list entries are written (a no-op for the
-// plain matching kernel).
-template <int IPT, int NT, typename Publish>
+// plain matching kernel).  SPT is the number of lifetimes a thread owns
+// (S / NT, at least 1) when known at compile time, so that the loops over them
+// unroll without scalar conditions; 0 takes it from S at run time.
+template <int IPT, int NT, int SPT, typename Publish>
 __device__ __forceinline__ void match_request(const MatchParams& p, const int r, unsigned char* lds,
                               Publish& publish, int* plan_counts = nullptr) {
   constexpr int MT = NT, MW = NT / 64;
@@ -549,7 +551,7 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   // lifetimes owned by this thread: [j0, j0 + spt) if it owns any (tid < S).
   // spt is uniform, so the Own loops branch on scalars; only tables smaller
   // than a workgroup leave threads without lifetimes.
-  const int spt = S >= MT ? S / MT : 1;
+  const int spt = SPT > 0 ? SPT : (S >= MT ? S / MT : 1);
   const bool owns = tid < S;
   const int j0 = owns ? tid * spt : 0;
   const int64_t rows_r = p.rows[r];
@@ -566,6 +568,9 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   const int32_t ver32 = (inv_all || inv_none) ? 0 : static_cast<int32_t>(n_verified);
   auto invalidated = [&](int32_t c) { return inv_all || (!inv_none && c >= ver32); };
   const uint32_t a1 = p.a1, a2 = p.a2, fmask = p.f_mask;
+  // (a x) mod S from the low m bits of a and x: their product is below 2^28
+  // (S <= 2^14), so the full-rate 24-bit multiply gives it exactly
+  const uint32_t a1m = a1 & smask, a2m = a2 & smask;
   const int m = p.m, L = p.L;
 
   int st_hits = 0, st_miss = 0, st_exh = 0, st_col = 0, st_rev = 0, st_bad = 0;
@@ -597,8 +602,8 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
     for (int u = 0; u < IPT; ++u) {
       act[u] = u * MT + tid < K;
       const uint32_t ux = static_cast<uint32_t>(xv[u]);
-      hh[u] = (a1 * ux) & smask;              // initial bucket (Eq. 9)
-      dd[u] = ((a2 * ux) & smask) | 1u;       // odd stride (Eq. 9)
+      hh[u] = __umul24(a1m, ux & smask) & smask;          // initial bucket (Eq. 9)
+      dd[u] = (__umul24(a2m, ux & smask) & smask) | 1u;   // odd stride (Eq. 9)
       found[u] = false;
       oo[u] = 0;
       if (act[u] && static_cast<uint32_t>(xv[u]) >= rows_u) st_bad++;
@@ -614,12 +619,12 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
       for (int u = 0; u < IPT; ++u)
 #pragma unroll
         for (int b = 0; b < kChainBatch; ++b)
-          if (act[u] && !found[u] && rd0 + b <= R) qw[u][b] = smap[(hh[u] + b * dd[u]) & smask];
+          if (u * MT < K && rd0 + b <= R) qw[u][b] = smap[(hh[u] + b * dd[u]) & smask];
 #pragma unroll
       for (int u = 0; u < IPT; ++u)
 #pragma unroll
         for (int b = 0; b < kChainBatch; ++b)
-          if (act[u] && !found[u] && rd0 + b <= R) cv[u][b] = sc[W.slot(qw[u][b])];   // Eq. 10
+          if (u * MT < K && rd0 + b <= R) cv[u][b] = sc[W.slot(qw[u][b])];   // Eq. 10
       bool pending = false;
 #pragma unroll
       for (int u = 0; u < IPT; ++u) {
@@ -750,15 +755,23 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
       bool mact[IPT], mv[IPT];
 #pragma unroll
       for (int u = 0; u < IPT; ++u) {
+        // the misses are ranks 0..n_g-1, one per lane: reads are issued for
+        // whole waves (a lane past n_g reads a valid entry and ignores it)
         const int k = u * MT + tid;
+        const int kr = k < n_g ? k : 0;
         mact[u] = k < n_g;
         mv[u] = false;
-        mt[u] = mact[u] ? smx[k] : 0;
-        mp[u] = mact[u] ? smp[k] : 0;
-        mo[u] = mact[u] ? (somiss[k] & static_cast<int>(smask)) : 0;
+        mt[u] = 0;
+        mp[u] = 0;
+        mo[u] = 0;
+        if (u * MT + wave * 64 < n_g) {   // the wave holds a miss
+          mt[u] = smx[kr];
+          mp[u] = smp[kr];
+          mo[u] = somiss[kr] & static_cast<int>(smask);
+        }
         const uint32_t ux = static_cast<uint32_t>(mt[u]);
-        mh[u] = (a1 * ux) & smask;
-        md[u] = ((a2 * ux) & smask) | 1u;
+        mh[u] = __umul24(a1m, ux & smask) & smask;
+        md[u] = (__umul24(a2m, ux & smask) & smask) | 1u;
       }
       // a batch of rounds at a time, as in the probe: every word of the batch,
       // then the lifetime and id of each word's slot, then the first
@@ -767,20 +780,32 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
         uint32_t qw[IPT][kChainBatch];
         int lf[IPT][kChainBatch];
         int32_t cv[IPT][kChainBatch];
+        // every lane of a wave that holds a miss reads every round of the
+        // batch (the buckets and slots are valid whatever the lane holds;
+        // rounds past R are read and ignored), so the reads go out together
+#pragma unroll
+        for (int u = 0; u < IPT; ++u) {
+#pragma unroll
+          for (int b = 0; b < kChainBatch; ++b) {
+            qw[u][b] = 0u;
+            lf[u][b] = 0;
+            cv[u][b] = 0;
+          }
+          if (u * MT + wave * 64 < n_g) {
+#pragma unroll
+            for (int b = 0; b < kChainBatch; ++b) qw[u][b] = smap[(mh[u] + b * md[u]) & smask];
+          }
+        }
 #pragma unroll
         for (int u = 0; u < IPT; ++u)
+          if (u * MT + wave * 64 < n_g) {
 #pragma unroll
-          for (int b = 0; b < kChainBatch; ++b)
-            if (mact[u] && !mv[u] && rd0 + b <= R) qw[u][b] = smap[(mh[u] + b * md[u]) & smask];
-#pragma unroll
-        for (int u = 0; u < IPT; ++u)
-#pragma unroll
-          for (int b = 0; b < kChainBatch; ++b)
-            if (mact[u] && !mv[u] && rd0 + b <= R) {
+            for (int b = 0; b < kChainBatch; ++b) {
               const uint32_t o2 = W.slot(qw[u][b]);
               lf[u][b] = slife[o2];
               cv[u][b] = sc[o2];
             }
+          }
         bool pending = false;
 #pragma unroll
         for (int u = 0; u < IPT; ++u) {
@@ -794,7 +819,7 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
               first = b;
           if (first >= 0) {
             mv[u] = true;
-            mh[u] = (mh[u] + static_cast<uint32_t>(first) * md[u]) & smask;
+            mh[u] = (mh[u] + __umul24(static_cast<uint32_t>(first), md[u])) & smask;
           } else {
             mh[u] = (mh[u] + kChainBatch * md[u]) & smask;
             pending = pending || rd0 + kChainBatch <= R;

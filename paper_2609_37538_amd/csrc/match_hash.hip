@@ -43,11 +43,11 @@ struct NoPublish {
   __device__ __forceinline__ void operator()(int, int, int) const {}
 };
 
-template <int IPT, int NT>
+template <int IPT, int NT, int SPT>
 __global__ __launch_bounds__(NT) void match_hash_kernel(MatchParams p) {
   extern __shared__ __align__(16) unsigned char lds[];
   NoPublish none;
-  match_request<IPT, NT>(p, static_cast<int>(blockIdx.x), lds, none);
+  match_request<IPT, NT, SPT>(p, static_cast<int>(blockIdx.x), lds, none);
 }
 
 __global__ void reset_tables_kernel(int32_t* c, uint32_t* q, size_t n) {
@@ -239,40 +239,68 @@ size_t stage_one_lds_bytes(int S, int K, int n_q, bool plan) {
   return plan_layout(S, K, n_q).total;
 }
 
-hipError_t prepare_match_hash(size_t lds) {
-  const void* kernels[] = {
-      reinterpret_cast<const void*>(&match_hash_kernel<1, kMatchThreads>),
-      reinterpret_cast<const void*>(&match_hash_kernel<2, kMatchThreads>),
-      reinterpret_cast<const void*>(&match_hash_kernel<3, kMatchThreads>),
-      reinterpret_cast<const void*>(&match_hash_kernel<4, kMatchThreads>),
-      reinterpret_cast<const void*>(&match_hash_kernel<1, kSmallThreads>),
-      reinterpret_cast<const void*>(&match_hash_kernel<2, kSmallThreads>)};
-  for (const void* k : kernels) {
-    const hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-    if (e != hipSuccess) return e;
+// The instantiations: lifetimes per thread S / NT is a power of two up to 16
+// with 1024 threads (S <= 16384) and up to 4 with 256 (S <= 1024).
+template <int IPT, int NT>
+static const void* match_kernel_for(int spt) {
+  switch (spt) {
+    case 1: return reinterpret_cast<const void*>(&match_hash_kernel<IPT, NT, 1>);
+    case 2: return reinterpret_cast<const void*>(&match_hash_kernel<IPT, NT, 2>);
+    case 4: return reinterpret_cast<const void*>(&match_hash_kernel<IPT, NT, 4>);
+    default: break;
   }
+  if constexpr (NT == kMatchThreads) {
+    if (spt == 8) return reinterpret_cast<const void*>(&match_hash_kernel<IPT, NT, 8>);
+    if (spt == 16) return reinterpret_cast<const void*>(&match_hash_kernel<IPT, NT, 16>);
+  }
+  return nullptr;
+}
+
+static const void* match_kernel(int S, int K) {
+  const int nt = match_threads(S, K), ipt = ipt_for(S, K), spt = S >= nt ? S / nt : 1;
+  if (nt == kSmallThreads) {
+    switch (ipt) {
+      case 1: return match_kernel_for<1, kSmallThreads>(spt);
+      case 2: return match_kernel_for<2, kSmallThreads>(spt);
+      default: return nullptr;
+    }
+  }
+  switch (ipt) {
+    case 1: return match_kernel_for<1, kMatchThreads>(spt);
+    case 2: return match_kernel_for<2, kMatchThreads>(spt);
+    case 3: return match_kernel_for<3, kMatchThreads>(spt);
+    case 4: return match_kernel_for<4, kMatchThreads>(spt);
+    default: return nullptr;
+  }
+}
+
+hipError_t prepare_match_hash(size_t lds) {
+  static const int spts[] = {1, 2, 4, 8, 16};
+  for (int ipt = 1; ipt <= kMaxIPT; ++ipt)
+    for (int spt : spts) {
+      const void* k[2] = {nullptr, nullptr};
+      switch (ipt) {
+        case 1: k[0] = match_kernel_for<1, kMatchThreads>(spt); k[1] = match_kernel_for<1, kSmallThreads>(spt); break;
+        case 2: k[0] = match_kernel_for<2, kMatchThreads>(spt); k[1] = match_kernel_for<2, kSmallThreads>(spt); break;
+        case 3: k[0] = match_kernel_for<3, kMatchThreads>(spt); break;
+        case 4: k[0] = match_kernel_for<4, kMatchThreads>(spt); break;
+        default: break;
+      }
+      for (const void* f : k) {
+        if (!f) continue;
+        const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+        if (e != hipSuccess) return e;
+      }
+    }
   return hipSuccess;
 }
 
 hipError_t launch_match_hash(const MatchParams& p, size_t lds, hipStream_t s) {
-  const dim3 grid(p.B);
-  if (match_threads(p.S, p.K) == kSmallThreads) {
-    switch (ipt_for(p.S, p.K)) {
-      case 1: hipLaunchKernelGGL((match_hash_kernel<1, kSmallThreads>), grid, dim3(kSmallThreads), lds, s, p); break;
-      case 2: hipLaunchKernelGGL((match_hash_kernel<2, kSmallThreads>), grid, dim3(kSmallThreads), lds, s, p); break;
-      default: return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
-  }
-  const dim3 block(kMatchThreads);
-  switch (ipt_for(p.S, p.K)) {
-    case 1: hipLaunchKernelGGL((match_hash_kernel<1, kMatchThreads>), grid, block, lds, s, p); break;
-    case 2: hipLaunchKernelGGL((match_hash_kernel<2, kMatchThreads>), grid, block, lds, s, p); break;
-    case 3: hipLaunchKernelGGL((match_hash_kernel<3, kMatchThreads>), grid, block, lds, s, p); break;
-    case 4: hipLaunchKernelGGL((match_hash_kernel<4, kMatchThreads>), grid, block, lds, s, p); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
+  const void* f = match_kernel(p.S, p.K);
+  if (!f) return hipErrorInvalidValue;
+  MatchParams args = p;
+  void* argv[] = {&args};
+  return hipLaunchKernel(f, dim3(p.B), dim3(match_threads(p.S, p.K)), argv, lds, s);
 }
 
 hipError_t launch_reset_tables(int32_t* c, uint32_t* q, size_t n, hipStream_t s) {

@@ -445,7 +445,7 @@ __global__ __launch_bounds__(NT) void step_early_kernel(MatchParams mp, EarlyPar
     const int r = static_cast<int>(blockIdx.x);
     NoPublish none;
     int counts[3] = {0, 0, 0};
-    match_request<IPT, NT>(mp, r, lds, none, counts);
+    match_request<IPT, NT, 0>(mp, r, lds, none, counts);
     __syncthreads();
     copy_request_lists<NT>(e, r, counts, lds);
   } else {

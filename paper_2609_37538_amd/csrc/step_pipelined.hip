@@ -156,7 +156,7 @@ __global__ __launch_bounds__(kMatchThreads) void step_pipelined_kernel(MatchPara
   if (q.epoch <= 0) q.epoch = 1;
   if (static_cast<int>(blockIdx.x) < mp.B) {
     QueuePublish pub{q};
-    match_request<IPT, kMatchThreads>(mp, static_cast<int>(blockIdx.x), lds, pub);
+    match_request<IPT, kMatchThreads, 0>(mp, static_cast<int>(blockIdx.x), lds, pub);
     __syncthreads();
     if (threadIdx.x == 0) {
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
