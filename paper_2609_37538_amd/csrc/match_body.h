@@ -66,22 +66,24 @@ __device__ __forceinline__ WavePrefix wave_prefix(const int* cnt, int nw, int wa
 
 __host__ __device__ constexpr size_t align16(size_t v) { return (v + 15) & ~size_t(15); }
 
-// Bucket words in LDS hold either the canonical low 24 bits of Eq. 3
-// (invalid | fingerprint | slot) or an install bid
-// (kBid | token << 24 | slot << (23 - m) | fingerprint), always a valid mapping.
+// Bucket words in LDS keep the fields of Eq. 3 with the slot above the
+// fingerprint: invalid << 23 | slot << (23 - m) | fingerprint, or, for an
+// install bid, kBid | token << 24 | slot << (23 - m) | fingerprint (bit 23
+// clear: a bid is a valid mapping).  Both forms decode alike; the table in
+// HBM keeps the Eq. 3 order (invalid | fingerprint | slot), converted as it
+// is staged in and written back.
 struct Word {
   uint32_t m, smask, fmask;
-  __device__ __forceinline__ uint32_t slot(uint32_t w) const {
-    return ((w & kBid) ? (w >> (23 - m)) : w) & smask;
-  }
-  __device__ __forceinline__ bool invalid(uint32_t w) const {
-    return !(w & kBid) && ((w >> 23) & 1u);
-  }
-  __device__ __forceinline__ uint32_t fp(uint32_t w) const {
-    return ((w & kBid) ? w : (w >> m)) & fmask;
-  }
+  __device__ __forceinline__ uint32_t slot(uint32_t w) const { return (w >> (23 - m)) & smask; }
+  __device__ __forceinline__ bool invalid(uint32_t w) const { return (w >> 23) & 1u; }
+  __device__ __forceinline__ uint32_t fp(uint32_t w) const { return w & fmask; }
+  // the low 24 bits of Eq. 3 from an LDS word
   __device__ __forceinline__ uint32_t canonical(uint32_t w) const {
-    return (w & kBid) ? ((fp(w) << m) | slot(w)) : (w & 0xFFFFFFu);
+    return (w & 0x800000u) | (fp(w) << m) | slot(w);
+  }
+  // an LDS word from the low 24 bits of Eq. 3
+  __device__ __forceinline__ uint32_t staged(uint32_t q) const {
+    return (q & 0x800000u) | ((q & smask) << (23 - m)) | ((q >> m) & fmask);
   }
 };
 
@@ -286,6 +288,7 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   }
 
   // (1) mark this step's reservations; one map word per distinct valid index
+  // with its largest reserved slot, and the second largest in its fan word
   for (int e = tid; e < listed; e += MT) {
     const int2 v = entry(e);
     const int32_t x = v.x, o = v.y;
@@ -513,9 +516,28 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   int32_t* gc = p.table_c + static_cast<size_t>(r) * S;
   uint32_t* gq = p.table_q + static_cast<size_t>(r) * S;
   // stage-in: 16-byte loads of 4 entries, the loads of two blocks issued
-  // before their LDS stores.  The first token's decay of every lifetime (the
-  // global pre-decay of Algorithm 1) is applied as the lifetimes come in.
-  if ((S & (4 * MT - 1)) == 0) {
+  // before their LDS stores (all of a thread's blocks when the lifetimes per
+  // thread are known: S = SPT * NT).  The first token's decay of every
+  // lifetime (the global pre-decay of Algorithm 1) is applied as the
+  // lifetimes come in.
+  auto stage_block = [&](int b, const i32x4 c, const u32x4 q) __attribute__((always_inline)) {
+    reinterpret_cast<i32x4*>(sc)[b] = c;
+    reinterpret_cast<u32x4*>(smap)[b] = u32x4{W.staged(q.x), W.staged(q.y), W.staged(q.z), W.staged(q.w)};
+    reinterpret_cast<uint32_t*>(slife)[b] =
+        Own::decay1((q.x >> 24) | ((q.y >> 24) << 8) | ((q.z >> 24) << 16) | (q.w & 0xFF000000u));
+  };
+  if constexpr (SPT >= 4) {
+    constexpr int NB = SPT / 4;
+    i32x4 cb[NB];
+    u32x4 qb[NB];
+#pragma unroll
+    for (int k = 0; k < NB; ++k) {
+      cb[k] = reinterpret_cast<const i32x4*>(gc)[tid + k * MT];
+      qb[k] = reinterpret_cast<const u32x4*>(gq)[tid + k * MT];
+    }
+#pragma unroll
+    for (int k = 0; k < NB; ++k) stage_block(tid + k * MT, cb[k], qb[k]);
+  } else if ((S & (4 * MT - 1)) == 0) {
     for (int b = tid; b < S / 4; b += 2 * MT) {
       const i32x4 c0 = reinterpret_cast<const i32x4*>(gc)[b];
       const u32x4 q0 = reinterpret_cast<const u32x4*>(gq)[b];
@@ -526,22 +548,14 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
         c1 = reinterpret_cast<const i32x4*>(gc)[b + MT];
         q1 = reinterpret_cast<const u32x4*>(gq)[b + MT];
       }
-      reinterpret_cast<i32x4*>(sc)[b] = c0;
-      reinterpret_cast<u32x4*>(smap)[b] = q0 & 0xFFFFFFu;
-      reinterpret_cast<uint32_t*>(slife)[b] =
-          Own::decay1((q0.x >> 24) | ((q0.y >> 24) << 8) | ((q0.z >> 24) << 16) | (q0.w & 0xFF000000u));
-      if (two) {
-        reinterpret_cast<i32x4*>(sc)[b + MT] = c1;
-        reinterpret_cast<u32x4*>(smap)[b + MT] = q1 & 0xFFFFFFu;
-        reinterpret_cast<uint32_t*>(slife)[b + MT] =
-            Own::decay1((q1.x >> 24) | ((q1.y >> 24) << 8) | ((q1.z >> 24) << 16) | (q1.w & 0xFF000000u));
-      }
+      stage_block(b, c0, q0);
+      if (two) stage_block(b + MT, c1, q1);
     }
   } else {
     for (int j = tid; j < S; j += MT) {
       const uint32_t q = gq[j];
       sc[j] = gc[j];
-      smap[j] = q & 0xFFFFFFu;
+      smap[j] = W.staged(q);
       const int life = static_cast<int8_t>(q >> 24);
       slife[j] = static_cast<int8_t>(life > -1 ? life - 1 : -1);
     }
@@ -933,16 +947,23 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
       *reinterpret_cast<u32x4*>(lds + o) = 0u;
   }
 
-  // counters: each wave adds its sums with atomics that return nothing
+  // counters: each wave adds its sums with atomics that return nothing.  Two
+  // counters share a wave sum, 16 bits each: a thread's counts are at most
+  // IPT * n_q (<= 508) and its collision count at least -spt (the last
+  // token's winning buckets among the words it wrote back), which the bias
+  // spt lifts to zero, so every sum stays below 2^16.
   {
     unsigned long long* st = p.stats + static_cast<size_t>(r) * kNumStats;
-    const int vals[6] = {st_hits, st_exh, st_col, st_rev, st_inv, st_bad};
+    const int s0 = wave_sum(st_hits | (st_exh << 16));
+    const int s1 = wave_sum(st_rev | (st_bad << 16));
+    const int s2 = wave_sum((st_col + spt) | (st_inv << 16));
+    const int vals[6] = {s0 & 0xFFFF, s0 >> 16, (s2 & 0xFFFF) - 64 * spt, s1 & 0xFFFF, s2 >> 16, s1 >> 16};
     const StatIndex idx[6] = {kStatHits, kStatLostExhausted, kStatLostCollision,
                               kStatRevivals, kStatInvalidations, kStatBadIndices};
+    if (lane == 0) {
 #pragma unroll
-    for (int k = 0; k < 6; ++k) {
-      const int v = wave_sum(vals[k]);
-      if (lane == 0 && v) atomicAdd(&st[idx[k]], static_cast<unsigned long long>(v));
+      for (int k = 0; k < 6; ++k)
+        if (vals[k]) atomicAdd(&st[idx[k]], static_cast<unsigned long long>(static_cast<long long>(vals[k])));
     }
     if (tid == 0) {
       if (st_miss) atomicAdd(&st[kStatMisses], static_cast<unsigned long long>(st_miss));
