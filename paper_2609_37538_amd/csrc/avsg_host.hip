@@ -40,6 +40,7 @@ struct avsg_handle {
   int32_t* plan_claim = nullptr;
   int plan_words = 0;
   int plan_list_off = 0;   // LDS offset of the transfer list the plan reads
+  int plan_scan_off = 0;   // LDS offset of the plan scan's candidate lists
   // early-fetch transfer (AVSG_GATHER_EARLY)
   int32_t* early_x = nullptr;
   int4* early_pos = nullptr;
@@ -307,6 +308,7 @@ void bind_workspace(avsg_handle* h, unsigned char* ws, const Layout& L) {
     h->plan_claim = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan + up(static_cast<size_t>(B) * 12));
     h->plan_words = plan_map_words(c.slots, c.topk, c.n_q);
     h->plan_list_off = static_cast<int>(plan_list_offset(c.slots, c.topk, c.n_q));
+    h->plan_scan_off = static_cast<int>(plan_scan_offset(c.slots, c.topk, c.n_q));
   }
   if (c.gather_mode == AVSG_GATHER_EARLY) {
     const std::array<size_t, 9> o = early_sections(c);
@@ -642,6 +644,7 @@ static avsg_status enqueue_step(avsg_handle* h, const int32_t* d_topk, const int
     p.stats = h->stats; p.hit_mask = nullptr;
     p.plan_words = h->plan_words;
     p.plan_list_off = h->plan_list_off;
+    p.plan_scan_off = h->plan_scan_off;
     p.host_list = h->host_list; p.host_fan = h->host_fan;
     p.res_list = h->res_list; p.rep_list = h->rep_list;
     p.plan_counts = h->plan_counts; p.plan_claim = h->plan_claim;
@@ -681,6 +684,7 @@ static avsg_status enqueue_step(avsg_handle* h, const int32_t* d_topk, const int
     if (c.gather_mode == AVSG_GATHER_RESIDENT) {
       p.plan_words = h->plan_words;
       p.plan_list_off = h->plan_list_off;
+      p.plan_scan_off = h->plan_scan_off;
       p.host_list = h->host_list;
       p.host_fan = h->host_fan;
       p.res_list = h->res_list;

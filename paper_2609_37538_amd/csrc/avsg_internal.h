@@ -52,6 +52,7 @@ struct MatchParams {
   // Stage Two plan of the resident-reuse gather (written when plan_words > 0)
   int32_t plan_words;           // words of the end-of-step index map in LDS
   int32_t plan_list_off;        // LDS byte offset of the step's transfer list kept as 16-bit slots
+  int32_t plan_scan_off;        // LDS byte offset of the scan's per-wave candidate lists (0: none)
   int2* host_list;              // [B][n_q*K] (index, slot) copied from the host
   int32_t* host_fan;            // [B][n_q*K] second slot a host entry is also copied to, or -1
   int2* res_list;               // [B][n_q*K] (source slot, slot): row already resident
@@ -169,6 +170,7 @@ hipError_t launch_gather_resident(const GatherParams& host, const GatherParams& 
 int plan_map_words(int S, int K, int n_q);
 // LDS byte offset of the transfer list the matching kernel keeps for the plan
 size_t plan_list_offset(int S, int K, int n_q);
+size_t plan_scan_offset(int S, int K, int n_q);
 // dynamic LDS of the matching workgroup for (S, K, n_q), with room for the
 // end-of-step plan when `plan`; 0 when it does not fit
 size_t stage_one_lds_bytes(int S, int K, int n_q, bool plan);

@@ -47,6 +47,14 @@ __device__ __forceinline__ int wave_inclusive_scan(int v, int /*lane*/) {
 __device__ __forceinline__ int wave_sum(int v) {
   return __builtin_amdgcn_readlane(wave_inclusive_scan(v, 0), 63);
 }
+// Orders this wave's LDS accesses before and after it for the compiler (the
+// hardware runs one wave's LDS instructions in order): lanes that read what
+// other lanes of the wave wrote call it in between.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 // Index of this thread's wave, held in a scalar register.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6); }
 // Per-wave values cnt[0..nw) (nw <= 64) as seen by wave `wave`: the sum over
@@ -65,6 +73,22 @@ __device__ __forceinline__ WavePrefix wave_prefix(const int* cnt, int nw, int wa
 }
 
 __host__ __device__ constexpr size_t align16(size_t v) { return (v + 15) & ~size_t(15); }
+
+// The low 32 bits of the product of the low 24 bits of a and b, as the
+// full-rate v_mul_u32_u24 (a uniform).  Written as that one instruction since
+// the compiler otherwise folds the masks around a 24-bit multiply into a
+// quarter-rate 32-bit one.
+__device__ __forceinline__ uint32_t mul24(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_mul_u32_u24 %0, %1, %2" : "=v"(r) : "s"(a), "v"(b));
+  return r;
+}
+// the same with a divergent first operand
+__device__ __forceinline__ uint32_t mul24v(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_mul_u32_u24 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
 
 // Bucket words in LDS keep the fields of Eq. 3 with the slot above the
 // fingerprint: invalid << 23 | slot << (23 - m) | fingerprint, or, for an
@@ -175,6 +199,9 @@ struct Own {
 // bitmap, the index map and its fan words: per-wave counts of the three lists
 // for two compaction rounds, plus totals.
 constexpr int kPlanMiscWords = 6 * kMaxWaves + 4;
+// 16-bit entries of a wave's list of scan candidates: a wave appends at most
+// 64 to fewer than 64 pending ones before it walks 64 of them.
+constexpr int kPlanScanList = 128;
 // Words of the plan's reservation bitmap for S slots, padded to a multiple of
 // four so that the map behind it starts 16-byte aligned.
 __host__ __device__ constexpr int plan_bitmap_words(int S) { return (((S + 31) >> 5) + 3) & ~3; }
@@ -193,23 +220,20 @@ constexpr uint32_t kPlanDisp = 0x00000001u;       // another index whose home is
 __device__ __forceinline__ uint32_t plan_val(int slot) { return (static_cast<uint32_t>(slot) + 1u) << 1; }
 __device__ __forceinline__ int plan_slot(uint32_t w) { return static_cast<int>((w & kPlanSlot) >> 1) - 1; }
 
-// Home word and tag of index x in the plan's map of P words, from one
-// multiplicative hash h = x * 0x9E3779B1: with P = 2^p the home is the top p
-// bits of h and the tag the six bits below them; otherwise the home is
-// floor(h * P / 2^32) and the tag bits 8..13 of h.  The tag is kept in the
-// map word so that a probe passes over most foreign words without reading the
-// slot they name.
+// Home word and tag of index x in the plan's map of P words (P < 2^16), from
+// one multiplicative hash of the low 24 bits of x, h = x * 0x9E3779 mod 2^32:
+// the home is floor((h >> 16) * P / 2^16) (the top p bits of h when P = 2^p)
+// and the tag bits 8..13 of h.  Both multiplies are full-rate 24-bit ones.
+// The tag is kept in the map word so that a probe passes over most foreign
+// words without reading the slot they name.  Indices that share their low 24
+// bits share a home and a tag; the slot's index, read through c[], tells them
+// apart.
 struct PlanHash {
   uint32_t P;
-  int shift;   // 32 - p when P = 2^p, else 0
-  __device__ __forceinline__ explicit PlanHash(uint32_t words) : P(words), shift(0) {
-    if ((words & (words - 1u)) == 0u) shift = 32 - (31 - __builtin_clz(words));
-  }
-  __device__ __forceinline__ uint32_t hash(int32_t x) const { return static_cast<uint32_t>(x) * 0x9E3779B1u; }
-  __device__ __forceinline__ uint32_t home(uint32_t h) const { return shift ? h >> shift : __umulhi(h, P); }
-  __device__ __forceinline__ uint32_t tag(uint32_t h) const {
-    return (shift ? (h >> (shift - 6)) & 0x3Fu : (h >> 8) & 0x3Fu) << 24;
-  }
+  __device__ __forceinline__ explicit PlanHash(uint32_t words) : P(words) {}
+  __device__ __forceinline__ uint32_t hash(int32_t x) const { return mul24(0x9E3779u, static_cast<uint32_t>(x)); }
+  __device__ __forceinline__ uint32_t home(uint32_t h) const { return mul24(P, h >> 16) >> 16; }
+  __device__ __forceinline__ uint32_t tag(uint32_t h) const { return ((h >> 8) & 0x3Fu) << 24; }
   __device__ __forceinline__ uint32_t next(uint32_t h) const { return h + 1u == P ? 0u : h + 1u; }
 };
 
@@ -326,6 +350,28 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   // second pass.  A key is often cached in several slots outside the
   // reservations (copies left by lost installs), so most candidates bid.
   constexpr int kScan = 8;
+  // the walk of one candidate slot j: find its index's word, bid the slot
+  auto walk = [&](int j) __attribute__((always_inline)) {
+    const int32_t x = sc[j];
+    const uint32_t hx = ph.hash(x), tag = ph.tag(hx);
+    uint32_t h = ph.home(hx);
+    for (uint32_t t = 0; t < P; ++t) {
+      const uint32_t w = smp[h];
+      if (w == 0u) break;
+      if ((w & kPlanTag) == tag && sc[plan_slot(w)] == x) {
+        // the marks are final by now: keep the word's own
+        atomicMax(&smp[h], kPlanResident | tag | plan_val(j) | (w & kPlanDisp));
+        break;
+      }
+      h = ph.next(h);
+    }
+  };
+  // a wave's candidates are appended to its list in LDS and walked 64 at a
+  // time, one per lane, where the layout has room for the lists; otherwise
+  // each lane walks its own
+  uint16_t* wl = p.plan_scan_off ? reinterpret_cast<uint16_t*>(lds + p.plan_scan_off) + wave * kPlanScanList
+                                 : nullptr;
+  int pending = 0;   // entries in the wave's list (the same in every lane)
   for (int j0 = tid; j0 < S; j0 += kScan * MT) {
     int32_t xs[kScan];
     uint32_t cand = 0u;
@@ -344,24 +390,33 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
                       ((w & kPlanTag) == ph.tag(hx) || (w & kPlanDisp));
       cand |= ok ? (1u << u) : 0u;
     }
-    while (cand) {
-      const int u = __builtin_ctz(cand);
-      cand &= cand - 1u;
-      const int j = j0 + u * MT;
-      const int32_t x = sc[j];
-      const uint32_t hx = ph.hash(x), tag = ph.tag(hx);
-      uint32_t h = ph.home(hx);
-      for (uint32_t t = 0; t < P; ++t) {
-        const uint32_t w = smp[h];
-        if (w == 0u) break;
-        if ((w & kPlanTag) == tag && sc[plan_slot(w)] == x) {
-          // the marks are final by now: keep the word's own
-          atomicMax(&smp[h], kPlanResident | tag | plan_val(j) | (w & kPlanDisp));
-          break;
+    if (wl) {
+#pragma unroll
+      for (int u = 0; u < kScan; ++u) {
+        const bool c = (cand >> u) & 1u;
+        const uint64_t mk = __ballot(c);
+        if (c) wl[pending + bits_below(mk)] = static_cast<uint16_t>(j0 + u * MT);
+        pending += __popcll(mk);
+        if (pending >= 64) {
+          wave_sync();
+          walk(wl[lane]);
+          pending -= 64;
+          const int rest = lane < pending ? wl[64 + lane] : 0;
+          wave_sync();
+          if (lane < pending) wl[lane] = static_cast<uint16_t>(rest);
         }
-        h = ph.next(h);
+      }
+    } else {
+      while (cand) {
+        const int u = __builtin_ctz(cand);
+        cand &= cand - 1u;
+        walk(j0 + u * MT);
       }
     }
+  }
+  if (wl) {
+    wave_sync();
+    if (lane < pending) walk(wl[lane]);
   }
   __syncthreads();
 
@@ -479,10 +534,12 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
                               Publish& publish, int* plan_counts = nullptr) {
   constexpr int MT = NT, MW = NT / 64;
   static_assert(NT % 64 == 0 && NT <= kMatchThreads, "whole waves, at most the largest workgroup");
-  // probe rounds whose LDS reads are issued together (fewer with more indices
-  // per thread, whose registers would otherwise spill)
-  constexpr int kChainBatch = IPT <= 1 ? 4 : (IPT == 2 ? 2 : 1);
-  const int S = p.S, K = p.K, R = p.R;
+  // probe and chain rounds whose LDS reads are issued together: all R + 1 = 4
+  // of the default retry count with up to two indices per thread, one at a
+  // time with more (whose registers would otherwise spill)
+  constexpr int kChainBatch = IPT <= 2 ? 4 : 1;
+  // with two or more lifetimes per thread the table has exactly SPT * NT slots
+  const int S = SPT >= 2 ? SPT * MT : p.S, K = p.K, R = p.R;
   const uint32_t smask = static_cast<uint32_t>(S - 1);
   const Word W{static_cast<uint32_t>(p.m), smask, p.f_mask};
   int32_t* sc = reinterpret_cast<int32_t*>(lds);
@@ -526,9 +583,11 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
     reinterpret_cast<uint32_t*>(slife)[b] =
         Own::decay1((q.x >> 24) | ((q.y >> 24) << 8) | ((q.z >> 24) << 16) | (q.w & 0xFF000000u));
   };
+  // with the lifetimes per thread known, a thread keeps the index blocks it
+  // staged in, and the write back stores only those that changed
+  i32x4 cb[SPT >= 4 ? SPT / 4 : 1];
   if constexpr (SPT >= 4) {
     constexpr int NB = SPT / 4;
-    i32x4 cb[NB];
     u32x4 qb[NB];
 #pragma unroll
     for (int k = 0; k < NB; ++k) {
@@ -582,8 +641,8 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   const int32_t ver32 = (inv_all || inv_none) ? 0 : static_cast<int32_t>(n_verified);
   auto invalidated = [&](int32_t c) { return inv_all || (!inv_none && c >= ver32); };
   const uint32_t a1 = p.a1, a2 = p.a2, fmask = p.f_mask;
-  // (a x) mod S from the low m bits of a and x: their product is below 2^28
-  // (S <= 2^14), so the full-rate 24-bit multiply gives it exactly
+  // (a x) mod S from the low 24 bits of a mod S and of x (S divides 2^24):
+  // the full-rate 24-bit multiply gives the low 32 bits of their product
   const uint32_t a1m = a1 & smask, a2m = a2 & smask;
   const int m = p.m, L = p.L;
 
@@ -616,8 +675,8 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
     for (int u = 0; u < IPT; ++u) {
       act[u] = u * MT + tid < K;
       const uint32_t ux = static_cast<uint32_t>(xv[u]);
-      hh[u] = __umul24(a1m, ux & smask) & smask;          // initial bucket (Eq. 9)
-      dd[u] = (__umul24(a2m, ux & smask) & smask) | 1u;   // odd stride (Eq. 9)
+      hh[u] = mul24(a1m, ux) & smask;          // initial bucket (Eq. 9)
+      dd[u] = (mul24(a2m, ux) & smask) | 1u;   // odd stride (Eq. 9)
       found[u] = false;
       oo[u] = 0;
       if (act[u] && static_cast<uint32_t>(xv[u]) >= rows_u) st_bad++;
@@ -627,31 +686,39 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
     // round trips per batch instead of two per round; the first round whose
     // slot holds the index decides, as in the round-by-round probe
     for (int rd0 = 0; rd0 <= R; rd0 += kChainBatch) {
+      // every round of the batch is read, also rounds past R (their buckets
+      // are valid addresses and their words are ignored), so the reads carry
+      // no conditions and go out together
       uint32_t qw[IPT][kChainBatch];
       int32_t cv[IPT][kChainBatch];
 #pragma unroll
       for (int u = 0; u < IPT; ++u)
 #pragma unroll
-        for (int b = 0; b < kChainBatch; ++b)
-          if (u * MT < K && rd0 + b <= R) qw[u][b] = smap[(hh[u] + b * dd[u]) & smask];
+        for (int b = 0; b < kChainBatch; ++b) qw[u][b] = smap[(hh[u] + b * dd[u]) & smask];
 #pragma unroll
       for (int u = 0; u < IPT; ++u)
 #pragma unroll
-        for (int b = 0; b < kChainBatch; ++b)
-          if (u * MT < K && rd0 + b <= R) cv[u][b] = sc[W.slot(qw[u][b])];   // Eq. 10
+        for (int b = 0; b < kChainBatch; ++b) cv[u][b] = sc[W.slot(qw[u][b])];   // Eq. 10
       bool pending = false;
 #pragma unroll
       for (int u = 0; u < IPT; ++u) {
-        if (!act[u] || found[u]) continue;
+        // the first round of the batch whose slot holds the index
+        uint32_t wf = 0u;
+        bool hit = false;
 #pragma unroll
-        for (int b = 0; b < kChainBatch; ++b)
-          if (!found[u] && rd0 + b <= R && cv[u][b] == xv[u]) {
-            found[u] = true;
-            oo[u] = static_cast<int>(W.slot(qw[u][b]));
+        for (int b = kChainBatch - 1; b >= 0; --b)
+          if (rd0 + b <= R && cv[u][b] == xv[u]) {
+            hit = true;
+            wf = qw[u][b];
           }
-        if (!found[u]) {
-          hh[u] = (hh[u] + kChainBatch * dd[u]) & smask;   // unresolved probes advance (Eq. 11)
-          pending = pending || rd0 + kChainBatch <= R;
+        if (act[u] && !found[u]) {
+          if (hit) {
+            found[u] = true;
+            oo[u] = static_cast<int>(W.slot(wf));
+          } else {
+            hh[u] = (hh[u] + kChainBatch * dd[u]) & smask;   // unresolved probes advance (Eq. 11)
+            pending = pending || rd0 + kChainBatch <= R;
+          }
         }
       }
       if (!__ballot(pending)) break;
@@ -784,8 +851,8 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
           mo[u] = somiss[kr] & static_cast<int>(smask);
         }
         const uint32_t ux = static_cast<uint32_t>(mt[u]);
-        mh[u] = __umul24(a1m, ux & smask) & smask;
-        md[u] = (__umul24(a2m, ux & smask) & smask) | 1u;
+        mh[u] = mul24(a1m, ux) & smask;
+        md[u] = (mul24(a2m, ux) & smask) | 1u;
       }
       // a batch of rounds at a time, as in the probe: every word of the batch,
       // then the lifetime and id of each word's slot, then the first
@@ -833,7 +900,7 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
               first = b;
           if (first >= 0) {
             mv[u] = true;
-            mh[u] = (mh[u] + __umul24(static_cast<uint32_t>(first), md[u])) & smask;
+            mh[u] = (mh[u] + mul24v(static_cast<uint32_t>(first), md[u])) & smask;
           } else {
             mh[u] = (mh[u] + kChainBatch * md[u]) & smask;
             pending = pending || rd0 + kChainBatch <= R;
@@ -896,7 +963,37 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
   // the rest of the plan's words, which the write back does not read.
   const bool plan = p.plan_words > 0;
   int st_inv = 0;
-  if ((S & (4 * MT - 1)) == 0) {
+  auto write_block = [&](int b, i32x4 c, bool store_c) __attribute__((always_inline)) {
+      const u32x4 m = reinterpret_cast<const u32x4*>(smap)[b];
+      const uint32_t l = reinterpret_cast<const uint32_t*>(slife)[b];
+      if (plan) {
+        reinterpret_cast<u32x4*>(smap)[b] = 0u;
+        reinterpret_cast<uint32_t*>(slife)[b] = 0u;
+      }
+      st_col -= last_token_bid(m.x) + last_token_bid(m.y) + last_token_bid(m.z) + last_token_bid(m.w);
+      u32x4 q;
+      q.x = (l << 24) | W.canonical(m.x);
+      q.y = ((l << 16) & 0xFF000000u) | W.canonical(m.y);
+      q.z = ((l << 8) & 0xFF000000u) | W.canonical(m.z);
+      q.w = (l & 0xFF000000u) | W.canonical(m.w);
+      if (store_c) reinterpret_cast<i32x4*>(gc)[b] = c;
+      reinterpret_cast<u32x4*>(gq)[b] = q;
+  };
+  if constexpr (SPT >= 4) {
+#pragma unroll
+    for (int k = 0; k < SPT / 4; ++k) {
+      const int b = tid + k * MT;
+      i32x4 c = reinterpret_cast<const i32x4*>(sc)[b];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (invalidated(c[e])) {
+          c[e] = -1;
+          st_inv++;
+        }
+      const bool same = c.x == cb[k].x && c.y == cb[k].y && c.z == cb[k].z && c.w == cb[k].w;
+      write_block(b, c, !same);
+    }
+  } else if ((S & (4 * MT - 1)) == 0) {
     // four entries per 16-byte store
     for (int b = tid; b < S / 4; b += MT) {
       i32x4 c = reinterpret_cast<const i32x4*>(sc)[b];

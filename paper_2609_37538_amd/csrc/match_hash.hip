@@ -183,9 +183,15 @@ constexpr size_t kWorkgroupLds = 160 * 1024;
 // The plan's LDS: c[] (4 S bytes, padded to 16) stays, then the reservation
 // bitmap, P map words, P fan words and its counters.  Where there is room, the
 // step's transfer list (2 bytes per entry, n_q K entries at most) is kept at
-// the end, past both the token loop's arrays and the plan's words; otherwise
-// the plan reads the list back from device memory.
+// the end, past both the token loop's arrays and the plan's words, and behind
+// it the scan's candidate lists (kPlanScanList 16-bit slots per wave);
+// otherwise the plan reads the list back from device memory, or walks each
+// lane's candidates in that lane.
 static size_t plan_list_bytes(int K, int n_q) { return align16(2 * static_cast<size_t>(n_q) * K); }
+
+static size_t plan_scan_bytes(int S, int K) {
+  return align16(2 * static_cast<size_t>(kPlanScanList) * (match_threads(S, K) / 64));
+}
 
 static size_t plan_words_end(int S, long long P) {
   return align16(4 * static_cast<size_t>(S)) + 4 * plan_state_words(S, static_cast<int>(P));
@@ -206,32 +212,37 @@ static long long plan_words_for(long long words, long long keys) {
 struct PlanLayout {
   int P;             // map words (0: no plan fits)
   size_t list_off;   // LDS offset of the kept transfer list (0: none)
+  size_t scan_off;   // LDS offset of the scan's candidate lists (0: none)
   size_t total;      // LDS bytes of the matching workgroup
 };
 
+// Tried in order: the list and the candidate lists, the list alone, neither.
 static PlanLayout plan_layout(int S, int K, int n_q) {
   const size_t m = match_lds_bytes(S, K);
-  if (m == 0 || n_q < 1 || S > 65536) return {0, 0, 0};   // kept slots are 16-bit values
+  if (m == 0 || n_q < 1 || S > 65536) return {0, 0, 0, 0};   // kept slots are 16-bit values
   const size_t A = align16(4 * static_cast<size_t>(S));
   const long long keys = static_cast<long long>(n_q) * K;
   const long long fixed = plan_bitmap_words(S) + kPlanMiscWords;   // besides map and fan words
-  const size_t list = plan_list_bytes(K, n_q);
-  if (align16(m) + list <= kWorkgroupLds) {
-    const long long P = plan_words_for(static_cast<long long>((kWorkgroupLds - list - A) / 4) - fixed, keys);
-    if (P > 0) {
-      const size_t e = plan_words_end(S, P), off = align16(m > e ? m : e);
-      return {static_cast<int>(P), off, off + list};
-    }
+  const size_t list = plan_list_bytes(K, n_q), scan = plan_scan_bytes(S, K);
+  for (int with_scan = 1; with_scan >= 0; --with_scan) {
+    const size_t extra = list + (with_scan ? scan : 0);
+    if (align16(m) + extra > kWorkgroupLds) continue;
+    const long long P = plan_words_for(static_cast<long long>((kWorkgroupLds - extra - A) / 4) - fixed, keys);
+    if (P == 0) continue;
+    const size_t e = plan_words_end(S, P), off = align16(m > e ? m : e);
+    return {static_cast<int>(P), off, with_scan ? off + list : 0, off + extra};
   }
   const long long P = plan_words_for(static_cast<long long>((kWorkgroupLds - A) / 4) - fixed, keys);
-  if (P == 0) return {0, 0, 0};
+  if (P == 0) return {0, 0, 0, 0};
   const size_t e = plan_words_end(S, P);
-  return {static_cast<int>(P), 0, m > e ? m : e};
+  return {static_cast<int>(P), 0, 0, m > e ? m : e};
 }
 
 int plan_map_words(int S, int K, int n_q) { return plan_layout(S, K, n_q).P; }
 
 size_t plan_list_offset(int S, int K, int n_q) { return plan_layout(S, K, n_q).list_off; }
+
+size_t plan_scan_offset(int S, int K, int n_q) { return plan_layout(S, K, n_q).scan_off; }
 
 size_t stage_one_lds_bytes(int S, int K, int n_q, bool plan) {
   const size_t m = match_lds_bytes(S, K);

@@ -441,7 +441,10 @@ RESIDENT_CASES = [
     ("batch_1024_max", dict(batch=1024, topk=16, slots=64, n_q=2, steps=6, ctx=400), 0),
     ("four_waves", dict(batch=3, topk=384, slots=1024, n_q=2, steps=12, ctx=6000, retention=0.8), 0),
     # the largest plans that fit one workgroup's LDS: with the transfer list
-    # kept in LDS (53 tokens) and read back from device memory (62 tokens)
+    # and the scan's per-wave candidate lists in LDS (39 tokens), with the
+    # transfer list alone (53 tokens; each lane walks its own candidates) and
+    # with the list read back from device memory (62 tokens)
+    ("lds_edge_scan", dict(batch=2, topk=128, slots=16384, n_q=39, steps=6, ctx=60000), 3),
     ("lds_edge_list", dict(batch=2, topk=128, slots=16384, n_q=53, steps=6, ctx=60000), 3),
     ("lds_edge_no_list", dict(batch=2, topk=128, slots=16384, n_q=62, steps=6, ctx=60000), 3),
 ]
