@@ -699,6 +699,8 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
       for (int u = 0; u < IPT; ++u)
 #pragma unroll
         for (int b = 0; b < kChainBatch; ++b) cv[u][b] = sc[W.slot(qw[u][b])];   // Eq. 10
+      // the decision takes selects and bitwise tests only: a branch on a
+      // round's test would let the compiler move that round's reads behind it
       bool pending = false;
 #pragma unroll
       for (int u = 0; u < IPT; ++u) {
@@ -706,20 +708,17 @@ __device__ __forceinline__ void match_request(const MatchParams& p, const int r,
         uint32_t wf = 0u;
         bool hit = false;
 #pragma unroll
-        for (int b = kChainBatch - 1; b >= 0; --b)
-          if (rd0 + b <= R && cv[u][b] == xv[u]) {
-            hit = true;
-            wf = qw[u][b];
-          }
-        if (act[u] && !found[u]) {
-          if (hit) {
-            found[u] = true;
-            oo[u] = static_cast<int>(W.slot(wf));
-          } else {
-            hh[u] = (hh[u] + kChainBatch * dd[u]) & smask;   // unresolved probes advance (Eq. 11)
-            pending = pending || rd0 + kChainBatch <= R;
-          }
+        for (int b = kChainBatch - 1; b >= 0; --b) {
+          const bool m = (cv[u][b] == xv[u]) & (rd0 + b <= R);
+          hit = hit | m;
+          wf = m ? qw[u][b] : wf;
         }
+        const bool open = act[u] & !found[u];
+        oo[u] = (open & hit) ? static_cast<int>(W.slot(wf)) : oo[u];
+        found[u] = found[u] | (open & hit);
+        // unresolved probes advance (Eq. 11)
+        hh[u] = (open & !hit) ? (hh[u] + kChainBatch * dd[u]) & smask : hh[u];
+        pending = pending | (open & !hit & (rd0 + kChainBatch <= R));
       }
       if (!__ballot(pending)) break;
     }
