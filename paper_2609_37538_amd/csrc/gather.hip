@@ -48,7 +48,7 @@ __global__ __launch_bounds__(GT) void gather_balanced_kernel(GatherParams p) {
 // spreads them over many CUs (one workgroup reads ~2.5 GB/s from the host).
 // claim[0] and claim[1] count the claimed resident and host rows; the
 // matching kernel resets both.
-constexpr int kHostTile = 32;
+constexpr int kHostTile = 6;
 
 // Rows per tile of a list of n entries shared by `group` workgroups.
 __device__ __forceinline__ int tile_rows(long long n, int group, int max_rows) {
