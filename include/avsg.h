@@ -75,8 +75,9 @@ typedef int32_t avsg_status;
                                    was lost to an exhausted probe chain or a bucket collision, so the probe of
                                    Eq. 8-11 cannot find it) is copied from that slot; a miss that repeats a
                                    miss of another token of the step (same index) is written by that index's
-                                   host copy (further repeats, from three tokens on, are copied from its slot).  Host rows go
-                                   in 32-row tiles claimed by every CU.  Slots, counts, tables and buffer
+                                   host copy, which fills up to two such repeats (further repeats, from four
+                                   tokens on, are copied from its slot).  Host rows go in 6-row tiles claimed
+                                   by every CU.  Slots, counts, tables and buffer
                                    contents are identical to AVSG_GATHER_BALANCED.  Relies on the same
                                    property as a hit: a cached row below the verified length does not change
                                    on the host. */
@@ -178,8 +179,8 @@ avsg_status avsg_resolve_config(const avsg_config *cfg, avsg_config *out);
  * workspace that avsg_create needs for cfg
  * (per-request tables of 8*S bytes, transfer lists of 8*N_q*K bytes, a hit
  * mask of N_q*K bytes, counters and pointer tables; with AVSG_GATHER_RESIDENT
- * or AVSG_GATHER_EARLY three more lists of 8*N_q*K bytes and fan slots of
- * 4*N_q*K bytes per request;
+ * or AVSG_GATHER_EARLY three more lists of 8*N_q*K bytes and fan slot pairs
+ * of 8*N_q*K bytes per request;
  * with AVSG_GATHER_EARLY also early keys, positions and finish entries of
  * 36*N_q*K bytes per request and the staging rows (early_staging_rows, by
  * default min(B*N_q*K, 16384), times the row bytes of every stream); with
@@ -290,15 +291,17 @@ avsg_status avsg_export_misses(avsg_handle *h, int32_t r, int32_t *n_out, int32_
  * indices), copied to host memory (synchronous); every list keeps
  * transfer-list order and has capacity N_q*K:
  *   n_host, host_x[k], host_o[k],  misses copied from host row host_x[k] into
- *   host_fan[k]                    slot host_o[k], and also into slot
- *                                  host_fan[k] when it is not -1 (the largest
- *                                  repeat destination of the index, below);
+ *   host_fan[2k], host_fan[2k+1]   slot host_o[k], and also into slots
+ *                                  host_fan[2k] and host_fan[2k+1] where they
+ *                                  are not -1 (the two largest repeat
+ *                                  destinations of the index, larger first;
+ *                                  host_fan has capacity 2*N_q*K);
  *   n_res, res_src[k], res_dst[k]  misses whose row is already in slot
  *                                  res_src[k] (the largest slot outside this
  *                                  step's reservations that caches the index
  *                                  below the verified length): copied slot to
  *                                  slot, alongside the host copies;
- *   n_rep, rep_src[k], rep_dst[k]  further repeats of an index missed by three
+ *   n_rep, rep_src[k], rep_dst[k]  further repeats of an index missed by four
  *                                  or more tokens of the step: copied from the
  *                                  largest slot this step reserved for it, after
  *                                  the host copies.
@@ -321,7 +324,7 @@ avsg_status avsg_export_early(avsg_handle *h, int32_t r, int32_t *n_out, int32_t
  * avsg_timing copies up to `cap` recorded steps (synchronizing):
  * match_ms[i] is the duration of step i's matching kernel, gather_ms[i] that
  * of its main Stage Two kernel (or copies), and tail_ms[i] (may be NULL) the
- * rest of Stage Two: the repeat copies of AVSG_GATHER_RESIDENT with three or
+ * rest of Stage Two: the repeat copies of AVSG_GATHER_RESIDENT with four or
  * more tokens per step, 0 otherwise.  AVSG_GATHER_EARLY: match_ms is the early
  * list kernel, gather_ms the launch that matches and copies, tail_ms the
  * finishing kernel. */

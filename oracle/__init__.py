@@ -324,11 +324,13 @@ def transfer_plan(miss_x, miss_o, c_after, rows_r: int):
         copy j -> o from the largest such j (its row arrived in an earlier step);
       - else, if o is the largest slot this step reserved for x, a host entry;
       - else a repeat of that host entry.
-    Each host entry also carries a fan slot: the largest repeat destination of
-    its index (-1 if none), which the host copy writes too; the other repeats
-    stay in the repeat list, copied from the host entry's slot.
+    Each host entry also carries two fan slots: the two largest repeat
+    destinations of its index, larger first (-1 where there are fewer), which
+    the host copy writes too; the other repeats stay in the repeat list,
+    copied from the host entry's slot.
     Each list keeps transfer-list order.  Returns
-    (host_x, host_o, host_fan, res_src, res_dst, rep_src, rep_dst) as int32 arrays.
+    (host_x, host_o, host_fan, res_src, res_dst, rep_src, rep_dst) as int32
+    arrays, host_fan of shape (n_host, 2).
     """
     miss_x = [int(v) for v in miss_x]
     miss_o = [int(v) for v in miss_o]
@@ -344,10 +346,11 @@ def transfer_plan(miss_x, miss_o, c_after, rows_r: int):
     for x, o in zip(miss_x, miss_o):
         if 0 <= x < rows_r:
             first[x] = max(first.get(x, -1), o)
-    fan = {}
+    repeats = {}
     for x, o in zip(miss_x, miss_o):
         if 0 <= x < rows_r and x not in resident and first[x] != o:
-            fan[x] = max(fan.get(x, -1), o)
+            repeats.setdefault(x, []).append(o)
+    fan = {x: sorted(v, reverse=True)[:2] for x, v in repeats.items()}
     lists = [[] for _ in range(7)]
     for x, o in zip(miss_x, miss_o):
         valid = 0 <= x < rows_r
@@ -355,14 +358,16 @@ def transfer_plan(miss_x, miss_o, c_after, rows_r: int):
             lists[3].append(resident[x])
             lists[4].append(o)
         elif valid and first[x] != o:
-            if fan[x] != o:
+            if o not in fan[x]:
                 lists[5].append(first[x])
                 lists[6].append(o)
         else:
             lists[0].append(x)
             lists[1].append(o)
-            lists[2].append(fan.get(x, -1) if valid else -1)
-    return tuple(np.asarray(v, dtype=np.int32) for v in lists)
+            lists[2].append(((fan.get(x, []) if valid else []) + [-1, -1])[:2])
+    out = [np.asarray(v, dtype=np.int32) for v in lists]
+    out[2] = out[2].reshape(-1, 2)
+    return tuple(out)
 
 
 EARLY_MAX_POSITIONS = 4

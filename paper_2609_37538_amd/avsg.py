@@ -263,14 +263,17 @@ def avsg_import_state(h, r: int, c, q, stream: int = 0) -> None:
 
 def avsg_export_plan(h, r: int, capacity: int):
     """(host_x, host_o, host_fan, res_src, res_dst, rep_src, rep_dst) of request
-    r's last Stage Two plan."""
+    r's last Stage Two plan; host_fan has two columns (the two fan slots of
+    each host entry, -1 = none)."""
     n = [ctypes.c_int32(0) for _ in range(3)]
-    a = [np.empty(capacity, dtype=np.int32) for _ in range(7)]
+    a = [np.empty(2 * capacity if k == 2 else capacity, dtype=np.int32) for k in range(7)]
     P = [x.ctypes.data_as(_P) for x in a]
     _check(load().avsg_export_plan(h, r, ctypes.byref(n[0]), P[0], P[1], P[2], ctypes.byref(n[1]), P[3], P[4],
                                    ctypes.byref(n[2]), P[5], P[6]), "avsg_export_plan", h)
     sizes = [n[0].value] * 3 + [n[1].value] * 2 + [n[2].value] * 2
-    return tuple(a[k][: sizes[k]].copy() for k in range(7))
+    out = [a[k][: sizes[k]].copy() for k in range(7)]
+    out[2] = a[2][: 2 * sizes[2]].reshape(sizes[2], 2).copy()
+    return tuple(out)
 
 
 def avsg_export_misses(h, r: int, capacity: int):

@@ -33,7 +33,7 @@ struct avsg_handle {
   int2* miss_list = nullptr;
   uint8_t* hit_mask = nullptr;
   int2* host_list = nullptr;    // resident-reuse plan (AVSG_GATHER_RESIDENT)
-  int32_t* host_fan = nullptr;
+  int2* host_fan = nullptr;
   int2* res_list = nullptr;
   int2* rep_list = nullptr;
   int32_t* plan_counts = nullptr;  // [B][3]
@@ -158,9 +158,8 @@ Layout layout_of(const avsg_config& c) {
   L.miss_list = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk * 8);
   L.hit_mask = off; off += up(B * static_cast<size_t>(c.n_q) * c.topk);
   L.plan = off;
-  if (has_plan(c))   // host, resident, repeat lists; fan slots; counts; claims
-    off += 3 * up(B * static_cast<size_t>(c.n_q) * c.topk * 8) + up(B * static_cast<size_t>(c.n_q) * c.topk * 4) +
-           up(B * 12) + up(8);
+  if (has_plan(c))   // host, resident, repeat lists; fan slot pairs; counts; claims
+    off += 4 * up(B * static_cast<size_t>(c.n_q) * c.topk * 8) + up(B * 12) + up(8);
   L.early = off;
   if (c.gather_mode == AVSG_GATHER_EARLY) off += early_sections(c)[8];
   L.pipe = off;
@@ -302,8 +301,8 @@ void bind_workspace(avsg_handle* h, unsigned char* ws, const Layout& L) {
     h->host_list = reinterpret_cast<int2*>(ws + L.plan);
     h->res_list = reinterpret_cast<int2*>(ws + L.plan + list);
     h->rep_list = reinterpret_cast<int2*>(ws + L.plan + 2 * list);
-    const size_t fan = up(static_cast<size_t>(B) * c.n_q * c.topk * 4);
-    h->host_fan = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list);
+    const size_t fan = list;   // two slots per host entry
+    h->host_fan = reinterpret_cast<int2*>(ws + L.plan + 3 * list);
     h->plan_counts = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan);
     h->plan_claim = reinterpret_cast<int32_t*>(ws + L.plan + 3 * list + fan + up(static_cast<size_t>(B) * 12));
     h->plan_words = plan_map_words(c.slots, c.topk, c.n_q);
@@ -714,7 +713,7 @@ static avsg_status enqueue_step(avsg_handle* h, const int32_t* d_topk, const int
     case AVSG_GATHER_REQUEST: HIP_TRY(h, launch_gather_request(g, s)); break;
     case AVSG_GATHER_POSITION: HIP_TRY(h, launch_gather_position(g, h->workers, s)); break;
     case AVSG_GATHER_RESIDENT: {
-      // host list (each row also to its fan slot) and resident copies in one
+      // host list (each row also to its fan slots) and resident copies in one
       // kernel, then the repeats left over
       GatherParams gh = g, gr = g;
       gh.miss_counts = h->plan_counts; gh.counts_per_req = 1; gh.count_stride = 3;
@@ -723,10 +722,10 @@ static avsg_status enqueue_step(avsg_handle* h, const int32_t* d_topk, const int
       gr.miss_list = h->res_list;
       HIP_TRY(h, launch_gather_resident(gh, gr, h->plan_claim, h->workers, s));
       if ((rc = record(h, 2, s)) != AVSG_OK) return rc;
-      // the host copies also fill each index's last repeat, so repeats are
-      // left only with three or more tokens per step; they are few and
-      // HBM-latency bound, so they get more, smaller workgroups
-      if (c.n_q > 2) {
+      // the host copies also fill each index's two largest repeats, so
+      // repeats are left only with four or more tokens per step; they are few
+      // and HBM-latency bound, so they get more, smaller workgroups
+      if (c.n_q > 3) {
         g.miss_counts = h->plan_counts + 2; g.counts_per_req = 1; g.count_stride = 3;
         g.miss_list = h->rep_list;
         HIP_TRY(h, launch_copy_device(g, kRepeatWorkersPerCu * std::max(1, h->cus), s));
@@ -740,7 +739,7 @@ static avsg_status enqueue_step(avsg_handle* h, const int32_t* d_topk, const int
   }
   // a fourth event only when Stage Two has a tail kernel (each record costs
   // the step stream a few microseconds)
-  const bool tail = c.gather_mode == AVSG_GATHER_RESIDENT && c.n_q > 2;
+  const bool tail = c.gather_mode == AVSG_GATHER_RESIDENT && c.n_q > 3;
   if (c.gather_mode != AVSG_GATHER_RESIDENT && (rc = record(h, 2, s)) != AVSG_OK) return rc;
   if (tail && (rc = record(h, 3, s)) != AVSG_OK) return rc;
   if (h->timing && h->n_timed < kMaxTimedSteps) h->has_tail[h->n_timed++] = tail;
@@ -959,7 +958,7 @@ avsg_status avsg_export_plan(avsg_handle* h, int32_t r, int32_t* n_host, int32_t
     }
   }
   if (cnt[0] > 0)
-    HIP_TRY(h, hipMemcpy(host_fan, h->host_fan + base, static_cast<size_t>(cnt[0]) * 4,
+    HIP_TRY(h, hipMemcpy(host_fan, h->host_fan + base, static_cast<size_t>(cnt[0]) * 8,
                          hipMemcpyDeviceToHost));
   *n_host = cnt[0];
   *n_res = cnt[1];

@@ -54,7 +54,7 @@ struct MatchParams {
   int32_t plan_list_off;        // LDS byte offset of the step's transfer list kept as 16-bit slots
   int32_t plan_scan_off;        // LDS byte offset of the scan's per-wave candidate lists (0: none)
   int2* host_list;              // [B][n_q*K] (index, slot) copied from the host
-  int32_t* host_fan;            // [B][n_q*K] second slot a host entry is also copied to, or -1
+  int2* host_fan;               // [B][n_q*K] the two further slots a host entry is also copied to (-1: none)
   int2* res_list;               // [B][n_q*K] (source slot, slot): row already resident
   int2* rep_list;               // [B][n_q*K] (source slot, slot): repeat of a host entry
   int32_t* plan_counts;         // [B][3] host, resident, repeat entries
@@ -72,7 +72,7 @@ struct GatherParams {
   const int32_t* miss_counts;
   int32_t counts_per_req, count_stride;
   const int2* miss_list;        // [B][n_q*K] (index or source slot, slot)
-  const int32_t* fan;           // [B][n_q*K] second destination slot per entry (-1: none), or nullptr
+  const int2* fan;              // [B][n_q*K] two further destination slots per entry (-1: none), or nullptr
   const int64_t* rows;          // [B]
   int32_t n_streams;
   const uint64_t* host_ptrs;    // [n_streams][B] device-visible addresses of host row 0
@@ -122,7 +122,7 @@ struct EarlyParams {
   int64_t row_bytes0, row_bytes1;
   // the matching workgroup's own lists (resident-reuse plan of the rest)
   const int2* host_list;
-  const int32_t* host_fan;
+  const int2* host_fan;
   const int2* res_list;
   const int2* rep_list;
 };

@@ -12,9 +12,9 @@
 // position kernel (S2, Eq. 14) splits the flattened N_g*K selected positions
 // into C near-equal contiguous ranges; hit positions issue no copy but still
 // occupy their worker's share.  With the resident-reuse plan of the matching
-// kernel, the resident kernel copies the host list (each row also to its fan
-// slot) and the rows already in the device buffer; with three or more tokens
-// per step the device-copy kernel then fills the repeats left over.
+// kernel, the resident kernel copies the host list (each row also to its two
+// fan slots) and the rows already in the device buffer; with four or more
+// tokens per step the device-copy kernel then fills the repeats left over.
 #include "gather_body.h"
 
 namespace avsg {
@@ -33,7 +33,7 @@ __global__ __launch_bounds__(GT) void gather_balanced_kernel(GatherParams p) {
 }
 
 // Resident-reuse Stage Two over two lists: host rows (each also written to
-// its fan slot, the last repeat of its index in the step), and rows already
+// its fan slots, the two largest repeats of its index in the step), and rows already
 // in a slot of the same request (not written this step).  The last quarter of the
 // workgroups starts with the resident list and the others with the host list,
 // so the HBM copies run while the host link is busy (the link saturates with
@@ -62,7 +62,7 @@ template <bool kDevice>
 __device__ void copy_tiles(const GatherParams& p, const long long* pre, long long n, int T, long long first,
                            long long base, int* counter, long long* next, uint64_t* src0,
                            uint64_t* dst0, uint64_t* src1, uint64_t* dst1, uint64_t* dstx0 = nullptr,
-                           uint64_t* dstx1 = nullptr) {
+                           uint64_t* dstx1 = nullptr, uint64_t* dsty0 = nullptr, uint64_t* dsty1 = nullptr) {
   long long t0 = first;
   for (;;) {
     if (t0 < 0) {
@@ -72,7 +72,8 @@ __device__ void copy_tiles(const GatherParams& p, const long long* pre, long lon
       __syncthreads();
     }
     if (t0 >= n) break;
-    copy_range<kDevice>(p, pre, t0, t0 + T < n ? t0 + T : n, src0, dst0, src1, dst1, dstx0, dstx1);
+    copy_range<kDevice>(p, pre, t0, t0 + T < n ? t0 + T : n, src0, dst0, src1, dst1, dstx0, dstx1, dsty0,
+                        dsty1);
     t0 = -1;
   }
 }
@@ -80,11 +81,11 @@ __device__ void copy_tiles(const GatherParams& p, const long long* pre, long lon
 __global__ __launch_bounds__(GT) void gather_resident_kernel(GatherParams hp, GatherParams rp,
                                                               int* claim) {
   __shared__ long long pre_h[kMaxBatch + 1], pre_r[kMaxBatch + 1];
-  __shared__ long long wtot[GT / 64];
-  __shared__ uint64_t src0[TILE], dst0[TILE], src1[TILE], dst1[TILE], dstx0[TILE], dstx1[TILE];
+  __shared__ long long wtot[2 * (GT / 64)];
+  __shared__ uint64_t src0[TILE], dst0[TILE], src1[TILE], dst1[TILE], dstx0[TILE], dstx1[TILE], dsty0[TILE],
+      dsty1[TILE];
   __shared__ long long next;
-  request_prefix(hp, pre_h, wtot);
-  request_prefix(rp, pre_r, wtot);
+  request_prefix2(hp, pre_h, rp, pre_r, wtot);
   const long long N = pre_h[hp.B], R = pre_r[rp.B];
   const int C = static_cast<int>(gridDim.x), w = static_cast<int>(blockIdx.x);
   const int cr = C / 4;                  // workgroups that start with the resident list (may be 0)
@@ -96,10 +97,10 @@ __global__ __launch_bounds__(GT) void gather_resident_kernel(GatherParams hp, Ga
     const long long i = C - 1 - w;       // 0 .. cr-1
     copy_tiles<true>(rp, pre_r, R, tr, i * tr, res_base, claim, &next, src0, dst0, src1, dst1);
     copy_tiles<false>(hp, pre_h, N, th, -1, host_base, claim + 1, &next, src0, dst0, src1, dst1,
-                      dstx0, dstx1);
+                      dstx0, dstx1, dsty0, dsty1);
   } else {
     copy_tiles<false>(hp, pre_h, N, th, static_cast<long long>(w) * th, host_base, claim + 1,
-                      &next, src0, dst0, src1, dst1, dstx0, dstx1);
+                      &next, src0, dst0, src1, dst1, dstx0, dstx1, dsty0, dsty1);
     copy_tiles<true>(rp, pre_r, R, tr, -1, res_base, claim, &next, src0, dst0, src1, dst1);
   }
 }

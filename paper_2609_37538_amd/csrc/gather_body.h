@@ -55,6 +55,65 @@ __device__ inline void request_prefix(const GatherParams& p, long long* pre, lon
   __syncthreads();
 }
 
+// The exclusive prefixes of two lists' per-request totals (pre_a and pre_b,
+// B + 1 entries each), both lists' counts loaded before either is summed so
+// the two reads of device memory overlap.  wtot: 2 * GT / 64 entries.
+__device__ inline void request_prefix2(const GatherParams& pa, long long* pre_a, const GatherParams& pb,
+                                       long long* pre_b, long long* wtot) {
+  const int tid = threadIdx.x, lane = lane_index(), wave = tid >> 6;
+  constexpr int NW = GT / 64;
+  const int per = (pa.B + GT - 1) / GT;
+  const int r0 = tid * per;
+  long long la = 0, lb = 0;
+  for (int k = 0; k < per; ++k) {
+    const int r = r0 + k;
+    if (r < pa.B) {
+      long long ta = 0, tb = 0;
+      for (int g = 0; g < pa.counts_per_req; ++g)
+        ta += pa.miss_counts[static_cast<size_t>(r) * pa.count_stride + g];
+      for (int g = 0; g < pb.counts_per_req; ++g)
+        tb += pb.miss_counts[static_cast<size_t>(r) * pb.count_stride + g];
+      pre_a[r + 1] = ta;
+      pre_b[r + 1] = tb;
+      la += ta;
+      lb += tb;
+    }
+  }
+  long long ia = la, ib = lb;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const long long ta = __shfl_up(ia, off, 64), tb = __shfl_up(ib, off, 64);
+    if (lane >= off) {
+      ia += ta;
+      ib += tb;
+    }
+  }
+  if (lane == 63) {
+    wtot[wave] = ia;
+    wtot[NW + wave] = ib;
+  }
+  __syncthreads();
+  long long ba = ia - la, bb = ib - lb;
+  for (int w = 0; w < wave; ++w) {
+    ba += wtot[w];
+    bb += wtot[NW + w];
+  }
+  for (int k = 0; k < per; ++k) {
+    const int r = r0 + k;
+    if (r < pa.B) {
+      ba += pre_a[r + 1];
+      bb += pre_b[r + 1];
+      pre_a[r + 1] = ba;
+      pre_b[r + 1] = bb;
+    }
+  }
+  if (tid == 0) {
+    pre_a[0] = 0;
+    pre_b[0] = 0;
+  }
+  __syncthreads();
+}
+
 __device__ __forceinline__ int find_request(const long long* pre, int B, long long j) {
   int lo = 0, hi = B;  // pre[lo] <= j < pre[hi]
   while (hi - lo > 1) {
@@ -70,28 +129,32 @@ __device__ __forceinline__ int find_request(const long long* pre, int B, long lo
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // Rows i < tn: copy chunks * sizeof(V) bytes from src[i] to dst[i] (src[i] == 0
-// skips the row), and also to dstx[i] when dstx is given and dstx[i] != 0, with
-// NT threads each keeping U loads in flight.
+// skips the row), and also to dstx[i] and dsty[i] where those are given and
+// nonzero, with NT threads each keeping U loads in flight.
 template <typename V, int U = kUnroll, int NT = GT>
 __device__ __forceinline__ void copy_rows(const uint64_t* src, const uint64_t* dst, int tn,
-                                          int chunks, const uint64_t* dstx = nullptr) {
+                                          int chunks, const uint64_t* dstx = nullptr,
+                                          const uint64_t* dsty = nullptr) {
   const int total = tn * chunks;
   for (int q0 = threadIdx.x; q0 < total; q0 += NT * U) {
     V v[U];
-    uint64_t da[U], xa[U];
+    uint64_t da[U], xa[U], ya[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int q = q0 + u * NT;
       da[u] = 0;
       xa[u] = 0;
+      ya[u] = 0;
       if (q < total) {
         const int i = q / chunks;
         const int ch = q - i * chunks;
         const uint64_t s = src[i];
         if (s) {
-          v[u] = *reinterpret_cast<const V*>(s + static_cast<uint64_t>(ch) * sizeof(V));
-          da[u] = dst[i] + static_cast<uint64_t>(ch) * sizeof(V);
-          if (dstx && dstx[i]) xa[u] = dstx[i] + static_cast<uint64_t>(ch) * sizeof(V);
+          const uint64_t off = static_cast<uint64_t>(ch) * sizeof(V);
+          v[u] = *reinterpret_cast<const V*>(s + off);
+          da[u] = dst[i] + off;
+          if (dstx && dstx[i]) xa[u] = dstx[i] + off;
+          if (dsty && dsty[i]) ya[u] = dsty[i] + off;
         }
       }
     }
@@ -99,6 +162,7 @@ __device__ __forceinline__ void copy_rows(const uint64_t* src, const uint64_t* d
     for (int u = 0; u < U; ++u) {
       if (da[u]) *reinterpret_cast<V*>(da[u]) = v[u];
       if (xa[u]) *reinterpret_cast<V*>(xa[u]) = v[u];
+      if (ya[u]) *reinterpret_cast<V*>(ya[u]) = v[u];
     }
   }
 }
@@ -121,12 +185,13 @@ __device__ inline void copy_tile_rows(const GatherParams& p, int tn, uint64_t* s
 
 // Copy entries [a, b) of the batch-wide list.  kDevice: an entry is (source
 // slot, slot) of the request's own buffers; otherwise (host row, slot), and
-// with p.fan and staging for it (dstx0/1), the row also goes to the entry's
-// fan slot.
+// with p.fan and staging for it (dstx0/1, dsty0/1), the row also goes to the
+// entry's fan slots.
 template <bool kDevice>
-__device__ void copy_range(const GatherParams& p, const long long* pre, long long a, long long b,
+__device__ __forceinline__ void copy_range(const GatherParams& p, const long long* pre, long long a, long long b,
                            uint64_t* src0, uint64_t* dst0, uint64_t* src1, uint64_t* dst1,
-                           uint64_t* dstx0 = nullptr, uint64_t* dstx1 = nullptr) {
+                           uint64_t* dstx0 = nullptr, uint64_t* dstx1 = nullptr,
+                           uint64_t* dsty0 = nullptr, uint64_t* dsty1 = nullptr) {
   const size_t per_req = static_cast<size_t>(p.n_q) * p.K;
   for (long long t0 = a; t0 < b; t0 += TILE) {
     const int tn = static_cast<int>((b - t0) < TILE ? (b - t0) : TILE);
@@ -140,29 +205,34 @@ __device__ void copy_range(const GatherParams& p, const long long* pre, long lon
       const uint64_t base0 = kDevice ? p.buf_ptrs[r] : p.host_ptrs[r];
       src0[i] = ok ? base0 + static_cast<uint64_t>(e.x) * p.row_bytes0 : 0;
       dst0[i] = p.buf_ptrs[r] + static_cast<uint64_t>(e.y) * p.row_bytes0;
-      int fan = -1;
+      int2 fan = make_int2(-1, -1);
       if (dstx0) {
         fan = p.fan[at];
-        if (fan < 0 || fan >= p.S) fan = -1;
-        dstx0[i] = fan >= 0 ? p.buf_ptrs[r] + static_cast<uint64_t>(fan) * p.row_bytes0 : 0;
+        if (fan.x < 0 || fan.x >= p.S) fan.x = -1;
+        if (fan.y < 0 || fan.y >= p.S) fan.y = -1;
+        dstx0[i] = fan.x >= 0 ? p.buf_ptrs[r] + static_cast<uint64_t>(fan.x) * p.row_bytes0 : 0;
+        dsty0[i] = fan.y >= 0 ? p.buf_ptrs[r] + static_cast<uint64_t>(fan.y) * p.row_bytes0 : 0;
       }
       if (p.n_streams > 1) {
         const uint64_t base1 = kDevice ? p.buf_ptrs[p.B + r] : p.host_ptrs[p.B + r];
         src1[i] = ok ? base1 + static_cast<uint64_t>(e.x) * p.row_bytes1 : 0;
         dst1[i] = p.buf_ptrs[p.B + r] + static_cast<uint64_t>(e.y) * p.row_bytes1;
-        if (dstx1) dstx1[i] = fan >= 0 ? p.buf_ptrs[p.B + r] + static_cast<uint64_t>(fan) * p.row_bytes1 : 0;
+        if (dstx1) {
+          dstx1[i] = fan.x >= 0 ? p.buf_ptrs[p.B + r] + static_cast<uint64_t>(fan.x) * p.row_bytes1 : 0;
+          dsty1[i] = fan.y >= 0 ? p.buf_ptrs[p.B + r] + static_cast<uint64_t>(fan.y) * p.row_bytes1 : 0;
+        }
       }
     }
     __syncthreads();
     if ((p.row_bytes0 & 15) == 0)
-      copy_rows<u32x4>(src0, dst0, tn, static_cast<int>(p.row_bytes0 / 16), dstx0);
+      copy_rows<u32x4>(src0, dst0, tn, static_cast<int>(p.row_bytes0 / 16), dstx0, dsty0);
     else
-      copy_rows<uint32_t>(src0, dst0, tn, static_cast<int>(p.row_bytes0 / 4), dstx0);
+      copy_rows<uint32_t>(src0, dst0, tn, static_cast<int>(p.row_bytes0 / 4), dstx0, dsty0);
     if (p.n_streams > 1) {
       if ((p.row_bytes1 & 15) == 0)
-        copy_rows<u32x4>(src1, dst1, tn, static_cast<int>(p.row_bytes1 / 16), dstx1);
+        copy_rows<u32x4>(src1, dst1, tn, static_cast<int>(p.row_bytes1 / 16), dstx1, dsty1);
       else
-        copy_rows<uint32_t>(src1, dst1, tn, static_cast<int>(p.row_bytes1 / 4), dstx1);
+        copy_rows<uint32_t>(src1, dst1, tn, static_cast<int>(p.row_bytes1 / 4), dstx1, dsty1);
     }
     __syncthreads();
   }

@@ -237,6 +237,26 @@ struct PlanHash {
   __device__ __forceinline__ uint32_t next(uint32_t h) const { return h + 1u == P ? 0u : h + 1u; }
 };
 
+// A fan word: the two largest bids (slot + 1, nonzero, below 2^16), the larger
+// in the low 16 bits, 0 = no bid.  Bids of one word are distinct slots.
+__device__ __forceinline__ void fan_bid(uint32_t* w, uint32_t v) {
+  uint32_t cur = *w;
+  for (;;) {
+    const uint32_t a = cur & 0xFFFFu, b = cur >> 16;
+    uint32_t nw;
+    if (v > a) nw = v | (a << 16);
+    else if (v > b) nw = a | (v << 16);
+    else return;   // not among the two largest
+    const uint32_t prev = atomicCAS(w, cur, nw);
+    if (prev == cur) return;
+    cur = prev;
+  }
+}
+// The two fan slots of a fan word (-1 = none).
+__device__ __forceinline__ int2 fan_slots(uint32_t w) {
+  return make_int2(static_cast<int>(w & 0xFFFFu) - 1, static_cast<int>(w >> 16) - 1);
+}
+
 // Position of index x's word in the map (its word in *word), or -1.
 __device__ __forceinline__ int plan_lookup(const uint32_t* smp, const int32_t* sc, const PlanHash& ph,
                                            int32_t x, uint32_t* word) {
@@ -264,14 +284,17 @@ __device__ __forceinline__ int plan_lookup(const uint32_t* smp, const int32_t* s
 //   a repeat copy from the largest slot this step reserved for x, when that is
 //   not o (a later token missed x again after its install was lost), or else
 //   a host copy.
-// A host entry also writes its row to the largest repeat destination of its
-// index (its fan slot: the second largest slot reserved for the index), so
-// with two tokens per step no repeat is left for a later copy.  The lists keep transfer-list order.  LDS: a map of P words,
+// A host entry also writes its row to the two largest repeat destinations of
+// its index (its fan slots: the second and third largest slots reserved for
+// the index), so with up to three tokens per step no repeat is left for a
+// later copy.  The lists keep transfer-list order.  LDS: a map of P words,
 // open addressing with linear probing keyed by the index a word names through
 // c[]; a word is (resident bit | early bit | tag | slot + 1), 0 = free, and
 // atomicMax makes every choice deterministic; beside it P fan words, one per
-// map word: the second largest slot + 1 reserved for the word's index (0 =
-// none), the largest destination among its repeats.  A word's lowest bit marks that an index whose home is that word
+// map word: the two largest repeat destinations of the word's index as two
+// 16-bit fields of slot + 1 (larger in the low field, 0 = none; a table holds
+// at most 2^14 slots), kept by a compare-and-swap loop, so the result does not
+// depend on the order of the bids.  A word's lowest bit marks that an index whose home is that word
 // sits further on (it may also be set on a word whose own index took a
 // larger slot; that only costs the scan below a probe).  The map holds at
 // most N_q * K keys and P >= 1.5 N_q K, so every probe sequence ends at a
@@ -327,11 +350,12 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
       if ((w & kPlanTag) == tag && sc[plan_slot(w)] == x) {
         // the largest reserved slot of the index (the mark bit is set with it
         // since a mark already on the word must not be lost); whichever of
-        // the old and the new slot is smaller bids for the fan word, so it
-        // ends as the second largest
+        // the old and the new slot is smaller bids for the fan word: every
+        // slot of the index but the largest bids once, and the word keeps the
+        // two largest bids
         const uint32_t old = atomicMax(&smp[h], val | kPlanDisp);
         const int other = (old & kPlanSlot) < (val & kPlanSlot) ? plan_slot(old) : o;
-        atomicMax(&sfan[h], static_cast<uint32_t>(other) + 1u);
+        fan_bid(&sfan[h], static_cast<uint32_t>(other) + 1u);
         break;
       }
       if (t == 0) atomicOr(&smp[h], kPlanDisp);   // another index holds the home word
@@ -473,11 +497,12 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   int n_list[3] = {0, 0, 0}, n_rep = 0;
   for (int e0 = 0, it = 0; e0 < listed; e0 += MT, ++it) {
     Entry c = it == 0 ? first : classify(e0 + tid);
-    int fan = -1;
-    if (c.kind == 0 && c.hw >= 0) fan = static_cast<int>(sfan[c.hw]) - 1;
+    int2 fan = make_int2(-1, -1);
+    if (c.kind == 0 && c.hw >= 0) fan = fan_slots(sfan[c.hw]);
     if (c.kind == 2) {
       ++n_rep;
-      if (static_cast<int>(sfan[c.hw]) - 1 == c.v.y) c.kind = 3;   // written by the host copy
+      const int2 f = fan_slots(sfan[c.hw]);
+      if (f.x == c.v.y || f.y == c.v.y) c.kind = 3;   // written by the host copy
     }
     if (c.kind == 5) ++n_rep;             // filled by the early fetch's copy of its index
     const int kind = c.kind;

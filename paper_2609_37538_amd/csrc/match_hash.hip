@@ -219,7 +219,7 @@ struct PlanLayout {
 // Tried in order: the list and the candidate lists, the list alone, neither.
 static PlanLayout plan_layout(int S, int K, int n_q) {
   const size_t m = match_lds_bytes(S, K);
-  if (m == 0 || n_q < 1 || S > 65536) return {0, 0, 0, 0};   // kept slots are 16-bit values
+  if (m == 0 || n_q < 1 || S > 32768) return {0, 0, 0, 0};   // kept slots and fan fields are 16-bit values
   const size_t A = align16(4 * static_cast<size_t>(S));
   const long long keys = static_cast<long long>(n_q) * K;
   const long long fixed = plan_bitmap_words(S) + kPlanMiscWords;   // besides map and fan words

@@ -368,7 +368,7 @@ __device__ void early_copy(const EarlyParams& e, unsigned char* lds) {
 }
 
 // The matching workgroup's own rows of request r after its plan: host entries
-// (each also to its fan slot) and resident copies, then the repeats, which
+// (each also to its fan slots) and resident copies, then the repeats, which
 // read slots the host copies just wrote.
 template <int NT>
 __device__ void copy_request_lists(const EarlyParams& e, int r, const int* counts, unsigned char* lds) {
@@ -376,9 +376,11 @@ __device__ void copy_request_lists(const EarlyParams& e, int r, const int* count
   uint64_t* src0 = reinterpret_cast<uint64_t*>(lds);
   uint64_t* dst0 = src0 + T;
   uint64_t* dx0 = dst0 + T;
-  uint64_t* src1 = dx0 + T;
+  uint64_t* dy0 = dx0 + T;
+  uint64_t* src1 = dy0 + T;
   uint64_t* dst1 = src1 + T;
   uint64_t* dx1 = dst1 + T;
+  uint64_t* dy1 = dx1 + T;
   const size_t lb = static_cast<size_t>(r) * e.n_q * e.K;
   const int64_t rows_r = e.rows[r];
   const uint64_t b0 = e.buf_ptrs[r], b1 = e.n_streams > 1 ? e.buf_ptrs[e.B + r] : 0;
@@ -410,27 +412,30 @@ __device__ void copy_request_lists(const EarlyParams& e, int r, const int* count
           s0 = b0 + static_cast<uint64_t>(v.x) * e.row_bytes0;
           s1 = b1 + static_cast<uint64_t>(v.x) * e.row_bytes1;
         }
-        int fan = list == 0 ? e.host_fan[lb + t0 + tid] : -1;
-        if (fan < 0 || fan >= e.S) fan = -1;
+        int2 fan = list == 0 ? e.host_fan[lb + t0 + tid] : make_int2(-1, -1);
+        if (fan.x < 0 || fan.x >= e.S) fan.x = -1;
+        if (fan.y < 0 || fan.y >= e.S) fan.y = -1;
         src0[tid] = ok ? s0 : 0;
         dst0[tid] = b0 + static_cast<uint64_t>(v.y) * e.row_bytes0;
-        dx0[tid] = fan >= 0 ? b0 + static_cast<uint64_t>(fan) * e.row_bytes0 : 0;
+        dx0[tid] = fan.x >= 0 ? b0 + static_cast<uint64_t>(fan.x) * e.row_bytes0 : 0;
+        dy0[tid] = fan.y >= 0 ? b0 + static_cast<uint64_t>(fan.y) * e.row_bytes0 : 0;
         if (e.n_streams > 1) {
           src1[tid] = ok ? s1 : 0;
           dst1[tid] = b1 + static_cast<uint64_t>(v.y) * e.row_bytes1;
-          dx1[tid] = fan >= 0 ? b1 + static_cast<uint64_t>(fan) * e.row_bytes1 : 0;
+          dx1[tid] = fan.x >= 0 ? b1 + static_cast<uint64_t>(fan.x) * e.row_bytes1 : 0;
+          dy1[tid] = fan.y >= 0 ? b1 + static_cast<uint64_t>(fan.y) * e.row_bytes1 : 0;
         }
       }
       __syncthreads();
       if ((e.row_bytes0 & 15) == 0)
-        copy_rows<u32x4, 1, NT>(src0, dst0, tn, static_cast<int>(e.row_bytes0 / 16), dx0);
+        copy_rows<u32x4, 1, NT>(src0, dst0, tn, static_cast<int>(e.row_bytes0 / 16), dx0, dy0);
       else
-        copy_rows<uint32_t, 1, NT>(src0, dst0, tn, static_cast<int>(e.row_bytes0 / 4), dx0);
+        copy_rows<uint32_t, 1, NT>(src0, dst0, tn, static_cast<int>(e.row_bytes0 / 4), dx0, dy0);
       if (e.n_streams > 1) {
         if ((e.row_bytes1 & 15) == 0)
-          copy_rows<u32x4, 1, NT>(src1, dst1, tn, static_cast<int>(e.row_bytes1 / 16), dx1);
+          copy_rows<u32x4, 1, NT>(src1, dst1, tn, static_cast<int>(e.row_bytes1 / 16), dx1, dy1);
         else
-          copy_rows<uint32_t, 1, NT>(src1, dst1, tn, static_cast<int>(e.row_bytes1 / 4), dx1);
+          copy_rows<uint32_t, 1, NT>(src1, dst1, tn, static_cast<int>(e.row_bytes1 / 4), dx1, dy1);
       }
       __syncthreads();
     }
@@ -511,7 +516,7 @@ size_t early_step_lds_bytes(int S, int K, int n_q) {
   if (m == 0) return 0;
   const size_t copier = match_threads(S, K) == kSmallThreads ? early_copy_lds<kSmallThreads>()
                                                              : early_copy_lds<kMatchThreads>();
-  const size_t lists = 6 * 8 * kListTile;
+  const size_t lists = 8 * 8 * kListTile;
   size_t v = m > copier ? m : copier;
   return v > lists ? v : lists;
 }

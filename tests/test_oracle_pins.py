@@ -482,15 +482,16 @@ def test_validate_two_tokens_share_ids(oracle_lib):
 # ---------------------------------------------------------------------------
 def _replay_plan(buf, plan, rows):
     """Apply a plan to a buffer of row ids in the kernels' order: host entries
-    into their slot and fan slot (ids outside [0, rows) are skipped, as by the
+    into their slot and fan slots (ids outside [0, rows) are skipped, as by the
     copy) and resident copies, then repeat copies."""
     hx, ho, hf, rs, rd, ps, pd = plan
     res = buf[rs].copy()                    # resident sources are not written this step
-    for x, o, f in zip(hx.tolist(), ho.tolist(), hf.tolist()):
+    for x, o, fs in zip(hx.tolist(), ho.tolist(), hf.tolist()):
         if 0 <= x < rows:
             buf[o] = x
-            if f >= 0:
-                buf[f] = x
+            for f in fs:
+                if f >= 0:
+                    buf[f] = x
     for v, o in zip(res.tolist(), rd.tolist()):
         buf[o] = v
     rep = buf[ps].copy()
@@ -503,6 +504,7 @@ def _replay_plan(buf, plan, rows):
     (8, 3, 32, 1, 2, 40, 40, False),
     (16, 4, 64, 0, 16, 120, 30, False),
     (16, 2, 32, 0, 4, 60, 30, True),
+    (16, 6, 128, 0, 16, 200, 30, False),
 ])
 def test_transfer_plan_replays_stage_two(oracle_lib, K, n_q, S, R, L, U, T, bad):
     """Replaying the plan on a buffer of row ids gives, step after step, the
@@ -514,7 +516,7 @@ def test_transfer_plan_replays_stage_two(oracle_lib, K, n_q, S, R, L, U, T, bad)
     orc = O.Oracle(B, K, n_q, S, retry=R, max_life=L, nthreads=1)
     paper = [np.full(S, -1, dtype=np.int64) for _ in range(B)]
     plan_buf = [np.full(S, -1, dtype=np.int64) for _ in range(B)]
-    n_res = n_dup = 0
+    n_res = n_dup = n_left = 0
     for t in range(T):
         X = np.stack([np.stack([rng.choice(U, size=K, replace=False) for _ in range(n_q)])
                       for _ in range(B)]).astype(np.int32)
@@ -542,7 +544,12 @@ def test_transfer_plan_replays_stage_two(oracle_lib, K, n_q, S, R, L, U, T, bad)
             assert np.array_equal(plan_buf[r], paper[r]), f"step {t} request {r}"
             n_res += nr
             n_dup += nd
+            n_left += len(ps)
     assert n_res > 0 and (n_q == 1 or n_dup > 0)
+    if n_q > 3:
+        assert n_left > 0                    # an index missed by four tokens leaves a repeat
+    else:
+        assert n_left == 0                   # two fan slots cover every repeat of three tokens
 
 
 def test_transfer_plan_finds_an_orphaned_slot(oracle_lib):
@@ -568,33 +575,46 @@ def test_transfer_plan_finds_an_orphaned_slot(oracle_lib):
     cc2 = cc.copy()
     cc2[5] = -1
     hx, ho, hf, rs, rd, ps, pd = O.transfer_plan(mx, mo, cc2, 100)
-    assert hx.tolist() == [42] and ho.tolist() == [new] and hf.tolist() == [-1]
+    assert hx.tolist() == [42] and ho.tolist() == [new] and hf.tolist() == [[-1, -1]]
     assert len(rs) == 0 and len(ps) == 0
 
 
 def test_transfer_plan_same_step_repeat(oracle_lib):
     """Hand case: the same id listed by two tokens of one step (its first
     install lost) is copied from the host once, into the larger slot, and the
-    same copy writes the other slot (its fan slot)."""
+    same copy writes the other slot (its first fan slot)."""
     mx = np.array([7, 9, 7], dtype=np.int32)
     mo = np.array([2, 3, 6], dtype=np.int32)
     c = np.full(8, -1, dtype=np.int32)
     c[2], c[3], c[6] = 7, 9, 7
     hx, ho, hf, rs, rd, ps, pd = O.transfer_plan(mx, mo, c, 10)
-    assert hx.tolist() == [9, 7] and ho.tolist() == [3, 6] and hf.tolist() == [-1, 2]
+    assert hx.tolist() == [9, 7] and ho.tolist() == [3, 6] and hf.tolist() == [[-1, -1], [2, -1]]
     assert len(ps) == 0 and len(rs) == 0
 
 
 def test_transfer_plan_three_tokens_repeat(oracle_lib):
     """Hand case: an id listed by three tokens: one host copy into the largest
-    slot, the largest other slot as its fan slot, the third copied after."""
+    slot that also writes the two other slots (its fan slots, larger first)."""
     mx = np.array([7, 7, 7], dtype=np.int32)
     mo = np.array([4, 1, 3], dtype=np.int32)
     c = np.full(8, -1, dtype=np.int32)
     c[1], c[3], c[4] = 7, 7, 7
     hx, ho, hf, rs, rd, ps, pd = O.transfer_plan(mx, mo, c, 10)
-    assert hx.tolist() == [7] and ho.tolist() == [4] and hf.tolist() == [3]
-    assert ps.tolist() == [4] and pd.tolist() == [1] and len(rs) == 0
+    assert hx.tolist() == [7] and ho.tolist() == [4] and hf.tolist() == [[3, 1]]
+    assert len(ps) == 0 and len(rs) == 0
+
+
+def test_transfer_plan_four_tokens_repeat(oracle_lib):
+    """Hand case: an id listed by four tokens: one host copy into the largest
+    slot and its two fan slots, the smallest slot copied after from the host
+    copy's slot."""
+    mx = np.array([7, 7, 7, 7], dtype=np.int32)
+    mo = np.array([4, 1, 6, 3], dtype=np.int32)
+    c = np.full(8, -1, dtype=np.int32)
+    c[1], c[3], c[4], c[6] = 7, 7, 7, 7
+    hx, ho, hf, rs, rd, ps, pd = O.transfer_plan(mx, mo, c, 10)
+    assert hx.tolist() == [7] and ho.tolist() == [6] and hf.tolist() == [[4, 3]]
+    assert ps.tolist() == [6] and pd.tolist() == [1] and len(rs) == 0
 
 
 # ---------------------------------------------------------------------------
