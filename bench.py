@@ -306,6 +306,14 @@ def main():
             reference["roofline"]["traffic_source"] = TRAFFIC_SUMMARY_S3
             reference["roofline"]["traffic_over_algorithmic"] = round(
                 s3_block["traffic_bytes_per_launch"] / s3_block["algorithmic_traffic_bytes_per_launch"], 3)
+            # what the host link itself carried (128-byte lines, per the
+            # counters): a row that several tokens of a step miss is read over
+            # the link once and served from L2 after, so `achieved` (every
+            # miss's row) can exceed what the link moves
+            link_gbps = s3_block["host_read_bytes_per_launch"] * args.steps / ref_gsec / 1e9 if ref_gsec else 0.0
+            reference["roofline"]["host_link_bytes_per_launch"] = s3_block["host_read_bytes_per_launch"]
+            reference["roofline"]["host_link_gbps"] = round(link_gbps, 3)
+            reference["roofline"]["host_link_frac"] = round(link_gbps / PCIE_GEN5_X16_GBPS, 4)
 
     K = args.steps
     us_per_step = wall / K * 1e6
@@ -446,6 +454,11 @@ def main():
                                          if traffic and traffic.get("algorithmic_traffic_bytes_per_launch")
                                          else None),
             "algorithmic_bytes_per_launch": round(host_moved / K) if host_moved else 0,
+            # what the host link itself carried per launch (128-byte lines,
+            # per the counters) and its rate over the same launches
+            "host_link_bytes_per_launch": traffic.get("host_read_bytes_per_launch") if traffic else None,
+            "host_link_gbps": (round(traffic["host_read_bytes_per_launch"] * K / gather_s / 1e9, 3)
+                               if traffic and gather_s > 0 else None),
             "measured_hipmemcpy_peak": round(memcpy_peak, 3),
         },
         "cpu_baseline": cpu,

@@ -12,6 +12,8 @@ constexpr int kMatchThreads = 1024;
 constexpr int kGatherThreads = 256;
 // Misses staged per gather tile.
 constexpr int kGatherTile = 64;
+// XCDs of an MI355X (gfx950): 8 accelerator dies of 32 CUs, each with its own L2.
+constexpr int kXcds = 8;
 
 // Per-request device counters (uint64 each, cumulative).
 enum StatIndex : int {

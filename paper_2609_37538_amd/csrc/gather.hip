@@ -1,9 +1,10 @@
 // Stage Two of AVSG on gfx950: miss-only copy of host rows into reserved slots.
 //
 // The miss list is ordered by (request, token, miss rank) (Section 3.4).  The
-// balanced kernel (S3, Eq. 6) runs C workgroups; workgroup w takes the
-// consecutive misses [floor(w N / C), floor((w+1) N / C)) of the batch-wide list
-// of N misses, so any two workgroups differ by at most one row.  The request
+// balanced kernel (S3, Eq. 6) runs C workers; worker w takes the consecutive
+// misses [floor(w N / C), floor((w+1) N / C)) of the batch-wide list of N
+// misses, so any two workers differ by at most one row, and consecutive
+// workers run on one XCD (xcd_worker).  The request
 // kernel (S1, Eq. 13) runs one workgroup per request.  Inside a workgroup a
 // tile of misses is staged in LDS as (source, destination) address pairs, and
 // the lanes copy the rows with 16-byte loads from pinned, device-mapped host
@@ -20,13 +21,26 @@
 namespace avsg {
 namespace {
 
+// Worker index of workgroup b among C workers.  The dispatcher deals
+// workgroups to the eight XCDs of the chip round-robin (workgroup b to XCD
+// b mod 8), and each XCD has its own L2; consecutive workers get consecutive
+// stretches of the miss list, which hold the same request's tokens, so they
+// go to one XCD: a row that several tokens of a step miss (a lost install) is
+// then read over the host link once and served from that XCD's L2 after.
+// A bijection of [0, C) for any C; the split of Eq. 6 and Eq. 14 is unchanged.
+__device__ __forceinline__ long long xcd_worker(long long b, long long C) {
+  constexpr long long X = kXcds;
+  const long long x = b % X, q = C / X, rem = C % X;
+  return x * q + (x < rem ? x : rem) + b / X;
+}
+
 __global__ __launch_bounds__(GT) void gather_balanced_kernel(GatherParams p) {
   __shared__ long long pre[kMaxBatch + 1];
   __shared__ long long wtot[GT / 64];
   __shared__ uint64_t src0[TILE], dst0[TILE], src1[TILE], dst1[TILE];
   request_prefix(p, pre, wtot);
   const long long N = pre[p.B];
-  const long long C = gridDim.x, w = blockIdx.x;
+  const long long C = gridDim.x, w = xcd_worker(blockIdx.x, C);
   const long long a = (w * N) / C;          // Eq. 6: consecutive, floor/ceil(N/C) each
   const long long b = ((w + 1) * N) / C;
   copy_range<false>(p, pre, a, b, src0, dst0, src1, dst1);
@@ -123,7 +137,7 @@ __global__ __launch_bounds__(GT) void gather_position_kernel(GatherParams p) {
   __shared__ uint64_t src0[TILE], dst0[TILE], src1[TILE], dst1[TILE];
   const long long per_req = static_cast<long long>(p.n_q) * p.K;
   const long long P = per_req * p.B;
-  const long long C = gridDim.x, w = blockIdx.x;
+  const long long C = gridDim.x, w = xcd_worker(blockIdx.x, C);
   const long long a = (w * P) / C;          // Eq. 14: near-equal ranges of positions
   const long long b = ((w + 1) * P) / C;
   for (long long t0 = a; t0 < b; t0 += TILE) {
