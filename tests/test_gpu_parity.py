@@ -129,6 +129,21 @@ def test_gather_modes_match_balanced(mode):
     run_parity(spec, table_every=0, buffers_every=4, gather_mode=mode)
 
 
+@pytest.mark.parametrize("workers", [1, 3, 7, 9, 13, 1000])
+def test_range_transfers_worker_counts(workers):
+    """S3 (Eq. 6) and S2 (Eq. 14) with grids whose size is not a multiple of
+    the eight XCDs, from one workgroup to more workgroups than rows: the
+    workgroup-to-worker order that gives consecutive workers to one XCD must
+    still hand every worker exactly one range, so every buffer byte equals the
+    oracle's.  Three tokens, so rows missed by several tokens of a step
+    (served from L2) are among them."""
+    from paper_2609_37538_amd import avsg as A
+    spec = W.custom_spec(name=f"range_workers_{workers}", batch=3, topk=256, slots=1024, n_q=3, steps=10,
+                         ctx=3000, retention=0.8, row_bytes=(1152, 132))
+    run_parity_modes(spec, (A.AVSG_GATHER_BALANCED, A.AVSG_GATHER_POSITION), table_every=0, buffers_every=1,
+                     miss_list_requests=3, retry=0, gather_workers=workers)
+
+
 @pytest.mark.parametrize("batch,n_q", [(2, 1), (2, 2)], ids=["s3_side", "resident_side"])
 def test_auto_transfer_parity(batch, n_q):
     """AVSG_GATHER_AUTO on both sides of its threshold (4096 and 8192 lookups
