@@ -411,6 +411,10 @@ def main():
                                          - before["lost_exhausted"] - before["lost_collision"]) / K, 1),
         "misses_per_step": round(misses / K, 1),
         "host_rows_per_step": round(host_moved / row_total / K, 1) if row_total else 0.0,
+        # resident reuse: misses filled from another slot of the request, and
+        # same-step repeats (written by their index's host copy or copied after)
+        "resident_rows_per_step": round((after["resident_rows"] - before["resident_rows"]) / K, 1),
+        "repeat_rows_per_step": round((after["duplicate_rows"] - before["duplicate_rows"]) / K, 1),
         "delivered_gbps": round(moved / wall / 1e9, 3) if moved else 0.0,
         "h2d_gbps_effective": round(eff_gbps, 3),
         "h2d_gbps_gather_kernel": round(gather_gbps, 3),
