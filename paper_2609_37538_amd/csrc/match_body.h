@@ -335,7 +335,8 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   }
 
   // (1) mark this step's reservations; one map word per distinct valid index
-  // with its largest reserved slot, and the second largest in its fan word
+  // with its largest reserved slot, and the second and third largest in its
+  // fan word
   for (int e = tid; e < listed; e += MT) {
     const int2 v = entry(e);
     const int32_t x = v.x, o = v.y;
@@ -493,7 +494,7 @@ __device__ __forceinline__ void plan_request(const MatchParams& p, const int r, 
   const Entry first = classify(tid);
 
   // (4) compact the three lists in transfer-list order; host entries carry
-  // their fan slot, repeats that won the fan word leave the repeat list
+  // their two fan slots, repeats that are in the fan word leave the repeat list
   int n_list[3] = {0, 0, 0}, n_rep = 0;
   for (int e0 = 0, it = 0; e0 < listed; e0 += MT, ++it) {
     Entry c = it == 0 ? first : classify(e0 + tid);
