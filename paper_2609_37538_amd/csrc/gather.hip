@@ -47,19 +47,20 @@ __global__ __launch_bounds__(GT) void gather_balanced_kernel(GatherParams p) {
 }
 
 // Resident-reuse Stage Two over two lists: host rows (each also written to
-// its fan slots, the two largest repeats of its index in the step), and rows already
-// in a slot of the same request (not written this step).  The last quarter of the
-// workgroups starts with the resident list and the others with the host list,
-// so the HBM copies run while the host link is busy (the link saturates with
-// far fewer workgroups); each group then moves to the other list.  Tile i of a
-// list first goes to the i-th workgroup of the group that starts with it (no
-// atomic: a step with few misses runs its host and device copies side by side
-// in one round), later tiles are claimed with an atomic counter, so the
-// workgroups that finish first take more (a CU's host-read rate varies up to
-// 2x across the chip; claimed tiles end the kernel more evenly than a static
-// Eq. 6 split).  A list shorter than one full tile per workgroup of its group
-// is cut into tiles of ceil(n / group) rows, so a step with few misses still
-// spreads them over many CUs (one workgroup reads ~2.5 GB/s from the host).
+// its fan slots, the two largest repeats of its index in the step), and rows
+// already in a slot of the same request (not written this step).  The last
+// quarter of the workgroups starts with the resident list and the others
+// with the host list, so the HBM copies run while the host link is busy (the
+// link saturates with far fewer workgroups); each group then moves to the
+// other list.  A host-first workgroup's first tile is a stretch of one
+// request's own host list (first_tiles), which needs no batch-wide prefix, so
+// host reads start one list read after the launch; the rest of the host list
+// goes in claimed tiles.  Tile i of the resident list first goes to the i-th
+// resident-first workgroup, later tiles are claimed.  Claimed tiles (an atomic
+// counter) let the workgroups that finish first take more (a CU's host-read
+// rate varies up to 2x across the chip; they end the kernel more evenly than a
+// static Eq. 6 split).  A resident list shorter than one full tile per
+// workgroup of its group is cut into tiles of ceil(n / group) rows.
 // claim[0] and claim[1] count the claimed resident and host rows; the
 // matching kernel resets both.
 constexpr int kHostTile = 6;
@@ -76,7 +77,8 @@ template <bool kDevice>
 __device__ void copy_tiles(const GatherParams& p, const long long* pre, long long n, int T, long long first,
                            long long base, int* counter, long long* next, uint64_t* src0,
                            uint64_t* dst0, uint64_t* src1, uint64_t* dst1, uint64_t* dstx0 = nullptr,
-                           uint64_t* dstx1 = nullptr, uint64_t* dsty0 = nullptr, uint64_t* dsty1 = nullptr) {
+                           uint64_t* dstx1 = nullptr, uint64_t* dsty0 = nullptr, uint64_t* dsty1 = nullptr,
+                           const long long* cov = nullptr) {
   long long t0 = first;
   for (;;) {
     if (t0 < 0) {
@@ -87,34 +89,56 @@ __device__ void copy_tiles(const GatherParams& p, const long long* pre, long lon
     }
     if (t0 >= n) break;
     copy_range<kDevice>(p, pre, t0, t0 + T < n ? t0 + T : n, src0, dst0, src1, dst1, dstx0, dstx1, dsty0,
-                        dsty1);
+                        dsty1, cov);
     t0 = -1;
   }
 }
 
 __global__ __launch_bounds__(GT) void gather_resident_kernel(GatherParams hp, GatherParams rp,
                                                               int* claim) {
-  __shared__ long long pre_h[kMaxBatch + 1], pre_r[kMaxBatch + 1];
+  __shared__ long long pre_h[kMaxBatch + 1], pre_r[kMaxBatch + 1], cov[kMaxBatch];
   __shared__ long long wtot[2 * (GT / 64)];
   __shared__ uint64_t src0[TILE], dst0[TILE], src1[TILE], dst1[TILE], dstx0[TILE], dstx1[TILE], dsty0[TILE],
       dsty1[TILE];
   __shared__ long long next;
-  request_prefix2(hp, pre_h, rp, pre_r, wtot);
-  const long long N = pre_h[hp.B], R = pre_r[rp.B];
   const int C = static_cast<int>(gridDim.x), w = static_cast<int>(blockIdx.x);
   const int cr = C / 4;                  // workgroups that start with the resident list (may be 0)
   const int ch = C - cr;                 // >= 1
-  const int th = tile_rows(N, ch, kHostTile), tr = tile_rows(R, cr > 0 ? cr : ch, TILE);
-  const long long host_base = static_cast<long long>(ch) * th;
+  const int B = hp.B;
+  // the counts of the prefixes below are requested before the first tile, so
+  // their latency overlaps it
+  long long ha = 0, hb = 0;
+  if (B <= GT && static_cast<int>(threadIdx.x) < B) {
+    ha = hp.miss_counts[static_cast<size_t>(threadIdx.x) * hp.count_stride];
+    hb = rp.miss_counts[static_cast<size_t>(threadIdx.x) * rp.count_stride];
+  }
+  if (w < ch) {
+    // first tile, before any prefix: entries [k T, (k+1) T) of request
+    // w mod B's host list, k = w div B (the host link starts one list read
+    // after the launch)
+    const int r = w % B, k = w / B;
+    const long long cnt = hp.miss_counts[static_cast<size_t>(r) * hp.count_stride];
+    const long long T = first_tile_rows(cnt, first_tiles(r, B, ch), kHostTile);
+    const long long lo = static_cast<long long>(k) * T;
+    const long long hi = lo + T < cnt ? lo + T : cnt;
+    if (lo < hi)
+      copy_range<false>(hp, nullptr, lo, hi, src0, dst0, src1, dst1, dstx0, dstx1, dsty0, dsty1, nullptr, r);
+  }
+  // the rest of the host list, batch-wide, in claimed tiles (every group),
+  // and the resident list (tile i of it first to the i-th resident-first
+  // workgroup, the rest claimed)
+  request_prefix_resid(hp, pre_h, cov, rp, pre_r, wtot, ch, kHostTile, ha, hb);
+  const long long N = pre_h[B], R = pre_r[rp.B];
+  const int tr = tile_rows(R, cr > 0 ? cr : ch, TILE);
   const long long res_base = static_cast<long long>(cr) * tr;
   if (w >= ch) {
     const long long i = C - 1 - w;       // 0 .. cr-1
     copy_tiles<true>(rp, pre_r, R, tr, i * tr, res_base, claim, &next, src0, dst0, src1, dst1);
-    copy_tiles<false>(hp, pre_h, N, th, -1, host_base, claim + 1, &next, src0, dst0, src1, dst1,
-                      dstx0, dstx1, dsty0, dsty1);
+    copy_tiles<false>(hp, pre_h, N, kHostTile, -1, 0, claim + 1, &next, src0, dst0, src1, dst1,
+                      dstx0, dstx1, dsty0, dsty1, cov);
   } else {
-    copy_tiles<false>(hp, pre_h, N, th, static_cast<long long>(w) * th, host_base, claim + 1,
-                      &next, src0, dst0, src1, dst1, dstx0, dstx1, dsty0, dsty1);
+    copy_tiles<false>(hp, pre_h, N, kHostTile, -1, 0, claim + 1, &next, src0, dst0, src1, dst1,
+                      dstx0, dstx1, dsty0, dsty1, cov);
     copy_tiles<true>(rp, pre_r, R, tr, -1, res_base, claim, &next, src0, dst0, src1, dst1);
   }
 }

@@ -55,11 +55,28 @@ __device__ inline void request_prefix(const GatherParams& p, long long* pre, lon
   __syncthreads();
 }
 
-// The exclusive prefixes of two lists' per-request totals (pre_a and pre_b,
-// B + 1 entries each), both lists' counts loaded before either is summed so
-// the two reads of device memory overlap.  wtot: 2 * GT / 64 entries.
-__device__ inline void request_prefix2(const GatherParams& pa, long long* pre_a, const GatherParams& pb,
-                                       long long* pre_b, long long* wtot) {
+// First tiles of the resident-reuse gather: workgroup w < ch copies tile
+// w div B of request w mod B's host list before any prefix is known.  Request
+// r has nfirst(r) such workgroups; its n host entries go to them in tiles of
+// ceil(n / nfirst) rows, at least one and at most T0, so few entries still
+// spread over many CUs (one workgroup reads ~2.5 GB/s from the host).
+__device__ __forceinline__ long long first_tiles(int r, int B, int ch) {
+  return r < ch ? (ch - 1 - r) / B + 1 : 0;
+}
+__device__ __forceinline__ long long first_tile_rows(long long n, long long nfirst, int T0) {
+  const long long t = nfirst > 0 ? (n + nfirst - 1) / nfirst : 1;
+  return t < 1 ? 1 : (t > T0 ? T0 : t);
+}
+
+// Prefixes for the resident-reuse gather: of the host entries that remain
+// after each request's first tiles (pre_a; cov[r] = the entries of request r
+// the first tiles copy) and of the resident entries (pre_b), B + 1 entries
+// each.  With at most GT requests thread r's two counts are ha and hb, which
+// the caller requested before its first tile so the loads overlap it.
+// wtot: 2 * GT / 64 entries.
+__device__ inline void request_prefix_resid(const GatherParams& pa, long long* pre_a, long long* cov,
+                                            const GatherParams& pb, long long* pre_b, long long* wtot,
+                                            int ch, int T0, long long ha, long long hb) {
   const int tid = threadIdx.x, lane = lane_index(), wave = tid >> 6;
   constexpr int NW = GT / 64;
   const int per = (pa.B + GT - 1) / GT;
@@ -68,11 +85,13 @@ __device__ inline void request_prefix2(const GatherParams& pa, long long* pre_a,
   for (int k = 0; k < per; ++k) {
     const int r = r0 + k;
     if (r < pa.B) {
-      long long ta = 0, tb = 0;
-      for (int g = 0; g < pa.counts_per_req; ++g)
-        ta += pa.miss_counts[static_cast<size_t>(r) * pa.count_stride + g];
-      for (int g = 0; g < pb.counts_per_req; ++g)
-        tb += pb.miss_counts[static_cast<size_t>(r) * pb.count_stride + g];
+      long long ta = per == 1 ? ha : pa.miss_counts[static_cast<size_t>(r) * pa.count_stride];
+      const long long tb = per == 1 ? hb : pb.miss_counts[static_cast<size_t>(r) * pb.count_stride];
+      const long long nfirst = first_tiles(r, pa.B, ch);
+      const long long span = nfirst * first_tile_rows(ta, nfirst, T0);
+      const long long c = ta < span ? ta : span;
+      cov[r] = c;
+      ta -= c;
       pre_a[r + 1] = ta;
       pre_b[r + 1] = tb;
       la += ta;
@@ -186,19 +205,24 @@ __device__ inline void copy_tile_rows(const GatherParams& p, int tn, uint64_t* s
 // Copy entries [a, b) of the batch-wide list.  kDevice: an entry is (source
 // slot, slot) of the request's own buffers; otherwise (host row, slot), and
 // with p.fan and staging for it (dstx0/1, dsty0/1), the row also goes to the
-// entry's fan slots.
+// entry's fan slots.  Entry j of the batch-wide list is entry cov[r] + j -
+// pre[r] of request r's list (cov: rows of each request left out of the
+// batch-wide list, or none); with fixed_r >= 0, [a, b) are entries of request
+// fixed_r's own list and pre is not read.
 template <bool kDevice>
 __device__ __forceinline__ void copy_range(const GatherParams& p, const long long* pre, long long a, long long b,
                            uint64_t* src0, uint64_t* dst0, uint64_t* src1, uint64_t* dst1,
                            uint64_t* dstx0 = nullptr, uint64_t* dstx1 = nullptr,
-                           uint64_t* dsty0 = nullptr, uint64_t* dsty1 = nullptr) {
+                           uint64_t* dsty0 = nullptr, uint64_t* dsty1 = nullptr,
+                           const long long* cov = nullptr, int fixed_r = -1) {
   const size_t per_req = static_cast<size_t>(p.n_q) * p.K;
   for (long long t0 = a; t0 < b; t0 += TILE) {
     const int tn = static_cast<int>((b - t0) < TILE ? (b - t0) : TILE);
     for (int i = threadIdx.x; i < tn; i += GT) {
       const long long j = t0 + i;
-      const int r = find_request(pre, p.B, j);
-      const size_t at = static_cast<size_t>(r) * per_req + static_cast<size_t>(j - pre[r]);
+      const int r = fixed_r >= 0 ? fixed_r : find_request(pre, p.B, j);
+      const long long k = fixed_r >= 0 ? j : (cov ? cov[r] : 0) + j - pre[r];   // entry of request r
+      const size_t at = static_cast<size_t>(r) * per_req + static_cast<size_t>(k);
       const int2 e = p.miss_list[at];
       const bool ok = e.x >= 0 && e.y >= 0 && e.y < p.S &&
                       (kDevice ? e.x < p.S : static_cast<int64_t>(e.x) < p.rows[r]);
