@@ -113,3 +113,64 @@ def test_static_step_refusals():
     assert status(A.make_config(2, 64, 1, 256, gather_mode=A.AVSG_GATHER_EARLY), 2) == A.AVSG_E_UNSUPPORTED
     # the last successful call (if any) had another configuration
     assert status(A.make_config(2, 64, 1, 512, retry=2, max_life=5), 2, cold=False) == A.AVSG_E_INVAL
+
+
+@pytest.mark.parametrize("gather_mode", [6, 0], ids=["resident", "balanced"])
+def test_static_step_graph_replays(gather_mode):
+    """A continuing avsg_step_static call captured into a HIP graph (the caller
+    it exists for) and replayed once per decode step, the next selections
+    copied into the captured input between replays: after every replay the
+    slots, counts and buffers equal a handle stepped eagerly."""
+    import torch
+    from paper_2609_37538_amd import avsg as A
+    spec = W.custom_spec(name=f"static_graph_{gather_mode}", batch=4, topk=256, slots=1024, n_q=2, steps=10,
+                         ctx=6000, row_bytes=(1152, 132), retention=0.8)
+    wl = W.Workload(spec)
+    host = HostRows(wl)
+    ref = GpuSide(wl, host, gather_mode=gather_mode)
+    cfg = ref.cfg
+    B, K, n_q, S = spec.batch, spec.topk, spec.n_q, spec.slots
+    dev = torch.device("cuda")
+    bufs = [torch.zeros((B, S, rb), dtype=torch.uint8, device=dev) for rb in spec.row_bytes]
+    buf_ptrs = [bufs[s][r].data_ptr() for s in range(len(bufs)) for r in range(B)]
+    slots = torch.empty((B, n_q, K), dtype=torch.int32, device=dev)
+    counts = torch.empty((B, n_q), dtype=torch.int32, device=dev)
+    X_in = torch.zeros((B, n_q, K), dtype=torch.int32, device=dev)
+    side = torch.cuda.Stream()
+    log(f"[no-alloc graph] {spec.name}: B={B} K={K} n_q={n_q} S={S} gather={gather_mode}")
+
+    def static_step(cold):
+        A.avsg_step_static(cfg, host.ptrs, wl.ctx, buf_ptrs, X_in.data_ptr(), None, slots.data_ptr(),
+                           counts.data_ptr(), cold_start=cold, stream=side.cuda_stream)
+
+    def check(t, X):
+        O_ref, n_ref = ref.step(X, None)
+        torch.cuda.synchronize()
+        compare_step(t, O_ref, n_ref, slots.cpu().numpy(), counts.cpu().numpy())
+        want = ref.buffers()
+        for s in range(len(bufs)):
+            assert np.array_equal(bufs[s].cpu().numpy(), want[s]), f"step {t} stream {s}: buffers differ"
+
+    g = torch.cuda.CUDAGraph()
+    try:
+        # step 0 eagerly, from a cold start
+        X = wl.topk(0)
+        X_in.copy_(torch.from_numpy(np.ascontiguousarray(X, dtype=np.int32)).to(dev))
+        torch.cuda.synchronize()
+        static_step(True)
+        check(0, X)
+        with torch.cuda.graph(g, stream=side):
+            static_step(False)
+        torch.cuda.synchronize()
+        for t in range(1, spec.steps):
+            log(f"[no-alloc graph] replay {t}")
+            X = wl.topk(t)
+            X_in.copy_(torch.from_numpy(np.ascontiguousarray(X, dtype=np.int32)).to(dev))
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            check(t, X)
+    finally:
+        del g
+        ref.close()
+        host.free()
