@@ -53,7 +53,8 @@ __global__ __launch_bounds__(GT) void gather_balanced_kernel(GatherParams p) {
 // with the host list, so the HBM copies run while the host link is busy (the
 // link saturates with far fewer workgroups); each group then moves to the
 // other list.  A host-first workgroup's first tile is a stretch of one
-// request's own host list (first_tiles), which needs no batch-wide prefix, so
+// request's own host list (first_tiles; none when a request would get more
+// than eight of them), which needs no batch-wide prefix, so
 // host reads start one list read after the launch; the rest of the host list
 // goes in claimed tiles.  Tile i of the resident list first goes to the i-th
 // resident-first workgroup, later tiles are claimed.  Claimed tiles (an atomic
@@ -112,7 +113,7 @@ __global__ __launch_bounds__(GT) void gather_resident_kernel(GatherParams hp, Ga
     ha = hp.miss_counts[static_cast<size_t>(threadIdx.x) * hp.count_stride];
     hb = rp.miss_counts[static_cast<size_t>(threadIdx.x) * rp.count_stride];
   }
-  if (w < ch) {
+  if (w < ch && first_tiles_on(B, ch)) {
     // first tile, before any prefix: entries [k T, (k+1) T) of request
     // w mod B's host list, k = w div B (the host link starts one list read
     // after the launch)

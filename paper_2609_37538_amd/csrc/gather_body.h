@@ -59,9 +59,13 @@ __device__ inline void request_prefix(const GatherParams& p, long long* pre, lon
 // w div B of request w mod B's host list before any prefix is known.  Request
 // r has nfirst(r) such workgroups; its n host entries go to them in tiles of
 // ceil(n / nfirst) rows, at least one and at most T0, so few entries still
-// spread over many CUs (one workgroup reads ~2.5 GB/s from the host).
+// spread over many CUs (one workgroup reads ~2.5 GB/s from the host).  No
+// request gets first tiles when one would get more than eight (ch > 8 B):
+// with 192 such workgroups, twelve per request (16 requests) made the step
+// slower than none, six (32 requests) and three (64) faster.
+__device__ __forceinline__ bool first_tiles_on(int B, int ch) { return ch <= 8 * B; }
 __device__ __forceinline__ long long first_tiles(int r, int B, int ch) {
-  return r < ch ? (ch - 1 - r) / B + 1 : 0;
+  return first_tiles_on(B, ch) && r < ch ? (ch - 1 - r) / B + 1 : 0;
 }
 __device__ __forceinline__ long long first_tile_rows(long long n, long long nfirst, int T0) {
   const long long t = nfirst > 0 ? (n + nfirst - 1) / nfirst : 1;
